@@ -1,0 +1,343 @@
+/*
+ * Plain CPU oracle for the SketchSSM decode path.
+ *
+ * TEST INFRASTRUCTURE ONLY.  This file is the slow, obviously-correct
+ * reference that the GPU kernels are checked against.  Only the test suite,
+ * the smoke check and the CPU-baseline leg of the benchmark may load it; the
+ * product path never links, loads or calls it.  It shares no code, header,
+ * table or helper with the HIP implementation.
+ *
+ * Everything is computed in fp64 from the plain definitions of the paper,
+ * one independent (request, head) item at a time:
+ *
+ *   - Notation follows the paper (Sec. 3.2): the state S is K x V, the read
+ *     is o = S^T q, the decay D_t is diagonal (scalar for Mamba-2 and GDN,
+ *     per channel for KDA), the transition is M_t = D_t for Mamba-2 and
+ *     M_t = (I - beta_t k_t k_t^T) D_t for GDN and KDA (eq. transition-update).
+ *   - Storage orientation at this interface: states are passed as [V][K]
+ *     (the transpose of the paper's K x V), sketches as [V][G].
+ *   - No WY factorisation, no cumulative log-decays, no pseudo-values, no
+ *     rank-W GEMM: effective queries are formed by applying M_s^T one token
+ *     at a time, buffer outputs by applying M_j to each buffered key one token
+ *     at a time (eq. m-reads), and flushes replay the buffered tokens one at a
+ *     time through the update (eq. transition-update, Algorithm 1).
+ *   - The only optional deviation from pure fp64 is `round_storage`, which
+ *     rounds the full state and the sketch to fp32 at the points where the
+ *     method writes them back (the paper keeps the state in FP32 storage,
+ *     Appendix "Detailed Evaluation Setup"); arithmetic stays fp64.
+ *
+ * Pins (see tests/test_oracle_pins.py): brute-force closed forms of the
+ * recurrence on tiny inputs, the delta-rule retrieval invariant, the
+ * state/buffer decomposition (Sec. 3.2), r = K with Omega = I, W = 1,
+ * projection behaviour of the sketch (Sec. 3.3), term isolation and
+ * linearity.
+ */
+#include <math.h>
+#include <stdint.h>
+#include <stdlib.h>
+#include <string.h>
+#ifdef _OPENMP
+#include <omp.h>
+#endif
+
+enum { ORC_MAMBA2 = 0, ORC_GDN = 1, ORC_KDA = 2 };
+
+typedef struct {
+  int32_t kind;          /* ORC_MAMBA2 | ORC_GDN | ORC_KDA                  */
+  int32_t n_items;       /* independent (request, head) items               */
+  int32_t K, V;          /* key and value channels                          */
+  int32_t G;             /* sketch rank (columns of Omega); 0 = no sketch   */
+  int32_t W;             /* window: tokens applied per flush                */
+  int32_t T;             /* decode steps                                    */
+  int32_t round_storage; /* 1: state and sketch stored as fp32              */
+} orc_cfg;
+
+/* Per-item views of the per-step inputs.  Step inputs are laid out
+ * [T][n_items][...]; log_decay is [T][n_items] (scalar decay) or
+ * [T][n_items][K] (KDA). */
+typedef struct {
+  const orc_cfg* c;
+  int item;
+  const float *q, *k, *v, *beta, *log_decay;
+} orc_tok;
+
+static const float* tok_q(const orc_tok* t, int n) { return t->q + ((size_t)n * t->c->n_items + t->item) * t->c->K; }
+static const float* tok_k(const orc_tok* t, int n) { return t->k + ((size_t)n * t->c->n_items + t->item) * t->c->K; }
+static const float* tok_v(const orc_tok* t, int n) { return t->v + ((size_t)n * t->c->n_items + t->item) * t->c->V; }
+static double tok_beta(const orc_tok* t, int n) { return (double)t->beta[(size_t)n * t->c->n_items + t->item]; }
+
+/* Diagonal of D_n: alpha = exp(log decay), per channel. */
+static double tok_decay(const orc_tok* t, int n, int kk)
+{
+  const orc_cfg* c = t->c;
+  if (c->kind == ORC_KDA)
+    return exp((double)t->log_decay[((size_t)n * c->n_items + t->item) * c->K + kk]);
+  return exp((double)t->log_decay[(size_t)n * c->n_items + t->item]);
+}
+
+static int has_erase(const orc_cfg* c) { return c->kind == ORC_GDN || c->kind == ORC_KDA; }
+
+/* y <- M_n y = (I - beta k k^T) D_n y   (GDN/KDA), or D_n y (Mamba-2). */
+static void apply_M(const orc_tok* t, int n, double* y)
+{
+  const int K = t->c->K;
+  for (int kk = 0; kk < K; ++kk) y[kk] *= tok_decay(t, n, kk);
+  if (has_erase(t->c)) {
+    const float* k = tok_k(t, n);
+    double dot = 0.0;
+    for (int kk = 0; kk < K; ++kk) dot += (double)k[kk] * y[kk];
+    const double bd = tok_beta(t, n) * dot;
+    for (int kk = 0; kk < K; ++kk) y[kk] -= bd * (double)k[kk];
+  }
+}
+
+/* x <- M_n^T x = D_n (I - beta k k^T) x   (GDN/KDA), or D_n x (Mamba-2). */
+static void apply_MT(const orc_tok* t, int n, double* x)
+{
+  const int K = t->c->K;
+  if (has_erase(t->c)) {
+    const float* k = tok_k(t, n);
+    double dot = 0.0;
+    for (int kk = 0; kk < K; ++kk) dot += (double)k[kk] * x[kk];
+    const double bd = tok_beta(t, n) * dot;
+    for (int kk = 0; kk < K; ++kk) x[kk] -= bd * (double)k[kk];
+  }
+  for (int kk = 0; kk < K; ++kk) x[kk] *= tok_decay(t, n, kk);
+}
+
+/* S <- M_n S + beta_n k_n v_n^T, S is K x V (paper orientation), S[kk*V+v].
+ * The erase acts after the decay: (I - beta k k^T)(D_n S). */
+static void update_state(const orc_tok* t, int n, double* S, double* tmpV)
+{
+  const int K = t->c->K, V = t->c->V;
+  const float* k = tok_k(t, n);
+  const float* v = tok_v(t, n);
+  const double beta = tok_beta(t, n);
+  for (int kk = 0; kk < K; ++kk) {
+    const double d = tok_decay(t, n, kk);
+    for (int j = 0; j < V; ++j) S[(size_t)kk * V + j] *= d;
+  }
+  if (has_erase(t->c)) {
+    /* tmpV = k^T (D S) */
+    for (int j = 0; j < V; ++j) tmpV[j] = 0.0;
+    for (int kk = 0; kk < K; ++kk)
+      for (int j = 0; j < V; ++j) tmpV[j] += (double)k[kk] * S[(size_t)kk * V + j];
+    for (int kk = 0; kk < K; ++kk)
+      for (int j = 0; j < V; ++j) S[(size_t)kk * V + j] -= beta * (double)k[kk] * tmpV[j];
+  }
+  for (int kk = 0; kk < K; ++kk)
+    for (int j = 0; j < V; ++j) S[(size_t)kk * V + j] += beta * (double)k[kk] * (double)v[j];
+}
+
+/* out = S^T x  (V entries). */
+static void read_state(int K, int V, const double* S, const double* x, double* out)
+{
+  for (int j = 0; j < V; ++j) out[j] = 0.0;
+  for (int kk = 0; kk < K; ++kk)
+    for (int j = 0; j < V; ++j) out[j] += S[(size_t)kk * V + j] * x[kk];
+}
+
+static void round_f32(double* a, size_t n)
+{
+  for (size_t i = 0; i < n; ++i) a[i] = (double)(float)a[i];
+}
+
+/* U = S^T Omega  (V x G), Omega is this head's K x G block. */
+static void make_sketch(int K, int V, int G, const double* S, const float* omega, double* U)
+{
+  for (int j = 0; j < V; ++j)
+    for (int g = 0; g < G; ++g) {
+      double acc = 0.0;
+      for (int kk = 0; kk < K; ++kk) acc += S[(size_t)kk * V + j] * (double)omega[(size_t)kk * G + g];
+      U[(size_t)j * G + g] = acc;
+    }
+}
+
+static void load_state(int K, int V, const float* S_vk, double* S)
+{
+  for (int j = 0; j < V; ++j)
+    for (int kk = 0; kk < K; ++kk) S[(size_t)kk * V + j] = (double)S_vk[(size_t)j * K + kk];
+}
+
+static void store_state(int K, int V, const double* S, double* S_vk)
+{
+  for (int j = 0; j < V; ++j)
+    for (int kk = 0; kk < K; ++kk) S_vk[(size_t)j * K + kk] = S[(size_t)kk * V + j];
+}
+
+/* ------------------------------------------------------------------------ */
+/* O1: the plain recurrence, one token at a time (eq. transition-update and  */
+/* m-reads, first forms).  o_exact[n] = S_n^T q_n, S_final = S_T.            */
+/* ------------------------------------------------------------------------ */
+int orc_recurrence(const orc_cfg* c, const float* S_init, const float* q, const float* k, const float* v,
+                   const float* beta, const float* log_decay, double* o_exact, double* S_final)
+{
+  if (!c || c->K <= 0 || c->V <= 0 || c->n_items <= 0 || c->T < 0) return -1;
+  if (c->K > 1024 || c->V > 1024) return -1;
+  const int K = c->K, V = c->V, NI = c->n_items;
+  int err = 0;
+#pragma omp parallel for schedule(dynamic, 1)
+  for (int i = 0; i < NI; ++i) {
+    double* S = (double*)malloc(sizeof(double) * (size_t)K * V);
+    double* tmp = (double*)malloc(sizeof(double) * (size_t)(K + V));
+    if (!S || !tmp) {
+      err = -2;
+      free(S);
+      free(tmp);
+      continue;
+    }
+    orc_tok t = {c, i, q, k, v, beta, log_decay};
+    load_state(K, V, S_init + (size_t)i * V * K, S);
+    for (int n = 0; n < c->T; ++n) {
+      update_state(&t, n, S, tmp);
+      double xq[1024];
+      const float* qn = tok_q(&t, n);
+      for (int kk = 0; kk < K; ++kk) xq[kk] = (double)qn[kk];
+      if (o_exact) read_state(K, V, S, xq, o_exact + ((size_t)n * NI + i) * V);
+    }
+    if (S_final) store_state(K, V, S, S_final + (size_t)i * V * K);
+    free(S);
+    free(tmp);
+  }
+  return err;
+}
+
+/* ------------------------------------------------------------------------ */
+/* O2: SketchSSM inference (Algorithm 1) for every item.                    */
+/*                                                                          */
+/* Window-local time t = 1..W.  At a non-flush step (t < W):                 */
+/*   q~_t   = M_1^T ... M_t^T q_t                 (effective query)          */
+/*   c_t    = C q~_t                              (coefficient vector)       */
+/*   o^state_hat = U c_t,   o^state = S0^T q~_t   (sketch and exact reads)   */
+/*   o^buf  = sum_{s<=t} beta_s <M_{s+1:t} k_s, q_t> v_s                     */
+/*   o_t    = o^state_hat + o^buf                                            */
+/* At the flush (t = W): replay the W buffered tokens into S0 one at a time, */
+/* o_t = S0^T q_t exactly, U = S0^T Omega, clear the buffer.                 */
+/*                                                                          */
+/* Per-item head index: heads[i] selects Omega [H][K][G] and C [H][G][K].    */
+/* Outputs (any may be NULL):                                                */
+/*   o            [T][n][V]  the method's output                             */
+/*   o_state_hat  [T][n][V]  U c_t at non-flush steps, S0^T q at flushes     */
+/*   o_state      [T][n][V]  S0^T q~_t at non-flush steps, S0^T q at flushes */
+/*   o_buf        [T][n][V]  buffer term (0 at flushes)                      */
+/*   S_final      [n][V][K]  the full state after the last flush             */
+/*   U_final      [n][V][G]  the sketch after the last flush                 */
+/* The exact windowed output (what a full-state read would give) is         */
+/* o_state + o_buf at every step.                                           */
+/* ------------------------------------------------------------------------ */
+int orc_sketchssm(const orc_cfg* c, const int32_t* heads, const float* omega, const float* coef,
+                  const float* S_init, const float* q, const float* k, const float* v, const float* beta,
+                  const float* log_decay, double* o, double* o_state_hat, double* o_state, double* o_buf,
+                  double* S_final, double* U_final)
+{
+  if (!c || c->K <= 0 || c->V <= 0 || c->n_items <= 0 || c->T < 0 || c->W < 1 || c->G < 0) return -1;
+  if (c->K > 1024 || c->V > 1024 || c->G > 1024) return -1;
+  const int K = c->K, V = c->V, G = c->G, NI = c->n_items, W = c->W;
+  int err = 0;
+#pragma omp parallel for schedule(dynamic, 1)
+  for (int i = 0; i < NI; ++i) {
+    const int h = heads ? heads[i] : 0;
+    const float* Om = omega ? omega + (size_t)h * K * G : NULL;
+    const float* Cm = coef ? coef + (size_t)h * G * K : NULL;
+    double* S0 = (double*)malloc(sizeof(double) * (size_t)K * V);
+    double* U = (double*)malloc(sizeof(double) * ((size_t)V * (G > 0 ? G : 1)));
+    double* tmp = (double*)malloc(sizeof(double) * (size_t)(K + V));
+    int* buf = (int*)malloc(sizeof(int) * (size_t)W);
+    if (!S0 || !U || !tmp || !buf) {
+      err = -2;
+      free(S0); free(U); free(tmp); free(buf);
+      continue;
+    }
+    orc_tok t = {c, i, q, k, v, beta, log_decay};
+    load_state(K, V, S_init + (size_t)i * V * K, S0);
+    /* Initialise the sketch from the prefill state (Algorithm 1). */
+    if (G > 0) {
+      make_sketch(K, V, G, S0, Om, U);
+      if (c->round_storage) round_f32(U, (size_t)V * G);
+    }
+    int len = 0; /* tokens in the buffer B */
+    double x[1024], y[1024], cvec[1024], ohat[1024], ostate[1024], obuf[1024];
+    for (int n = 0; n < c->T; ++n) {
+      buf[len++] = n; /* append the current update inputs to B */
+      const size_t oi = ((size_t)n * NI + i) * V;
+      const float* qn = tok_q(&t, n);
+      if (len < W) {
+        /* effective query q~ = M_1^T (M_2^T ( ... M_t^T q)) */
+        for (int kk = 0; kk < K; ++kk) x[kk] = (double)qn[kk];
+        for (int s = len - 1; s >= 0; --s) apply_MT(&t, buf[s], x);
+        /* exact state read and sketch read */
+        read_state(K, V, S0, x, ostate);
+        for (int j = 0; j < V; ++j) ohat[j] = 0.0;
+        if (G > 0) {
+          for (int g = 0; g < G; ++g) {
+            double acc = 0.0;
+            for (int kk = 0; kk < K; ++kk) acc += (double)Cm[(size_t)g * K + kk] * x[kk];
+            cvec[g] = acc;
+          }
+          for (int j = 0; j < V; ++j) {
+            double acc = 0.0;
+            for (int g = 0; g < G; ++g) acc += U[(size_t)j * G + g] * cvec[g];
+            ohat[j] = acc;
+          }
+        }
+        /* buffer output: sum_s beta_s <M_{s+1:t} k_s, q_t> v_s */
+        for (int j = 0; j < V; ++j) obuf[j] = 0.0;
+        for (int s = 0; s < len; ++s) {
+          const float* ks = tok_k(&t, buf[s]);
+          for (int kk = 0; kk < K; ++kk) y[kk] = (double)ks[kk];
+          for (int r = s + 1; r < len; ++r) apply_M(&t, buf[r], y);
+          double a = 0.0;
+          for (int kk = 0; kk < K; ++kk) a += y[kk] * (double)qn[kk];
+          const double w = tok_beta(&t, buf[s]) * a;
+          const float* vs = tok_v(&t, buf[s]);
+          for (int j = 0; j < V; ++j) obuf[j] += w * (double)vs[j];
+        }
+        for (int j = 0; j < V; ++j) {
+          if (o) o[oi + j] = ohat[j] + obuf[j];
+          if (o_state_hat) o_state_hat[oi + j] = ohat[j];
+          if (o_state) o_state[oi + j] = ostate[j];
+          if (o_buf) o_buf[oi + j] = obuf[j];
+        }
+      } else {
+        /* flush: apply every buffered update exactly, in order */
+        for (int s = 0; s < len; ++s) update_state(&t, buf[s], S0, tmp);
+        if (c->round_storage) round_f32(S0, (size_t)K * V);
+        for (int kk = 0; kk < K; ++kk) x[kk] = (double)qn[kk];
+        read_state(K, V, S0, x, ostate);
+        if (G > 0) {
+          make_sketch(K, V, G, S0, Om, U);
+          if (c->round_storage) round_f32(U, (size_t)V * G);
+        }
+        for (int j = 0; j < V; ++j) {
+          if (o) o[oi + j] = ostate[j];
+          if (o_state_hat) o_state_hat[oi + j] = ostate[j];
+          if (o_state) o_state[oi + j] = ostate[j];
+          if (o_buf) o_buf[oi + j] = 0.0;
+        }
+        len = 0; /* clear B */
+      }
+    }
+    if (S_final) store_state(K, V, S0, S_final + (size_t)i * V * K);
+    if (U_final && G > 0) memcpy(U_final + (size_t)i * V * G, U, sizeof(double) * (size_t)V * G);
+    free(S0); free(U); free(tmp); free(buf);
+  }
+  return err;
+}
+
+int orc_max_threads(void)
+{
+#ifdef _OPENMP
+  return omp_get_max_threads();
+#else
+  return 1;
+#endif
+}
+
+void orc_set_threads(int n)
+{
+#ifdef _OPENMP
+  if (n > 0) omp_set_num_threads(n);
+#else
+  (void)n;
+#endif
+}

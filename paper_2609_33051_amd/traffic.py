@@ -1,0 +1,133 @@
+"""Byte accounting for the decode path.
+
+Two models live here.
+
+paper_* -- the paper's state-memory traffic model (Appendix "State Memory
+Traffic Reduction", Table tab:m-traffic): per state head per decode step,
+Standard reads and writes the fp32 state (8KV bytes); ReplaySSM reads it every
+step and writes it every W steps; SketchSSM reads a bf16 sketch, coefficient
+map and (delta-rule families) projected erase vectors between flushes,
+T_G = 2G(V + K + eW), and reads and writes the state once per window.  Ring
+buffer traffic is excluded there.
+
+algorithmic_* -- the bytes this implementation's kernels must move per
+(request, head) item, ring buffer included (the ring is as large as the sketch
+read at these shapes, so leaving it out would flatter the result).  Shared
+per-head tensors (Omega, C) are amortised over the batch and not counted.
+These are the numerators of the reported HBM roofline fractions.
+"""
+from __future__ import annotations
+
+from dataclasses import dataclass
+
+HBM_PEAK_GBPS = 8000.0  # MI355X HBM3E, published peak
+
+
+def paper_state_bytes(K: int, V: int) -> float:
+    """D = 4KV: the fp32 state of one head."""
+    return 4.0 * K * V
+
+
+def paper_sketch_read_bytes(K: int, V: int, G: float, W: int, e: int) -> float:
+    """T_G = 2G(V + K + eW): bf16 U, C and (e = 1) projected erase vectors."""
+    return 2.0 * G * (V + K + e * W)
+
+
+def paper_sketchssm_avg_read(K: int, V: int, G: float, W: int, e: int) -> float:
+    """B_G = ((W - 1) T_G + D) / W."""
+    return ((W - 1) * paper_sketch_read_bytes(K, V, G, W, e) + paper_state_bytes(K, V)) / W
+
+
+def paper_reduction(K: int, V: int, G: float, W: int, e: int) -> float:
+    """R_G = 8KV / ((W - 1) T_G / W + 8KV / W), reduction relative to Standard."""
+    return 8.0 * K * V / ((W - 1) * paper_sketch_read_bytes(K, V, G, W, e) / W + 8.0 * K * V / W)
+
+
+def paper_replay_reduction(W: int) -> float:
+    """ReplaySSM: (D + D) / (D + D/W) = 2W / (W + 1)."""
+    return 2.0 * W / (W + 1)
+
+
+@dataclass(frozen=True)
+class Shape:
+    kind: str      # "mamba2" | "gdn" | "kda"
+    dk: int
+    dv: int
+    rank: int
+    window: int
+    io_bytes: int  # 2 (bf16) or 4 (fp32)
+
+    @property
+    def erase(self) -> bool:
+        return self.kind in ("gdn", "kda")
+
+    @property
+    def decay_bytes(self) -> int:
+        """Per-token log decay / cumulative log decay: a scalar, or K values (KDA)."""
+        return 4 * self.dk if self.kind == "kda" else 4
+
+
+def step_input_bytes(s: Shape) -> int:
+    """q, k, v in the io dtype plus beta and the log decay."""
+    return s.io_bytes * (2 * s.dk + s.dv) + 4 + s.decay_bytes
+
+
+def ring_slot_read_bytes(s: Shape, baseline: bool = False) -> int:
+    """Ring fields an earlier slot contributes to a non-flush read.
+
+    Mamba-2: raw key and value, cumulative log decay, beta.
+    GDN/KDA: raw key, pseudo-value u (fp32), cumulative log decay, and either
+    the projected erase vector f (r fp32, sketch path) or the full erase
+    factor pi (K fp32, exact full-read baseline)."""
+    if not s.erase:
+        return s.io_bytes * (s.dk + s.dv) + 4 + 4
+    extra = 4 * s.dk if baseline else 4 * s.rank
+    return s.io_bytes * s.dk + 4 * s.dv + s.decay_bytes + extra
+
+
+def ring_slot_write_bytes(s: Shape, n: int, baseline: bool = False) -> int:
+    """Fields written for the slot appended at position n (0-based)."""
+    if not s.erase:
+        return s.io_bytes * (s.dk + s.dv) + 4 + 4
+    extra = 4 * s.dk if baseline else 4 * s.rank
+    return s.io_bytes * s.dk + 4 * s.dv + s.decay_bytes + 4 + extra + 4 * n
+
+
+def decode_bytes(s: Shape, n: int) -> int:
+    """Sketch read at slot n: inputs + n earlier slots + the appended slot + U + o."""
+    return (step_input_bytes(s) + n * ring_slot_read_bytes(s) + ring_slot_write_bytes(s, n)
+            + 4 * s.dv * s.rank + 4 * s.dv)
+
+
+def full_read_bytes(s: Shape, n: int) -> int:
+    """Exact full-state read at slot n: as decode with S (4KV) in place of U."""
+    return (step_input_bytes(s) + n * ring_slot_read_bytes(s, True) + ring_slot_write_bytes(s, n, True)
+            + 4 * s.dk * s.dv + 4 * s.dv)
+
+
+def flush_bytes(s: Shape, n_buffered: int, rank: int | None = None) -> int:
+    """Flush with n_buffered earlier slots: S read + write, the ring, the
+    current token, the sketch write (rank columns) and o."""
+    r = s.rank if rank is None else rank
+    if s.erase:
+        slot = s.io_bytes * s.dk + 4 * s.dv + s.decay_bytes + 4
+        bcoef = 4 * n_buffered * (n_buffered - 1) // 2
+    else:
+        slot = s.io_bytes * (s.dk + s.dv) + 4 + 4
+        bcoef = 0
+    return (8 * s.dk * s.dv + n_buffered * slot + bcoef + step_input_bytes(s)
+            + 4 * s.dv * r + 4 * s.dv)
+
+
+def init_bytes(s: Shape) -> int:
+    """Sketch construction from S alone: S read + U write."""
+    return 4 * s.dk * s.dv + 4 * s.dv * s.rank
+
+
+def window_bytes(s: Shape, baseline: bool = False) -> dict:
+    """Per-item bytes over one window: W-1 non-flush reads and one flush."""
+    W = s.window
+    reads = [full_read_bytes(s, n) if baseline else decode_bytes(s, n) for n in range(W - 1)]
+    fl = flush_bytes(s, W - 1, 0 if baseline else None)
+    return {"nonflush": reads, "flush": fl, "total": sum(reads) + fl,
+            "nonflush_mean": (sum(reads) / len(reads)) if reads else 0.0}

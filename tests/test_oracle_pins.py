@@ -1,0 +1,229 @@
+"""Pins for the CPU oracle: it is checked against things other than itself.
+
+Each test states what the paper or the mathematics fixes.  Together they are
+chosen so that a plausible slip in the oracle (erase before decay, a dropped
+self term, a transposed operand, a missing flush token, the sketch taken on
+the wrong side of S) fails at least one of them.
+"""
+import numpy as np
+import pytest
+
+import oracle
+
+KINDS = ["mamba2", "gdn", "kda"]
+
+
+def tiny_inputs(kind, n=3, K=5, V=4, T=9, seed=0, unit_keys=False, beta_one=False, strong_decay=False):
+    rng = np.random.default_rng(seed)
+    S0 = rng.standard_normal((n, V, K)).astype(np.float32)
+    q = rng.standard_normal((T, n, K)).astype(np.float32)
+    k = rng.standard_normal((T, n, K)).astype(np.float32)
+    if unit_keys:
+        k = (k / np.linalg.norm(k, axis=-1, keepdims=True)).astype(np.float32)
+    else:
+        k = (0.6 * k).astype(np.float32)
+    v = rng.standard_normal((T, n, V)).astype(np.float32)
+    beta = np.ones((T, n), np.float32) if beta_one else rng.uniform(0.1, 0.9, (T, n)).astype(np.float32)
+    lo = -1.5 if strong_decay else -0.4
+    shape = (T, n, K) if kind == "kda" else (T, n)
+    logd = rng.uniform(lo, 0.0, shape).astype(np.float32)
+    return S0, q, k, v, beta, logd
+
+
+def explicit_M(kind, k, beta, logd):
+    """M_t as an explicit K x K matrix (Sec. 3.2): D_t, or (I - beta k k^T) D_t."""
+    K = k.shape[0]
+    d = np.exp(logd.astype(np.float64)) * np.ones(K)
+    D = np.diag(d)
+    if kind == "mamba2":
+        return D
+    kk = k.astype(np.float64)
+    return (np.eye(K) - float(beta) * np.outer(kk, kk)) @ D
+
+
+def brute_force_outputs(kind, S0, q, k, v, beta, logd):
+    """o_n = S_n^T q_n with S_n = M_{1:n} S_0 + sum_m beta_m M_{m+1:n} k_m v_m^T,
+    every ordered product formed explicitly (second form of eq. transition-update)."""
+    T, n, K = q.shape
+    V = v.shape[2]
+    out = np.zeros((T, n, V))
+    for i in range(n):
+        Ms = [explicit_M(kind, k[t, i], beta[t, i], logd[t, i]) for t in range(T)]
+        S_init = S0[i].astype(np.float64).T  # K x V
+        for t in range(T):
+            def prod(a, b):  # M_{a:b} = M_b ... M_a  (1-based, inclusive); identity when a > b
+                P = np.eye(K)
+                for j in range(a, b + 1):
+                    P = Ms[j - 1] @ P
+                return P
+            S = prod(1, t + 1) @ S_init
+            for m in range(1, t + 2):
+                S = S + float(beta[m - 1, i]) * np.outer(prod(m + 1, t + 1) @ k[m - 1, i].astype(np.float64),
+                                                         v[m - 1, i].astype(np.float64))
+            out[t, i] = S.T @ q[t, i].astype(np.float64)
+    return out
+
+
+@pytest.mark.parametrize("kind", KINDS)
+def test_recurrence_equals_explicit_products(kind):
+    """O1 against the closed form with explicitly multiplied transition matrices."""
+    S0, q, k, v, beta, logd = tiny_inputs(kind, seed=1)
+    o, _ = oracle.recurrence(kind, S0, q, k, v, beta, logd)
+    ref = brute_force_outputs(kind, S0, q, k, v, beta, logd)
+    np.testing.assert_allclose(o, ref, rtol=1e-11, atol=1e-11)
+
+
+def test_scalar_decay_is_decay_masked_attention():
+    """Mamba-2 form (M_t = alpha_t I): the read is causal attention with a
+    multiplicative decay mask plus the decayed initial-state read."""
+    S0, q, k, v, beta, logd = tiny_inputs("mamba2", n=2, K=6, V=3, T=11, seed=2)
+    o, _ = oracle.recurrence("mamba2", S0, q, k, v, beta, logd)
+    T = q.shape[0]
+    for i in range(S0.shape[0]):
+        L = np.cumsum(logd[:, i].astype(np.float64))          # log prod_{j<=n} alpha_j
+        mask = np.tril(np.exp(L[:, None] - L[None, :]))        # prod_{m<j<=n} alpha_j
+        Q = q[:, i].astype(np.float64)
+        Kx = k[:, i].astype(np.float64)
+        Vx = v[:, i].astype(np.float64)
+        att = (Q @ Kx.T) * mask * beta[:, i].astype(np.float64)[None, :]
+        ref = att @ Vx + np.exp(L)[:, None] * (Q @ S0[i].astype(np.float64).T)
+        np.testing.assert_allclose(o[:, i], ref, rtol=1e-11, atol=1e-11)
+    assert T == 11
+
+
+@pytest.mark.parametrize("kind", ["gdn", "kda"])
+@pytest.mark.parametrize("beta_one", [False, True])
+def test_delta_rule_retrieval(kind, beta_one):
+    """The delta-rule write of token t leaves
+    S_t^T k_t = (1 - beta_t |k_t|^2) (D_t S_{t-1})^T k_t + beta_t |k_t|^2 v_t,
+    so with unit keys and beta_t = 1 the state returns v_t at key k_t.  This
+    holds only if the erase acts after the decay (M_t = (I - beta k k^T) D_t)."""
+    K, V, T = 6, 5, 7
+    S0, q, k, v, beta, logd = tiny_inputs(kind, n=2, K=K, V=V, T=T, seed=3 + beta_one, unit_keys=True,
+                                          beta_one=beta_one, strong_decay=True)
+    _, S_prev = oracle.recurrence(kind, S0, q[:T - 1], k[:T - 1], v[:T - 1], beta[:T - 1], logd[:T - 1])
+    _, S_last = oracle.recurrence(kind, S0, q, k, v, beta, logd)
+    for i in range(2):
+        kt = k[T - 1, i].astype(np.float64)
+        nk = float(kt @ kt)
+        b = float(beta[T - 1, i])
+        d = np.exp(logd[T - 1, i].astype(np.float64)) * np.ones(K)
+        lhs = S_last[i] @ kt                                     # S_t^T k_t  (storage is [V][K])
+        rhs = (1 - b * nk) * (S_prev[i] @ (d * kt)) + b * nk * v[T - 1, i].astype(np.float64)
+        np.testing.assert_allclose(lhs, rhs, rtol=1e-12, atol=1e-12)
+        if beta_one:
+            np.testing.assert_allclose(lhs, v[T - 1, i], rtol=0, atol=1e-6)
+
+
+def orthonormal(K, G, seed):
+    Q, R = np.linalg.qr(np.random.default_rng(seed).standard_normal((K, G)))
+    return (Q * np.sign(np.diag(R))[None, :]).astype(np.float32)
+
+
+def heads_omega(H, K, G, seed):
+    om = np.stack([orthonormal(K, G, seed + h) for h in range(H)])
+    return om, np.ascontiguousarray(om.transpose(0, 2, 1))
+
+
+@pytest.mark.parametrize("kind", KINDS)
+@pytest.mark.parametrize("W", [3, 4])
+def test_flush_equals_recurrence(kind, W):
+    """Algorithm 1's flush replays the buffer exactly: after every W-th token
+    the state and the output equal the plain recurrence."""
+    T = 3 * W
+    S0, q, k, v, beta, logd = tiny_inputs(kind, T=T, seed=5)
+    om, C = heads_omega(2, 5, 2, 10)
+    heads = np.array([0, 1, 0], np.int32)
+    o_ex, S_ex = oracle.recurrence(kind, S0, q, k, v, beta, logd)
+    r = oracle.sketchssm(kind, W, heads, om, C, S0, q, k, v, beta, logd)
+    np.testing.assert_allclose(r.S_final, S_ex, rtol=1e-12, atol=1e-12)
+    flush = np.arange(W - 1, T, W)
+    np.testing.assert_allclose(r.o[flush], o_ex[flush], rtol=1e-12, atol=1e-12)
+
+
+@pytest.mark.parametrize("kind", KINDS)
+def test_state_buffer_decomposition(kind):
+    """Eq. m-reads: S_t^T q_t = S_0^T q~_t + o^buffer_t at every step."""
+    W, T = 5, 12
+    S0, q, k, v, beta, logd = tiny_inputs(kind, T=T, seed=6)
+    om, C = heads_omega(1, 5, 2, 11)
+    r = oracle.sketchssm(kind, W, np.zeros(3, np.int32), om, C, S0, q, k, v, beta, logd)
+    o_ex, _ = oracle.recurrence(kind, S0, q, k, v, beta, logd)
+    np.testing.assert_allclose(r.o_exact_windowed, o_ex, rtol=1e-11, atol=1e-11)
+    # the buffer term is nonzero between flushes and the state term is not the whole output
+    assert np.abs(r.o_buf).max() > 1e-3
+
+
+@pytest.mark.parametrize("kind", KINDS)
+def test_full_rank_identity_sketch_is_exact(kind):
+    """r = K with Omega = I (so C = I): the sketch read is the exact state read."""
+    K, V, W, T = 5, 3, 4, 13
+    S0, q, k, v, beta, logd = tiny_inputs(kind, K=K, V=V, T=T, seed=7)
+    om = np.eye(K, dtype=np.float32)[None]
+    r = oracle.sketchssm(kind, W, np.zeros(3, np.int32), om, om.copy(), S0, q, k, v, beta, logd)
+    o_ex, S_ex = oracle.recurrence(kind, S0, q, k, v, beta, logd)
+    np.testing.assert_allclose(r.o, o_ex, rtol=1e-11, atol=1e-11)
+    np.testing.assert_allclose(r.U_final, r.S_final, rtol=1e-12, atol=1e-12)  # U = S^T I, storage [V][K]
+
+
+@pytest.mark.parametrize("kind", KINDS)
+def test_window_one_is_plain_recurrence(kind):
+    """W = 1: every token is a flush, the sketch is never read."""
+    S0, q, k, v, beta, logd = tiny_inputs(kind, T=6, seed=8)
+    om, C = heads_omega(1, 5, 2, 12)
+    r = oracle.sketchssm(kind, 1, np.zeros(3, np.int32), om, C, S0, q, k, v, beta, logd)
+    o_ex, S_ex = oracle.recurrence(kind, S0, q, k, v, beta, logd)
+    np.testing.assert_allclose(r.o, o_ex, rtol=1e-12, atol=1e-12)
+    np.testing.assert_allclose(r.S_final, S_ex, rtol=1e-12, atol=1e-12)
+
+
+def test_sketch_projection_behaviour():
+    """Sec. 3.3 with C = Omega^T and orthonormal Omega (K > G): a Mamba-2 query in
+    span(Omega) is read exactly, a query orthogonal to it reads zero state."""
+    K, V, G, W, T, n = 7, 4, 3, 6, 5, 2
+    S0, q, k, v, beta, logd = tiny_inputs("mamba2", n=n, K=K, V=V, T=T, seed=9)
+    om = orthonormal(K, G, 13)[None]
+    C = np.ascontiguousarray(om.transpose(0, 2, 1))
+    rng = np.random.default_rng(14)
+    q_in = np.einsum("kg,tng->tnk", om[0].astype(np.float64), rng.standard_normal((T, n, G))).astype(np.float32)
+    r = oracle.sketchssm("mamba2", W, np.zeros(n, np.int32), om, C, S0, q_in, k, v, beta, logd)
+    np.testing.assert_allclose(r.o_state_hat, r.o_state, rtol=1e-6, atol=1e-6)  # limited by fp32 rounding of q
+    P = np.eye(K) - om[0].astype(np.float64) @ om[0].astype(np.float64).T
+    q_perp = np.einsum("kj,tnj->tnk", P, rng.standard_normal((T, n, K))).astype(np.float32)
+    r = oracle.sketchssm("mamba2", W, np.zeros(n, np.int32), om, C, S0, q_perp, k, v, beta, logd)
+    assert np.abs(r.o_state_hat).max() < 1e-6 * max(1.0, np.abs(r.o_state).max())
+    assert np.abs(r.o_state).max() > 1e-2
+
+
+@pytest.mark.parametrize("kind", KINDS)
+def test_term_isolation_and_linearity(kind):
+    """v = 0 removes the buffer term; S0 = 0 removes the state term in the first
+    window; outputs are jointly linear in (S0, v) for fixed keys, queries, gates."""
+    W, T = 4, 10
+    S0, q, k, v, beta, logd = tiny_inputs(kind, T=T, seed=15)
+    om, C = heads_omega(1, 5, 2, 16)
+    hz = np.zeros(3, np.int32)
+    r0 = oracle.sketchssm(kind, W, hz, om, C, S0, q, k, np.zeros_like(v), beta, logd)
+    assert np.abs(r0.o_buf).max() == 0.0
+    nf = [t for t in range(T) if (t + 1) % W != 0]
+    np.testing.assert_allclose(r0.o[nf], r0.o_state_hat[nf], rtol=0, atol=0)
+    rz = oracle.sketchssm(kind, W, hz, om, C, np.zeros_like(S0), q, k, v, beta, logd)
+    assert np.abs(rz.o_state_hat[:W - 1]).max() == 0.0 and np.abs(rz.o_state[:W - 1]).max() == 0.0
+    S1, _, _, v1, _, _ = tiny_inputs(kind, T=T, seed=17)
+    a, b = 0.7, -1.3
+    ra = oracle.sketchssm(kind, W, hz, om, C, S0, q, k, v, beta, logd)
+    rb = oracle.sketchssm(kind, W, hz, om, C, S1, q, k, v1, beta, logd)
+    rab = oracle.sketchssm(kind, W, hz, om, C, a * S0 + b * S1, q, k, a * v + b * v1, beta, logd)
+    np.testing.assert_allclose(rab.o, a * ra.o + b * rb.o, rtol=1e-5, atol=1e-5)  # fp32 rounding of a*S0+b*S1
+
+
+def test_storage_rounding_only_changes_state_at_fp32_level():
+    """round_storage mirrors fp32 state/sketch storage; the result moves by at most fp32 rounding."""
+    S0, q, k, v, beta, logd = tiny_inputs("gdn", T=12, seed=18)
+    om, C = heads_omega(1, 5, 2, 19)
+    hz = np.zeros(3, np.int32)
+    r = oracle.sketchssm("gdn", 4, hz, om, C, S0, q, k, v, beta, logd)
+    rr = oracle.sketchssm("gdn", 4, hz, om, C, S0, q, k, v, beta, logd, round_storage=True)
+    rel = np.linalg.norm(rr.o - r.o) / np.linalg.norm(r.o)
+    assert 0 < rel < 1e-6
+    np.testing.assert_array_equal(rr.S_final, rr.S_final.astype(np.float32).astype(np.float64))

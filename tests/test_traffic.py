@@ -1,0 +1,40 @@
+"""The byte accounting reproduces the paper's printed traffic reductions."""
+import csv
+import os
+
+import pytest
+
+from paper_2609_33051_amd import traffic
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden", "traffic_reduction.csv")
+
+
+def rows():
+    with open(GOLDEN) as f:
+        return list(csv.DictReader(line for line in f if not line.startswith("#")))
+
+
+@pytest.mark.parametrize("row", rows(), ids=lambda r: f"{r['model']}-G{r['G']}")
+def test_reduction_matches_printed_tables(row):
+    K, V, e, W, G = (int(row[x]) for x in ("K", "V", "e", "W", "G"))
+    assert round(traffic.paper_reduction(K, V, G, W, e), 2) == pytest.approx(float(row["printed"]), abs=1e-9)
+
+
+def test_replay_reduction_printed():
+    # Appendix "State Memory Traffic Reduction": 32/17 = 1.88x at W = 16
+    assert round(traffic.paper_replay_reduction(16), 2) == 1.88
+
+
+def test_reduction_limits():
+    # G -> 0 leaves only the flush: reduction W; a sketch as large as the state is worse than ReplaySSM
+    assert traffic.paper_reduction(128, 64, 0, 16, 0) == pytest.approx(16.0)
+    assert traffic.paper_reduction(128, 64, 128, 16, 0) < traffic.paper_replay_reduction(16) * 1.5
+
+
+def test_algorithmic_bytes_mamba2_decode():
+    # Mamba-2 decode layer, bf16 io, fp32 U: 8,136 bytes per item averaged over the window
+    s = traffic.Shape("mamba2", 128, 64, 16, 16, 2)
+    wb = traffic.window_bytes(s)
+    assert len(wb["nonflush"]) == 15
+    assert wb["nonflush_mean"] == pytest.approx(8136.0)
+    assert traffic.full_read_bytes(s, 0) - traffic.decode_bytes(s, 0) == 4 * 128 * 64 - 4 * 64 * 16

@@ -1,0 +1,130 @@
+"""ctypes binding of libsketchssm.so (include/sketchssm.h).
+
+Argument marshalling only: every step of the path runs in the HIP kernels.
+The functions keep the C names and take device pointers either as integers
+or as torch tensors (their data_ptr()); `stream` is a hipStream_t handle
+(torch.cuda.current_stream().cuda_stream) or None for the default stream.
+A non-OK status raises SketchSSMError with the library's message.  There is
+no fallback: if the library is not built, loading raises.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(PKG, "libsketchssm.so")
+
+MAMBA2, GDN, KDA = 0, 1, 2
+KIND_IDS = {"mamba2": MAMBA2, "gdn": GDN, "kda": KDA}
+F32, BF16 = 0, 1
+
+STATUS = {0: "SKSSM_OK", -1: "SKSSM_EINVAL", -2: "SKSSM_EUNSUPPORTED", -3: "SKSSM_EALIGN",
+          -4: "SKSSM_ESTATE", -5: "SKSSM_EHIP"}
+
+FUNCTIONS = ("sketchssm_update", "sketchssm_decode", "sketchssm_full_read_baseline",
+             "sketchssm_status_string", "sketchssm_last_error", "sketchssm_check_config")
+
+
+class SketchSSMError(RuntimeError):
+    def __init__(self, status: int, message: str):
+        super().__init__(f"{STATUS.get(status, status)}: {message}")
+        self.status = status
+
+
+class Config(ctypes.Structure):
+    _fields_ = [(name, ctypes.c_int32) for name in
+                ("kind", "batch", "heads", "dk", "dv", "rank", "window", "io_dtype")]
+
+
+class Step(ctypes.Structure):
+    _fields_ = [(name, ctypes.c_void_p) for name in ("q", "k", "v", "beta", "log_decay")]
+
+
+class Ring(ctypes.Structure):
+    _fields_ = [(name, ctypes.c_void_p) for name in ("k", "v", "u", "f", "pi", "g", "beta", "bcoef")]
+
+
+_lib = None
+
+
+def load(path: str = LIB_PATH):
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(path):
+        raise FileNotFoundError(f"{path} is not built; run `python -m paper_2609_33051_amd.build`")
+    lib = ctypes.CDLL(path)
+    P = ctypes.c_void_p
+    cfgp = ctypes.POINTER(Config)
+    lib.sketchssm_update.argtypes = [cfgp, P, P, ctypes.POINTER(Ring), ctypes.c_int32, ctypes.POINTER(Step), P, P, P]
+    lib.sketchssm_decode.argtypes = [cfgp, P, P, ctypes.POINTER(Ring), ctypes.c_int32, ctypes.POINTER(Step), P, P]
+    lib.sketchssm_full_read_baseline.argtypes = [cfgp, P, ctypes.POINTER(Ring), ctypes.c_int32,
+                                                 ctypes.POINTER(Step), P, P]
+    for f in ("sketchssm_update", "sketchssm_decode", "sketchssm_full_read_baseline", "sketchssm_check_config"):
+        getattr(lib, f).restype = ctypes.c_int
+    lib.sketchssm_check_config.argtypes = [cfgp]
+    lib.sketchssm_status_string.argtypes = [ctypes.c_int]
+    lib.sketchssm_status_string.restype = ctypes.c_char_p
+    lib.sketchssm_last_error.argtypes = []
+    lib.sketchssm_last_error.restype = ctypes.c_char_p
+    _lib = lib
+    return lib
+
+
+def ptr(x) -> int | None:
+    """Device address of a tensor (or an int / None passed through)."""
+    if x is None:
+        return None
+    if isinstance(x, int):
+        return x
+    return x.data_ptr()
+
+
+def make_config(kind, batch, heads, dk, dv, rank, window, io) -> Config:
+    k = KIND_IDS[kind] if isinstance(kind, str) else int(kind)
+    d = {"f32": F32, "bf16": BF16}.get(io, io) if isinstance(io, str) else int(io)
+    return Config(k, batch, heads, dk, dv, rank, window, d)
+
+
+def make_step(q, k, v, beta, log_decay) -> Step:
+    return Step(ptr(q), ptr(k), ptr(v), ptr(beta), ptr(log_decay))
+
+
+def make_ring(k=None, v=None, u=None, f=None, pi=None, g=None, beta=None, bcoef=None) -> Ring:
+    return Ring(ptr(k), ptr(v), ptr(u), ptr(f), ptr(pi), ptr(g), ptr(beta), ptr(bcoef))
+
+
+def _check(rc: int):
+    if rc != 0:
+        raise SketchSSMError(rc, load().sketchssm_last_error().decode())
+
+
+def sketchssm_update(cfg: Config, S, omega, ring: Ring | None, n_buffered: int, step: Step | None, U, o, stream=None):
+    lib = load()
+    _check(lib.sketchssm_update(ctypes.byref(cfg), ptr(S), ptr(omega), ctypes.byref(ring) if ring else None,
+                                int(n_buffered), ctypes.byref(step) if step else None, ptr(U), ptr(o), stream))
+
+
+def sketchssm_decode(cfg: Config, U, coef, ring: Ring, n_buffered: int, step: Step, o, stream=None):
+    lib = load()
+    _check(lib.sketchssm_decode(ctypes.byref(cfg), ptr(U), ptr(coef), ctypes.byref(ring), int(n_buffered),
+                                ctypes.byref(step), ptr(o), stream))
+
+
+def sketchssm_full_read_baseline(cfg: Config, S, ring: Ring, n_buffered: int, step: Step, o, stream=None):
+    lib = load()
+    _check(lib.sketchssm_full_read_baseline(ctypes.byref(cfg), ptr(S), ctypes.byref(ring), int(n_buffered),
+                                            ctypes.byref(step), ptr(o), stream))
+
+
+def sketchssm_check_config(cfg: Config) -> int:
+    return int(load().sketchssm_check_config(ctypes.byref(cfg)))
+
+
+def sketchssm_status_string(status: int) -> str:
+    return load().sketchssm_status_string(int(status)).decode()
+
+
+def sketchssm_last_error() -> str:
+    return load().sketchssm_last_error().decode()

@@ -1,0 +1,223 @@
+// Host side of the C ABI declared in include/sketchssm.h: argument
+// validation (before anything is enqueued), dispatch to the compiled kernel
+// of the shape, and error reporting.  No allocation, no synchronisation.
+#include <hip/hip_runtime.h>
+
+#include <stdarg.h>
+#include <stdint.h>
+#include <stdio.h>
+
+#include "../../include/sketchssm.h"
+#include "args.h"
+
+namespace {
+
+thread_local char g_err[512] = "";
+
+int fail(int code, const char* fmt, ...) {
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(g_err, sizeof(g_err), fmt, ap);
+  va_end(ap);
+  return code;
+}
+
+bool aligned(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+// Shape checks common to every entry point.
+int check_shape(const skssm_config* c, bool need_rank, bool allow_rank0) {
+  if (!c) return fail(SKSSM_EINVAL, "cfg is NULL");
+  if (c->kind < SKSSM_MAMBA2 || c->kind > SKSSM_KDA) return fail(SKSSM_EINVAL, "unknown kind %d", c->kind);
+  if (c->batch < 1 || c->heads < 1) return fail(SKSSM_EINVAL, "batch and heads must be >= 1");
+  if ((int64_t)c->batch * c->heads > (int64_t)1 << 30) return fail(SKSSM_EINVAL, "batch*heads too large");
+  if (c->io_dtype != SKSSM_F32 && c->io_dtype != SKSSM_BF16) return fail(SKSSM_EINVAL, "unknown io_dtype %d", c->io_dtype);
+  if (c->window < 1 || c->window > 32) return fail(SKSSM_EUNSUPPORTED, "window %d outside 1..32", c->window);
+  const bool kv_ok = (c->dk == 64 && c->dv == 64) || (c->dk == 128 && c->dv == 64) || (c->dk == 128 && c->dv == 128);
+  if (!kv_ok) return fail(SKSSM_EUNSUPPORTED, "(dk, dv) = (%d, %d) not compiled", c->dk, c->dv);
+  if (need_rank) {
+    const bool r_ok = c->rank == 8 || c->rank == 16 || c->rank == 32 || c->rank == c->dk || (allow_rank0 && c->rank == 0);
+    if (!r_ok) return fail(c->rank < 0 ? SKSSM_EINVAL : SKSSM_EUNSUPPORTED, "rank %d not supported", c->rank);
+  }
+  return SKSSM_OK;
+}
+
+int check_step(const skssm_config* c, const skssm_step* st) {
+  if (!st) return fail(SKSSM_EINVAL, "step is NULL");
+  if (!st->q || !st->k || !st->v || !st->beta || !st->log_decay) return fail(SKSSM_EINVAL, "step field is NULL");
+  if (!aligned(st->q) || !aligned(st->k) || !aligned(st->v) || !aligned(st->beta) || !aligned(st->log_decay))
+    return fail(SKSSM_EALIGN, "step pointer not 16-byte aligned");
+  (void)c;
+  return SKSSM_OK;
+}
+
+// Ring fields read or written by a call: `baseline` selects pi instead of f.
+int check_ring(const skssm_config* c, const skssm_ring* r, bool needs_f, bool needs_pi) {
+  if (!r) return fail(SKSSM_EINVAL, "ring is NULL");
+  const bool erase = c->kind != SKSSM_MAMBA2;
+  if (!r->k || !r->g || !r->beta) return fail(SKSSM_EINVAL, "ring k/g/beta is NULL");
+  if (!aligned(r->k) || !aligned(r->g) || !aligned(r->beta)) return fail(SKSSM_EALIGN, "ring pointer not aligned");
+  if (!erase) {
+    if (!r->v) return fail(SKSSM_EINVAL, "ring v is NULL (Mamba-2)");
+    if (!aligned(r->v)) return fail(SKSSM_EALIGN, "ring v not aligned");
+  } else {
+    if (!r->u || !r->bcoef) return fail(SKSSM_EINVAL, "ring u/bcoef is NULL (GDN/KDA)");
+    if (!aligned(r->u) || !aligned(r->bcoef)) return fail(SKSSM_EALIGN, "ring u/bcoef not aligned");
+    if (needs_f && !r->f) return fail(SKSSM_EINVAL, "ring f is NULL (GDN/KDA sketch read)");
+    if (needs_f && !aligned(r->f)) return fail(SKSSM_EALIGN, "ring f not aligned");
+    if (needs_pi && !r->pi) return fail(SKSSM_EINVAL, "ring pi is NULL (GDN/KDA baseline)");
+    if (needs_pi && !aligned(r->pi)) return fail(SKSSM_EALIGN, "ring pi not aligned");
+  }
+  return SKSSM_OK;
+}
+
+int launched(int rc, const char* what) {
+  if (rc == -2) return fail(SKSSM_EUNSUPPORTED, "%s: no kernel compiled for this shape", what);
+  const hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return fail(SKSSM_EHIP, "%s: %s", what, hipGetErrorString(e));
+  g_err[0] = '\0';
+  return SKSSM_OK;
+}
+
+skssm::DecodeArgs decode_args(const skssm_config* c, const skssm_ring* r, int32_t n, const skssm_step* st, float* o) {
+  skssm::DecodeArgs a{};
+  a.B = c->batch;
+  a.H = c->heads;
+  a.W = c->window;
+  a.n = n;
+  a.q = st->q;
+  a.k = st->k;
+  a.v = st->v;
+  a.beta = st->beta;
+  a.logd = st->log_decay;
+  a.rk = r->k;
+  a.rv = r->v;
+  a.ru = r->u;
+  a.rf = r->f;
+  a.rpi = r->pi;
+  a.rg = r->g;
+  a.rbeta = r->beta;
+  a.rb = r->bcoef;
+  a.o = o;
+  return a;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* sketchssm_status_string(int status) {
+  switch (status) {
+    case SKSSM_OK: return "ok";
+    case SKSSM_EINVAL: return "invalid argument";
+    case SKSSM_EUNSUPPORTED: return "unsupported shape";
+    case SKSSM_EALIGN: return "pointer not 16-byte aligned";
+    case SKSSM_ESTATE: return "n_buffered out of range";
+    case SKSSM_EHIP: return "HIP runtime error";
+    default: return "unknown status";
+  }
+}
+
+const char* sketchssm_last_error(void) { return g_err; }
+
+int sketchssm_check_config(const skssm_config* cfg) { return check_shape(cfg, true, false); }
+
+int sketchssm_update(const skssm_config* cfg, float* S, const float* omega, const skssm_ring* ring,
+                     int32_t n_buffered, const skssm_step* step, float* U, float* o, void* stream) {
+  int rc = check_shape(cfg, true, true);
+  if (rc) return rc;
+  if (!S) return fail(SKSSM_EINVAL, "S is NULL");
+  if (!aligned(S)) return fail(SKSSM_EALIGN, "S not aligned");
+  if (cfg->rank > 0) {
+    if (!U || !omega) return fail(SKSSM_EINVAL, "U and omega are required when rank > 0");
+    if (!aligned(U) || !aligned(omega)) return fail(SKSSM_EALIGN, "U/omega not aligned");
+  }
+  if (o && !aligned(o)) return fail(SKSSM_EALIGN, "o not aligned");
+  skssm::UpdateArgs a{};
+  a.B = cfg->batch;
+  a.H = cfg->heads;
+  a.W = cfg->window;
+  a.n = n_buffered;
+  a.S = S;
+  a.omega = omega;
+  a.U = cfg->rank > 0 ? U : nullptr;
+  if (step) {
+    if (n_buffered < 0 || n_buffered > cfg->window - 1)
+      return fail(SKSSM_ESTATE, "n_buffered %d outside 0..%d", n_buffered, cfg->window - 1);
+    if ((rc = check_step(cfg, step))) return rc;
+    if (n_buffered > 0 && (rc = check_ring(cfg, ring, false, false))) return rc;
+    a.nt = n_buffered + 1;
+    if (ring) {
+      a.rk = ring->k;
+      a.rv = ring->v;
+      a.ru = ring->u;
+      a.rg = ring->g;
+      a.rbeta = ring->beta;
+      a.rb = ring->bcoef;
+    }
+    a.q = step->q;
+    a.k = step->k;
+    a.v = step->v;
+    a.beta = step->beta;
+    a.logd = step->log_decay;
+    a.o = o;
+  } else {
+    if (n_buffered != 0) return fail(SKSSM_ESTATE, "sketch-only update needs n_buffered = 0");
+    if (cfg->rank == 0 || !U) return fail(SKSSM_EINVAL, "sketch-only update needs rank > 0 and U");
+    a.nt = 0;
+    a.o = nullptr;
+  }
+  int r;
+  switch (cfg->kind) {
+    case SKSSM_MAMBA2: r = skssm::run_update_mamba2(a, cfg->dk, cfg->dv, cfg->rank, cfg->io_dtype, stream); break;
+    case SKSSM_GDN: r = skssm::run_update_gdn(a, cfg->dk, cfg->dv, cfg->rank, cfg->io_dtype, stream); break;
+    default: r = skssm::run_update_kda(a, cfg->dk, cfg->dv, cfg->rank, cfg->io_dtype, stream); break;
+  }
+  return launched(r, "sketchssm_update");
+}
+
+int sketchssm_decode(const skssm_config* cfg, const float* U, const float* coef, const skssm_ring* ring,
+                     int32_t n_buffered, const skssm_step* step, float* o, void* stream) {
+  int rc = check_shape(cfg, true, false);
+  if (rc) return rc;
+  if (cfg->window < 2) return fail(SKSSM_EINVAL, "decode needs window >= 2 (window 1 flushes every token)");
+  if (n_buffered < 0 || n_buffered > cfg->window - 2)
+    return fail(SKSSM_ESTATE, "n_buffered %d outside 0..%d", n_buffered, cfg->window - 2);
+  if (!U || !coef || !o) return fail(SKSSM_EINVAL, "U, coef and o are required");
+  if (!aligned(U) || !aligned(coef) || !aligned(o)) return fail(SKSSM_EALIGN, "U/coef/o not aligned");
+  if ((rc = check_step(cfg, step))) return rc;
+  if ((rc = check_ring(cfg, ring, true, false))) return rc;
+  skssm::DecodeArgs a = decode_args(cfg, ring, n_buffered, step, o);
+  a.U = U;
+  a.coef = coef;
+  int r;
+  switch (cfg->kind) {
+    case SKSSM_MAMBA2: r = skssm::run_decode_mamba2(a, cfg->dk, cfg->dv, cfg->rank, cfg->io_dtype, stream); break;
+    case SKSSM_GDN: r = skssm::run_decode_gdn(a, cfg->dk, cfg->dv, cfg->rank, cfg->io_dtype, stream); break;
+    default: r = skssm::run_decode_kda(a, cfg->dk, cfg->dv, cfg->rank, cfg->io_dtype, stream); break;
+  }
+  return launched(r, "sketchssm_decode");
+}
+
+int sketchssm_full_read_baseline(const skssm_config* cfg, const float* S, const skssm_ring* ring,
+                                 int32_t n_buffered, const skssm_step* step, float* o, void* stream) {
+  int rc = check_shape(cfg, false, false);
+  if (rc) return rc;
+  if (cfg->window < 2) return fail(SKSSM_EINVAL, "baseline read needs window >= 2");
+  if (n_buffered < 0 || n_buffered > cfg->window - 2)
+    return fail(SKSSM_ESTATE, "n_buffered %d outside 0..%d", n_buffered, cfg->window - 2);
+  if (!S || !o) return fail(SKSSM_EINVAL, "S and o are required");
+  if (!aligned(S) || !aligned(o)) return fail(SKSSM_EALIGN, "S/o not aligned");
+  if ((rc = check_step(cfg, step))) return rc;
+  if ((rc = check_ring(cfg, ring, false, true))) return rc;
+  skssm::DecodeArgs a = decode_args(cfg, ring, n_buffered, step, o);
+  a.S = S;
+  int r;
+  switch (cfg->kind) {
+    case SKSSM_MAMBA2: r = skssm::run_full_read_mamba2(a, cfg->dk, cfg->dv, cfg->io_dtype, stream); break;
+    case SKSSM_GDN: r = skssm::run_full_read_gdn(a, cfg->dk, cfg->dv, cfg->io_dtype, stream); break;
+    default: r = skssm::run_full_read_kda(a, cfg->dk, cfg->dv, cfg->io_dtype, stream); break;
+  }
+  return launched(r, "sketchssm_full_read_baseline");
+}
+
+}  // extern "C"

@@ -1,0 +1,158 @@
+// Device helpers shared by the SketchSSM kernels (gfx950, wave64).
+//
+// Lane layouts used by the kernels:
+//   row layout    the wave is 4 rows of 16 lanes (DPP rows).  A K-vector is
+//                 spread over the 16 lanes of a row, K/16 consecutive channels
+//                 per lane; the 4 rows either hold copies or 4 different
+//                 ring slots, so one wide load fetches 4 slots at once and a
+//                 16-lane DPP reduction finishes 4 dot products together.
+//   value layout  lane l owns V/64 consecutive value channels.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace skssm {
+
+enum Kind { MAMBA2 = 0, GDN = 1, KDA = 2 };
+
+typedef uint16_t bf16_t;
+typedef float floatx4 __attribute__((ext_vector_type(4)));
+
+__device__ __forceinline__ float bf16_lo(uint32_t w) { return __uint_as_float(w << 16); }
+__device__ __forceinline__ float bf16_hi(uint32_t w) { return __uint_as_float(w & 0xFFFF0000u); }
+
+// N raw elements of the io dtype, moved with the widest aligned accesses.
+template <typename IO, int N> struct Raw;
+
+template <int N> struct Raw<float, N> {
+  float e[N];
+  __device__ __forceinline__ void zero() {
+#pragma unroll
+    for (int i = 0; i < N; ++i) e[i] = 0.f;
+  }
+  __device__ __forceinline__ void load(const float* p) {
+    if constexpr (N % 4 == 0) {
+#pragma unroll
+      for (int i = 0; i < N / 4; ++i) {
+        const float4 t = reinterpret_cast<const float4*>(p)[i];
+        e[4 * i] = t.x; e[4 * i + 1] = t.y; e[4 * i + 2] = t.z; e[4 * i + 3] = t.w;
+      }
+    } else if constexpr (N == 2) {
+      const float2 t = *reinterpret_cast<const float2*>(p);
+      e[0] = t.x; e[1] = t.y;
+    } else {
+      static_assert(N == 1, "unsupported width");
+      e[0] = *p;
+    }
+  }
+  __device__ __forceinline__ void store(float* p) const {
+    if constexpr (N % 4 == 0) {
+#pragma unroll
+      for (int i = 0; i < N / 4; ++i)
+        reinterpret_cast<float4*>(p)[i] = make_float4(e[4 * i], e[4 * i + 1], e[4 * i + 2], e[4 * i + 3]);
+    } else if constexpr (N == 2) {
+      *reinterpret_cast<float2*>(p) = make_float2(e[0], e[1]);
+    } else {
+      *p = e[0];
+    }
+  }
+  __device__ __forceinline__ float get(int i) const { return e[i]; }
+};
+
+template <int N> struct Raw<bf16_t, N> {
+  static constexpr int NW = (N + 1) / 2;
+  uint32_t w[NW];
+  __device__ __forceinline__ void zero() {
+#pragma unroll
+    for (int i = 0; i < NW; ++i) w[i] = 0u;
+  }
+  __device__ __forceinline__ void load(const bf16_t* p) {
+    if constexpr (N % 8 == 0) {
+#pragma unroll
+      for (int i = 0; i < N / 8; ++i) {
+        const uint4 t = reinterpret_cast<const uint4*>(p)[i];
+        w[4 * i] = t.x; w[4 * i + 1] = t.y; w[4 * i + 2] = t.z; w[4 * i + 3] = t.w;
+      }
+    } else if constexpr (N == 4) {
+      const uint2 t = *reinterpret_cast<const uint2*>(p);
+      w[0] = t.x; w[1] = t.y;
+    } else if constexpr (N == 2) {
+      w[0] = *reinterpret_cast<const uint32_t*>(p);
+    } else {
+      static_assert(N == 1, "unsupported width");
+      w[0] = (uint32_t)(*p);
+    }
+  }
+  __device__ __forceinline__ void store(bf16_t* p) const {
+    if constexpr (N % 8 == 0) {
+#pragma unroll
+      for (int i = 0; i < N / 8; ++i)
+        reinterpret_cast<uint4*>(p)[i] = make_uint4(w[4 * i], w[4 * i + 1], w[4 * i + 2], w[4 * i + 3]);
+    } else if constexpr (N == 4) {
+      *reinterpret_cast<uint2*>(p) = make_uint2(w[0], w[1]);
+    } else if constexpr (N == 2) {
+      *reinterpret_cast<uint32_t*>(p) = w[0];
+    } else {
+      *p = (bf16_t)(w[0] & 0xFFFFu);
+    }
+  }
+  __device__ __forceinline__ float get(int i) const {
+    return (i & 1) ? bf16_hi(w[i >> 1]) : bf16_lo(w[i >> 1]);
+  }
+};
+
+template <int N> struct Vec {
+  float e[N];
+  __device__ __forceinline__ void load(const float* p) {
+    Raw<float, N> r;
+    r.load(p);
+#pragma unroll
+    for (int i = 0; i < N; ++i) e[i] = r.e[i];
+  }
+  __device__ __forceinline__ void store(float* p) const {
+    Raw<float, N> r;
+#pragma unroll
+    for (int i = 0; i < N; ++i) r.e[i] = e[i];
+    r.store(p);
+  }
+};
+
+// ---- cross-lane reductions -------------------------------------------------
+
+template <int CTRL> __device__ __forceinline__ float dpp(float x) {
+  return __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(x), CTRL, 0xF, 0xF, true));
+}
+
+// Sum over the 16 lanes of a DPP row; every lane of the row receives it.
+__device__ __forceinline__ float row_sum16(float x) {
+  x += dpp<0xB1>(x);   // quad_perm [1,0,3,2]
+  x += dpp<0x4E>(x);   // quad_perm [2,3,0,1]
+  x += dpp<0x141>(x);  // row_half_mirror
+  x += dpp<0x140>(x);  // row_mirror
+  return x;
+}
+
+// Sum over the 4 rows (lanes l, l^16, l^32, l^48); every lane receives it.
+__device__ __forceinline__ float cross_row_sum(float x) {
+  x += __shfl_xor(x, 16);
+  x += __shfl_xor(x, 32);
+  return x;
+}
+
+__device__ __forceinline__ float wave_sum(float x) { return cross_row_sum(row_sum16(x)); }
+
+__device__ __forceinline__ float lane_bcast(float x, int lane) {
+  return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(x), lane));
+}
+
+// Order LDS traffic between lanes of one wave (writes before later reads).
+__device__ __forceinline__ void wave_lds_sync() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
+
+__device__ __forceinline__ float fast_exp(float x) { return __expf(x); }
+
+}  // namespace skssm

@@ -1,0 +1,107 @@
+// Maps a runtime shape to its compiled kernel instantiation and launches it.
+// Compiled shapes: (K, V) in {(64,64), (128,64), (128,128)}; R in {8, 16, 32, K}
+// (update also R = 0); windows up to 16 or 32 slots; fp32 or bf16 io.
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include "decode.h"
+#include "update.h"
+
+namespace skssm {
+
+constexpr int kUnsupported = -2;
+
+template <int KIND, int K, int V, int R, int WM, typename IO>
+int launch_decode(const DecodeArgs& a, hipStream_t s) {
+  const unsigned tiles = (unsigned)((a.B + 3) / 4);
+  hipLaunchKernelGGL((decode_kernel<KIND, K, V, R, WM, IO>), dim3((unsigned)a.H * tiles), dim3(256), 0, s, a);
+  return 0;
+}
+
+template <int KIND, int K, int V, int WM, typename IO>
+int launch_full_read(const DecodeArgs& a, hipStream_t s) {
+  const size_t items = (size_t)a.B * a.H;
+  hipLaunchKernelGGL((full_read_kernel<KIND, K, V, WM, IO>), dim3((unsigned)((items + 3) / 4)), dim3(256), 0, s, a);
+  return 0;
+}
+
+template <int KIND, int K, int V, int R, int WM, typename IO>
+int launch_update(const UpdateArgs& a, hipStream_t s) {
+  const size_t items = (size_t)a.B * a.H;
+  hipLaunchKernelGGL((update_kernel<KIND, K, V, R, WM, IO>), dim3((unsigned)items), dim3(256), 0, s, a);
+  return 0;
+}
+
+template <int KIND, int K, int V, int R>
+int decode_w(const DecodeArgs& a, int io, hipStream_t s) {
+  if (a.W <= 16)
+    return io ? launch_decode<KIND, K, V, R, 16, bf16_t>(a, s) : launch_decode<KIND, K, V, R, 16, float>(a, s);
+  return io ? launch_decode<KIND, K, V, R, 32, bf16_t>(a, s) : launch_decode<KIND, K, V, R, 32, float>(a, s);
+}
+
+template <int KIND, int K, int V>
+int decode_r(const DecodeArgs& a, int R, int io, hipStream_t s) {
+  switch (R) {
+    case 8: return decode_w<KIND, K, V, 8>(a, io, s);
+    case 16: return decode_w<KIND, K, V, 16>(a, io, s);
+    case 32: return decode_w<KIND, K, V, 32>(a, io, s);
+    case K: return decode_w<KIND, K, V, K>(a, io, s);
+    default: return kUnsupported;
+  }
+}
+
+template <int KIND>
+int run_decode(const DecodeArgs& a, int K, int V, int R, int io, void* stream) {
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  if (K == 64 && V == 64) return decode_r<KIND, 64, 64>(a, R, io, s);
+  if (K == 128 && V == 64) return decode_r<KIND, 128, 64>(a, R, io, s);
+  if (K == 128 && V == 128) return decode_r<KIND, 128, 128>(a, R, io, s);
+  return kUnsupported;
+}
+
+template <int KIND, int K, int V>
+int full_read_w(const DecodeArgs& a, int io, hipStream_t s) {
+  if (a.W <= 16)
+    return io ? launch_full_read<KIND, K, V, 16, bf16_t>(a, s) : launch_full_read<KIND, K, V, 16, float>(a, s);
+  return io ? launch_full_read<KIND, K, V, 32, bf16_t>(a, s) : launch_full_read<KIND, K, V, 32, float>(a, s);
+}
+
+template <int KIND>
+int run_full_read(const DecodeArgs& a, int K, int V, int io, void* stream) {
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  if (K == 64 && V == 64) return full_read_w<KIND, 64, 64>(a, io, s);
+  if (K == 128 && V == 64) return full_read_w<KIND, 128, 64>(a, io, s);
+  if (K == 128 && V == 128) return full_read_w<KIND, 128, 128>(a, io, s);
+  return kUnsupported;
+}
+
+template <int KIND, int K, int V, int R>
+int update_w(const UpdateArgs& a, int io, hipStream_t s) {
+  if (a.W <= 16)
+    return io ? launch_update<KIND, K, V, R, 16, bf16_t>(a, s) : launch_update<KIND, K, V, R, 16, float>(a, s);
+  return io ? launch_update<KIND, K, V, R, 32, bf16_t>(a, s) : launch_update<KIND, K, V, R, 32, float>(a, s);
+}
+
+template <int KIND, int K, int V>
+int update_r(const UpdateArgs& a, int R, int io, hipStream_t s) {
+  switch (R) {
+    case 0: return update_w<KIND, K, V, 0>(a, io, s);
+    case 8: return update_w<KIND, K, V, 8>(a, io, s);
+    case 16: return update_w<KIND, K, V, 16>(a, io, s);
+    case 32: return update_w<KIND, K, V, 32>(a, io, s);
+    case K: return update_w<KIND, K, V, K>(a, io, s);
+    default: return kUnsupported;
+  }
+}
+
+template <int KIND>
+int run_update(const UpdateArgs& a, int K, int V, int R, int io, void* stream) {
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  if (K == 64 && V == 64) return update_r<KIND, 64, 64>(a, R, io, s);
+  if (K == 128 && V == 64) return update_r<KIND, 128, 64>(a, R, io, s);
+  if (K == 128 && V == 128) return update_r<KIND, 128, 128>(a, R, io, s);
+  return kUnsupported;
+}
+
+}  // namespace skssm

@@ -1,0 +1,134 @@
+"""The C-ABI library loads, exports every function its header declares, and
+rejects invalid calls on the host before anything is enqueued.
+
+No compute call is made here.  Every invalid call below carries a defect the
+host validation reports; the fake device addresses used are never launched
+on.  (The cases are skipped where a GPU is visible, so that a validation bug
+could never turn into a launch on bogus addresses.)
+"""
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2609_33051_amd import binding as B
+from paper_2609_33051_amd import build as builder
+
+HEADER = os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))), "include", "sketchssm.h")
+
+
+@pytest.fixture(scope="module")
+def lib():
+    if not os.path.exists(B.LIB_PATH):
+        builder.build()
+    return B.load()
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(sketchssm_\w+)\s*\(", text)))
+
+
+def test_header_declares_the_entry_points():
+    names = declared_functions()
+    for f in ("sketchssm_update", "sketchssm_decode", "sketchssm_full_read_baseline"):
+        assert f in names
+    assert set(names) == set(B.FUNCTIONS)
+
+
+def test_library_exports_every_declared_symbol(lib):
+    for name in declared_functions():
+        assert hasattr(lib, name), name
+    out = os.popen(f"nm -D --defined-only {B.LIB_PATH}").read()
+    for name in declared_functions():
+        assert re.search(rf"\bT {name}\b", out), name
+
+
+def test_status_strings(lib):
+    assert B.sketchssm_status_string(0) == "ok"
+    assert "aligned" in B.sketchssm_status_string(-3)
+    assert B.sketchssm_status_string(12345) == "unknown status"
+
+
+def _gpu_visible():
+    try:
+        import torch
+        return torch.cuda.is_available()
+    except Exception:
+        return False
+
+
+ADDR = 1 << 20  # a 16-byte aligned fake address, never dereferenced (every case fails validation)
+
+
+def cfg(**kw):
+    d = dict(kind="mamba2", batch=2, heads=4, dk=128, dv=64, rank=16, window=16, io="bf16")
+    d.update(kw)
+    return B.make_config(d["kind"], d["batch"], d["heads"], d["dk"], d["dv"], d["rank"], d["window"], d["io"])
+
+
+def good_step(**kw):
+    d = dict(q=ADDR, k=ADDR, v=ADDR, beta=ADDR, log_decay=ADDR)
+    d.update(kw)
+    return B.make_step(**d)
+
+
+def good_ring(**kw):
+    d = dict(k=ADDR, v=ADDR, u=ADDR, f=ADDR, pi=ADDR, g=ADDR, beta=ADDR, bcoef=ADDR)
+    d.update(kw)
+    return B.make_ring(**d)
+
+
+def status(fn, *args):
+    try:
+        fn(*args)
+    except B.SketchSSMError as e:
+        return e.status
+    return 0
+
+
+@pytest.mark.skipif(_gpu_visible(), reason="host-validation cases use fake addresses; run on CPU only")
+class TestValidation:
+    def test_decode_rejections(self, lib):
+        d = B.sketchssm_decode
+        assert check_config_ok(lib)
+        assert status(d, cfg(kind=7), ADDR, ADDR, good_ring(), 0, good_step(), ADDR) == -1
+        assert status(d, cfg(dk=96), ADDR, ADDR, good_ring(), 0, good_step(), ADDR) == -2
+        assert status(d, cfg(rank=12), ADDR, ADDR, good_ring(), 0, good_step(), ADDR) == -2
+        assert status(d, cfg(window=33), ADDR, ADDR, good_ring(), 0, good_step(), ADDR) == -2
+        assert status(d, cfg(window=1), ADDR, ADDR, good_ring(), 0, good_step(), ADDR) == -1
+        assert status(d, cfg(), ADDR, ADDR, good_ring(), 15, good_step(), ADDR) == -4
+        assert status(d, cfg(), ADDR, ADDR, good_ring(), -1, good_step(), ADDR) == -4
+        assert status(d, cfg(), ADDR + 4, ADDR, good_ring(), 0, good_step(), ADDR) == -3
+        assert status(d, cfg(), ADDR, ADDR, good_ring(), 0, good_step(q=ADDR + 8), ADDR) == -3
+        assert status(d, cfg(), ADDR, ADDR, good_ring(v=None), 0, good_step(), ADDR) == -1
+        assert status(d, cfg(kind="gdn", dv=128), ADDR, ADDR, good_ring(f=None), 0, good_step(), ADDR) == -1
+        assert status(d, cfg(), None, ADDR, good_ring(), 0, good_step(), ADDR) == -1
+        assert status(d, cfg(batch=0), ADDR, ADDR, good_ring(), 0, good_step(), ADDR) == -1
+        assert status(d, cfg(io=5), ADDR, ADDR, good_ring(), 0, good_step(), ADDR) == -1
+        assert "n_buffered" in B.sketchssm_status_string(-4)
+
+    def test_update_rejections(self, lib):
+        u = B.sketchssm_update
+        assert status(u, cfg(), ADDR, ADDR, good_ring(), 16, good_step(), ADDR, ADDR) == -4
+        assert status(u, cfg(), ADDR, ADDR, None, 3, None, ADDR, None) == -4          # sketch-only needs n = 0
+        assert status(u, cfg(rank=0), ADDR, None, None, 0, None, None, None) == -1   # sketch-only needs rank
+        assert status(u, cfg(), None, ADDR, good_ring(), 15, good_step(), ADDR, ADDR) == -1
+        assert status(u, cfg(), ADDR, None, good_ring(), 15, good_step(), ADDR, ADDR) == -1
+        assert status(u, cfg(kind="kda", dv=128), ADDR, ADDR, good_ring(u=None), 15, good_step(), ADDR, ADDR) == -1
+        assert status(u, cfg(), ADDR, ADDR, None, 15, good_step(), ADDR, ADDR) == -1  # ring needed when n > 0
+        assert status(u, cfg(), ADDR, ADDR, good_ring(), 15, good_step(), ADDR, ADDR + 2) == -3
+
+    def test_full_read_rejections(self, lib):
+        f = B.sketchssm_full_read_baseline
+        assert status(f, cfg(kind="gdn", dv=128), ADDR, good_ring(pi=None), 0, good_step(), ADDR) == -1
+        assert status(f, cfg(), ADDR, good_ring(), 15, good_step(), ADDR) == -4
+        assert "n_buffered" in B.sketchssm_last_error()
+        assert status(f, cfg(), None, good_ring(), 0, good_step(), ADDR) == -1
+        assert status(f, cfg(dv=32), ADDR, good_ring(), 0, good_step(), ADDR) == -2
+
+
+def check_config_ok(lib):
+    return B.sketchssm_check_config(cfg()) == 0 and B.sketchssm_check_config(cfg(rank=5)) == -2

@@ -1,0 +1,272 @@
+#!/usr/bin/env python3
+"""Decode-path benchmark: decode steps/s per layer and state-access GB/s
+(fraction of the MI355X HBM roofline) at batch B, on one GPU.
+
+    python bench.py [--steps K] [--warmup W] [--workload NAME] [--layers L]
+
+A step is one decode token of one linear-attention layer for the whole batch
+(B requests x H heads): a non-flush sketch read (sketchssm_decode) while the
+window is open, the flush (sketchssm_update) on its W-th token.  K is rounded
+up to whole windows, so the timed region holds both in the method's ratio.
+L independent layers (own state, sketch and ring) are stepped in turn, as a
+hybrid model interleaves its recurrent layers; this keeps the working set far
+above the 256 MB last-level cache so the reads come from HBM.  Inputs are
+seeded synthetic tensors, generated before timing and resident in HBM.
+
+Reported (one JSON line):
+  value          decode steps/s per layer over the timed region
+  roofline       the non-flush read kernel (the dominant one): algorithmic
+                 bytes per launch / mean launch time from HIP events recorded
+                 on the launch stream, against the 8 TB/s HBM peak
+  kernels        the same for the flush and the window-averaged figures
+  full_read      the exact full-state-read (ReplaySSM-style) baseline path
+  cpu_baseline   the CPU oracle timed on a bounded sample of the same
+                 workload on the host cores, scaled to steps/s per layer
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+METRIC = "decode steps/s per layer + state-access GB/s (% HBM roofline) at batch B"
+
+
+def parse():
+    p = argparse.ArgumentParser()
+    p.add_argument("--gpus", type=int, default=1)
+    p.add_argument("--steps", type=int, default=256)
+    p.add_argument("--warmup", type=int, default=32)
+    p.add_argument("--workload", default="mamba2_b256")
+    p.add_argument("--rank", type=int, default=None)
+    p.add_argument("--window", type=int, default=None)
+    p.add_argument("--layers", type=int, default=4)
+    p.add_argument("--no-full-read", action="store_true", help="skip the exact baseline path")
+    p.add_argument("--no-cpu-baseline", action="store_true")
+    p.add_argument("--cpu-seconds", type=float, default=12.0, help="target CPU time of the oracle sample")
+    p.add_argument("--copy-calibration", action="store_true",
+                   help="also run a plain 1 GiB device copy (scales HBM byte counters)")
+    return p.parse_args()
+
+
+def main():
+    args = parse()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
+        print("bench.py runs on one GPU only: the decode path has no cross-GPU work "
+              "(items shard with zero exchange); run it per GPU with --gpus 1.", file=sys.stderr)
+        return 2
+
+    import torch
+
+    from paper_2609_33051_amd import inputs, traffic
+    from paper_2609_33051_amd import binding as B
+    from paper_2609_33051_amd.layer import SketchSSMLayer
+
+    if not torch.cuda.is_available():
+        print("bench.py needs an MI355X GPU", file=sys.stderr)
+        return 2
+    B.load()  # fails loudly if the HIP library is not built
+    dev = torch.device("cuda:0")
+    wl = inputs.WORKLOADS[args.workload]
+    rank = wl.rank if args.rank is None else args.rank
+    W = wl.window if args.window is None else args.window
+    wl = wl.with_(rank=rank, window=W)
+    K_steps = -(-args.steps // W) * W
+    warm = -(-args.warmup // W) * W
+    L = args.layers
+    io_bytes = 2 if wl.io == "bf16" else 4
+    shape = traffic.Shape(wl.kind, wl.dk, wl.dv, rank, W, io_bytes)
+    items = wl.items
+
+    om, C = inputs.omega(wl, rank)
+    om_t, C_t = torch.as_tensor(om), torch.as_tensor(C)
+    pool = [inputs.step_inputs(wl, t, dev) for t in range(W)]  # one window of resident inputs, reused
+
+    def make_layers(baseline):
+        layers = []
+        for li in range(L):
+            S = inputs.initial_state(wl, dev, seed=inputs.SEED + li)
+            lay = SketchSSMLayer(wl.kind, wl.batch, wl.heads, wl.dk, wl.dv, rank, W, wl.io, dev,
+                                 baseline=baseline, S=S, omega=om_t, coef=C_t)
+            lay.init_sketch()
+            layers.append(lay)
+        torch.cuda.synchronize()
+        return layers
+
+    def run(layers, n_tokens, record):
+        """n_tokens decode tokens through every layer; with `record`, HIP events
+        bracket every launch on the launch stream."""
+        ev = []
+        for t in range(n_tokens):
+            inp = pool[t % W]
+            for lay in layers:
+                n = lay.n
+                if record:
+                    e0 = torch.cuda.Event(enable_timing=True)
+                    e1 = torch.cuda.Event(enable_timing=True)
+                    e0.record()
+                lay.step(inp)
+                if record:
+                    e1.record()
+                    ev.append((n, e0, e1))
+        return ev
+
+    def timed(baseline):
+        layers = make_layers(baseline)
+        run(layers, warm, False)
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        ev = run(layers, K_steps, True)
+        torch.cuda.synchronize()
+        elapsed = time.perf_counter() - t0
+        per_n = {}
+        for n, e0, e1 in ev:
+            per_n.setdefault(n, []).append(e0.elapsed_time(e1) * 1e-3)
+        del layers
+        torch.cuda.empty_cache()
+        return elapsed, per_n
+
+    # ---- the SketchSSM path
+    elapsed, per_n = timed(False)
+    layer_steps = K_steps * L
+    value = layer_steps / elapsed
+    dec_n = [n for n in per_n if n < W - 1]
+    dec_time = sum(sum(per_n[n]) for n in dec_n)
+    dec_launches = sum(len(per_n[n]) for n in dec_n)
+    dec_bytes = sum(traffic.decode_bytes(shape, n) * items * len(per_n[n]) for n in dec_n)
+    dec_mean_s = dec_time / dec_launches
+    dec_bytes_per_launch = dec_bytes / dec_launches
+    dec_gbps = dec_bytes / dec_time / 1e9
+    fl = per_n.get(W - 1, [])
+    fl_mean_s = sum(fl) / len(fl)
+    fl_bytes = traffic.flush_bytes(shape, W - 1) * items
+    mfma_flops = items * (2 * wl.dv * wl.dk * W * (2 if shape.erase else 1) + 2 * wl.dv * wl.dk * rank)
+    window_s = sum(sum(v) / len(v) for v in per_n.values())
+
+    out = {
+        "metric": METRIC,
+        "value": round(value, 2),
+        "unit": "steps/s",
+        "n_gpus": 1,
+        "steps": K_steps,
+        "warmup": warm,
+        "ms_per_step": round(elapsed / layer_steps * 1e3, 5),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic",
+        "config": {"workload": wl.name, "kind": wl.kind, "batch": wl.batch, "heads": wl.heads, "dk": wl.dk,
+                   "dv": wl.dv, "rank": rank, "window": W, "io": wl.io, "state": "f32", "sketch": "f32",
+                   "layers_rotated": L},
+        "roofline": {
+            "kernel": "decode_kernel (sketchssm_decode)",
+            "bound": "hbm",
+            "achieved": round(dec_gbps, 1),
+            "peak": traffic.HBM_PEAK_GBPS,
+            "unit": "GB/s",
+            "frac": round(dec_gbps / traffic.HBM_PEAK_GBPS, 4),
+            "traffic": None,
+            "bytes_per_launch": int(dec_bytes_per_launch),
+            "mean_launch_us": round(dec_mean_s * 1e6, 2),
+        },
+        "state_access_gbps": round(dec_gbps, 1),
+        "kernels": {
+            "decode": {"mean_us": round(dec_mean_s * 1e6, 2), "gbps": round(dec_gbps, 1),
+                       "per_slot_us": {int(n): round(sum(v) / len(v) * 1e6, 2) for n, v in sorted(per_n.items())
+                                       if n < W - 1}},
+            "flush": {"mean_us": round(fl_mean_s * 1e6, 2), "bytes": fl_bytes,
+                      "gbps": round(fl_bytes / fl_mean_s / 1e9, 1),
+                      "mfma_tflops": round(mfma_flops / fl_mean_s / 1e12, 2), "mfma_peak_tflops": 157.3},
+            "window_us": round(window_s * 1e6, 1),
+            "window_avg_steps_per_s": round(W / window_s, 1),
+        },
+    }
+
+    # ---- the exact full-state-read baseline (same inputs; flush with rank 0)
+    if not args.no_full_read:
+        e_b, per_b = timed(True)
+        fr_n = [n for n in per_b if n < W - 1]
+        fr_time = sum(sum(per_b[n]) for n in fr_n)
+        fr_bytes = sum(traffic.full_read_bytes(shape, n) * items * len(per_b[n]) for n in fr_n)
+        fr_launch = fr_time / sum(len(per_b[n]) for n in fr_n)
+        fb = per_b.get(W - 1, [])
+        win_b = sum(sum(v) / len(v) for v in per_b.values())
+        out["full_read"] = {
+            "value": round(layer_steps / e_b, 2), "unit": "steps/s",
+            "read_mean_us": round(fr_launch * 1e6, 2), "read_gbps": round(fr_bytes / fr_time / 1e9, 1),
+            "read_frac": round(fr_bytes / fr_time / 1e9 / traffic.HBM_PEAK_GBPS, 4),
+            "flush_mean_us": round(sum(fb) / len(fb) * 1e6, 2),
+            "window_avg_steps_per_s": round(W / win_b, 1),
+            "speedup_sketch_vs_full_read": round(value / (layer_steps / e_b), 3),
+            "read_bytes_ratio": round(traffic.full_read_bytes(shape, 0) / traffic.decode_bytes(shape, 0), 3),
+        }
+    out["traffic_model"] = {
+        "paper_R_G_bf16": round(traffic.paper_reduction(wl.dk, wl.dv, rank, W, 1 if shape.erase else 0), 3),
+        "state_vs_sketch_read": round(wl.dk / rank, 3),
+        "decode_bytes_per_item_mean": traffic.window_bytes(shape)["nonflush_mean"],
+        "full_read_bytes_per_item_mean": traffic.window_bytes(shape, baseline=True)["nonflush_mean"],
+    }
+
+    if args.copy_calibration:
+        n = 1 << 28  # 1 GiB of fp32
+        a = torch.empty(n, dtype=torch.float32, device=dev).fill_(1.0)
+        b = torch.empty_like(a)
+        for _ in range(3):
+            b.copy_(a)
+        torch.cuda.synchronize()
+        out["copy_calibration_bytes"] = 2 * n * 4
+
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline(wl, rank, W, args.cpu_seconds, dev)
+
+    print(json.dumps(out), flush=True)
+    return 0
+
+
+def cpu_baseline(wl, rank, W, target_s, dev):
+    """The oracle (plain fp64, one item at a time) on the host cores, on a
+    sample of items over one window, scaled to steps/s per layer."""
+    import numpy as np
+    import torch
+
+    import oracle
+    from paper_2609_33051_amd import inputs
+
+    items = wl.items
+    threads = oracle.max_threads()
+    om, C = inputs.omega(wl, rank)
+    pool = [inputs.step_inputs(wl, t, dev) for t in range(W)]
+    S = inputs.initial_state(wl, dev)
+
+    def sample(n_sel):
+        sel = torch.arange(n_sel, device=dev) * (items // n_sel)
+        cut = lambda x: x.reshape(items, -1)[sel].to("cpu", torch.float32).numpy()
+        q = np.stack([cut(p["q"]) for p in pool])
+        k = np.stack([cut(p["k"]) for p in pool])
+        v = np.stack([cut(p["v"]) for p in pool])
+        beta = np.stack([cut(p["beta"])[:, 0] for p in pool])
+        ld = np.stack([cut(p["log_decay"]) for p in pool])
+        if wl.kind != "kda":
+            ld = ld[:, :, 0]
+        S0 = S.reshape(items, wl.dv, wl.dk)[sel].cpu().numpy()
+        heads = (sel.cpu().numpy() % wl.heads).astype(np.int32)
+        t0 = time.perf_counter()
+        oracle.sketchssm(wl.kind, W, heads, om, C, S0, q, k, v, beta, ld, round_storage=True, diagnostics=False)
+        return time.perf_counter() - t0
+
+    n_sel = max(threads, 16)
+    dt = sample(n_sel)
+    n_sel = int(min(items, max(n_sel, n_sel * target_s / max(dt, 1e-3))))
+    dt = sample(n_sel)
+    per_item_step = dt / (n_sel * W)
+    return {"value": round(1.0 / (per_item_step * items), 4), "unit": "steps/s", "cores": threads,
+            "kind": "oracle",
+            "sample": f"{n_sel} of {items} (request, head) items x one window of {W} steps, "
+                      f"{dt:.1f} s wall, scaled linearly to all items (items are independent)"}
+
+
+if __name__ == "__main__":
+    sys.exit(main())

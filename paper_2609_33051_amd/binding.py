@@ -37,12 +37,9 @@ class Config(ctypes.Structure):
                 ("kind", "batch", "heads", "dk", "dv", "rank", "window", "io_dtype")]
 
 
-class Step(ctypes.Structure):
-    _fields_ = [(name, ctypes.c_void_p) for name in ("q", "k", "v", "beta", "log_decay")]
-
-
 class Ring(ctypes.Structure):
-    _fields_ = [(name, ctypes.c_void_p) for name in ("k", "v", "u", "f", "pi", "g", "beta", "bcoef")]
+    _fields_ = [(name, ctypes.c_void_p) for name in
+                ("k", "v", "beta", "log_decay", "g", "u", "f", "pi", "bcoef")]
 
 
 _lib = None
@@ -57,10 +54,10 @@ def load(path: str = LIB_PATH):
     lib = ctypes.CDLL(path)
     P = ctypes.c_void_p
     cfgp = ctypes.POINTER(Config)
-    lib.sketchssm_update.argtypes = [cfgp, P, P, ctypes.POINTER(Ring), ctypes.c_int32, ctypes.POINTER(Step), P, P, P]
-    lib.sketchssm_decode.argtypes = [cfgp, P, P, ctypes.POINTER(Ring), ctypes.c_int32, ctypes.POINTER(Step), P, P]
-    lib.sketchssm_full_read_baseline.argtypes = [cfgp, P, ctypes.POINTER(Ring), ctypes.c_int32,
-                                                 ctypes.POINTER(Step), P, P]
+    ringp = ctypes.POINTER(Ring)
+    lib.sketchssm_update.argtypes = [cfgp, P, P, ringp, ctypes.c_int32, P, P, P, P]
+    lib.sketchssm_decode.argtypes = [cfgp, P, P, ringp, ctypes.c_int32, P, P, P]
+    lib.sketchssm_full_read_baseline.argtypes = [cfgp, P, ringp, ctypes.c_int32, P, P, P]
     for f in ("sketchssm_update", "sketchssm_decode", "sketchssm_full_read_baseline", "sketchssm_check_config"):
         getattr(lib, f).restype = ctypes.c_int
     lib.sketchssm_check_config.argtypes = [cfgp]
@@ -87,12 +84,8 @@ def make_config(kind, batch, heads, dk, dv, rank, window, io) -> Config:
     return Config(k, batch, heads, dk, dv, rank, window, d)
 
 
-def make_step(q, k, v, beta, log_decay) -> Step:
-    return Step(ptr(q), ptr(k), ptr(v), ptr(beta), ptr(log_decay))
-
-
-def make_ring(k=None, v=None, u=None, f=None, pi=None, g=None, beta=None, bcoef=None) -> Ring:
-    return Ring(ptr(k), ptr(v), ptr(u), ptr(f), ptr(pi), ptr(g), ptr(beta), ptr(bcoef))
+def make_ring(k=None, v=None, beta=None, log_decay=None, g=None, u=None, f=None, pi=None, bcoef=None) -> Ring:
+    return Ring(ptr(k), ptr(v), ptr(beta), ptr(log_decay), ptr(g), ptr(u), ptr(f), ptr(pi), ptr(bcoef))
 
 
 def _check(rc: int):
@@ -100,22 +93,22 @@ def _check(rc: int):
         raise SketchSSMError(rc, load().sketchssm_last_error().decode())
 
 
-def sketchssm_update(cfg: Config, S, omega, ring: Ring | None, n_buffered: int, step: Step | None, U, o, stream=None):
+def sketchssm_update(cfg: Config, S, omega, ring: Ring | None, n_buffered: int, q, U, o, stream=None):
     lib = load()
     _check(lib.sketchssm_update(ctypes.byref(cfg), ptr(S), ptr(omega), ctypes.byref(ring) if ring else None,
-                                int(n_buffered), ctypes.byref(step) if step else None, ptr(U), ptr(o), stream))
+                                int(n_buffered), ptr(q), ptr(U), ptr(o), stream))
 
 
-def sketchssm_decode(cfg: Config, U, coef, ring: Ring, n_buffered: int, step: Step, o, stream=None):
+def sketchssm_decode(cfg: Config, U, coef, ring: Ring, n_buffered: int, q, o, stream=None):
     lib = load()
-    _check(lib.sketchssm_decode(ctypes.byref(cfg), ptr(U), ptr(coef), ctypes.byref(ring), int(n_buffered),
-                                ctypes.byref(step), ptr(o), stream))
+    _check(lib.sketchssm_decode(ctypes.byref(cfg), ptr(U), ptr(coef), ctypes.byref(ring) if ring else None,
+                                int(n_buffered), ptr(q), ptr(o), stream))
 
 
-def sketchssm_full_read_baseline(cfg: Config, S, ring: Ring, n_buffered: int, step: Step, o, stream=None):
+def sketchssm_full_read_baseline(cfg: Config, S, ring: Ring, n_buffered: int, q, o, stream=None):
     lib = load()
-    _check(lib.sketchssm_full_read_baseline(ctypes.byref(cfg), ptr(S), ctypes.byref(ring), int(n_buffered),
-                                            ctypes.byref(step), ptr(o), stream))
+    _check(lib.sketchssm_full_read_baseline(ctypes.byref(cfg), ptr(S), ctypes.byref(ring) if ring else None,
+                                            int(n_buffered), ptr(q), ptr(o), stream))
 
 
 def sketchssm_check_config(cfg: Config) -> int:

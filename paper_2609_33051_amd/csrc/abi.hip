@@ -41,31 +41,25 @@ int check_shape(const skssm_config* c, bool need_rank, bool allow_rank0) {
   return SKSSM_OK;
 }
 
-int check_step(const skssm_config* c, const skssm_step* st) {
-  if (!st) return fail(SKSSM_EINVAL, "step is NULL");
-  if (!st->q || !st->k || !st->v || !st->beta || !st->log_decay) return fail(SKSSM_EINVAL, "step field is NULL");
-  if (!aligned(st->q) || !aligned(st->k) || !aligned(st->v) || !aligned(st->beta) || !aligned(st->log_decay))
-    return fail(SKSSM_EALIGN, "step pointer not 16-byte aligned");
-  (void)c;
-  return SKSSM_OK;
-}
-
-// Ring fields read or written by a call: `baseline` selects pi instead of f.
-int check_ring(const skssm_config* c, const skssm_ring* r, bool needs_f, bool needs_pi) {
+// Ring fields read or written by a call: the raw inputs always, the derived
+// fields of the family, and f (`derived_f`, sketch read) or pi
+// (`derived_pi`, exact baseline).
+int check_ring(const skssm_config* c, const skssm_ring* r, bool derived_f, bool derived_pi) {
   if (!r) return fail(SKSSM_EINVAL, "ring is NULL");
-  const bool erase = c->kind != SKSSM_MAMBA2;
-  if (!r->k || !r->g || !r->beta) return fail(SKSSM_EINVAL, "ring k/g/beta is NULL");
-  if (!aligned(r->k) || !aligned(r->g) || !aligned(r->beta)) return fail(SKSSM_EALIGN, "ring pointer not aligned");
-  if (!erase) {
-    if (!r->v) return fail(SKSSM_EINVAL, "ring v is NULL (Mamba-2)");
-    if (!aligned(r->v)) return fail(SKSSM_EALIGN, "ring v not aligned");
-  } else {
+  if (!r->k || !r->v || !r->beta || !r->log_decay) return fail(SKSSM_EINVAL, "ring k/v/beta/log_decay is NULL");
+  if (!aligned(r->k) || !aligned(r->v) || !aligned(r->beta) || !aligned(r->log_decay))
+    return fail(SKSSM_EALIGN, "ring input field not 16-byte aligned");
+  if (c->kind == SKSSM_KDA) {
+    if (!r->g) return fail(SKSSM_EINVAL, "ring g is NULL (KDA)");
+    if (!aligned(r->g)) return fail(SKSSM_EALIGN, "ring g not aligned");
+  }
+  if (c->kind != SKSSM_MAMBA2) {
     if (!r->u || !r->bcoef) return fail(SKSSM_EINVAL, "ring u/bcoef is NULL (GDN/KDA)");
     if (!aligned(r->u) || !aligned(r->bcoef)) return fail(SKSSM_EALIGN, "ring u/bcoef not aligned");
-    if (needs_f && !r->f) return fail(SKSSM_EINVAL, "ring f is NULL (GDN/KDA sketch read)");
-    if (needs_f && !aligned(r->f)) return fail(SKSSM_EALIGN, "ring f not aligned");
-    if (needs_pi && !r->pi) return fail(SKSSM_EINVAL, "ring pi is NULL (GDN/KDA baseline)");
-    if (needs_pi && !aligned(r->pi)) return fail(SKSSM_EALIGN, "ring pi not aligned");
+    if (derived_f && !r->f) return fail(SKSSM_EINVAL, "ring f is NULL (GDN/KDA sketch read)");
+    if (derived_f && !aligned(r->f)) return fail(SKSSM_EALIGN, "ring f not aligned");
+    if (derived_pi && !r->pi) return fail(SKSSM_EINVAL, "ring pi is NULL (GDN/KDA baseline)");
+    if (derived_pi && !aligned(r->pi)) return fail(SKSSM_EALIGN, "ring pi not aligned");
   }
   return SKSSM_OK;
 }
@@ -78,24 +72,21 @@ int launched(int rc, const char* what) {
   return SKSSM_OK;
 }
 
-skssm::DecodeArgs decode_args(const skssm_config* c, const skssm_ring* r, int32_t n, const skssm_step* st, float* o) {
+skssm::DecodeArgs decode_args(const skssm_config* c, const skssm_ring* r, int32_t n, const void* q, float* o) {
   skssm::DecodeArgs a{};
   a.B = c->batch;
   a.H = c->heads;
   a.W = c->window;
   a.n = n;
-  a.q = st->q;
-  a.k = st->k;
-  a.v = st->v;
-  a.beta = st->beta;
-  a.logd = st->log_decay;
+  a.q = q;
   a.rk = r->k;
   a.rv = r->v;
+  a.rbeta = r->beta;
+  a.rla = r->log_decay;
+  a.rg = r->g;
   a.ru = r->u;
   a.rf = r->f;
   a.rpi = r->pi;
-  a.rg = r->g;
-  a.rbeta = r->beta;
   a.rb = r->bcoef;
   a.o = o;
   return a;
@@ -122,7 +113,7 @@ const char* sketchssm_last_error(void) { return g_err; }
 int sketchssm_check_config(const skssm_config* cfg) { return check_shape(cfg, true, false); }
 
 int sketchssm_update(const skssm_config* cfg, float* S, const float* omega, const skssm_ring* ring,
-                     int32_t n_buffered, const skssm_step* step, float* U, float* o, void* stream) {
+                     int32_t n_buffered, const void* q, float* U, float* o, void* stream) {
   int rc = check_shape(cfg, true, true);
   if (rc) return rc;
   if (!S) return fail(SKSSM_EINVAL, "S is NULL");
@@ -140,25 +131,20 @@ int sketchssm_update(const skssm_config* cfg, float* S, const float* omega, cons
   a.S = S;
   a.omega = omega;
   a.U = cfg->rank > 0 ? U : nullptr;
-  if (step) {
+  if (q) {
     if (n_buffered < 0 || n_buffered > cfg->window - 1)
       return fail(SKSSM_ESTATE, "n_buffered %d outside 0..%d", n_buffered, cfg->window - 1);
-    if ((rc = check_step(cfg, step))) return rc;
-    if (n_buffered > 0 && (rc = check_ring(cfg, ring, false, false))) return rc;
+    if (!aligned(q)) return fail(SKSSM_EALIGN, "q not aligned");
+    if ((rc = check_ring(cfg, ring, false, false))) return rc;
     a.nt = n_buffered + 1;
-    if (ring) {
-      a.rk = ring->k;
-      a.rv = ring->v;
-      a.ru = ring->u;
-      a.rg = ring->g;
-      a.rbeta = ring->beta;
-      a.rb = ring->bcoef;
-    }
-    a.q = step->q;
-    a.k = step->k;
-    a.v = step->v;
-    a.beta = step->beta;
-    a.logd = step->log_decay;
+    a.q = q;
+    a.rk = ring->k;
+    a.rv = ring->v;
+    a.rbeta = ring->beta;
+    a.rla = ring->log_decay;
+    a.rg = ring->g;
+    a.ru = ring->u;
+    a.rb = ring->bcoef;
     a.o = o;
   } else {
     if (n_buffered != 0) return fail(SKSSM_ESTATE, "sketch-only update needs n_buffered = 0");
@@ -176,17 +162,16 @@ int sketchssm_update(const skssm_config* cfg, float* S, const float* omega, cons
 }
 
 int sketchssm_decode(const skssm_config* cfg, const float* U, const float* coef, const skssm_ring* ring,
-                     int32_t n_buffered, const skssm_step* step, float* o, void* stream) {
+                     int32_t n_buffered, const void* q, float* o, void* stream) {
   int rc = check_shape(cfg, true, false);
   if (rc) return rc;
   if (cfg->window < 2) return fail(SKSSM_EINVAL, "decode needs window >= 2 (window 1 flushes every token)");
   if (n_buffered < 0 || n_buffered > cfg->window - 2)
     return fail(SKSSM_ESTATE, "n_buffered %d outside 0..%d", n_buffered, cfg->window - 2);
-  if (!U || !coef || !o) return fail(SKSSM_EINVAL, "U, coef and o are required");
-  if (!aligned(U) || !aligned(coef) || !aligned(o)) return fail(SKSSM_EALIGN, "U/coef/o not aligned");
-  if ((rc = check_step(cfg, step))) return rc;
+  if (!U || !coef || !o || !q) return fail(SKSSM_EINVAL, "U, coef, q and o are required");
+  if (!aligned(U) || !aligned(coef) || !aligned(o) || !aligned(q)) return fail(SKSSM_EALIGN, "U/coef/q/o not aligned");
   if ((rc = check_ring(cfg, ring, true, false))) return rc;
-  skssm::DecodeArgs a = decode_args(cfg, ring, n_buffered, step, o);
+  skssm::DecodeArgs a = decode_args(cfg, ring, n_buffered, q, o);
   a.U = U;
   a.coef = coef;
   int r;
@@ -199,17 +184,16 @@ int sketchssm_decode(const skssm_config* cfg, const float* U, const float* coef,
 }
 
 int sketchssm_full_read_baseline(const skssm_config* cfg, const float* S, const skssm_ring* ring,
-                                 int32_t n_buffered, const skssm_step* step, float* o, void* stream) {
+                                 int32_t n_buffered, const void* q, float* o, void* stream) {
   int rc = check_shape(cfg, false, false);
   if (rc) return rc;
   if (cfg->window < 2) return fail(SKSSM_EINVAL, "baseline read needs window >= 2");
   if (n_buffered < 0 || n_buffered > cfg->window - 2)
     return fail(SKSSM_ESTATE, "n_buffered %d outside 0..%d", n_buffered, cfg->window - 2);
-  if (!S || !o) return fail(SKSSM_EINVAL, "S and o are required");
-  if (!aligned(S) || !aligned(o)) return fail(SKSSM_EALIGN, "S/o not aligned");
-  if ((rc = check_step(cfg, step))) return rc;
+  if (!S || !o || !q) return fail(SKSSM_EINVAL, "S, q and o are required");
+  if (!aligned(S) || !aligned(o) || !aligned(q)) return fail(SKSSM_EALIGN, "S/q/o not aligned");
   if ((rc = check_ring(cfg, ring, false, true))) return rc;
-  skssm::DecodeArgs a = decode_args(cfg, ring, n_buffered, step, o);
+  skssm::DecodeArgs a = decode_args(cfg, ring, n_buffered, q, o);
   a.S = S;
   int r;
   switch (cfg->kind) {

@@ -1,4 +1,9 @@
 // Kernel argument blocks (passed by value to the kernels).
+//
+// Replay buffer (ring) fields are slot-major over the batch: slot s of item
+// i (= b*H + h) of a field of width w sits at field + (s * B*H + i) * w.
+// Raw inputs of token s (k, v, beta, log decay) are written into slot s by
+// the producer of the token; the kernels derive and store the rest.
 #pragma once
 
 #include <stddef.h>
@@ -7,43 +12,37 @@
 namespace skssm {
 
 struct DecodeArgs {
-  int B, H, W, n;                 // batch, heads, window, slot being appended
-  const void* q;                  // [B][H][K] io
-  const void* k;                  // [B][H][K] io
-  const void* v;                  // [B][H][V] io
-  const float* beta;              // [B][H]
-  const float* logd;              // [B][H] or [B][H][K]
-  const float* U;                 // [B][H][V][R]       (sketch read)
-  const float* coef;              // [H][R][K]          (sketch read)
-  const float* S;                 // [B][H][V][K]       (exact baseline)
-  void* rk;                       // ring [B][H][W][K] io
-  void* rv;                       // ring [B][H][W][V] io   (Mamba-2)
-  float* ru;                      // ring [B][H][W][V]      (GDN/KDA)
-  float* rf;                      // ring [B][H][W][R]      (GDN/KDA sketch read)
-  float* rpi;                     // ring [B][H][W][K]      (GDN/KDA baseline)
-  float* rg;                      // ring [B][H][W] or [B][H][W][K]
-  float* rbeta;                   // ring [B][H][W]
-  float* rb;                      // ring [B][H][W][W]      (GDN/KDA)
+  int B, H, W, n;                 // batch, heads, window, slot of the current token
+  const void* q;                  // [B][H][K] io, current query
+  const float* U;                 // [B][H][R/4][V][4]   (sketch read)
+  const float* coef;              // [H][R][K]           (sketch read)
+  const float* S;                 // [B][H][V][K]        (exact baseline)
+  const void* rk;                 // ring [W][B][H][K] io      raw keys
+  const void* rv;                 // ring [W][B][H][V] io      raw values
+  const float* rbeta;             // ring [W][B][H]            write gates
+  const float* rla;               // ring [W][B][H] or [..][K] log decays
+  float* rg;                      // ring [W][B][H][K]  cumulative log decay (KDA)
+  float* ru;                      // ring [W][B][H][V]  pseudo-values (GDN/KDA)
+  float* rf;                      // ring [W][B][H][R]  projected erase factors (GDN/KDA sketch read)
+  float* rpi;                     // ring [W][B][H][K]  erase factors (GDN/KDA baseline)
+  float* rb;                      // ring [W][B][H][W]  erase couplings (GDN/KDA)
   float* o;                       // [B][H][V]
 };
 
 struct UpdateArgs {
-  int B, H, W, n;                 // n = ring slots already filled (0..W-1)
-  int nt;                         // tokens applied: n + 1, or 0 (sketch only)
+  int B, H, W, n;                 // n = slot of the current token (tokens applied: n + 1)
+  int nt;                         // n + 1, or 0 (sketch only)
   float* S;                       // [B][H][V][K]
   const float* omega;             // [H][K][R]
+  const void* q;                  // [B][H][K] io, current query (NULL when nt == 0)
   const void* rk;
   const void* rv;
-  const float* ru;
-  const float* rg;
   const float* rbeta;
-  const float* rb;
-  const void* q;                  // current token (NULL when nt == 0)
-  const void* k;
-  const void* v;
-  const float* beta;
-  const float* logd;
-  float* U;                       // [B][H][V][R] or NULL
+  const float* rla;
+  const float* rg;                // KDA cumulative log decay, slots < n
+  const float* ru;                // GDN/KDA pseudo-values, slots < n
+  const float* rb;                // GDN/KDA erase couplings, slots < n
+  float* U;                       // [B][H][R/4][V][4] or NULL
   float* o;                       // [B][H][V] or NULL
 };
 

@@ -1,8 +1,9 @@
 // Non-flush read of SketchSSM (Algorithm 1, t < W) and the exact
-// full-state-read baseline, both appending the token to the replay buffer.
+// full-state-read baseline.
 //
-// Per (request, head) item, with t = n + 1 tokens in the window:
-//   g_t      = g_{t-1} + log alpha_t                       (cumulative log decay)
+// Per (request, head) item, with the current token in ring slot n (t = n + 1
+// tokens in the window):
+//   g_t      = sum_{j<=t} log alpha_j                      (window-local cumulative log decay)
 //   a_{t,s}  = <exp(g_t - g_s) . k_s, q_t>,  s <= t       (Appendix C.2, key reuse)
 //   b_{t,j}  = <exp(g_t - g_j) . k_j, k_t>,  j <  t       (erase couplings)
 //   u_t      = beta_t (v_t - sum_j b_{t,j} u_j)           (pseudo-values; Mamba-2: beta_t v_t)
@@ -12,10 +13,22 @@
 // The exact baseline replaces f by the full erase factors pi (eq. wy) and
 // U c_t by S_0^T q~_t with q~_t = e^{g_t} . q_t - sum_s a_{t,s} pi_s.
 //
-// Mapping: one wave per item.  Keys, decays and erase factors of the ring
-// are read in the row layout (4 slots per load, 16-lane DPP dot products);
-// the sketch U, the values / pseudo-values and the output use the value
-// layout.  No matrix cores: every contraction here is a matrix-vector product.
+// The token's raw update inputs (k, v, beta, log alpha) were written into
+// ring slot n by their producer, so appending costs no copy: the kernels read
+// them there and store only derived fields (GDN/KDA: u, f or pi, the row of
+// couplings b; KDA: the cumulative log decay).  For scalar decays the
+// cumulative log decays are rebuilt on the fly from the ring's log alphas.
+//
+// Mapping: one wave per item; the item index is wave-uniform, so per-item
+// base addresses live in scalar registers.  Everything read from the replay
+// buffer uses the row layout: row r of the wave holds ring slot 4 gi + r, so
+// one load instruction fetches four slots and the slot sums of the buffer
+// term reduce inside each row before a single cross-row sum.  The sketch and
+// the output use the value layout (lane l owns v = l + 64 j); the sketch sits
+// in 4-column panels U[B][H][r/4][V][4], one float4 per lane per panel, 1 KB
+// contiguous per load.  The buffer term crosses from the row layout to the
+// value layout through a small LDS transpose.  No matrix cores: every
+// contraction here is a matrix-vector product.
 #pragma once
 
 #include "args.h"
@@ -23,77 +36,114 @@
 
 namespace skssm {
 
+// Loads shared by the sketch read and the exact baseline (row layout).
 template <int KIND, int K, int V, int WMAX, typename IO>
 struct RowLoads {
   static constexpr bool ERASE = KIND != MAMBA2;
   static constexpr bool CHAN = KIND == KDA;
-  static constexpr int KPL = K / 16;
-  static constexpr int VPL = V / 64;
-  static constexpr int NG = WMAX / 4;
+  static constexpr int KPL = K / 16;  // key channels per lane
+  static constexpr int VR = V / 16;   // value channels per lane
+  static constexpr int NG = WMAX / 4; // groups of four slots
   static constexpr int GD = CHAN ? KPL : 1;
 
-  Raw<IO, KPL> q_raw, k_raw;  // current token, row layout (same in every row)
-  Raw<IO, VPL> v_raw;         // current token, value layout
+  Raw<IO, KPL> q_raw, k_raw;          // current query and key (same in every row)
+  Raw<IO, VR> v_raw;                  // current value (same in every row)
   float beta_t;
-  float la[GD];               // log alpha_t
-  float gprev[GD];            // g_{t-1}
-  Raw<IO, KPL> ks[NG];        // ring keys of slot 4*gi + row
-  float gs[NG][GD];           // ring cumulative log decay of slot 4*gi + row
-  float bs[NG];               // ring beta of slot 4*gi + row (Mamba-2)
+  float la[GD];                       // log alpha_t
+  float gprev[GD];                    // g_{t-1} (KDA: loaded; scalar decay: rebuilt)
+  Raw<IO, KPL> ks[NG];                // ring keys of slot 4 gi + row, s < n
+  float gs[NG][GD];                   // cumulative log decay of slot 4 gi + row
+  Raw<IO, VR> vs[ERASE ? 1 : NG];     // ring raw values (Mamba-2)
+  float bs[ERASE ? 1 : NG];           // ring beta (Mamba-2)
+  Vec<VR> us[ERASE ? NG : 1];         // ring pseudo-values (GDN, KDA)
 
-  __device__ __forceinline__ void load(const DecodeArgs& a, size_t item, int row, int col, int lane) {
-    const int n = a.n, W = a.W;
-    const size_t slot0 = item * (size_t)W;
-    q_raw.load(static_cast<const IO*>(a.q) + item * K + col * KPL);
-    k_raw.load(static_cast<const IO*>(a.k) + item * K + col * KPL);
-    v_raw.load(static_cast<const IO*>(a.v) + item * V + lane * VPL);
-    beta_t = a.beta[item];
+  // `item` is wave-uniform.  Slot s of a ring field of width w sits at
+  // field + ((s * NI + item) * w).
+  __device__ __forceinline__ void load(const DecodeArgs& a, size_t item, int row, int col) {
+    const int n = a.n;
+    const size_t NI = (size_t)a.B * a.H;
+    const uint32_t koff = (uint32_t)(col * KPL), voff = (uint32_t)(col * VR);
+    const size_t cur = (size_t)n * NI + item;        // slot n of this item
+    q_raw.load(static_cast<const IO*>(a.q) + item * K + koff);
+    k_raw.load(static_cast<const IO*>(a.rk) + cur * K + koff);
+    v_raw.load(static_cast<const IO*>(a.rv) + cur * V + voff);
+    beta_t = a.rbeta[cur];
     if constexpr (CHAN) {
       Vec<KPL> t;
-      t.load(a.logd + item * K + col * KPL);
+      t.load(a.rla + cur * K + koff);
 #pragma unroll
       for (int m = 0; m < KPL; ++m) la[m] = t.e[m];
-    } else {
-      la[0] = a.logd[item];
-    }
 #pragma unroll
-    for (int m = 0; m < GD; ++m) gprev[m] = 0.f;
-    if (n > 0) {
-      if constexpr (CHAN) {
-        Vec<KPL> t;
-        t.load(a.rg + (slot0 + n - 1) * K + col * KPL);
+      for (int m = 0; m < KPL; ++m) gprev[m] = 0.f;
+      if (n > 0) {
+        Vec<KPL> g;
+        g.load(a.rg + (cur - NI) * K + koff);
 #pragma unroll
-        for (int m = 0; m < KPL; ++m) gprev[m] = t.e[m];
-      } else {
-        gprev[0] = a.rg[slot0 + n - 1];
+        for (int m = 0; m < KPL; ++m) gprev[m] = g.e[m];
       }
+    } else {
+      la[0] = a.rla[cur];
     }
+    const size_t rowslot = (size_t)row * NI + item;  // slot `row` of this item
 #pragma unroll
     for (int gi = 0; gi < NG; ++gi) {
       const int s = 4 * gi + row;
+      const size_t si = rowslot + (size_t)(4 * gi) * NI;
       ks[gi].zero();
 #pragma unroll
       for (int m = 0; m < GD; ++m) gs[gi][m] = 0.f;
-      bs[gi] = 0.f;
+      if constexpr (ERASE) {
+#pragma unroll
+        for (int m = 0; m < VR; ++m) us[gi].e[m] = 0.f;
+      } else {
+        vs[gi].zero();
+        bs[gi] = 0.f;
+      }
       if (4 * gi < n && s < n) {
-        ks[gi].load(static_cast<const IO*>(a.rk) + (slot0 + s) * K + col * KPL);
+        ks[gi].load(static_cast<const IO*>(a.rk) + si * K + koff);
         if constexpr (CHAN) {
           Vec<KPL> t;
-          t.load(a.rg + (slot0 + s) * K + col * KPL);
+          t.load(a.rg + si * K + koff);
 #pragma unroll
           for (int m = 0; m < KPL; ++m) gs[gi][m] = t.e[m];
         } else {
-          gs[gi][0] = a.rg[slot0 + s];
+          gs[gi][0] = a.rla[si];  // log alpha_s for now; made cumulative in prefix_decay()
         }
-        if constexpr (!ERASE) bs[gi] = a.rbeta[slot0 + s];
+        if constexpr (ERASE) {
+          us[gi].load(a.ru + si * V + voff);
+        } else {
+          vs[gi].load(static_cast<const IO*>(a.rv) + si * V + voff);
+          bs[gi] = a.rbeta[si];
+        }
       }
+    }
+  }
+
+  // Scalar decay: turn the per-slot log alphas into cumulative log decays
+  // g_s = sum_{j<=s} log alpha_j (slots in order), and g_{t-1}.
+  __device__ __forceinline__ void prefix_decay(int n, int row) {
+    if constexpr (!CHAN) {
+      float tot = 0.f;
+#pragma unroll
+      for (int gi = 0; gi < NG; ++gi) {
+        if (4 * gi < n) {
+          const float x = gs[gi][0];
+          const float p0 = tot + lane_bcast(x, 0);
+          const float p1 = p0 + lane_bcast(x, 16);
+          const float p2 = p1 + lane_bcast(x, 32);
+          const float p3 = p2 + lane_bcast(x, 48);
+          gs[gi][0] = row == 0 ? p0 : row == 1 ? p1 : row == 2 ? p2 : p3;
+          tot = p3;  // log alphas of slots >= n are zero
+        }
+      }
+      gprev[0] = tot;
     }
   }
 };
 
 // Dot products of the current query / key with every buffered key.
-// Returns, in the row layout, av[gi] = a_{t,s} (Mamba-2: a_{t,s} beta_s) and
-// bv[gi] = b_{t,s} for s = 4*gi + row (0 for s >= n), plus at = <k_t, q_t>.
+// Returns, in the row layout, av[gi] = a_{t,s} and bv[gi] = b_{t,s} for
+// s = 4 gi + row (0 for s >= n), plus at = <k_t, q_t>.
 template <class L>
 __device__ __forceinline__ void slot_dots(const L& r, int n, int row, const float (&qv)[L::KPL],
                                           const float (&kv)[L::KPL], const float (&gt)[L::GD],
@@ -124,10 +174,70 @@ __device__ __forceinline__ void slot_dots(const L& r, int n, int row, const floa
         pa = 0.f;
         pb = 0.f;
       }
-      if constexpr (!L::ERASE) pa *= r.bs[gi];
     }
     av[gi] = pa;
     bv[gi] = pb;
+  }
+}
+
+// Buffer term and current pseudo-value in the row layout (every row ends
+// with the full sums): ut = u_t, ob = sum_{s<=t} a_{t,s} u_s.
+template <class L>
+__device__ __forceinline__ void buffer_term(const L& r, const float (&av)[L::NG], const float (&bv)[L::NG],
+                                            float at, float (&ut)[L::VR], float (&ob)[L::VR]) {
+#pragma unroll
+  for (int m = 0; m < L::VR; ++m) {
+    float sa = 0.f, sb = 0.f;
+#pragma unroll
+    for (int gi = 0; gi < L::NG; ++gi) {
+      if constexpr (L::ERASE) {
+        sa += av[gi] * r.us[gi].e[m];
+        sb += bv[gi] * r.us[gi].e[m];
+      } else {
+        sa += av[gi] * r.bs[gi] * r.vs[gi].get(m);
+      }
+    }
+    sa = cross_row_sum(sa);
+    if constexpr (L::ERASE) {
+      sb = cross_row_sum(sb);
+      ut[m] = r.beta_t * (r.v_raw.get(m) - sb);
+    } else {
+      ut[m] = r.beta_t * r.v_raw.get(m);
+    }
+    ob[m] = sa + at * ut[m];
+  }
+}
+
+// Store the derived fields of the token at ring slot n (GDN/KDA: u_t and the
+// coupling row b_{t,.}; KDA: g_t).  Mamba-2 derives nothing.
+template <class L>
+__device__ __forceinline__ void append_derived(const DecodeArgs& a, size_t item, int row, int col, int lane,
+                                               const float (&gt)[L::GD], const float (&ut)[L::VR],
+                                               const float (&bv)[L::NG], float* b_l) {
+  constexpr int K = L::KPL * 16, V = L::VR * 16, KPL = L::KPL, VR = L::VR, NG = L::NG;
+  if constexpr (L::ERASE) {
+    const int n = a.n, W = a.W;
+    const size_t sl = (size_t)n * a.B * a.H + item;
+    if (row == 0) {
+      if constexpr (L::CHAN) {
+        Vec<KPL> t;
+#pragma unroll
+        for (int m = 0; m < KPL; ++m) t.e[m] = gt[m];
+        t.store(a.rg + sl * K + col * KPL);
+      }
+      Vec<VR> t;
+#pragma unroll
+      for (int m = 0; m < VR; ++m) t.e[m] = ut[m];
+      t.store(a.ru + sl * V + col * VR);
+    }
+    // b_{t,s}, s < n: gather through LDS, then one contiguous store of the row
+    if (col == 0) {
+#pragma unroll
+      for (int gi = 0; gi < NG; ++gi)
+        if (4 * gi < n) b_l[4 * gi + row] = bv[gi];
+    }
+    wave_lds_sync();
+    if (lane < n) a.rb[sl * W + lane] = b_l[lane];
   }
 }
 
@@ -135,71 +245,55 @@ template <int KIND, int K, int V, int R, int WMAX, typename IO>
 __global__ __launch_bounds__(256) void decode_kernel(const DecodeArgs a) {
   using L = RowLoads<KIND, K, V, WMAX, IO>;
   constexpr bool ERASE = L::ERASE, CHAN = L::CHAN;
-  constexpr int KPL = L::KPL, VPL = L::VPL, NG = L::NG, GD = L::GD;
-  constexpr int RP = (R + 15) / 16;  // sketch components per lane in the row layout
-  constexpr int CP = K + 4;          // padded LDS row pitch of C
-  constexpr int KQ = K / 4;          // channels each row covers in C x
-  constexpr int WS = 2 * K + R;      // per-wave LDS scratch: x_q, x_k, c
+  constexpr int KPL = L::KPL, VR = L::VR, NG = L::NG, GD = L::GD;
+  constexpr int VPL = V / 64;                    // value channels per lane (value layout)
+  constexpr int RP = (R + 15) / 16;              // sketch components per lane (row layout)
+  constexpr int NP = R / 4;                      // 4-column sketch panels
+  constexpr int CP = K + 4;                      // padded LDS row pitch of C
+  constexpr int KQ = K / 4;                      // channels each row covers in C x
+  constexpr int WS = 2 * K + R + V + WMAX;       // per-wave LDS: x_q, x_k, c, o_buf, b row
   constexpr bool U_PRELOAD = R <= 32;
-  constexpr int UR = U_PRELOAD ? R : 1;
+  constexpr int UP = U_PRELOAD ? NP : 1;
 
   __shared__ __align__(16) float c_lds[R * CP];
   __shared__ __align__(16) float wscr[4 * WS];
 
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int row = lane >> 4, col = lane & 15;
-  const int H = a.H, W = a.W, n = a.n;
+  const int H = a.H, n = a.n;
+  const size_t NI = (size_t)a.B * H;
   const int h = blockIdx.x % H;
   const int b = (blockIdx.x / H) * 4 + wave;
   const bool valid = b < a.B;
   const size_t item = (size_t)(valid ? b : 0) * H + h;
-  const size_t slot0 = item * (size_t)W;
+  const float* Ub = a.U + item * (size_t)V * R;
 
-  // ---- issue every global load of this item first
+  // ---- every global load of this item
   L r;
-  float fs[NG][RP];                  // ring f of slot 4*gi + row, component col + 16p
-  float us[ERASE ? WMAX : 1][VPL];   // ring u (value layout)
-  Raw<IO, VPL> vs[ERASE ? 1 : WMAX]; // ring v (value layout)
-  float Ur[VPL][UR];
+  float fs[ERASE ? NG : 1][RP];      // ring f of slot 4 gi + row, component col + 16 p
+  float4 Ur[VPL][UP];                // sketch panels (value layout)
   if (valid) {
-    r.load(a, item, row, col, lane);
+    r.load(a, item, row, col);
     if constexpr (ERASE) {
+      const size_t rowslot = (size_t)row * NI + item;
 #pragma unroll
       for (int gi = 0; gi < NG; ++gi) {
         const int s = 4 * gi + row;
+        const float* fp = a.rf + (rowslot + (size_t)(4 * gi) * NI) * R;
 #pragma unroll
         for (int p = 0; p < RP; ++p) {
           const int j = col + 16 * p;
-          fs[gi][p] = (4 * gi < n && s < n && j < R) ? a.rf[(slot0 + s) * R + j] : 0.f;
+          fs[gi][p] = (4 * gi < n && s < n && j < R) ? fp[j] : 0.f;
         }
-      }
-#pragma unroll
-      for (int s = 0; s < WMAX; ++s) {
-        if (s < n) {
-          Vec<VPL> t;
-          t.load(a.ru + (slot0 + s) * V + lane * VPL);
-#pragma unroll
-          for (int vv = 0; vv < VPL; ++vv) us[s][vv] = t.e[vv];
-        } else {
-#pragma unroll
-          for (int vv = 0; vv < VPL; ++vv) us[s][vv] = 0.f;
-        }
-      }
-    } else {
-#pragma unroll
-      for (int s = 0; s < WMAX; ++s) {
-        vs[s].zero();
-        if (s < n) vs[s].load(static_cast<const IO*>(a.rv) + (slot0 + s) * V + lane * VPL);
       }
     }
     if constexpr (U_PRELOAD) {
 #pragma unroll
-      for (int vv = 0; vv < VPL; ++vv) {
-        Vec<R> t;
-        t.load(a.U + (item * V + lane * VPL + vv) * R);
+      for (int p = 0; p < NP; ++p)
 #pragma unroll
-        for (int j = 0; j < R; ++j) Ur[vv][j] = t.e[j];
-      }
+        for (int vv = 0; vv < VPL; ++vv)
+          Ur[vv][p] = reinterpret_cast<const float4*>(Ub)[(uint32_t)(p * V + lane + 64 * vv)];
     }
   }
 
@@ -217,7 +311,10 @@ __global__ __launch_bounds__(256) void decode_kernel(const DecodeArgs a) {
   float* xq_l = wscr + wave * WS;
   float* xk_l = xq_l + K;
   float* c_l = xq_l + 2 * K;
+  float* ob_l = c_l + R;
+  float* b_l = ob_l + V;
 
+  r.prefix_decay(n, row);
   float qv[KPL], kv[KPL], gt[GD];
 #pragma unroll
   for (int m = 0; m < KPL; ++m) {
@@ -229,46 +326,19 @@ __global__ __launch_bounds__(256) void decode_kernel(const DecodeArgs a) {
 
   float av[NG], bv[NG], at;
   slot_dots(r, n, row, qv, kv, gt, av, bv, at);
-
-  // wave-uniform copies of a_{t,s} (and b_{t,s}) for the value-layout sums
-  float a_u[WMAX], b_u[ERASE ? WMAX : 1];
-#pragma unroll
-  for (int gi = 0; gi < NG; ++gi)
-#pragma unroll
-    for (int r4 = 0; r4 < 4; ++r4) {
-      a_u[4 * gi + r4] = (4 * gi < n) ? lane_bcast(av[gi], 16 * r4) : 0.f;
-      if constexpr (ERASE) b_u[4 * gi + r4] = (4 * gi < n) ? lane_bcast(bv[gi], 16 * r4) : 0.f;
-    }
-
-  // ---- pseudo-value of the current token (value layout)
-  float ut[VPL];
-#pragma unroll
-  for (int vv = 0; vv < VPL; ++vv) {
-    float acc = r.v_raw.get(vv);
-    if constexpr (ERASE) {
-#pragma unroll
-      for (int s = 0; s < WMAX; ++s)
-        if (s < n) acc -= b_u[s] * us[s][vv];
-    }
-    ut[vv] = r.beta_t * acc;
-  }
+  float ut[VR], ob[VR];
+  buffer_term(r, av, bv, at, ut, ob);
 
   // ---- C (e^{g_t} . q_t) and C (e^{g_t} . k_t): each row covers K/4 channels
-  {
-    float xq[KPL], xk[KPL];
+  if (row == 0) {
 #pragma unroll
     for (int m = 0; m < KPL; ++m) {
       const float e = CHAN ? fast_exp(gt[m]) : 1.f;
-      xq[m] = e * qv[m];
-      xk[m] = e * kv[m];
+      xq_l[col * KPL + m] = e * qv[m];
+      if constexpr (ERASE) xk_l[col * KPL + m] = e * kv[m];
     }
-    if (row == 0) {
 #pragma unroll
-      for (int m = 0; m < KPL; ++m) {
-        xq_l[col * KPL + m] = xq[m];
-        if constexpr (ERASE) xk_l[col * KPL + m] = xk[m];
-      }
-    }
+    for (int m = 0; m < VR; ++m) ob_l[col * VR + m] = ob[m];
   }
   wave_lds_sync();
   const float eg = CHAN ? 1.f : fast_exp(gt[0]);
@@ -317,80 +387,31 @@ __global__ __launch_bounds__(256) void decode_kernel(const DecodeArgs a) {
   }
   wave_lds_sync();
 
-  // ---- o = U c + sum_s a_{t,s} u_s  (value layout)
-  float ov[VPL];
+  // ---- o = U c + buffer term  (value layout)
+  float* ob_g = a.o + item * V;
 #pragma unroll
   for (int vv = 0; vv < VPL; ++vv) {
-    float acc = 0.f;
-    if constexpr (U_PRELOAD) {
+    float acc = ob_l[lane + 64 * vv];
 #pragma unroll
-      for (int j = 0; j < R; j += 4) {
-        const float4 c4 = *reinterpret_cast<const float4*>(c_l + j);
-        acc += Ur[vv][j] * c4.x + Ur[vv][j + 1] * c4.y + Ur[vv][j + 2] * c4.z + Ur[vv][j + 3] * c4.w;
-      }
-    } else {
-      const float* up = a.U + (item * V + lane * VPL + vv) * R;
-#pragma unroll 4
-      for (int j = 0; j < R; j += 4) {
-        const float4 u4 = *reinterpret_cast<const float4*>(up + j);
-        const float4 c4 = *reinterpret_cast<const float4*>(c_l + j);
-        acc += u4.x * c4.x + u4.y * c4.y + u4.z * c4.z + u4.w * c4.w;
-      }
+    for (int p = 0; p < NP; ++p) {
+      const float4 c4 = *reinterpret_cast<const float4*>(c_l + 4 * p);
+      float4 u4;
+      if constexpr (U_PRELOAD) u4 = Ur[vv][p];
+      else u4 = reinterpret_cast<const float4*>(Ub)[(uint32_t)(p * V + lane + 64 * vv)];
+      acc += u4.x * c4.x + u4.y * c4.y + u4.z * c4.z + u4.w * c4.w;
     }
-    if constexpr (ERASE) {
-#pragma unroll
-      for (int s = 0; s < WMAX; ++s)
-        if (s < n) acc += a_u[s] * us[s][vv];
-      acc += at * ut[vv];
-    } else {
-#pragma unroll
-      for (int s = 0; s < WMAX; ++s)
-        if (s < n) acc += a_u[s] * vs[s].get(vv);
-      acc += at * ut[vv];
-    }
-    ov[vv] = acc;
-  }
-  {
-    Vec<VPL> t;
-#pragma unroll
-    for (int vv = 0; vv < VPL; ++vv) t.e[vv] = ov[vv];
-    t.store(a.o + item * V + lane * VPL);
+    ob_g[lane + 64 * vv] = acc;
   }
 
-  // ---- append the token at ring slot n
-  const size_t sl = slot0 + n;
-  if (row == 0) {
-    r.k_raw.store(static_cast<IO*>(a.rk) + sl * K + col * KPL);
-    if constexpr (CHAN) {
-      Vec<KPL> t;
-#pragma unroll
-      for (int m = 0; m < KPL; ++m) t.e[m] = gt[m];
-      t.store(a.rg + sl * K + col * KPL);
-    }
-  }
-  if (lane == 0) {
-    if constexpr (!CHAN) a.rg[sl] = gt[0];
-    a.rbeta[sl] = r.beta_t;
-  }
+  // ---- derived fields of the token at ring slot n
+  append_derived<L>(a, item, row, col, lane, gt, ut, bv, b_l);
   if constexpr (ERASE) {
-    Vec<VPL> t;
-#pragma unroll
-    for (int vv = 0; vv < VPL; ++vv) t.e[vv] = ut[vv];
-    t.store(a.ru + sl * V + lane * VPL);
     if (row == 0) {
+      const size_t sl = (size_t)n * NI + item;
 #pragma unroll
       for (int p = 0; p < RP; ++p)
         if (col + 16 * p < R) a.rf[sl * R + col + 16 * p] = ft[p];
     }
-    if (col == 0) {
-#pragma unroll
-      for (int gi = 0; gi < NG; ++gi) {
-        const int s = 4 * gi + row;
-        if (4 * gi < n && s < n) a.rb[sl * W + s] = bv[gi];
-      }
-    }
-  } else {
-    r.v_raw.store(static_cast<IO*>(a.rv) + sl * V + lane * VPL);
   }
 }
 
@@ -398,51 +419,43 @@ template <int KIND, int K, int V, int WMAX, typename IO>
 __global__ __launch_bounds__(256) void full_read_kernel(const DecodeArgs a) {
   using L = RowLoads<KIND, K, V, WMAX, IO>;
   constexpr bool ERASE = L::ERASE, CHAN = L::CHAN;
-  constexpr int KPL = L::KPL, VPL = L::VPL, NG = L::NG, GD = L::GD;
+  constexpr int KPL = L::KPL, VR = L::VR, NG = L::NG, GD = L::GD;
+  constexpr int VPL = V / 64;
+  constexpr int WS = 2 * V + WMAX;   // per-wave LDS: o^state, o_buf, b row
 
-  __shared__ __align__(16) float os_lds[4 * V];
+  __shared__ __align__(16) float wscr[4 * WS];
 
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int row = lane >> 4, col = lane & 15;
-  const int W = a.W, n = a.n;
-  const size_t n_items = (size_t)a.B * a.H;
+  const int n = a.n;
+  const size_t NI = (size_t)a.B * a.H;
   const size_t item = (size_t)blockIdx.x * 4 + wave;
-  if (item >= n_items) return;  // wave-uniform; no block barrier in this kernel
-  const size_t slot0 = item * (size_t)W;
+  if (item >= NI) return;  // wave-uniform; no block barrier in this kernel
+  const uint32_t koff = (uint32_t)(col * KPL);
 
   L r;
-  r.load(a, item, row, col, lane);
-  float ps[ERASE ? NG : 1][KPL];     // ring pi of slot 4*gi + row (row layout)
-  float us[ERASE ? WMAX : 1][VPL];
-  Raw<IO, VPL> vs[ERASE ? 1 : WMAX];
+  r.load(a, item, row, col);
+  float ps[ERASE ? NG : 1][KPL];     // ring pi of slot 4 gi + row (row layout)
   if constexpr (ERASE) {
+    const size_t rowslot = (size_t)row * NI + item;
 #pragma unroll
     for (int gi = 0; gi < NG; ++gi) {
       const int s = 4 * gi + row;
       Vec<KPL> t;
 #pragma unroll
       for (int m = 0; m < KPL; ++m) t.e[m] = 0.f;
-      if (4 * gi < n && s < n) t.load(a.rpi + (slot0 + s) * K + col * KPL);
+      if (4 * gi < n && s < n) t.load(a.rpi + (rowslot + (size_t)(4 * gi) * NI) * K + koff);
 #pragma unroll
       for (int m = 0; m < KPL; ++m) ps[gi][m] = t.e[m];
     }
-#pragma unroll
-    for (int s = 0; s < WMAX; ++s) {
-      Vec<VPL> t;
-#pragma unroll
-      for (int vv = 0; vv < VPL; ++vv) t.e[vv] = 0.f;
-      if (s < n) t.load(a.ru + (slot0 + s) * V + lane * VPL);
-#pragma unroll
-      for (int vv = 0; vv < VPL; ++vv) us[s][vv] = t.e[vv];
-    }
-  } else {
-#pragma unroll
-    for (int s = 0; s < WMAX; ++s) {
-      vs[s].zero();
-      if (s < n) vs[s].load(static_cast<const IO*>(a.rv) + (slot0 + s) * V + lane * VPL);
-    }
   }
 
+  float* os_l = wscr + wave * WS;
+  float* ob_l = os_l + V;
+  float* b_l = ob_l + V;
+
+  r.prefix_decay(n, row);
   float qv[KPL], kv[KPL], gt[GD];
 #pragma unroll
   for (int m = 0; m < KPL; ++m) {
@@ -454,14 +467,8 @@ __global__ __launch_bounds__(256) void full_read_kernel(const DecodeArgs a) {
 
   float av[NG], bv[NG], at;
   slot_dots(r, n, row, qv, kv, gt, av, bv, at);
-  float a_u[WMAX], b_u[ERASE ? WMAX : 1];
-#pragma unroll
-  for (int gi = 0; gi < NG; ++gi)
-#pragma unroll
-    for (int r4 = 0; r4 < 4; ++r4) {
-      a_u[4 * gi + r4] = (4 * gi < n) ? lane_bcast(av[gi], 16 * r4) : 0.f;
-      if constexpr (ERASE) b_u[4 * gi + r4] = (4 * gi < n) ? lane_bcast(bv[gi], 16 * r4) : 0.f;
-    }
+  float ut[VR], ob[VR];
+  buffer_term(r, av, bv, at, ut, ob);
 
   // ---- effective query q~_t and erase factor pi_t (row layout, all rows equal)
   float qe[KPL], pit[KPL];
@@ -485,84 +492,36 @@ __global__ __launch_bounds__(256) void full_read_kernel(const DecodeArgs a) {
     }
   }
 
-  // ---- o^state = S_0^T q~_t : rows v = 4*vi + row of S, K channels over 16 lanes
-  float* os_l = os_lds + wave * V;
+  // ---- o^state = S_0^T q~_t : rows v = 4 vi + row of S, K channels over 16 lanes
+  const float* Sb = a.S + item * (size_t)V * K;
 #pragma unroll
   for (int vi = 0; vi < V / 4; ++vi) {
     const int v = 4 * vi + row;
     Vec<KPL> x;
-    x.load(a.S + (item * V + v) * K + col * KPL);
+    x.load(Sb + (uint32_t)(v * K) + koff);
     float d = 0.f;
 #pragma unroll
     for (int m = 0; m < KPL; ++m) d += x.e[m] * qe[m];
     d = row_sum16(d);
     if (col == 0) os_l[v] = d;
   }
-  wave_lds_sync();
-
-  float ut[VPL], ov[VPL];
-#pragma unroll
-  for (int vv = 0; vv < VPL; ++vv) {
-    float acc = r.v_raw.get(vv);
-    if constexpr (ERASE) {
-#pragma unroll
-      for (int s = 0; s < WMAX; ++s)
-        if (s < n) acc -= b_u[s] * us[s][vv];
-    }
-    ut[vv] = r.beta_t * acc;
-    float o = os_l[lane * VPL + vv] + at * ut[vv];
-    if constexpr (ERASE) {
-#pragma unroll
-      for (int s = 0; s < WMAX; ++s)
-        if (s < n) o += a_u[s] * us[s][vv];
-    } else {
-#pragma unroll
-      for (int s = 0; s < WMAX; ++s)
-        if (s < n) o += a_u[s] * vs[s].get(vv);
-    }
-    ov[vv] = o;
-  }
-  {
-    Vec<VPL> t;
-#pragma unroll
-    for (int vv = 0; vv < VPL; ++vv) t.e[vv] = ov[vv];
-    t.store(a.o + item * V + lane * VPL);
-  }
-
-  const size_t sl = slot0 + n;
   if (row == 0) {
-    r.k_raw.store(static_cast<IO*>(a.rk) + sl * K + col * KPL);
-    if constexpr (CHAN) {
-      Vec<KPL> t;
 #pragma unroll
-      for (int m = 0; m < KPL; ++m) t.e[m] = gt[m];
-      t.store(a.rg + sl * K + col * KPL);
-    }
-    if constexpr (ERASE) {
+    for (int m = 0; m < VR; ++m) ob_l[col * VR + m] = ob[m];
+  }
+  wave_lds_sync();
+  float* ob_g = a.o + item * V;
+#pragma unroll
+  for (int vv = 0; vv < VPL; ++vv) ob_g[lane + 64 * vv] = os_l[lane + 64 * vv] + ob_l[lane + 64 * vv];
+
+  append_derived<L>(a, item, row, col, lane, gt, ut, bv, b_l);
+  if constexpr (ERASE) {
+    if (row == 0) {
       Vec<KPL> t;
 #pragma unroll
       for (int m = 0; m < KPL; ++m) t.e[m] = pit[m];
-      t.store(a.rpi + sl * K + col * KPL);
+      t.store(a.rpi + ((size_t)n * NI + item) * K + koff);
     }
-  }
-  if (lane == 0) {
-    if constexpr (!CHAN) a.rg[sl] = gt[0];
-    a.rbeta[sl] = r.beta_t;
-  }
-  if constexpr (ERASE) {
-    Vec<VPL> t;
-#pragma unroll
-    for (int vv = 0; vv < VPL; ++vv) t.e[vv] = ut[vv];
-    t.store(a.ru + sl * V + lane * VPL);
-    if (col == 0) {
-#pragma unroll
-      for (int gi = 0; gi < NG; ++gi) {
-        const int s = 4 * gi + row;
-        if (4 * gi < n && s < n) a.rb[sl * W + s] = bv[gi];
-      }
-    }
-  } else {
-    r.v_raw.store(static_cast<IO*>(a.rv) + sl * V + lane * VPL);
   }
 }
 

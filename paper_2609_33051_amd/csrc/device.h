@@ -6,7 +6,8 @@
 //                 per lane; the 4 rows either hold copies or 4 different
 //                 ring slots, so one wide load fetches 4 slots at once and a
 //                 16-lane DPP reduction finishes 4 dot products together.
-//   value layout  lane l owns V/64 consecutive value channels.
+//   value layout  lane l owns value channels l + 64 j, j < V/64, so a load
+//                 instruction over the value axis reads one contiguous run.
 #pragma once
 
 #include <hip/hip_runtime.h>
@@ -21,6 +22,28 @@ typedef float floatx4 __attribute__((ext_vector_type(4)));
 
 __device__ __forceinline__ float bf16_lo(uint32_t w) { return __uint_as_float(w << 16); }
 __device__ __forceinline__ float bf16_hi(uint32_t w) { return __uint_as_float(w & 0xFFFF0000u); }
+
+// One io element kept in a full 32-bit register (raw bits, zero-extended for
+// bf16): loads need no packing into register halves, so the compiler does not
+// have to wait for them early.
+template <typename IO> __device__ __forceinline__ uint32_t ld_bits(const IO* p, uint32_t off);
+template <> __device__ __forceinline__ uint32_t ld_bits<float>(const float* p, uint32_t off) {
+  return __float_as_uint(p[off]);
+}
+template <> __device__ __forceinline__ uint32_t ld_bits<bf16_t>(const bf16_t* p, uint32_t off) {
+  return (uint32_t)p[off];
+}
+template <typename IO> __device__ __forceinline__ void st_bits(IO* p, uint32_t off, uint32_t x);
+template <> __device__ __forceinline__ void st_bits<float>(float* p, uint32_t off, uint32_t x) {
+  p[off] = __uint_as_float(x);
+}
+template <> __device__ __forceinline__ void st_bits<bf16_t>(bf16_t* p, uint32_t off, uint32_t x) {
+  p[off] = (bf16_t)x;
+}
+template <typename IO> __device__ __forceinline__ float bits_f32(uint32_t x) {
+  if constexpr (sizeof(IO) == 2) return bf16_lo(x);
+  else return __uint_as_float(x);
+}
 
 // N raw elements of the io dtype, moved with the widest aligned accesses.
 template <typename IO, int N> struct Raw;

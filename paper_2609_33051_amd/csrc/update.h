@@ -1,4 +1,4 @@
-// Flush step of SketchSSM (Algorithm 1, t = W; Sec. 4.1 "Per-window: Sketch")
+// Flush step of SketchSSM (Algorithm 1, t = W; Sec. 4.1, per-window sketch)
 // and the initial sketch: one read and one write of the full state.
 //
 // With n ring slots plus the current token (nt = n + 1 tokens) and the
@@ -59,13 +59,14 @@ __global__ __launch_bounds__(256) void update_kernel(const UpdateArgs a) {
   __shared__ __align__(16) float qs[K];
   __shared__ __align__(16) float ds[K];
 
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int lr = lane & 15, lg = lane >> 4;
   const int H = a.H, W = a.W, n = a.n;
   const size_t item = blockIdx.x;
   const int h = (int)(item % (size_t)H);
   const bool flush = a.nt > 0;
-  const size_t slot0 = item * (size_t)W;
+  const size_t NI = (size_t)a.B * H;  // slot s of item: ring field + (s * NI + item) * width
 
   // ---- the single read of the state: issue every tile load first
   floatx4 xs[VTW][MT];
@@ -83,29 +84,34 @@ __global__ __launch_bounds__(256) void update_kernel(const UpdateArgs a) {
   }
 
   if (flush) {
-    // ---- channel work: thread tid owns channel k = tid
-    float gk[SP], kc[SP], gn = 0.f, kn = 0.f;
+    // ---- channel work: thread tid owns channel k = tid.  Slots 0..n of the
+    // ring hold the window's tokens (slot n: the current one).
+    float gk[SP], kc[SP], gn = 0.f;
     if (tid < K) {
       const int kk = tid;
+      float acc = 0.f;  // running cumulative log decay (scalar decay)
 #pragma unroll
       for (int s = 0; s < SP; ++s) {
         gk[s] = 0.f;
         kc[s] = 0.f;
-        if (s < n) {
-          gk[s] = CHAN ? a.rg[(slot0 + s) * K + kk] : a.rg[slot0 + s];
-          kc[s] = load1<IO>(static_cast<const IO*>(a.rk) + (slot0 + s) * K + kk);
+        if (s <= n) {
+          const size_t si = (size_t)s * NI + item;
+          kc[s] = load1<IO>(static_cast<const IO*>(a.rk) + si * K + kk);
+          if constexpr (CHAN) {
+            gk[s] = (s < n) ? a.rg[si * K + kk] : ((n > 0 ? a.rg[(si - NI) * K + kk] : 0.f) + a.rla[si * K + kk]);
+          } else {
+            acc += a.rla[si];
+            gk[s] = acc;
+          }
+          if (s == n) gn = gk[s];
         }
       }
-      const float gp = (n > 0) ? (CHAN ? a.rg[(slot0 + n - 1) * K + kk] : a.rg[slot0 + n - 1]) : 0.f;
-      gn = gp + (CHAN ? a.logd[item * K + kk] : a.logd[item]);
-      kn = load1<IO>(static_cast<const IO*>(a.k) + item * K + kk);
       qs[kk] = load1<IO>(static_cast<const IO*>(a.q) + item * K + kk);
       ds[kk] = fast_exp(gn);
+      const float kn = load1<IO>(static_cast<const IO*>(a.rk) + ((size_t)n * NI + item) * K + kk);
 #pragma unroll
       for (int s = 0; s < SP; ++s) {
-        float l = 0.f;
-        if (s < n) l = fast_exp(gn - gk[s]) * kc[s];
-        else if (s == n) l = kn;
+        const float l = (s <= n) ? fast_exp(gn - gk[s]) * kc[s] : 0.f;
         Ls[s * LP + kk] = l;
         if constexpr (ERASE) {
           // b_{n,s} = <exp(g_n - g_s) . k_s, k_n>: reduce over the channels of this wave
@@ -120,27 +126,29 @@ __global__ __launch_bounds__(256) void update_kernel(const UpdateArgs a) {
     for (int idx = tid; idx < SP * V; idx += 256) {
       const int s = idx / V, v = idx % V;
       float val = 0.f;
-      if (s < n) {
-        if constexpr (ERASE) val = a.ru[(slot0 + s) * V + v];
-        else val = a.rbeta[slot0 + s] * load1<IO>(static_cast<const IO*>(a.rv) + (slot0 + s) * V + v);
-      } else if (s == n && !ERASE) {
-        val = a.beta[item] * load1<IO>(static_cast<const IO*>(a.v) + item * V + v);
+      const size_t si = (size_t)s * NI + item;
+      if constexpr (ERASE) {
+        if (s < n) val = a.ru[si * V + v];
+      } else {
+        if (s <= n) val = a.rbeta[si] * load1<IO>(static_cast<const IO*>(a.rv) + si * V + v);
       }
       Us[s * UP + v] = val;
     }
     if constexpr (ERASE) {
       for (int idx = tid; idx < SP * SP; idx += 256) {
         const int s = idx / SP, j = idx % SP;
-        Bs[idx] = (s < n && j < s) ? a.rb[(slot0 + s) * W + j] : 0.f;
+        Bs[idx] = (s < n && j < s) ? a.rb[((size_t)s * NI + item) * W + j] : 0.f;
       }
     }
     __syncthreads();
 
     if constexpr (ERASE) {
-      // b_{n,j} (current token) from the per-wave partial sums
+      const size_t cur = (size_t)n * NI + item;
+      const float beta_n = a.rbeta[cur];
+      // pseudo-value of the current token from the per-wave partial sums of b_{n,j}
       if (tid < V) {
         const int v = tid;
-        float acc = load1<IO>(static_cast<const IO*>(a.v) + item * V + v);
+        float acc = load1<IO>(static_cast<const IO*>(a.rv) + cur * V + v);
 #pragma unroll
         for (int j = 0; j < SP; ++j) {
           if (j < n) {
@@ -150,7 +158,7 @@ __global__ __launch_bounds__(256) void update_kernel(const UpdateArgs a) {
             acc -= bj * Us[j * UP + v];
           }
         }
-        Us[n * UP + v] = a.beta[item] * acc;   // u_n
+        Us[n * UP + v] = beta_n * acc;   // u_n
       }
       if (tid < K) {
         // erase factors pi_s of this channel, s = 0..n (forward substitution)
@@ -160,10 +168,8 @@ __global__ __launch_bounds__(256) void update_kernel(const UpdateArgs a) {
         for (int s = 0; s < SP; ++s) {
           pi[s] = 0.f;
           if (s <= n) {
-            const float bet = (s < n) ? a.rbeta[slot0 + s] : a.beta[item];
-            const float gs_ = (s < n) ? gk[s] : gn;
-            const float ks_ = (s < n) ? kc[s] : kn;
-            float acc = fast_exp(gs_) * ks_;
+            const float bet = a.rbeta[(size_t)s * NI + item];
+            float acc = fast_exp(gk[s]) * kc[s];
 #pragma unroll
             for (int j = 0; j < s; ++j) {
               float bj;
@@ -245,9 +251,10 @@ __global__ __launch_bounds__(256) void update_kernel(const UpdateArgs a) {
               const float w = (jj < R) ? om[(16 * kt + 4 * lg + i) * R + jj] : 0.f;
               acc = mfma4(w, xs[t][kt][i], acc);
             }
-          const int j0 = 16 * jt + 4 * lg;
-          if (j0 < R)
-            *reinterpret_cast<float4*>(a.U + (item * V + v) * R + j0) = make_float4(acc[0], acc[1], acc[2], acc[3]);
+          // 4-column panel 4 jt + lg of U[B][H][R/4][V][4]
+          if (16 * jt + 4 * lg < R)
+            reinterpret_cast<float4*>(a.U + item * (size_t)V * R)[(4 * jt + lg) * V + v] =
+                make_float4(acc[0], acc[1], acc[2], acc[3]);
         }
       }
     }

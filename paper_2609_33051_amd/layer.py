@@ -5,11 +5,13 @@ torch supplies device memory and the stream; every computation is a call
 into libsketchssm.so.  Buffers (caller-owned, as the ABI requires):
 
   S      [B][H][V][K]  fp32 full state (stored transposed: K contiguous)
-  U      [B][H][V][r]  fp32 sketch  U = S^T Omega
+  U      [B][H][r/4][V][4] fp32 sketch U = S^T Omega in 4-column panels
+         (sketch_matrix() gives the [B][H][V][r] view)
   omega  [H][K][r]     fp32 sketching matrix, coef [H][r][K] its coefficient map
-  ring   k [B][H][W][K] io, g [B][H][W] (KDA: [..][K]), beta [B][H][W];
-         Mamba-2: v [B][H][W][V] io; GDN/KDA: u [B][H][W][V], bcoef [B][H][W][W],
-         f [B][H][W][r] (sketch read) or pi [B][H][W][K] (exact baseline).
+  ring   slot-major replay buffer, [W][B][H][...]:
+         raw inputs k, v (io dtype), beta, log_decay ([..][K] for KDA), written
+         into slot n by the token's producer (write_token);
+         derived: g (KDA), u, bcoef (GDN/KDA), f (sketch read) or pi (baseline).
 """
 from __future__ import annotations
 
@@ -33,25 +35,32 @@ class SketchSSMLayer:
         self.S = S if S is not None else torch.zeros((Bt, H, V, K), dtype=f32, device=dev)
         r = 0 if baseline else rank
         self.cfg = B.make_config(kind, Bt, H, K, V, r, W, io)
-        self.cfg_flush = B.make_config(kind, Bt, H, K, V, r, W, io)
         if not baseline:
             self.omega = omega.to(dev).contiguous()
             self.coef = coef.to(dev).contiguous()
-            self.U = torch.zeros((Bt, H, V, rank), dtype=f32, device=dev)
+            self.U = torch.zeros((Bt, H, rank // 4, V, 4), dtype=f32, device=dev)
         else:
             self.omega = self.coef = self.U = None
-        self.rk = torch.zeros((Bt, H, W, K), dtype=iodt, device=dev)
-        self.rg = torch.zeros((Bt, H, W, K) if kind == "kda" else (Bt, H, W), dtype=f32, device=dev)
-        self.rbeta = torch.zeros((Bt, H, W), dtype=f32, device=dev)
-        self.rv = torch.zeros((Bt, H, W, V), dtype=iodt, device=dev) if not erase else None
-        self.ru = torch.zeros((Bt, H, W, V), dtype=f32, device=dev) if erase else None
-        self.rb = torch.zeros((Bt, H, W, W), dtype=f32, device=dev) if erase else None
-        self.rf = torch.zeros((Bt, H, W, rank), dtype=f32, device=dev) if (erase and not baseline) else None
-        self.rpi = torch.zeros((Bt, H, W, K), dtype=f32, device=dev) if (erase and baseline) else None
-        self.ring = B.make_ring(k=self.rk, v=self.rv, u=self.ru, f=self.rf, pi=self.rpi, g=self.rg,
-                                beta=self.rbeta, bcoef=self.rb)
+        # raw inputs, written by the producer of each token
+        self.rk = torch.zeros((W, Bt, H, K), dtype=iodt, device=dev)
+        self.rv = torch.zeros((W, Bt, H, V), dtype=iodt, device=dev)
+        self.rbeta = torch.zeros((W, Bt, H), dtype=f32, device=dev)
+        self.rla = torch.zeros((W, Bt, H, K) if kind == "kda" else (W, Bt, H), dtype=f32, device=dev)
+        # derived fields, written by the library
+        self.rg = torch.zeros((W, Bt, H, K), dtype=f32, device=dev) if kind == "kda" else None
+        self.ru = torch.zeros((W, Bt, H, V), dtype=f32, device=dev) if erase else None
+        self.rb = torch.zeros((W, Bt, H, W), dtype=f32, device=dev) if erase else None
+        self.rf = torch.zeros((W, Bt, H, rank), dtype=f32, device=dev) if (erase and not baseline) else None
+        self.rpi = torch.zeros((W, Bt, H, K), dtype=f32, device=dev) if (erase and baseline) else None
+        self.ring = B.make_ring(k=self.rk, v=self.rv, beta=self.rbeta, log_decay=self.rla, g=self.rg,
+                                u=self.ru, f=self.rf, pi=self.rpi, bcoef=self.rb)
         self.o = torch.zeros((Bt, H, V), dtype=f32, device=dev)
-        self.n = 0  # ring slots filled in the current window
+        self.n = 0  # slot of the next token in the current window
+
+    def sketch_matrix(self) -> torch.Tensor:
+        """The sketch as [B][H][V][r] (a copy; U itself is stored in panels)."""
+        Bt, H, V, r = self.batch, self.heads, self.dv, self.rank
+        return self.U.permute(0, 1, 3, 2, 4).reshape(Bt, H, V, r)
 
     @staticmethod
     def stream() -> int:
@@ -63,18 +72,32 @@ class SketchSSMLayer:
         if not self.baseline:
             B.sketchssm_update(self.cfg, self.S, self.omega, None, 0, None, self.U, None, self.stream())
 
-    def step(self, inp: dict, out: torch.Tensor | None = None) -> torch.Tensor:
-        """One decode token: a non-flush read (sketch, or exact full read for
-        the baseline) while the window is open, the flush on its W-th token."""
+    def write_token(self, inp: dict, slot: int | None = None):
+        """The producer's side: the token's k, v, beta and log decay go into
+        ring slot `slot` (default: the next slot of the window)."""
+        s = self.n if slot is None else slot
+        self.rk[s].copy_(inp["k"])
+        self.rv[s].copy_(inp["v"])
+        self.rbeta[s].copy_(inp["beta"])
+        self.rla[s].copy_(inp["log_decay"])
+
+    def read(self, q: torch.Tensor, out: torch.Tensor | None = None) -> torch.Tensor:
+        """One decode token whose inputs already sit in ring slot n: a non-flush
+        read (sketch, or exact full read for the baseline) while the window is
+        open, the flush on its W-th token."""
         o = self.o if out is None else out
-        st = B.make_step(inp["q"], inp["k"], inp["v"], inp["beta"], inp["log_decay"])
         if self.n == self.window - 1:
-            B.sketchssm_update(self.cfg_flush, self.S, self.omega, self.ring, self.n, st, self.U, o, self.stream())
+            B.sketchssm_update(self.cfg, self.S, self.omega, self.ring, self.n, q, self.U, o, self.stream())
             self.n = 0
         elif self.baseline:
-            B.sketchssm_full_read_baseline(self.cfg, self.S, self.ring, self.n, st, o, self.stream())
+            B.sketchssm_full_read_baseline(self.cfg, self.S, self.ring, self.n, q, o, self.stream())
             self.n += 1
         else:
-            B.sketchssm_decode(self.cfg, self.U, self.coef, self.ring, self.n, st, o, self.stream())
+            B.sketchssm_decode(self.cfg, self.U, self.coef, self.ring, self.n, q, o, self.stream())
             self.n += 1
         return o
+
+    def step(self, inp: dict, out: torch.Tensor | None = None) -> torch.Tensor:
+        """write_token + read."""
+        self.write_token(inp)
+        return self.read(inp["q"], out)

@@ -67,55 +67,58 @@ class Shape:
         return 4 * self.dk if self.kind == "kda" else 4
 
 
-def step_input_bytes(s: Shape) -> int:
-    """q, k, v in the io dtype plus beta and the log decay."""
-    return s.io_bytes * (2 * s.dk + s.dv) + 4 + s.decay_bytes
+def slot_read_bytes(s: Shape, baseline: bool = False) -> int:
+    """What a non-flush read takes from each earlier slot of the ring.
 
-
-def ring_slot_read_bytes(s: Shape, baseline: bool = False) -> int:
-    """Ring fields an earlier slot contributes to a non-flush read.
-
-    Mamba-2: raw key and value, cumulative log decay, beta.
-    GDN/KDA: raw key, pseudo-value u (fp32), cumulative log decay, and either
-    the projected erase vector f (r fp32, sketch path) or the full erase
-    factor pi (K fp32, exact full-read baseline)."""
+    Mamba-2: raw key and value, beta, log decay.
+    GDN/KDA: raw key, pseudo-value u (fp32), the projected erase vector f
+    (r fp32, sketch read) or erase factor pi (K fp32, exact baseline), and the
+    log decay (GDN) or cumulative log decay (KDA, K fp32)."""
     if not s.erase:
         return s.io_bytes * (s.dk + s.dv) + 4 + 4
     extra = 4 * s.dk if baseline else 4 * s.rank
-    return s.io_bytes * s.dk + 4 * s.dv + s.decay_bytes + extra
+    return s.io_bytes * s.dk + 4 * s.dv + extra + s.decay_bytes
 
 
-def ring_slot_write_bytes(s: Shape, n: int, baseline: bool = False) -> int:
-    """Fields written for the slot appended at position n (0-based)."""
+def current_read_bytes(s: Shape) -> int:
+    """The current token's raw inputs in ring slot n: k, v, beta, log decay."""
+    return s.io_bytes * (s.dk + s.dv) + 4 + s.decay_bytes
+
+
+def derived_write_bytes(s: Shape, n: int, baseline: bool = False) -> int:
+    """Fields a read derives and stores for slot n: GDN/KDA u, f (or pi), the
+    coupling row b_{n,.}; KDA the cumulative log decay.  Mamba-2: none."""
     if not s.erase:
-        return s.io_bytes * (s.dk + s.dv) + 4 + 4
+        return 0
     extra = 4 * s.dk if baseline else 4 * s.rank
-    return s.io_bytes * s.dk + 4 * s.dv + s.decay_bytes + 4 + extra + 4 * n
+    return 4 * s.dv + extra + 4 * n + (4 * s.dk if s.kind == "kda" else 0)
 
 
 def decode_bytes(s: Shape, n: int) -> int:
-    """Sketch read at slot n: inputs + n earlier slots + the appended slot + U + o."""
-    return (step_input_bytes(s) + n * ring_slot_read_bytes(s) + ring_slot_write_bytes(s, n)
+    """Sketch read at slot n: the query, n earlier slots, the current slot, the
+    derived fields, U (fp32) and o."""
+    return (s.io_bytes * s.dk + n * slot_read_bytes(s) + current_read_bytes(s) + derived_write_bytes(s, n)
             + 4 * s.dv * s.rank + 4 * s.dv)
 
 
 def full_read_bytes(s: Shape, n: int) -> int:
     """Exact full-state read at slot n: as decode with S (4KV) in place of U."""
-    return (step_input_bytes(s) + n * ring_slot_read_bytes(s, True) + ring_slot_write_bytes(s, n, True)
-            + 4 * s.dk * s.dv + 4 * s.dv)
+    return (s.io_bytes * s.dk + n * slot_read_bytes(s, True) + current_read_bytes(s)
+            + derived_write_bytes(s, n, True) + 4 * s.dk * s.dv + 4 * s.dv)
 
 
 def flush_bytes(s: Shape, n_buffered: int, rank: int | None = None) -> int:
-    """Flush with n_buffered earlier slots: S read + write, the ring, the
-    current token, the sketch write (rank columns) and o."""
+    """Flush of the token in slot n_buffered: S read + write, the earlier
+    slots (k, u or v, beta, decay) and their coupling rows, the current slot,
+    the query, the sketch write (rank columns) and o."""
     r = s.rank if rank is None else rank
     if s.erase:
-        slot = s.io_bytes * s.dk + 4 * s.dv + s.decay_bytes + 4
+        slot = s.io_bytes * s.dk + 4 * s.dv + 4 + s.decay_bytes
         bcoef = 4 * n_buffered * (n_buffered - 1) // 2
     else:
         slot = s.io_bytes * (s.dk + s.dv) + 4 + 4
         bcoef = 0
-    return (8 * s.dk * s.dv + n_buffered * slot + bcoef + step_input_bytes(s)
+    return (8 * s.dk * s.dv + n_buffered * slot + bcoef + current_read_bytes(s) + s.io_bytes * s.dk
             + 4 * s.dv * r + 4 * s.dv)
 
 

@@ -69,14 +69,8 @@ def cfg(**kw):
     return B.make_config(d["kind"], d["batch"], d["heads"], d["dk"], d["dv"], d["rank"], d["window"], d["io"])
 
 
-def good_step(**kw):
-    d = dict(q=ADDR, k=ADDR, v=ADDR, beta=ADDR, log_decay=ADDR)
-    d.update(kw)
-    return B.make_step(**d)
-
-
 def good_ring(**kw):
-    d = dict(k=ADDR, v=ADDR, u=ADDR, f=ADDR, pi=ADDR, g=ADDR, beta=ADDR, bcoef=ADDR)
+    d = dict(k=ADDR, v=ADDR, beta=ADDR, log_decay=ADDR, g=ADDR, u=ADDR, f=ADDR, pi=ADDR, bcoef=ADDR)
     d.update(kw)
     return B.make_ring(**d)
 
@@ -94,40 +88,44 @@ class TestValidation:
     def test_decode_rejections(self, lib):
         d = B.sketchssm_decode
         assert check_config_ok(lib)
-        assert status(d, cfg(kind=7), ADDR, ADDR, good_ring(), 0, good_step(), ADDR) == -1
-        assert status(d, cfg(dk=96), ADDR, ADDR, good_ring(), 0, good_step(), ADDR) == -2
-        assert status(d, cfg(rank=12), ADDR, ADDR, good_ring(), 0, good_step(), ADDR) == -2
-        assert status(d, cfg(window=33), ADDR, ADDR, good_ring(), 0, good_step(), ADDR) == -2
-        assert status(d, cfg(window=1), ADDR, ADDR, good_ring(), 0, good_step(), ADDR) == -1
-        assert status(d, cfg(), ADDR, ADDR, good_ring(), 15, good_step(), ADDR) == -4
-        assert status(d, cfg(), ADDR, ADDR, good_ring(), -1, good_step(), ADDR) == -4
-        assert status(d, cfg(), ADDR + 4, ADDR, good_ring(), 0, good_step(), ADDR) == -3
-        assert status(d, cfg(), ADDR, ADDR, good_ring(), 0, good_step(q=ADDR + 8), ADDR) == -3
-        assert status(d, cfg(), ADDR, ADDR, good_ring(v=None), 0, good_step(), ADDR) == -1
-        assert status(d, cfg(kind="gdn", dv=128), ADDR, ADDR, good_ring(f=None), 0, good_step(), ADDR) == -1
-        assert status(d, cfg(), None, ADDR, good_ring(), 0, good_step(), ADDR) == -1
-        assert status(d, cfg(batch=0), ADDR, ADDR, good_ring(), 0, good_step(), ADDR) == -1
-        assert status(d, cfg(io=5), ADDR, ADDR, good_ring(), 0, good_step(), ADDR) == -1
+        assert status(d, cfg(kind=7), ADDR, ADDR, good_ring(), 0, ADDR, ADDR) == -1
+        assert status(d, cfg(dk=96), ADDR, ADDR, good_ring(), 0, ADDR, ADDR) == -2
+        assert status(d, cfg(rank=12), ADDR, ADDR, good_ring(), 0, ADDR, ADDR) == -2
+        assert status(d, cfg(window=33), ADDR, ADDR, good_ring(), 0, ADDR, ADDR) == -2
+        assert status(d, cfg(window=1), ADDR, ADDR, good_ring(), 0, ADDR, ADDR) == -1
+        assert status(d, cfg(), ADDR, ADDR, good_ring(), 15, ADDR, ADDR) == -4
+        assert status(d, cfg(), ADDR, ADDR, good_ring(), -1, ADDR, ADDR) == -4
+        assert status(d, cfg(), ADDR + 4, ADDR, good_ring(), 0, ADDR, ADDR) == -3
+        assert status(d, cfg(), ADDR, ADDR, good_ring(), 0, ADDR + 8, ADDR) == -3
+        assert status(d, cfg(), ADDR, ADDR, good_ring(v=None), 0, ADDR, ADDR) == -1
+        assert status(d, cfg(), ADDR, ADDR, good_ring(log_decay=ADDR + 4), 0, ADDR, ADDR) == -3
+        assert status(d, cfg(kind="kda", dv=128), ADDR, ADDR, good_ring(g=None), 0, ADDR, ADDR) == -1
+        assert status(d, cfg(), ADDR, ADDR, good_ring(), 0, None, ADDR) == -1
+        assert status(d, cfg(kind="gdn", dv=128), ADDR, ADDR, good_ring(f=None), 0, ADDR, ADDR) == -1
+        assert status(d, cfg(), None, ADDR, good_ring(), 0, ADDR, ADDR) == -1
+        assert status(d, cfg(batch=0), ADDR, ADDR, good_ring(), 0, ADDR, ADDR) == -1
+        assert status(d, cfg(io=5), ADDR, ADDR, good_ring(), 0, ADDR, ADDR) == -1
         assert "n_buffered" in B.sketchssm_status_string(-4)
 
     def test_update_rejections(self, lib):
         u = B.sketchssm_update
-        assert status(u, cfg(), ADDR, ADDR, good_ring(), 16, good_step(), ADDR, ADDR) == -4
+        assert status(u, cfg(), ADDR, ADDR, good_ring(), 16, ADDR, ADDR, ADDR) == -4
         assert status(u, cfg(), ADDR, ADDR, None, 3, None, ADDR, None) == -4          # sketch-only needs n = 0
+        assert status(u, cfg(), ADDR, ADDR, good_ring(), 3, ADDR + 4, ADDR, None) == -3  # misaligned query
         assert status(u, cfg(rank=0), ADDR, None, None, 0, None, None, None) == -1   # sketch-only needs rank
-        assert status(u, cfg(), None, ADDR, good_ring(), 15, good_step(), ADDR, ADDR) == -1
-        assert status(u, cfg(), ADDR, None, good_ring(), 15, good_step(), ADDR, ADDR) == -1
-        assert status(u, cfg(kind="kda", dv=128), ADDR, ADDR, good_ring(u=None), 15, good_step(), ADDR, ADDR) == -1
-        assert status(u, cfg(), ADDR, ADDR, None, 15, good_step(), ADDR, ADDR) == -1  # ring needed when n > 0
-        assert status(u, cfg(), ADDR, ADDR, good_ring(), 15, good_step(), ADDR, ADDR + 2) == -3
+        assert status(u, cfg(), None, ADDR, good_ring(), 15, ADDR, ADDR, ADDR) == -1
+        assert status(u, cfg(), ADDR, None, good_ring(), 15, ADDR, ADDR, ADDR) == -1
+        assert status(u, cfg(kind="kda", dv=128), ADDR, ADDR, good_ring(u=None), 15, ADDR, ADDR, ADDR) == -1
+        assert status(u, cfg(), ADDR, ADDR, None, 15, ADDR, ADDR, ADDR) == -1  # ring needed when n > 0
+        assert status(u, cfg(), ADDR, ADDR, good_ring(), 15, ADDR, ADDR, ADDR + 2) == -3
 
     def test_full_read_rejections(self, lib):
         f = B.sketchssm_full_read_baseline
-        assert status(f, cfg(kind="gdn", dv=128), ADDR, good_ring(pi=None), 0, good_step(), ADDR) == -1
-        assert status(f, cfg(), ADDR, good_ring(), 15, good_step(), ADDR) == -4
+        assert status(f, cfg(kind="gdn", dv=128), ADDR, good_ring(pi=None), 0, ADDR, ADDR) == -1
+        assert status(f, cfg(), ADDR, good_ring(), 15, ADDR, ADDR) == -4
         assert "n_buffered" in B.sketchssm_last_error()
-        assert status(f, cfg(), None, good_ring(), 0, good_step(), ADDR) == -1
-        assert status(f, cfg(dv=32), ADDR, good_ring(), 0, good_step(), ADDR) == -2
+        assert status(f, cfg(), None, good_ring(), 0, ADDR, ADDR) == -1
+        assert status(f, cfg(dv=32), ADDR, good_ring(), 0, ADDR, ADDR) == -2
 
 
 def check_config_ok(lib):

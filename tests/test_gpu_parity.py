@@ -42,7 +42,7 @@ def check(wl, window=None, rank=None, steps=None, sel=None, omega_coef=None, bas
     errS = rel_l2(to_np32(layer.S.reshape(n_items, wl.dv, wl.dk)[idx]), ref.S_final)
     errU = 0.0
     if not baseline:
-        errU = rel_l2(to_np32(layer.U.reshape(n_items, wl.dv, rank)[idx]), ref.U_final)
+        errU = rel_l2(to_np32(layer.sketch_matrix().reshape(n_items, wl.dv, rank)[idx]), ref.U_final)
     print(f"  max step rel-L2 {err:.3e}  state {errS:.3e}  sketch {errU:.3e}", flush=True)
     tol = TOL[wl.io]
     assert err <= tol and errS <= tol and errU <= tol

@@ -32,9 +32,19 @@ def test_reduction_limits():
 
 
 def test_algorithmic_bytes_mamba2_decode():
-    # Mamba-2 decode layer, bf16 io, fp32 U: 8,136 bytes per item averaged over the window
+    # Mamba-2 decode layer, bf16 io, fp32 U: per item the query (256 B), slots
+    # 0..n of the ring (392 B each: k, v, beta, log decay), U (4 KiB) and o (256 B)
     s = traffic.Shape("mamba2", 128, 64, 16, 16, 2)
     wb = traffic.window_bytes(s)
     assert len(wb["nonflush"]) == 15
-    assert wb["nonflush_mean"] == pytest.approx(8136.0)
+    assert traffic.decode_bytes(s, 0) == 256 + 392 + 4096 + 256
+    assert wb["nonflush_mean"] == pytest.approx(256 + 8 * 392 + 4096 + 256)
     assert traffic.full_read_bytes(s, 0) - traffic.decode_bytes(s, 0) == 4 * 128 * 64 - 4 * 64 * 16
+
+
+def test_algorithmic_bytes_gdn_decode():
+    s = traffic.Shape("gdn", 128, 128, 16, 16, 2)
+    # slot 0: q 256, current k, v 512 + beta 4 + log decay 4, derived u 512 + f 64, U 8 KiB, o 512
+    assert traffic.decode_bytes(s, 0) == 256 + 520 + 576 + 8192 + 512
+    # each earlier slot adds k 256 + u 512 + f 64 + log decay 4 = 836, and one coupling (4 B)
+    assert traffic.decode_bytes(s, 3) - traffic.decode_bytes(s, 2) == 836 + 4

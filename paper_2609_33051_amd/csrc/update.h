@@ -1,25 +1,29 @@
 // Flush step of SketchSSM (Algorithm 1, t = W; Sec. 4.1, per-window sketch)
 // and the initial sketch: one read and one write of the full state.
 //
-// With n ring slots plus the current token (nt = n + 1 tokens) and the
-// window-local cumulative log decay g (g_n of the last token):
+// With the window's tokens in ring slots 0..n (slot n: the current token),
+// cumulative log decays g_s and c_s = exp(g_n - g_s):
 //   L[s]   = exp(g_n - g_s) . k_s                  (left factors l_s(W), Appendix C.1)
 //   pi_s   = beta_s (e^{g_s} . k_s - sum_{j<s} b_{s,j} pi_j)           (eq. wy)
 //   w_s    = u_s - X_0 pi_s                         (true write vectors; Mamba-2: beta_s v_s)
-//   X_W    = X_0 Diag(e^{g_n}) + sum_s w_s L[s]^T   (eq. update in rank-nt form)
+//   X_W    = X_0 Diag(e^{g_n}) + sum_s w_s L[s]^T   (eq. update in rank-(n+1) form)
 //   o_W    = X_W q_W,   U = X_W Omega
-// where X = S^T is the stored [V][K] state.  The two contractions over the
-// state (X_0 Pi^T, K-deep; the rank-nt update, W-deep) and the sketch
+// where X = S^T is the stored [V][K] state.  For a scalar decay c_s is one
+// number per slot and moves to the value side (w_s L[s]^T = (c_s w_s) k_s^T),
+// so the raw keys are the matrix-core operand.  The two contractions over the
+// state (X_0 Pi^T, K-deep; the rank-(n+1) update, slot-deep) and the sketch
 // projection X_W Omega run on fp32 matrix cores (v_mfma_f32_16x16x4f32).
 //
-// Mapping: one workgroup (4 waves) per (request, head) item; each wave owns
-// 16-column value tiles of X^T (K rows x 16 values).  The state tile is held
-// in MFMA accumulator layout: lane l holds X[v0 + l%16][16 kt + 4 (l/16) + i],
+// Mapping: one workgroup (4 waves) per (request, head) item.  The window's
+// slots are staged into LDS with wide loads (row layout: four slots per load
+// instruction, wave w taking slot groups w, w + 4, ...).  Each wave owns
+// 16-column value tiles of X^T (K rows x 16 values), held in MFMA
+// accumulator layout: lane l holds X[v0 + l%16][16 kt + 4 (l/16) + i],
 // i = 0..3, a 16-byte contiguous piece of a state row.  Because the
 // contraction index of the K-deep products may be visited in any order, the
 // same registers serve as the B operand of X_0 Pi^T and X_W Omega (step i of
 // k-tile kt contracts over k = 16 kt + 4 g + i for lane group g) and as the
-// accumulator of the rank-nt update, so the state never leaves registers
+// accumulator of the rank update, so the state never leaves registers
 // between its load and its store.
 #pragma once
 
@@ -45,23 +49,28 @@ __global__ __launch_bounds__(256) void update_kernel(const UpdateArgs a) {
   constexpr int VTW = (VT + 3) / 4;   // value tiles per wave
   constexpr int SP = WMAX;            // slot rows (16 or 32)
   constexpr int ST = SP / 16;         // slot tiles
+  constexpr int NG = SP / 4;          // slot groups of four
   constexpr int RT = (R + 15) / 16;   // sketch tiles
+  constexpr int KPL = K / 16;         // key channels per lane (row layout)
+  constexpr int VR = V / 16;          // value channels per lane (row layout)
   constexpr int LP = K + 4;           // LDS pitches chosen so that the 4 lane
   constexpr int PP = SP + 4;          // groups of an operand read land in
   constexpr int UP = V + 4;           // different banks
   constexpr int KW = (K + 63) / 64;   // waves that carry channel work
 
-  __shared__ __align__(16) float Ls[SP * LP];                 // L[s][k]
+  __shared__ __align__(16) float Ls[SP * LP];                 // keys k_s (KDA: then L[s]), [s][k]
   __shared__ __align__(16) float PiT[ERASE ? K * PP : 4];     // Pi^T[k][s]
-  __shared__ __align__(16) float Us[SP * UP];                 // w-vector source: u_s[v]
+  __shared__ __align__(16) float Us[SP * UP];                 // c_s beta_s v_s (Mamba-2) or u_s
   __shared__ float Bs[ERASE ? SP * SP : 1];                   // b_{s,j}
   __shared__ float bpart[ERASE ? KW * SP : 1];                // partial sums of b_{n,j}
   __shared__ __align__(16) float qs[K];
-  __shared__ __align__(16) float ds[K];
+  __shared__ __align__(16) float ds[CHAN ? K : 4];            // e^{g_n} per channel (KDA)
+  __shared__ float csc[SP];                                   // c_s (scalar decay)
 
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const int lr = lane & 15, lg = lane >> 4;
+  const int lr = lane & 15, lg = lane >> 4;   // MFMA lane coordinates
+  const int row = lg, col = lr;               // row-layout coordinates (same lanes)
   const int H = a.H, W = a.W, n = a.n;
   const size_t item = blockIdx.x;
   const int h = (int)(item % (size_t)H);
@@ -83,56 +92,108 @@ __global__ __launch_bounds__(256) void update_kernel(const UpdateArgs a) {
     }
   }
 
+  float egn = 1.f;  // e^{g_n} (scalar decay)
   if (flush) {
-    // ---- channel work: thread tid owns channel k = tid.  Slots 0..n of the
-    // ring hold the window's tokens (slot n: the current one).
-    float gk[SP], kc[SP], gn = 0.f;
-    if (tid < K) {
-      const int kk = tid;
-      float acc = 0.f;  // running cumulative log decay (scalar decay)
+    // ---- per-slot scalars, uniform in every wave: beta_s and (scalar decay)
+    // the cumulative log decay g_s, summed in slot order
+    float bsv[SP], gsv[SP];
+    {
+      float acc = 0.f;
 #pragma unroll
       for (int s = 0; s < SP; ++s) {
-        gk[s] = 0.f;
-        kc[s] = 0.f;
+        bsv[s] = 0.f;
+        gsv[s] = 0.f;
         if (s <= n) {
           const size_t si = (size_t)s * NI + item;
-          kc[s] = load1<IO>(static_cast<const IO*>(a.rk) + si * K + kk);
-          if constexpr (CHAN) {
-            gk[s] = (s < n) ? a.rg[si * K + kk] : ((n > 0 ? a.rg[(si - NI) * K + kk] : 0.f) + a.rla[si * K + kk]);
-          } else {
+          bsv[s] = a.rbeta[si];
+          if constexpr (!CHAN) {
             acc += a.rla[si];
-            gk[s] = acc;
-          }
-          if (s == n) gn = gk[s];
-        }
-      }
-      qs[kk] = load1<IO>(static_cast<const IO*>(a.q) + item * K + kk);
-      ds[kk] = fast_exp(gn);
-      const float kn = load1<IO>(static_cast<const IO*>(a.rk) + ((size_t)n * NI + item) * K + kk);
-#pragma unroll
-      for (int s = 0; s < SP; ++s) {
-        const float l = (s <= n) ? fast_exp(gn - gk[s]) * kc[s] : 0.f;
-        Ls[s * LP + kk] = l;
-        if constexpr (ERASE) {
-          // b_{n,s} = <exp(g_n - g_s) . k_s, k_n>: reduce over the channels of this wave
-          if (s < n) {
-            const float bsum = wave_sum(l * kn);
-            if (lane == 0) bpart[wave * SP + s] = bsum;
+            gsv[s] = acc;
           }
         }
       }
     }
-    // ---- value-side staging: u_s (Mamba-2: beta_s v_s), b_{s,j}
-    for (int idx = tid; idx < SP * V; idx += 256) {
-      const int s = idx / V, v = idx % V;
-      float val = 0.f;
-      const size_t si = (size_t)s * NI + item;
-      if constexpr (ERASE) {
-        if (s < n) val = a.ru[si * V + v];
-      } else {
-        if (s <= n) val = a.rbeta[si] * load1<IO>(static_cast<const IO*>(a.rv) + si * V + v);
+    float gn = 0.f, bn = 0.f;
+#pragma unroll
+    for (int s = 0; s < SP; ++s)
+      if (s == n) {
+        gn = gsv[s];
+        bn = bsv[s];
       }
-      Us[s * UP + v] = val;
+    if constexpr (!CHAN) egn = fast_exp(gn);
+    // KDA: per-channel cumulative log decays, thread tid owns channel tid
+    float gk[CHAN ? SP : 1];
+    if constexpr (CHAN) {
+      if (tid < K) {
+#pragma unroll
+        for (int s = 0; s < SP; ++s) {
+          gk[s] = 0.f;
+          if (s <= n) {
+            const size_t si = (size_t)s * NI + item;
+            gk[s] = (s < n) ? a.rg[si * K + tid] : ((n > 0 ? a.rg[(si - NI) * K + tid] : 0.f) + a.rla[si * K + tid]);
+          }
+        }
+      }
+    }
+
+    // ---- stage the window with wide loads: row r of wave w holds slot 4 gi + r
+#pragma unroll
+    for (int gq = 0; gq < NG / 4; ++gq) {
+      const int gi = wave + 4 * gq;  // slot group of this wave (wave-uniform)
+      const int s = 4 * gi + row;
+      const size_t si = (size_t)s * NI + item;
+      float ksv[KPL], vsv[VR];
+#pragma unroll
+      for (int m = 0; m < KPL; ++m) ksv[m] = 0.f;
+#pragma unroll
+      for (int m = 0; m < VR; ++m) vsv[m] = 0.f;
+      if (s <= n) {
+        Raw<IO, KPL> kr;
+        kr.load(static_cast<const IO*>(a.rk) + si * K + col * KPL);
+#pragma unroll
+        for (int m = 0; m < KPL; ++m) ksv[m] = kr.get(m);
+        if (ERASE && s < n) {
+          Vec<VR> ur;
+          ur.load(a.ru + si * V + col * VR);
+#pragma unroll
+          for (int m = 0; m < VR; ++m) vsv[m] = ur.e[m];
+        } else {
+          // raw value: Mamba-2 scales it into c_s beta_s v_s; GDN/KDA keep v_n
+          // in row n until u_n is formed
+          Raw<IO, VR> vr;
+          vr.load(static_cast<const IO*>(a.rv) + si * V + col * VR);
+          float sc = 1.f;
+          if constexpr (!ERASE) {
+            // select this row's slot from the wave-uniform tables (compile-time indices only)
+            float gs = 0.f, bs = 0.f;
+#pragma unroll
+            for (int j = 0; j < SP; ++j)
+              if (j == s) {
+                gs = gsv[j];
+                bs = bsv[j];
+              }
+            sc = bs * fast_exp(gn - gs);
+          }
+#pragma unroll
+          for (int m = 0; m < VR; ++m) vsv[m] = sc * vr.get(m);
+        }
+      }
+#pragma unroll
+      for (int m = 0; m < KPL; m += 4)
+        *reinterpret_cast<float4*>(&Ls[s * LP + col * KPL + m]) = make_float4(ksv[m], ksv[m + 1], ksv[m + 2], ksv[m + 3]);
+#pragma unroll
+      for (int m = 0; m < VR; m += 4)
+        *reinterpret_cast<float4*>(&Us[s * UP + col * VR + m]) = make_float4(vsv[m], vsv[m + 1], vsv[m + 2], vsv[m + 3]);
+    }
+    if (tid < K) qs[tid] = load1<IO>(static_cast<const IO*>(a.q) + item * K + tid);
+    if constexpr (!CHAN) {
+      if (tid < SP) {
+        float c = 0.f;
+#pragma unroll
+        for (int j = 0; j < SP; ++j)
+          if (j == tid && j <= n) c = fast_exp(gn - gsv[j]);
+        csc[tid] = c;
+      }
     }
     if constexpr (ERASE) {
       for (int idx = tid; idx < SP * SP; idx += 256) {
@@ -143,12 +204,50 @@ __global__ __launch_bounds__(256) void update_kernel(const UpdateArgs a) {
     __syncthreads();
 
     if constexpr (ERASE) {
-      const size_t cur = (size_t)n * NI + item;
-      const float beta_n = a.rbeta[cur];
-      // pseudo-value of the current token from the per-wave partial sums of b_{n,j}
+      // ---- channel work: thread tid owns channel k = tid.  Ls holds raw keys.
+      float pi[SP], kn = 0.f;
+      if (tid < K) {
+        const int kk = tid;
+        kn = Ls[n * LP + kk];
+        float gnk = gn;
+        if constexpr (CHAN) {
+#pragma unroll
+          for (int s = 0; s < SP; ++s)
+            if (s == n) gnk = gk[s];
+        }
+        // erase factors pi_s, s < n, by forward substitution over the stored couplings
+#pragma unroll
+        for (int s = 0; s < SP; ++s) {
+          pi[s] = 0.f;
+          if (s < n) {
+            float acc = fast_exp(CHAN ? gk[s] : gsv[s]) * Ls[s * LP + kk];
+#pragma unroll
+            for (int j = 0; j < s; ++j) acc -= Bs[s * SP + j] * pi[j];
+            pi[s] = bsv[s] * acc;
+          }
+        }
+        // b_{n,s} = <exp(g_n - g_s) . k_s, k_n>: partial sums over this wave's channels
+#pragma unroll
+        for (int s = 0; s < SP; ++s) {
+          if (s < n) {
+            const float e = CHAN ? fast_exp(gnk - gk[s]) : csc[s];
+            const float bsum = wave_sum(e * Ls[s * LP + kk] * kn);
+            if (lane == 0) bpart[wave * SP + s] = bsum;
+          }
+        }
+        if constexpr (CHAN) {
+          // left factors L[s] = exp(g_n - g_s) k_s replace the keys in place
+          ds[kk] = fast_exp(gnk);
+#pragma unroll
+          for (int s = 0; s < SP; ++s)
+            if (s < n) Ls[s * LP + kk] *= fast_exp(gnk - gk[s]);
+        }
+      }
+      __syncthreads();
+      // ---- the current token: u_n and pi_n need b_{n,j} from every wave
       if (tid < V) {
         const int v = tid;
-        float acc = load1<IO>(static_cast<const IO*>(a.rv) + cur * V + v);
+        float acc = Us[n * UP + v];  // raw v_n
 #pragma unroll
         for (int j = 0; j < SP; ++j) {
           if (j < n) {
@@ -158,34 +257,29 @@ __global__ __launch_bounds__(256) void update_kernel(const UpdateArgs a) {
             acc -= bj * Us[j * UP + v];
           }
         }
-        Us[n * UP + v] = beta_n * acc;   // u_n
+        Us[n * UP + v] = bn * acc;  // u_n
       }
       if (tid < K) {
-        // erase factors pi_s of this channel, s = 0..n (forward substitution)
         const int kk = tid;
-        float pi[SP];
+        float gnk = gn;
+        if constexpr (CHAN) {
 #pragma unroll
-        for (int s = 0; s < SP; ++s) {
-          pi[s] = 0.f;
-          if (s <= n) {
-            const float bet = a.rbeta[(size_t)s * NI + item];
-            float acc = fast_exp(gk[s]) * kc[s];
-#pragma unroll
-            for (int j = 0; j < s; ++j) {
-              float bj;
-              if (s < n) {
-                bj = Bs[s * SP + j];
-              } else {
-                bj = 0.f;
-#pragma unroll
-                for (int w = 0; w < KW; ++w) bj += bpart[w * SP + j];
-              }
-              acc -= bj * pi[j];
-            }
-            pi[s] = bet * acc;
-          }
-          PiT[kk * PP + s] = pi[s];
+          for (int s = 0; s < SP; ++s)
+            if (s == n) gnk = gk[s];
         }
+        float acc = fast_exp(gnk) * kn;
+#pragma unroll
+        for (int j = 0; j < SP; ++j) {
+          if (j < n) {
+            float bj = 0.f;
+#pragma unroll
+            for (int w = 0; w < KW; ++w) bj += bpart[w * SP + j];
+            acc -= bj * pi[j];
+          }
+        }
+        const float pin = bn * acc;
+#pragma unroll
+        for (int s = 0; s < SP; ++s) PiT[kk * PP + s] = (s < n) ? pi[s] : (s == n ? pin : 0.f);
       }
       __syncthreads();
     }
@@ -198,12 +292,13 @@ __global__ __launch_bounds__(256) void update_kernel(const UpdateArgs a) {
     if (vt >= VT) continue;
     const int v = 16 * vt + lr;
     if (flush) {
-      // w-vectors W^T[s][v] = u_s[v] - (Pi X_0^T)[s][v]   (C layout: s = 16 st + 4 lg + i)
+      // value-side factors of the rank update, C layout: slot s = 16 st + 4 lg + i
       floatx4 wv[ST];
 #pragma unroll
       for (int st = 0; st < ST; ++st) {
         floatx4 acc = {0.f, 0.f, 0.f, 0.f};
         if constexpr (ERASE) {
+          // w_s = u_s - (Pi X_0^T)[s]
 #pragma unroll
           for (int kt = 0; kt < MT; ++kt)
 #pragma unroll
@@ -211,14 +306,19 @@ __global__ __launch_bounds__(256) void update_kernel(const UpdateArgs a) {
               acc = mfma4(PiT[(16 * kt + 4 * lg + i) * PP + 16 * st + lr], xs[t][kt][i], acc);
         }
 #pragma unroll
-        for (int i = 0; i < 4; ++i) wv[st][i] = Us[(16 * st + 4 * lg + i) * UP + v] - acc[i];
+        for (int i = 0; i < 4; ++i) {
+          const int s = 16 * st + 4 * lg + i;
+          float w = Us[s * UP + v] - acc[i];
+          if constexpr (ERASE && !CHAN) w *= csc[s];  // GDN: c_s w_s
+          wv[st][i] = w;
+        }
       }
-      // X_W^T = Diag(e^{g_n}) X_0^T + L^T W^T   (accumulates onto the decayed state)
+      // X_W^T = Diag(e^{g_n}) X_0^T + (keys or L)^T W^T, accumulated onto the decayed state
 #pragma unroll
       for (int kt = 0; kt < MT; ++kt) {
         floatx4 acc;
 #pragma unroll
-        for (int i = 0; i < 4; ++i) acc[i] = xs[t][kt][i] * ds[16 * kt + 4 * lg + i];
+        for (int i = 0; i < 4; ++i) acc[i] = xs[t][kt][i] * (CHAN ? ds[16 * kt + 4 * lg + i] : egn);
 #pragma unroll
         for (int st = 0; st < ST; ++st)
 #pragma unroll

@@ -100,35 +100,40 @@ def main():
         torch.cuda.synchronize()
         return layers
 
-    def run(layers, n_tokens, record):
-        """n_tokens decode tokens through every layer; with `record`, HIP events
-        bracket every launch on the launch stream."""
-        ev = []
+    def run(layers, n_tokens, events=None):
+        """n_tokens decode tokens through every layer, from calls marshalled
+        once per (slot, layer).  The L launches of one token are the same
+        kernel at the same slot, back to back on one stream; with `events`, a
+        pre-created pair of HIP events brackets each such group."""
+        plan = [[lay.prepared_read(pool[t]["q"], t) for lay in layers] for t in range(W)]
+        stream = torch.cuda.current_stream()
         for t in range(n_tokens):
-            q = pool[t % W]["q"]
-            for lay in layers:
-                n = lay.n
-                if record:
-                    e0 = torch.cuda.Event(enable_timing=True)
-                    e1 = torch.cuda.Event(enable_timing=True)
-                    e0.record()
-                lay.read(q)
-                if record:
-                    e1.record()
-                    ev.append((n, e0, e1))
-        return ev
+            if events is not None:
+                events[t][1].record(stream)
+            for call in plan[t % W]:
+                call()
+            if events is not None:
+                events[t][2].record(stream)
+        for lay in layers:
+            lay.n = n_tokens % W
 
     def timed(baseline):
         layers = make_layers(baseline)
-        run(layers, warm, False)
+        stream = torch.cuda.current_stream()
+        events = [(t % W, torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+                  for t in range(K_steps)]
+        for _, e0, e1 in events:  # create the HIP events before the timed region
+            e0.record(stream)
+            e1.record(stream)
+        run(layers, warm, None)
         torch.cuda.synchronize()
         t0 = time.perf_counter()
-        ev = run(layers, K_steps, True)
+        run(layers, K_steps, events)
         torch.cuda.synchronize()
         elapsed = time.perf_counter() - t0
-        per_n = {}
-        for n, e0, e1 in ev:
-            per_n.setdefault(n, []).append(e0.elapsed_time(e1) * 1e-3)
+        per_n = {}  # slot -> per-launch seconds, one entry per token (group of L launches)
+        for n, e0, e1 in events:
+            per_n.setdefault(n, []).append(e0.elapsed_time(e1) * 1e-3 / L)
         del layers
         torch.cuda.empty_cache()
         return elapsed, per_n
@@ -138,6 +143,7 @@ def main():
     layer_steps = K_steps * L
     value = layer_steps / elapsed
     dec_n = [n for n in per_n if n < W - 1]
+    traffic_rec = recorded_traffic("decode", wl, rank, W)
     dec_time = sum(sum(per_n[n]) for n in dec_n)
     dec_launches = sum(len(per_n[n]) for n in dec_n)
     dec_bytes = sum(traffic.decode_bytes(shape, n) * items * len(per_n[n]) for n in dec_n)
@@ -173,7 +179,7 @@ def main():
             "peak": traffic.HBM_PEAK_GBPS,
             "unit": "GB/s",
             "frac": round(dec_gbps / traffic.HBM_PEAK_GBPS, 4),
-            "traffic": None,
+            "traffic": traffic_rec and traffic_rec["bytes_per_launch"],
             "bytes_per_launch": int(dec_bytes_per_launch),
             "mean_launch_us": round(dec_mean_s * 1e6, 2),
         },
@@ -219,8 +225,8 @@ def main():
         n = 1 << 28  # 1 GiB of fp32
         a = torch.empty(n, dtype=torch.float32, device=dev).fill_(1.0)
         b = torch.empty_like(a)
-        for _ in range(3):
-            b.copy_(a)
+        for _ in range(3):  # a streaming kernel named neg_kernel: reads 1 GiB, writes 1 GiB
+            torch.neg(a, out=b)
         torch.cuda.synchronize()
         out["copy_calibration_bytes"] = 2 * n * 4
 
@@ -231,9 +237,32 @@ def main():
     return 0
 
 
+def recorded_traffic(entry, wl, rank, W):
+    """HBM bytes per launch of the `entry` kernel ("decode", ...) on this
+    workload, from the FETCH_SIZE and WRITE_SIZE counter runs recorded under
+    profiles/, each scaled by the factor a plain copy kernel's counters gave
+    in the same runs.  None when no run was recorded for this configuration
+    or the kernel's sources have changed since (their digest differs)."""
+    from paper_2609_33051_amd import build as hip_build
+
+    path = os.path.join(os.path.dirname(os.path.abspath(__file__)), "profiles", "traffic.json")
+    if not os.path.exists(path):
+        return None
+    with open(path) as f:
+        table = json.load(f)
+    unit = f"{entry}_{wl.kind}"
+    rec = table.get(f"{unit}:{wl.name}:r{rank}:w{W}")
+    if rec is None or rec.get("digest") != hip_build.source_digest(unit):
+        return None
+    b = rec["fetch_kib"] * 1024 * rec["fetch_scale"] + rec["write_kib"] * 1024 * rec["write_scale"]
+    return {"bytes_per_launch": int(round(b)), "record": rec}
+
+
 def cpu_baseline(wl, rank, W, target_s, dev):
-    """The oracle (plain fp64, one item at a time) on the host cores, on a
-    sample of items over one window, scaled to steps/s per layer."""
+    """The oracle (plain fp64 C, items spread over the host threads) on every
+    item of the workload, for as many consecutive windows as fill about
+    `target_s` seconds (the state carries from window to window), scaled to
+    steps/s per layer."""
     import numpy as np
     import torch
 
@@ -243,34 +272,35 @@ def cpu_baseline(wl, rank, W, target_s, dev):
     items = wl.items
     threads = oracle.max_threads()
     om, C = inputs.omega(wl, rank)
+    heads = (np.arange(items) % wl.heads).astype(np.int32)
+    host = lambda x, w: x.reshape(items, w).to("cpu", torch.float32).numpy()
     pool = [inputs.step_inputs(wl, t, dev) for t in range(W)]
-    S = inputs.initial_state(wl, dev)
+    q = np.stack([host(p["q"], wl.dk) for p in pool])
+    k = np.stack([host(p["k"], wl.dk) for p in pool])
+    v = np.stack([host(p["v"], wl.dv) for p in pool])
+    beta = np.stack([host(p["beta"], 1)[:, 0] for p in pool])
+    ld = np.stack([host(p["log_decay"], wl.dk if wl.kind == "kda" else 1) for p in pool])
+    if wl.kind != "kda":
+        ld = ld[:, :, 0]
+    S0 = inputs.initial_state(wl, dev).reshape(items, wl.dv, wl.dk).cpu().numpy()
+    del pool
 
-    def sample(n_sel):
-        sel = torch.arange(n_sel, device=dev) * (items // n_sel)
-        cut = lambda x: x.reshape(items, -1)[sel].to("cpu", torch.float32).numpy()
-        q = np.stack([cut(p["q"]) for p in pool])
-        k = np.stack([cut(p["k"]) for p in pool])
-        v = np.stack([cut(p["v"]) for p in pool])
-        beta = np.stack([cut(p["beta"])[:, 0] for p in pool])
-        ld = np.stack([cut(p["log_decay"]) for p in pool])
-        if wl.kind != "kda":
-            ld = ld[:, :, 0]
-        S0 = S.reshape(items, wl.dv, wl.dk)[sel].cpu().numpy()
-        heads = (sel.cpu().numpy() % wl.heads).astype(np.int32)
+    def windows(n_win, S):
         t0 = time.perf_counter()
-        oracle.sketchssm(wl.kind, W, heads, om, C, S0, q, k, v, beta, ld, round_storage=True, diagnostics=False)
-        return time.perf_counter() - t0
+        for _ in range(n_win):
+            S = oracle.sketchssm(wl.kind, W, heads, om, C, S, q, k, v, beta, ld, round_storage=True,
+                                 diagnostics=False).S_final
+        return time.perf_counter() - t0, S
 
-    n_sel = max(threads, 16)
-    dt = sample(n_sel)
-    n_sel = int(min(items, max(n_sel, n_sel * target_s / max(dt, 1e-3))))
-    dt = sample(n_sel)
-    per_item_step = dt / (n_sel * W)
-    return {"value": round(1.0 / (per_item_step * items), 4), "unit": "steps/s", "cores": threads,
-            "kind": "oracle",
-            "sample": f"{n_sel} of {items} (request, head) items x one window of {W} steps, "
-                      f"{dt:.1f} s wall, scaled linearly to all items (items are independent)"}
+    dt, S1 = windows(1, S0)
+    n_win = 1
+    if dt < 0.5 * target_s:  # too short to time alone: run enough further windows
+        n_win = int(min(64, max(1, round(target_s / max(dt, 1e-3)))))
+        dt, _ = windows(n_win, S1)
+    steps = n_win * W
+    return {"value": round(steps / dt, 4), "unit": "steps/s", "cores": threads, "kind": "oracle",
+            "sample": f"all {items} (request, head) items x {n_win} consecutive windows of {W} steps "
+                      f"({steps} decode steps), {dt:.1f} s wall on {threads} threads"}
 
 
 if __name__ == "__main__":

@@ -93,6 +93,48 @@ def _check(rc: int):
         raise SketchSSMError(rc, load().sketchssm_last_error().decode())
 
 
+class Prepared:
+    """One entry-point call with its arguments marshalled once, so that a
+    caller replaying the same launch (a decode loop over resident buffers)
+    pays only the foreign call.  The Config and Ring it points to are kept
+    alive with it."""
+
+    __slots__ = ("fn", "args", "keep")
+
+    def __init__(self, fn, args, keep):
+        self.fn, self.args, self.keep = fn, args, keep
+
+    def __call__(self):
+        rc = self.fn(*self.args)
+        if rc:
+            _check(rc)
+
+
+def _vp(x):
+    p = ptr(x)
+    return None if p is None else ctypes.c_void_p(p)
+
+
+def prepare_update(cfg: Config, S, omega, ring: Ring | None, n_buffered: int, q, U, o, stream=None) -> Prepared:
+    lib = load()
+    args = (ctypes.byref(cfg), _vp(S), _vp(omega), ctypes.byref(ring) if ring else None, ctypes.c_int32(n_buffered),
+            _vp(q), _vp(U), _vp(o), _vp(stream))
+    return Prepared(lib.sketchssm_update, args, (cfg, ring))
+
+
+def prepare_decode(cfg: Config, U, coef, ring: Ring, n_buffered: int, q, o, stream=None) -> Prepared:
+    lib = load()
+    args = (ctypes.byref(cfg), _vp(U), _vp(coef), ctypes.byref(ring), ctypes.c_int32(n_buffered), _vp(q), _vp(o),
+            _vp(stream))
+    return Prepared(lib.sketchssm_decode, args, (cfg, ring))
+
+
+def prepare_full_read_baseline(cfg: Config, S, ring: Ring, n_buffered: int, q, o, stream=None) -> Prepared:
+    lib = load()
+    args = (ctypes.byref(cfg), _vp(S), ctypes.byref(ring), ctypes.c_int32(n_buffered), _vp(q), _vp(o), _vp(stream))
+    return Prepared(lib.sketchssm_full_read_baseline, args, (cfg, ring))
+
+
 def sketchssm_update(cfg: Config, S, omega, ring: Ring | None, n_buffered: int, q, U, o, stream=None):
     lib = load()
     _check(lib.sketchssm_update(ctypes.byref(cfg), ptr(S), ptr(omega), ctypes.byref(ring) if ring else None,

@@ -39,6 +39,29 @@ def headers():
     return glob.glob(os.path.join(CSRC, "*.h")) + glob.glob(os.path.join(INCLUDE, "*.h"))
 
 
+KERNEL_HEADERS = {"decode": "decode.h", "full_read": "decode.h", "update": "update.h"}
+
+
+def unit_sources(unit: str) -> list[str]:
+    """The files whose text decides the machine code of one unit's kernels
+    (unit = "decode_mamba2", "update_gdn", ...): the unit, the shared device
+    and argument headers, the launch table and the kernel's own header."""
+    entry = unit.rsplit("_", 1)[0]
+    names = ["device.h", "args.h", "dispatch.h", KERNEL_HEADERS[entry]]
+    return [os.path.join(CSRC, "units", unit + ".hip")] + [os.path.join(CSRC, n) for n in names]
+
+
+def source_digest(unit: str) -> str:
+    """sha256 over unit_sources(unit), with the build flags: a recorded
+    measurement of a kernel is current only while this digest is unchanged."""
+    import hashlib
+    h = hashlib.sha256(" ".join(FLAGS[1:-2]).encode())
+    for f in unit_sources(unit):
+        with open(f, "rb") as fh:
+            h.update(os.path.basename(f).encode() + b"\0" + fh.read())
+    return h.hexdigest()[:16]
+
+
 def _obj(src):
     return os.path.join(BUILD, os.path.splitext(os.path.basename(src))[0] + ".o")
 

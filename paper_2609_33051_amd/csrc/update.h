@@ -298,12 +298,16 @@ __global__ __launch_bounds__(256) void update_kernel(const UpdateArgs a) {
       for (int st = 0; st < ST; ++st) {
         floatx4 acc = {0.f, 0.f, 0.f, 0.f};
         if constexpr (ERASE) {
-          // w_s = u_s - (Pi X_0^T)[s]
+          // w_s = u_s - (Pi X_0^T)[s]; four independent accumulation chains
+          floatx4 pc[4];
+#pragma unroll
+          for (int i = 0; i < 4; ++i) pc[i] = floatx4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
           for (int kt = 0; kt < MT; ++kt)
 #pragma unroll
             for (int i = 0; i < 4; ++i)
-              acc = mfma4(PiT[(16 * kt + 4 * lg + i) * PP + 16 * st + lr], xs[t][kt][i], acc);
+              pc[i] = mfma4(PiT[(16 * kt + 4 * lg + i) * PP + 16 * st + lr], xs[t][kt][i], pc[i]);
+          acc = (pc[0] + pc[1]) + (pc[2] + pc[3]);
         }
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
@@ -343,14 +347,18 @@ __global__ __launch_bounds__(256) void update_kernel(const UpdateArgs a) {
 #pragma unroll
         for (int jt = 0; jt < RT; ++jt) {
           const int jj = 16 * jt + lr;
-          floatx4 acc = {0.f, 0.f, 0.f, 0.f};
+          // four independent accumulation chains over the K-deep contraction
+          floatx4 uc[4];
+#pragma unroll
+          for (int i = 0; i < 4; ++i) uc[i] = floatx4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
           for (int kt = 0; kt < MT; ++kt)
 #pragma unroll
             for (int i = 0; i < 4; ++i) {
               const float w = (jj < R) ? om[(16 * kt + 4 * lg + i) * R + jj] : 0.f;
-              acc = mfma4(w, xs[t][kt][i], acc);
+              uc[i] = mfma4(w, xs[t][kt][i], uc[i]);
             }
+          const floatx4 acc = (uc[0] + uc[1]) + (uc[2] + uc[3]);
           // 4-column panel 4 jt + lg of U[B][H][R/4][V][4]
           if (16 * jt + 4 * lg < R)
             reinterpret_cast<float4*>(a.U + item * (size_t)V * R)[(4 * jt + lg) * V + v] =

@@ -97,6 +97,19 @@ class SketchSSMLayer:
             self.n += 1
         return o
 
+    def prepared_read(self, q: torch.Tensor, n: int, out: torch.Tensor | None = None) -> B.Prepared:
+        """The read of ring slot `n` (as `read` would issue it with self.n == n)
+        with its arguments marshalled once, on the current stream.  Replaying
+        the W calls n = 0..W-1 in order is the same as W calls of `read`; the
+        caller owns that order (self.n is not touched)."""
+        o = self.o if out is None else out
+        st = self.stream()
+        if n == self.window - 1:
+            return B.prepare_update(self.cfg, self.S, self.omega, self.ring, n, q, self.U, o, st)
+        if self.baseline:
+            return B.prepare_full_read_baseline(self.cfg, self.S, self.ring, n, q, o, st)
+        return B.prepare_decode(self.cfg, self.U, self.coef, self.ring, n, q, o, st)
+
     def step(self, inp: dict, out: torch.Tensor | None = None) -> torch.Tensor:
         """write_token + read."""
         self.write_token(inp)

@@ -1,0 +1,161 @@
+"""Summarise rocprofv3 CSV output of a bench.py run into short text records.
+
+    python -m paper_2609_33051_amd.profile_summary --trace DIR --fetch DIR --write DIR \
+        --workload mamba2_b256 --command "..." --out profiles/
+
+--trace is the output directory of `rocprofv3 --kernel-trace --stats
+--output-format csv`, --fetch / --write those of two `--pmc FETCH_SIZE` and
+`--pmc WRITE_SIZE` runs of a bench.py command with --copy-calibration, whose
+1 GiB fp32 copy fixes the scale of each counter (bytes it reads or writes
+divided by what the counter reports for it).
+
+Writes <entry>_<workload>.txt per kernel of this library that ran (duration
+statistics, counter means per dispatch, scaled bytes, algorithmic bytes) and
+merges the per-launch counter records into traffic.json, keyed
+"<entry>_<kind>:<workload>:r<rank>:w<window>" with the kernel's source digest,
+for bench.py's roofline `traffic` field.
+"""
+from __future__ import annotations
+
+import argparse
+import csv
+import glob
+import json
+import os
+import re
+import sys
+
+COPY_BYTES = 1 << 30  # the calibration copy: 2^28 fp32 read and written
+
+
+def _rows(d, suffix):
+    fs = glob.glob(os.path.join(d, "*" + suffix))
+    if len(fs) != 1:
+        raise SystemExit(f"expected one *{suffix} under {d}, found {fs}")
+    with open(fs[0]) as f:
+        return list(csv.DictReader(f))
+
+
+def _short(name: str) -> str:
+    name = name.replace("void ", "")
+    m = re.match(r"([\w:]+)(<[^()]*>)?", name)
+    return (m.group(1).split("::")[-1] + (m.group(2) or "")) if m else name[:80]
+
+
+def _entry(short: str) -> str | None:
+    for e in ("decode", "full_read", "update"):
+        if short.startswith(f"{e}_kernel<"):
+            return e
+    return None
+
+
+def _counter(d, counter):
+    """(per-kernel list of values in KiB, copy-kernel value) from one pmc run."""
+    per, copy = {}, []
+    for r in _rows(d, "_counter_collection.csv"):
+        if r["Counter_Name"] != counter:
+            continue
+        s = _short(r["Kernel_Name"])
+        v = float(r["Counter_Value"])
+        per.setdefault(s, []).append(v)
+        if "neg_kernel" in r["Kernel_Name"]:
+            copy.append(v)  # bench.py --copy-calibration: 2^28 fp32 negated, 1 GiB in, 1 GiB out
+    if not copy:
+        raise SystemExit(f"no calibration copy kernel found in {d} (run bench.py with --copy-calibration)")
+    return per, sum(copy) / len(copy)
+
+
+def main(argv=None):
+    p = argparse.ArgumentParser()
+    p.add_argument("--trace", required=True)
+    p.add_argument("--fetch", required=True)
+    p.add_argument("--write", required=True)
+    p.add_argument("--workload", required=True)
+    p.add_argument("--rank", type=int, default=None)
+    p.add_argument("--window", type=int, default=None)
+    p.add_argument("--command", required=True, help="the rocprofv3 commands, as run")
+    p.add_argument("--out", required=True)
+    a = p.parse_args(argv)
+
+    from . import build as hip_build
+    from . import inputs, traffic
+
+    wl = inputs.WORKLOADS[a.workload]
+    rank = wl.rank if a.rank is None else a.rank
+    W = wl.window if a.window is None else a.window
+    shape = traffic.Shape(wl.kind, wl.dk, wl.dv, rank, W, 2 if wl.io == "bf16" else 4)
+    items = wl.items
+    algo = {
+        "decode": sum(traffic.decode_bytes(shape, n) for n in range(W - 1)) / (W - 1) * items,
+        "full_read": sum(traffic.full_read_bytes(shape, n) for n in range(W - 1)) / (W - 1) * items,
+    }
+
+    stats = {}
+    for r in _rows(a.trace, "_kernel_stats.csv"):
+        s = _short(r["Name"])
+        stats[s] = r
+    fetch, copy_f = _counter(a.fetch, "FETCH_SIZE")
+    write, copy_w = _counter(a.write, "WRITE_SIZE")
+    f_scale = COPY_BYTES / (copy_f * 1024)
+    w_scale = COPY_BYTES / (copy_w * 1024)
+
+    os.makedirs(a.out, exist_ok=True)
+    tpath = os.path.join(a.out, "traffic.json")
+    table = json.load(open(tpath)) if os.path.exists(tpath) else {}
+    for s, r in sorted(stats.items()):
+        e = _entry(s)
+        if e is None:
+            continue
+        unit = f"{e}_{wl.kind}"
+        digest = hip_build.source_digest(unit)
+        fv, wv = fetch.get(s, []), write.get(s, [])
+        lines = [
+            f"# {s} on {a.workload} (rank {rank}, window {W})",
+            "",
+            "Commands (from the repository root of the run; CSV output):",
+            *[f"    {c}" for c in a.command.split(" ;; ")],
+            "",
+            f"source digest of {unit}: {digest}",
+            "",
+            "kernel trace (--kernel-trace --stats):",
+            f"    calls {r['Calls']}, average {float(r['AverageNs']) / 1e3:.2f} us, "
+            f"min {float(r['MinNs']) / 1e3:.2f} us, max {float(r['MaxNs']) / 1e3:.2f} us, "
+            f"{float(r['Percentage']):.2f} % of GPU kernel time",
+            "",
+            "counters per dispatch (KiB as reported; scaled by the calibration copy of 1 GiB:",
+            f"    FETCH_SIZE read {copy_f:.1f} KiB for it -> scale {f_scale:.4f};"
+            f" WRITE_SIZE wrote {copy_w:.1f} KiB -> scale {w_scale:.4f})",
+        ]
+        if fv and wv:
+            fm, wm = sum(fv) / len(fv), sum(wv) / len(wv)
+            hbm = fm * 1024 * f_scale + wm * 1024 * w_scale
+            lines += [
+                f"    FETCH_SIZE dispatches {len(fv)}, mean {fm:.1f}, min {min(fv):.1f}, max {max(fv):.1f}",
+                f"    WRITE_SIZE dispatches {len(wv)}, mean {wm:.1f}, min {min(wv):.1f}, max {max(wv):.1f}",
+                f"    HBM bytes per launch (scaled): read {fm * 1024 * f_scale / 1e6:.2f} MB + "
+                f"write {wm * 1024 * w_scale / 1e6:.2f} MB = {hbm / 1e6:.2f} MB",
+            ]
+            if e in algo:
+                lines.append(f"    algorithmic bytes per launch (mean over slots 0..{W - 2}): {algo[e] / 1e6:.2f} MB"
+                             f" -> measured / algorithmic = {hbm / algo[e]:.3f}")
+                table[f"{unit}:{a.workload}:r{rank}:w{W}"] = {
+                    "kernel": s, "digest": digest, "fetch_kib": round(fm, 1), "write_kib": round(wm, 1),
+                    "fetch_scale": round(f_scale, 6), "write_scale": round(w_scale, 6),
+                    "dispatches": len(fv), "algorithmic_bytes": int(algo[e]),
+                }
+            else:
+                lines.append("    (flush and sketch-only dispatches of this kernel are mixed in these means)")
+        name = f"{e}_{a.workload}" + ("" if rank == wl.rank and W == wl.window else f"_r{rank}_w{W}")
+        if "<" in s and e == "update" and re.search(r"<\d+, \d+, \d+, 0,", s):
+            name += "_rank0"
+        with open(os.path.join(a.out, name + ".txt"), "w") as f:
+            f.write("\n".join(lines) + "\n")
+        print("wrote", name + ".txt")
+    with open(tpath, "w") as f:
+        json.dump(table, f, indent=1, sort_keys=True)
+        f.write("\n")
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())

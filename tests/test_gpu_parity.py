@@ -136,6 +136,34 @@ def test_rerun_is_bitwise_identical():
     assert torch.equal(la.S, lb.S) and torch.equal(la.U, lb.U)
 
 
+@pytest.mark.parametrize("fam,baseline", [("gdn", False), ("kda", False), ("mamba2", True)])
+def test_prepared_calls_match_read(fam, baseline):
+    """Calls marshalled once and replayed (the benchmark's launch loop) give
+    bitwise the results of `read`, over two windows."""
+    from paper_2609_33051_amd.layer import SketchSSMLayer
+
+    wl = inputs.tiny(fam, batch=6, heads=2, dk=128, dv=64, rank=16, window=4, steps=8, io="bf16")
+    announce(f"prepared calls {fam} baseline={baseline}")
+    om, C = inputs.omega(wl, wl.rank)
+    S0 = inputs.initial_state(wl, "cuda")
+    pool = [inputs.step_inputs(wl, t, "cuda") for t in range(wl.window)]
+    lays = [SketchSSMLayer(wl.kind, wl.batch, wl.heads, wl.dk, wl.dv, wl.rank, wl.window, wl.io, "cuda",
+                           baseline=baseline, S=S0.clone(), omega=torch.as_tensor(om), coef=torch.as_tensor(C))
+            for _ in range(2)]
+    for lay in lays:
+        lay.init_sketch()
+        for slot in range(wl.window):
+            lay.write_token(pool[slot], slot)
+    plan = [lays[1].prepared_read(pool[t]["q"], t) for t in range(wl.window)]
+    for t in range(2 * wl.window):
+        a = lays[0].read(pool[t % wl.window]["q"]).clone()
+        plan[t % wl.window]()
+        assert torch.equal(a, lays[1].o), f"step {t}"
+    assert torch.equal(lays[0].S, lays[1].S)
+    if not baseline:
+        assert torch.equal(lays[0].U, lays[1].U)
+
+
 # --- the paper-shape workloads at full size, sampled items ---------------------------------------
 def sample_items(wl, n=48, seed=7):
     rng = np.random.default_rng(seed)

@@ -176,6 +176,16 @@ __device__ __forceinline__ void wave_lds_sync() {
   __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
 }
 
+// Workgroup barrier for LDS traffic only: waits for this wave's LDS (and
+// scalar) operations, then meets the other waves.  Unlike __syncthreads it
+// leaves this wave's global loads in flight, so a kernel can keep a large
+// read outstanding while its waves exchange staged data through LDS.  The
+// memory clobber keeps the compiler from moving memory operations across it.
+__device__ __forceinline__ void lds_barrier() { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); }
+
+// Compiler-only fence: memory operations stay on their side of it.
+__device__ __forceinline__ void compiler_fence() { asm volatile("" ::: "memory"); }
+
 __device__ __forceinline__ float fast_exp(float x) { return __expf(x); }
 
 }  // namespace skssm

@@ -41,7 +41,7 @@ template <> __device__ __forceinline__ float load1<float>(const float* p) { retu
 template <> __device__ __forceinline__ float load1<bf16_t>(const bf16_t* p) { return bf16_lo((uint32_t)*p); }
 
 template <int KIND, int K, int V, int R, int WMAX, typename IO>
-__global__ __launch_bounds__(256) void update_kernel(const UpdateArgs a) {
+__global__ __launch_bounds__(256, 3) void update_kernel(const UpdateArgs a) {
   constexpr bool ERASE = KIND != MAMBA2;
   constexpr bool CHAN = KIND == KDA;
   constexpr int MT = K / 16;          // k tiles
@@ -77,26 +77,28 @@ __global__ __launch_bounds__(256) void update_kernel(const UpdateArgs a) {
   const bool flush = a.nt > 0;
   const size_t NI = (size_t)a.B * H;  // slot s of item: ring field + (s * NI + item) * width
 
-  // ---- the single read of the state: issue every tile load first
-  floatx4 xs[VTW][MT];
-#pragma unroll
-  for (int t = 0; t < VTW; ++t) {
-    const int vt = wave + 4 * t;
-    if (vt < VT) {
-      const float* src = a.S + (item * V + 16 * vt + lr) * K + 4 * lg;
-#pragma unroll
-      for (int kt = 0; kt < MT; ++kt) {
-        const float4 x = *reinterpret_cast<const float4*>(src + 16 * kt);
-        xs[t][kt] = floatx4{x.x, x.y, x.z, x.w};
-      }
-    }
-  }
+  // Omega of this head goes to LDS (rows padded to whole 16-column tiles plus
+  // four words, so the four lane groups of an operand read hit different banks)
+  // when it is small; the full-rank case reads it from global memory.
+  constexpr bool OM_LDS = R > 0 && R <= 32;
+  constexpr int OPJ = 16 * RT + 4;
+  constexpr int OQ = OM_LDS ? (K * R / 4 + 255) / 256 : 1;  // float4 of Omega per thread
+  __shared__ __align__(16) float OmL[OM_LDS ? K * OPJ : 4];
+  const bool want_U = R > 0 && a.U != nullptr;
 
-  float egn = 1.f;  // e^{g_n} (scalar decay)
+  // ---- every small load first (window, query, couplings, Omega), then the
+  // state: the staged values reach LDS while the state read is still in flight
+  float egn = 1.f, gn = 0.f, bn = 0.f;  // e^{g_n} (scalar decay), g_n, beta_n
+  float bsv[SP], gsv[SP];               // beta_s and (scalar decay) g_s, wave-uniform
+  float gk[CHAN ? SP : 1];              // KDA: g_s of channel tid
+  Raw<IO, KPL> kr[NG / 4];              // ring keys, row layout (slot 4 (wave + 4 gq) + row)
+  Vec<ERASE ? VR : 1> ur[NG / 4];       // GDN/KDA: pseudo-values u_s (s < n)
+  Raw<IO, VR> vr[NG / 4];               // raw values (Mamba-2: all slots; GDN/KDA: slot n)
+  float qv = 0.f;
+  constexpr int BQ = ERASE ? (SP * SP + 255) / 256 : 1;
+  float bv[BQ];
+  Vec<4> omv[OQ];
   if (flush) {
-    // ---- per-slot scalars, uniform in every wave: beta_s and (scalar decay)
-    // the cumulative log decay g_s, summed in slot order
-    float bsv[SP], gsv[SP];
     {
       float acc = 0.f;
 #pragma unroll
@@ -113,7 +115,6 @@ __global__ __launch_bounds__(256) void update_kernel(const UpdateArgs a) {
         }
       }
     }
-    float gn = 0.f, bn = 0.f;
 #pragma unroll
     for (int s = 0; s < SP; ++s)
       if (s == n) {
@@ -121,8 +122,6 @@ __global__ __launch_bounds__(256) void update_kernel(const UpdateArgs a) {
         bn = bsv[s];
       }
     if constexpr (!CHAN) egn = fast_exp(gn);
-    // KDA: per-channel cumulative log decays, thread tid owns channel tid
-    float gk[CHAN ? SP : 1];
     if constexpr (CHAN) {
       if (tid < K) {
 #pragma unroll
@@ -135,33 +134,91 @@ __global__ __launch_bounds__(256) void update_kernel(const UpdateArgs a) {
         }
       }
     }
-
-    // ---- stage the window with wide loads: row r of wave w holds slot 4 gi + r
 #pragma unroll
     for (int gq = 0; gq < NG / 4; ++gq) {
-      const int gi = wave + 4 * gq;  // slot group of this wave (wave-uniform)
-      const int s = 4 * gi + row;
+      const int s = 4 * (wave + 4 * gq) + row;
       const size_t si = (size_t)s * NI + item;
+      if (s <= n) {
+        kr[gq].load(static_cast<const IO*>(a.rk) + si * K + col * KPL);
+        if (ERASE && s < n) {
+          if constexpr (ERASE) ur[gq].load(a.ru + si * V + col * VR);
+        } else {
+          vr[gq].load(static_cast<const IO*>(a.rv) + si * V + col * VR);
+        }
+      }
+    }
+    if (tid < K) qv = load1<IO>(static_cast<const IO*>(a.q) + item * K + tid);
+    if constexpr (ERASE) {
+#pragma unroll
+      for (int c = 0; c < BQ; ++c) {
+        const int idx = tid + 256 * c;
+        const int s = idx / SP, j = idx % SP;
+        bv[c] = (idx < SP * SP && s < n && j < s) ? a.rb[((size_t)s * NI + item) * W + j] : 0.f;
+      }
+    }
+  }
+  if constexpr (OM_LDS) {
+    if (want_U) {
+#pragma unroll
+      for (int c = 0; c < OQ; ++c) {
+        const int i = tid + 256 * c;
+        if (i < K * R / 4) omv[c].load(a.omega + (size_t)h * K * R + 4 * i);
+      }
+    }
+  }
+
+  // ---- the single read of the state
+  floatx4 xs[VTW][MT];
+#pragma unroll
+  for (int t = 0; t < VTW; ++t) {
+    const int vt = wave + 4 * t;
+    if (vt < VT) {
+      const float* src = a.S + (item * V + 16 * vt + lr) * K + 4 * lg;
+#pragma unroll
+      for (int kt = 0; kt < MT; ++kt) {
+        const float4 x = *reinterpret_cast<const float4*>(src + 16 * kt);
+        xs[t][kt] = floatx4{x.x, x.y, x.z, x.w};
+      }
+    }
+  }
+  compiler_fence();
+
+  // ---- staged values into LDS
+  if constexpr (OM_LDS) {
+    if (want_U) {
+#pragma unroll
+      for (int c = 0; c < OQ; ++c) {
+        const int i = tid + 256 * c;
+        if (i < K * R / 4)
+          omv[c].store(&OmL[(i / (R / 4)) * OPJ + 4 * (i % (R / 4))]);
+      }
+      if constexpr (R < 16 * RT) {  // zero columns R..16 RT-1
+        constexpr int ZQ = (16 * RT - R) / 4;
+        for (int i = tid; i < K * ZQ; i += 256)
+          *reinterpret_cast<float4*>(&OmL[(i / ZQ) * OPJ + R + 4 * (i % ZQ)]) = make_float4(0.f, 0.f, 0.f, 0.f);
+      }
+    }
+  }
+  if (flush) {
+#pragma unroll
+    for (int gq = 0; gq < NG / 4; ++gq) {
+      const int s = 4 * (wave + 4 * gq) + row;
       float ksv[KPL], vsv[VR];
 #pragma unroll
       for (int m = 0; m < KPL; ++m) ksv[m] = 0.f;
 #pragma unroll
       for (int m = 0; m < VR; ++m) vsv[m] = 0.f;
       if (s <= n) {
-        Raw<IO, KPL> kr;
-        kr.load(static_cast<const IO*>(a.rk) + si * K + col * KPL);
 #pragma unroll
-        for (int m = 0; m < KPL; ++m) ksv[m] = kr.get(m);
+        for (int m = 0; m < KPL; ++m) ksv[m] = kr[gq].get(m);
         if (ERASE && s < n) {
-          Vec<VR> ur;
-          ur.load(a.ru + si * V + col * VR);
+          if constexpr (ERASE) {
 #pragma unroll
-          for (int m = 0; m < VR; ++m) vsv[m] = ur.e[m];
+            for (int m = 0; m < VR; ++m) vsv[m] = ur[gq].e[m];
+          }
         } else {
           // raw value: Mamba-2 scales it into c_s beta_s v_s; GDN/KDA keep v_n
           // in row n until u_n is formed
-          Raw<IO, VR> vr;
-          vr.load(static_cast<const IO*>(a.rv) + si * V + col * VR);
           float sc = 1.f;
           if constexpr (!ERASE) {
             // select this row's slot from the wave-uniform tables (compile-time indices only)
@@ -175,7 +232,7 @@ __global__ __launch_bounds__(256) void update_kernel(const UpdateArgs a) {
             sc = bs * fast_exp(gn - gs);
           }
 #pragma unroll
-          for (int m = 0; m < VR; ++m) vsv[m] = sc * vr.get(m);
+          for (int m = 0; m < VR; ++m) vsv[m] = sc * vr[gq].get(m);
         }
       }
 #pragma unroll
@@ -185,7 +242,7 @@ __global__ __launch_bounds__(256) void update_kernel(const UpdateArgs a) {
       for (int m = 0; m < VR; m += 4)
         *reinterpret_cast<float4*>(&Us[s * UP + col * VR + m]) = make_float4(vsv[m], vsv[m + 1], vsv[m + 2], vsv[m + 3]);
     }
-    if (tid < K) qs[tid] = load1<IO>(static_cast<const IO*>(a.q) + item * K + tid);
+    if (tid < K) qs[tid] = qv;
     if constexpr (!CHAN) {
       if (tid < SP) {
         float c = 0.f;
@@ -196,13 +253,16 @@ __global__ __launch_bounds__(256) void update_kernel(const UpdateArgs a) {
       }
     }
     if constexpr (ERASE) {
-      for (int idx = tid; idx < SP * SP; idx += 256) {
-        const int s = idx / SP, j = idx % SP;
-        Bs[idx] = (s < n && j < s) ? a.rb[((size_t)s * NI + item) * W + j] : 0.f;
+#pragma unroll
+      for (int c = 0; c < BQ; ++c) {
+        const int idx = tid + 256 * c;
+        if (idx < SP * SP) Bs[idx] = bv[c];
       }
     }
-    __syncthreads();
+  }
+  lds_barrier();
 
+  if (flush) {
     if constexpr (ERASE) {
       // ---- channel work: thread tid owns channel k = tid.  Ls holds raw keys.
       float pi[SP], kn = 0.f;
@@ -243,7 +303,7 @@ __global__ __launch_bounds__(256) void update_kernel(const UpdateArgs a) {
             if (s < n) Ls[s * LP + kk] *= fast_exp(gnk - gk[s]);
         }
       }
-      __syncthreads();
+      lds_barrier();
       // ---- the current token: u_n and pi_n need b_{n,j} from every wave
       if (tid < V) {
         const int v = tid;
@@ -281,7 +341,7 @@ __global__ __launch_bounds__(256) void update_kernel(const UpdateArgs a) {
 #pragma unroll
         for (int s = 0; s < SP; ++s) PiT[kk * PP + s] = (s < n) ? pi[s] : (s == n ? pin : 0.f);
       }
-      __syncthreads();
+      lds_barrier();
     }
   }
 
@@ -342,23 +402,23 @@ __global__ __launch_bounds__(256) void update_kernel(const UpdateArgs a) {
     }
     // sketch U^T = Omega^T X^T  (rows j = 16 jt + 4 lg + i of the C layout)
     if constexpr (R > 0) {
-      if (a.U) {
+      if (want_U) {
         const float* om = a.omega + (size_t)h * K * R;
 #pragma unroll
         for (int jt = 0; jt < RT; ++jt) {
           const int jj = 16 * jt + lr;
-          // four independent accumulation chains over the K-deep contraction
-          floatx4 uc[4];
-#pragma unroll
-          for (int i = 0; i < 4; ++i) uc[i] = floatx4{0.f, 0.f, 0.f, 0.f};
+          floatx4 acc = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
           for (int kt = 0; kt < MT; ++kt)
 #pragma unroll
             for (int i = 0; i < 4; ++i) {
-              const float w = (jj < R) ? om[(16 * kt + 4 * lg + i) * R + jj] : 0.f;
-              uc[i] = mfma4(w, xs[t][kt][i], uc[i]);
+              float w;
+              if constexpr (OM_LDS)
+                w = OmL[(16 * kt + 4 * lg + i) * OPJ + jj];
+              else
+                w = (jj < R) ? om[(16 * kt + 4 * lg + i) * R + jj] : 0.f;
+              acc = mfma4(w, xs[t][kt][i], acc);
             }
-          const floatx4 acc = (uc[0] + uc[1]) + (uc[2] + uc[3]);
           // 4-column panel 4 jt + lg of U[B][H][R/4][V][4]
           if (16 * jt + 4 * lg < R)
             reinterpret_cast<float4*>(a.U + item * (size_t)V * R)[(4 * jt + lg) * V + v] =

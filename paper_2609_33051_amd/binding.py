@@ -45,10 +45,12 @@ class Ring(ctypes.Structure):
 _lib = None
 
 
-def load(path: str = LIB_PATH):
+def load(path: str | None = None):
+    """Load the library: `path`, else $SKETCHSSM_LIBRARY, else the in-tree build."""
     global _lib
     if _lib is not None:
         return _lib
+    path = path or os.environ.get("SKETCHSSM_LIBRARY") or LIB_PATH
     if not os.path.exists(path):
         raise FileNotFoundError(f"{path} is not built; run `python -m paper_2609_33051_amd.build`")
     lib = ctypes.CDLL(path)

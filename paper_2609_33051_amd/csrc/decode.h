@@ -269,7 +269,15 @@ __global__ __launch_bounds__(256) void decode_kernel(const DecodeArgs a) {
   const size_t item = (size_t)(valid ? b : 0) * H + h;
   const float* Ub = a.U + item * (size_t)V * R;
 
-  // ---- every global load of this item
+  // ---- C first, then every global load of this item
+  constexpr int CQ = (R * K / 4 + 255) / 256;  // float4 of C per thread
+  Vec<4> cv[CQ];
+#pragma unroll
+  for (int c = 0; c < CQ; ++c) {
+    const int i = tid + 256 * c;
+    if (CQ * 256 == R * K / 4 || i < R * K / 4) cv[c].load(a.coef + (size_t)h * R * K + 4 * i);
+  }
+  compiler_fence();
   L r;
   float fs[ERASE ? NG : 1][RP];      // ring f of slot 4 gi + row, component col + 16 p
   float4 Ur[VPL][UP];                // sketch panels (value layout)
@@ -297,15 +305,14 @@ __global__ __launch_bounds__(256) void decode_kernel(const DecodeArgs a) {
     }
   }
 
-  // ---- stage this head's coefficient map C (R x K) in LDS
-  {
-    const float4* src = reinterpret_cast<const float4*>(a.coef + (size_t)h * R * K);
-    for (int i = tid; i < R * K / 4; i += 256) {
-      const int j = (4 * i) / K, kk = (4 * i) % K;
-      *reinterpret_cast<float4*>(&c_lds[j * CP + kk]) = src[i];
-    }
+  // ---- this head's coefficient map C (R x K) into LDS; its loads were issued
+  // first, so the LDS-only barrier leaves the item's own loads in flight
+#pragma unroll
+  for (int c = 0; c < CQ; ++c) {
+    const int i = tid + 256 * c;
+    if (CQ * 256 == R * K / 4 || i < R * K / 4) cv[c].store(&c_lds[((4 * i) / K) * CP + (4 * i) % K]);
   }
-  __syncthreads();
+  lds_barrier();
   if (!valid) return;
 
   float* xq_l = wscr + wave * WS;
@@ -430,7 +437,11 @@ __global__ __launch_bounds__(256) void full_read_kernel(const DecodeArgs a) {
   const int row = lane >> 4, col = lane & 15;
   const int n = a.n;
   const size_t NI = (size_t)a.B * a.H;
-  const size_t item = (size_t)blockIdx.x * 4 + wave;
+  // XCD x runs a contiguous share of the items (neighbouring items share the
+  // cache lines of the per-slot scalars); plain order when the grid does not split
+  const uint32_t G = gridDim.x, wg = blockIdx.x;
+  const uint32_t lwg = (G % 8 == 0) ? (wg % 8) * (G / 8) + wg / 8 : wg;
+  const size_t item = (size_t)lwg * 4 + wave;
   if (item >= NI) return;  // wave-uniform; no block barrier in this kernel
   const uint32_t koff = (uint32_t)(col * KPL);
 

@@ -259,10 +259,13 @@ def recorded_traffic(entry, wl, rank, W):
 
 
 def cpu_baseline(wl, rank, W, target_s, dev):
-    """The oracle (plain fp64 C, items spread over the host threads) on every
-    item of the workload, for as many consecutive windows as fill about
-    `target_s` seconds (the state carries from window to window), scaled to
-    steps/s per layer."""
+    """The oracle (plain fp64 C, items spread over the host threads) on the
+    first n_sel items of the workload (all of them when one window of all
+    takes under about a third of `target_s`), for as many consecutive windows
+    as fill about `target_s` seconds (the state carries from window to
+    window), scaled linearly to all items (items are independent) and
+    reported as steps/s per layer.  A one-thread figure on a sixteenth of
+    that sample is reported beside it."""
     import numpy as np
     import torch
 
@@ -272,35 +275,59 @@ def cpu_baseline(wl, rank, W, target_s, dev):
     items = wl.items
     threads = oracle.max_threads()
     om, C = inputs.omega(wl, rank)
-    heads = (np.arange(items) % wl.heads).astype(np.int32)
-    host = lambda x, w: x.reshape(items, w).to("cpu", torch.float32).numpy()
     pool = [inputs.step_inputs(wl, t, dev) for t in range(W)]
-    q = np.stack([host(p["q"], wl.dk) for p in pool])
-    k = np.stack([host(p["k"], wl.dk) for p in pool])
-    v = np.stack([host(p["v"], wl.dv) for p in pool])
-    beta = np.stack([host(p["beta"], 1)[:, 0] for p in pool])
-    ld = np.stack([host(p["log_decay"], wl.dk if wl.kind == "kda" else 1) for p in pool])
-    if wl.kind != "kda":
-        ld = ld[:, :, 0]
-    S0 = inputs.initial_state(wl, dev).reshape(items, wl.dv, wl.dk).cpu().numpy()
-    del pool
+    S_all = inputs.initial_state(wl, dev).reshape(items, wl.dv, wl.dk)
 
-    def windows(n_win, S):
+    def host(x, w, n):
+        return x.reshape(items, w)[:n].to("cpu", torch.float32).numpy()
+
+    def sample(n):
+        q = np.stack([host(p["q"], wl.dk, n) for p in pool])
+        k = np.stack([host(p["k"], wl.dk, n) for p in pool])
+        v = np.stack([host(p["v"], wl.dv, n) for p in pool])
+        beta = np.stack([host(p["beta"], 1, n)[:, 0] for p in pool])
+        ld = np.stack([host(p["log_decay"], wl.dk if wl.kind == "kda" else 1, n) for p in pool])
+        if wl.kind != "kda":
+            ld = ld[:, :, 0]
+        heads = (np.arange(n) % wl.heads).astype(np.int32)
+        return heads, q, k, v, beta, ld, S_all[:n].cpu().numpy()
+
+    def windows(n_win, data, S):
+        heads, q, k, v, beta, ld, _ = data
         t0 = time.perf_counter()
         for _ in range(n_win):
             S = oracle.sketchssm(wl.kind, W, heads, om, C, S, q, k, v, beta, ld, round_storage=True,
                                  diagnostics=False).S_final
         return time.perf_counter() - t0, S
 
-    dt, S1 = windows(1, S0)
+    # calibrate on a small slice, then size the sample
+    n_cal = min(items, 2048)
+    cal = sample(n_cal)
+    dt_cal, _ = windows(1, cal, cal[-1])
+    per_item_window = dt_cal / n_cal
+    n_sel = int(min(items, max(n_cal, target_s / 3 / max(per_item_window, 1e-9))))
+    data = sample(n_sel)
+    dt, S1 = windows(1, data, data[-1])
     n_win = 1
     if dt < 0.5 * target_s:  # too short to time alone: run enough further windows
         n_win = int(min(64, max(1, round(target_s / max(dt, 1e-3)))))
-        dt, _ = windows(n_win, S1)
+        dt, _ = windows(n_win, data, S1)
     steps = n_win * W
-    return {"value": round(steps / dt, 4), "unit": "steps/s", "cores": threads, "kind": "oracle",
-            "sample": f"all {items} (request, head) items x {n_win} consecutive windows of {W} steps "
-                      f"({steps} decode steps), {dt:.1f} s wall on {threads} threads"}
+    value = steps / dt * n_sel / items
+    # one thread, a sixteenth of the sample, one window
+    n1 = max(1, n_sel // 16)
+    heads, q, k, v, beta, ld, S0 = data
+    one = (heads[:n1], q[:, :n1], k[:, :n1], v[:, :n1], beta[:, :n1], ld[:, :n1], S0[:n1])
+    oracle.set_threads(1)
+    try:
+        dt1, _ = windows(1, one, one[-1])
+    finally:
+        oracle.set_threads(threads)
+    value1 = W / dt1 * n1 / items
+    return {"value": round(value, 4), "unit": "steps/s", "cores": threads, "kind": "oracle",
+            "sample": f"{n_sel} of {items} (request, head) items x {n_win} consecutive windows of {W} steps "
+                      f"({steps} decode steps), {dt:.1f} s wall on {threads} threads, scaled linearly to all items",
+            "one_thread": {"value": round(value1, 5), "sample": f"{n1} items x one window, {dt1:.1f} s"}}
 
 
 if __name__ == "__main__":

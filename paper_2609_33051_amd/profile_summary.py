@@ -65,6 +65,30 @@ def _counter(d, counter):
     return per, sum(copy) / len(copy)
 
 
+XCDS, SIMDS = 8, 1024  # MI355X: GRBM_GUI_ACTIVE is summed over the 8 XCDs; 256 CUs x 4 SIMDs
+
+
+def _mfma_lines(d, kernel):
+    """Matrix-core utilisation per group of dispatches with the same MFMA op
+    count (the initial sketch and the flush differ): busy cycles of all SIMDs
+    over (active cycles per XCD x SIMDs), and fp32 MFMA flops (512 per op)."""
+    per = {}
+    for r in _rows(d, "_counter_collection.csv"):
+        if _short(r["Kernel_Name"]) != kernel:
+            continue
+        per.setdefault(r["Dispatch_Id"], {})[r["Counter_Name"]] = float(r["Counter_Value"])
+    groups = {}
+    for c in per.values():
+        groups.setdefault(c.get("SQ_INSTS_VALU_MFMA_MOPS_F32", 0.0), []).append(c)
+    out = []
+    for mops, cs in sorted(groups.items()):
+        busy = sum(c["SQ_VALU_MFMA_BUSY_CYCLES"] for c in cs) / len(cs)
+        active = sum(c["GRBM_GUI_ACTIVE"] for c in cs) / len(cs) / XCDS
+        out.append(f"    {len(cs)} dispatches with {mops:.0f} MFMA MOPS ({mops * 512 / 1e9:.2f} GFLOP fp32, 512 flops per MOP): "
+                   f"MFMA busy {100 * busy / (active * SIMDS):.1f} % of {active:.0f} active cycles per SIMD")
+    return out
+
+
 def main(argv=None):
     p = argparse.ArgumentParser()
     p.add_argument("--trace", required=True)
@@ -74,6 +98,10 @@ def main(argv=None):
     p.add_argument("--rank", type=int, default=None)
     p.add_argument("--window", type=int, default=None)
     p.add_argument("--command", required=True, help="the rocprofv3 commands, as run")
+    p.add_argument("--mfma", default=None,
+                   help="output of a --pmc SQ_VALU_MFMA_BUSY_CYCLES SQ_INSTS_VALU_MFMA_MOPS_F32 SQ_BUSY_CYCLES "
+                        "GRBM_GUI_ACTIVE run (matrix-core utilisation of the update kernel)")
+    p.add_argument("--mfma-command", default="", help="the command of the --mfma run")
     p.add_argument("--out", required=True)
     a = p.parse_args(argv)
 
@@ -143,8 +171,12 @@ def main(argv=None):
                     "fetch_scale": round(f_scale, 6), "write_scale": round(w_scale, 6),
                     "dispatches": len(fv), "algorithmic_bytes": int(algo[e]),
                 }
-            else:
-                lines.append("    (flush and sketch-only dispatches of this kernel are mixed in these means)")
+            elif not re.search(r"<\d+, \d+, \d+, 0,", s):
+                lines.append("    (initial-sketch and flush dispatches of this kernel are mixed in these means)")
+        if a.mfma and e == "update":
+            m = _mfma_lines(a.mfma, s)
+            if m:
+                lines += ["", "matrix cores (" + a.mfma_command + "):"] + m
         name = f"{e}_{a.workload}" + ("" if rank == wl.rank and W == wl.window else f"_r{rank}_w{W}")
         if "<" in s and e == "update" and re.search(r"<\d+, \d+, \d+, 0,", s):
             name += "_rank0"

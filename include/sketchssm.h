@@ -78,10 +78,15 @@ typedef struct {
   int32_t io_dtype; /* skssm_dtype of q, k, v and ring.k / ring.v           */
 } skssm_config;
 
-/* Replay buffer ("ring"): W slots per (b, h), slot-major over the whole
- * batch, field[W][B][H][...], so the slot a step fills is one contiguous
- * region and each read fetches four slots per load.  Slot s holds the s-th
- * token of the current window (0-based).
+/* Replay buffer ("ring"): W slots per (b, h) item.  Slot s holds the s-th
+ * token of the current window (0-based).  Two layouts, by who writes:
+ *   - raw inputs (k, v, beta, log_decay), written by the producer and only
+ *     read here, are item-major, field[B][H][W][...]: the window of an item
+ *     is one contiguous block, so a read fetches four consecutive slots per
+ *     load instruction and the flush stages the window in one sweep;
+ *   - derived fields (g, u, f, pi, bcoef), written by each read for its own
+ *     slot, are slot-major, field[W][B][H][...]: one step's writes for all
+ *     items form one contiguous region of whole cache lines.
  *
  * Raw update inputs of token s are written into slot s by the token's
  * producer (the layer's projections) before the call that consumes it;
@@ -103,10 +108,10 @@ typedef struct {
  *   pi     erase factors pi_s in R^K (eq. wy), read by the exact baseline.
  * Unused fields may be NULL. */
 typedef struct {
-  const void* k;          /* [W][B][H][K] io_dtype raw keys (producer)              all kinds */
-  const void* v;          /* [W][B][H][V] io_dtype raw values (producer)            all kinds */
-  const float* beta;      /* [W][B][H] write gates (producer)                       all kinds */
-  const float* log_decay; /* [W][B][H] (MAMBA2, GDN) or [W][B][H][K] (KDA), <= 0 (producer) */
+  const void* k;          /* [B][H][W][K] io_dtype raw keys (producer)              all kinds */
+  const void* v;          /* [B][H][W][V] io_dtype raw values (producer)            all kinds */
+  const float* beta;      /* [B][H][W] write gates (producer)                       all kinds */
+  const float* log_decay; /* [B][H][W] (MAMBA2, GDN) or [B][H][W][K] (KDA), <= 0 (producer) */
   float* g;               /* [W][B][H][K] cumulative log decay                      KDA       */
   float* u;               /* [W][B][H][V] pseudo-values                             GDN, KDA  */
   float* f;               /* [W][B][H][rank] projected erase factors   GDN, KDA (sketch read) */

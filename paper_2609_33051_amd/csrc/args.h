@@ -1,7 +1,8 @@
 // Kernel argument blocks (passed by value to the kernels).
 //
-// Replay buffer (ring) fields are slot-major over the batch: slot s of item
-// i (= b*H + h) of a field of width w sits at field + (s * B*H + i) * w.
+// Replay buffer (ring): slot s of item i (= b*H + h) of a field of width w
+// sits at field + (i * W + s) * w for the raw inputs (item-major) and at
+// field + (s * B*H + i) * w for the derived fields (slot-major).
 // Raw inputs of token s (k, v, beta, log decay) are written into slot s by
 // the producer of the token; the kernels derive and store the rest.
 #pragma once
@@ -17,10 +18,10 @@ struct DecodeArgs {
   const float* U;                 // [B][H][R/4][V][4]   (sketch read)
   const float* coef;              // [H][R][K]           (sketch read)
   const float* S;                 // [B][H][V][K]        (exact baseline)
-  const void* rk;                 // ring [W][B][H][K] io      raw keys
-  const void* rv;                 // ring [W][B][H][V] io      raw values
-  const float* rbeta;             // ring [W][B][H]            write gates
-  const float* rla;               // ring [W][B][H] or [..][K] log decays
+  const void* rk;                 // ring [B][H][W][K] io      raw keys
+  const void* rv;                 // ring [B][H][W][V] io      raw values
+  const float* rbeta;             // ring [B][H][W]            write gates
+  const float* rla;               // ring [B][H][W] or [..][K] log decays
   float* rg;                      // ring [W][B][H][K]  cumulative log decay (KDA)
   float* ru;                      // ring [W][B][H][V]  pseudo-values (GDN/KDA)
   float* rf;                      // ring [W][B][H][R]  projected erase factors (GDN/KDA sketch read)

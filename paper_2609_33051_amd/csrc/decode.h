@@ -57,13 +57,15 @@ struct RowLoads {
   float bs[ERASE ? 1 : NG];           // ring beta (Mamba-2)
   Vec<VR> us[ERASE ? NG : 1];         // ring pseudo-values (GDN, KDA)
 
-  // `item` is wave-uniform.  Slot s of a ring field of width w sits at
-  // field + ((s * NI + item) * w).
+  // `item` is wave-uniform.  Slot s of a raw ring field (k, v, beta, log
+  // alpha) of width w sits at field + (item * W + s) * w, the W slots of an
+  // item contiguous; slot s of a derived field (g, u, f, pi, b) at
+  // field + (s * B*H + item) * w, one slot of all items contiguous.
   __device__ __forceinline__ void load(const DecodeArgs& a, size_t item, int row, int col) {
     const int n = a.n;
-    const size_t NI = (size_t)a.B * a.H;
+    const size_t W = (size_t)a.W, NI = (size_t)a.B * a.H;
     const uint32_t koff = (uint32_t)(col * KPL), voff = (uint32_t)(col * VR);
-    const size_t cur = (size_t)n * NI + item;        // slot n of this item
+    const size_t cur = item * W + n;                 // slot n of this item (raw fields)
     q_raw.load(static_cast<const IO*>(a.q) + item * K + koff);
     k_raw.load(static_cast<const IO*>(a.rk) + cur * K + koff);
     v_raw.load(static_cast<const IO*>(a.rv) + cur * V + voff);
@@ -77,18 +79,20 @@ struct RowLoads {
       for (int m = 0; m < KPL; ++m) gprev[m] = 0.f;
       if (n > 0) {
         Vec<KPL> g;
-        g.load(a.rg + (cur - NI) * K + koff);
+        g.load(a.rg + ((size_t)(n - 1) * NI + item) * K + koff);
 #pragma unroll
         for (int m = 0; m < KPL; ++m) gprev[m] = g.e[m];
       }
     } else {
       la[0] = a.rla[cur];
     }
-    const size_t rowslot = (size_t)row * NI + item;  // slot `row` of this item
+    const size_t rowslot = item * W + row;           // slot `row` of this item (raw fields)
+    const size_t rowder = (size_t)row * NI + item;   // the same slot in the derived fields
 #pragma unroll
     for (int gi = 0; gi < NG; ++gi) {
       const int s = 4 * gi + row;
-      const size_t si = rowslot + (size_t)(4 * gi) * NI;
+      const size_t si = rowslot + 4 * gi;
+      const size_t sd = rowder + (size_t)(4 * gi) * NI;
       ks[gi].zero();
 #pragma unroll
       for (int m = 0; m < GD; ++m) gs[gi][m] = 0.f;
@@ -103,14 +107,14 @@ struct RowLoads {
         ks[gi].load(static_cast<const IO*>(a.rk) + si * K + koff);
         if constexpr (CHAN) {
           Vec<KPL> t;
-          t.load(a.rg + si * K + koff);
+          t.load(a.rg + sd * K + koff);
 #pragma unroll
           for (int m = 0; m < KPL; ++m) gs[gi][m] = t.e[m];
         } else {
           gs[gi][0] = a.rla[si];  // log alpha_s for now; made cumulative in prefix_decay()
         }
         if constexpr (ERASE) {
-          us[gi].load(a.ru + si * V + voff);
+          us[gi].load(a.ru + sd * V + voff);
         } else {
           vs[gi].load(static_cast<const IO*>(a.rv) + si * V + voff);
           bs[gi] = a.rbeta[si];
@@ -262,7 +266,6 @@ __global__ __launch_bounds__(256) void decode_kernel(const DecodeArgs a) {
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int row = lane >> 4, col = lane & 15;
   const int H = a.H, n = a.n;
-  const size_t NI = (size_t)a.B * H;
   const int h = blockIdx.x % H;
   const int b = (blockIdx.x / H) * 4 + wave;
   const bool valid = b < a.B;
@@ -284,11 +287,12 @@ __global__ __launch_bounds__(256) void decode_kernel(const DecodeArgs a) {
   if (valid) {
     r.load(a, item, row, col);
     if constexpr (ERASE) {
-      const size_t rowslot = (size_t)row * NI + item;
+      const size_t NI = (size_t)a.B * H;
+      const size_t rowder = (size_t)row * NI + item;
 #pragma unroll
       for (int gi = 0; gi < NG; ++gi) {
         const int s = 4 * gi + row;
-        const float* fp = a.rf + (rowslot + (size_t)(4 * gi) * NI) * R;
+        const float* fp = a.rf + (rowder + (size_t)(4 * gi) * NI) * R;
 #pragma unroll
         for (int p = 0; p < RP; ++p) {
           const int j = col + 16 * p;
@@ -414,7 +418,7 @@ __global__ __launch_bounds__(256) void decode_kernel(const DecodeArgs a) {
   append_derived<L>(a, item, row, col, lane, gt, ut, bv, b_l);
   if constexpr (ERASE) {
     if (row == 0) {
-      const size_t sl = (size_t)n * NI + item;
+      const size_t sl = (size_t)n * a.B * H + item;
 #pragma unroll
       for (int p = 0; p < RP; ++p)
         if (col + 16 * p < R) a.rf[sl * R + col + 16 * p] = ft[p];
@@ -449,14 +453,14 @@ __global__ __launch_bounds__(256) void full_read_kernel(const DecodeArgs a) {
   r.load(a, item, row, col);
   float ps[ERASE ? NG : 1][KPL];     // ring pi of slot 4 gi + row (row layout)
   if constexpr (ERASE) {
-    const size_t rowslot = (size_t)row * NI + item;
+    const size_t rowder = (size_t)row * NI + item;
 #pragma unroll
     for (int gi = 0; gi < NG; ++gi) {
       const int s = 4 * gi + row;
       Vec<KPL> t;
 #pragma unroll
       for (int m = 0; m < KPL; ++m) t.e[m] = 0.f;
-      if (4 * gi < n && s < n) t.load(a.rpi + (rowslot + (size_t)(4 * gi) * NI) * K + koff);
+      if (4 * gi < n && s < n) t.load(a.rpi + (rowder + (size_t)(4 * gi) * NI) * K + koff);
 #pragma unroll
       for (int m = 0; m < KPL; ++m) ps[gi][m] = t.e[m];
     }

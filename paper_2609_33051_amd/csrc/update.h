@@ -75,7 +75,9 @@ __global__ __launch_bounds__(256, 3) void update_kernel(const UpdateArgs a) {
   const size_t item = blockIdx.x;
   const int h = (int)(item % (size_t)H);
   const bool flush = a.nt > 0;
-  const size_t NI = (size_t)a.B * H;  // slot s of item: ring field + (s * NI + item) * width
+  // slot s of an item: raw ring fields at (item * W + s) * width, derived
+  // fields at (s * B*H + item) * width
+  const size_t NI = (size_t)a.B * H;
 
   // Omega of this head goes to LDS (rows padded to whole 16-column tiles plus
   // four words, so the four lane groups of an operand read hit different banks)
@@ -106,7 +108,7 @@ __global__ __launch_bounds__(256, 3) void update_kernel(const UpdateArgs a) {
         bsv[s] = 0.f;
         gsv[s] = 0.f;
         if (s <= n) {
-          const size_t si = (size_t)s * NI + item;
+          const size_t si = item * W + s;
           bsv[s] = a.rbeta[si];
           if constexpr (!CHAN) {
             acc += a.rla[si];
@@ -128,8 +130,9 @@ __global__ __launch_bounds__(256, 3) void update_kernel(const UpdateArgs a) {
         for (int s = 0; s < SP; ++s) {
           gk[s] = 0.f;
           if (s <= n) {
-            const size_t si = (size_t)s * NI + item;
-            gk[s] = (s < n) ? a.rg[si * K + tid] : ((n > 0 ? a.rg[(si - NI) * K + tid] : 0.f) + a.rla[si * K + tid]);
+            const size_t si = item * W + s;
+            const size_t sd = (size_t)s * NI + item;
+            gk[s] = (s < n) ? a.rg[sd * K + tid] : ((n > 0 ? a.rg[(sd - NI) * K + tid] : 0.f) + a.rla[si * K + tid]);
           }
         }
       }
@@ -137,11 +140,11 @@ __global__ __launch_bounds__(256, 3) void update_kernel(const UpdateArgs a) {
 #pragma unroll
     for (int gq = 0; gq < NG / 4; ++gq) {
       const int s = 4 * (wave + 4 * gq) + row;
-      const size_t si = (size_t)s * NI + item;
+      const size_t si = item * W + s;
       if (s <= n) {
         kr[gq].load(static_cast<const IO*>(a.rk) + si * K + col * KPL);
         if (ERASE && s < n) {
-          if constexpr (ERASE) ur[gq].load(a.ru + si * V + col * VR);
+          if constexpr (ERASE) ur[gq].load(a.ru + ((size_t)s * NI + item) * V + col * VR);
         } else {
           vr[gq].load(static_cast<const IO*>(a.rv) + si * V + col * VR);
         }

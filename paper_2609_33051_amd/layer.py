@@ -8,10 +8,11 @@ into libsketchssm.so.  Buffers (caller-owned, as the ABI requires):
   U      [B][H][r/4][V][4] fp32 sketch U = S^T Omega in 4-column panels
          (sketch_matrix() gives the [B][H][V][r] view)
   omega  [H][K][r]     fp32 sketching matrix, coef [H][r][K] its coefficient map
-  ring   slot-major replay buffer, [W][B][H][...]:
-         raw inputs k, v (io dtype), beta, log_decay ([..][K] for KDA), written
-         into slot n by the token's producer (write_token);
-         derived: g (KDA), u, bcoef (GDN/KDA), f (sketch read) or pi (baseline).
+  ring   replay buffer of W slots per item:
+         raw inputs k, v (io dtype), beta, log_decay ([..][K] for KDA), item-major
+         [B][H][W][...], written into slot n by the token's producer (write_token);
+         derived fields, slot-major [W][B][H][...]: g (KDA), u, bcoef (GDN/KDA),
+         f (sketch read) or pi (baseline).
 """
 from __future__ import annotations
 
@@ -42,10 +43,10 @@ class SketchSSMLayer:
         else:
             self.omega = self.coef = self.U = None
         # raw inputs, written by the producer of each token
-        self.rk = torch.zeros((W, Bt, H, K), dtype=iodt, device=dev)
-        self.rv = torch.zeros((W, Bt, H, V), dtype=iodt, device=dev)
-        self.rbeta = torch.zeros((W, Bt, H), dtype=f32, device=dev)
-        self.rla = torch.zeros((W, Bt, H, K) if kind == "kda" else (W, Bt, H), dtype=f32, device=dev)
+        self.rk = torch.zeros((Bt, H, W, K), dtype=iodt, device=dev)
+        self.rv = torch.zeros((Bt, H, W, V), dtype=iodt, device=dev)
+        self.rbeta = torch.zeros((Bt, H, W), dtype=f32, device=dev)
+        self.rla = torch.zeros((Bt, H, W, K) if kind == "kda" else (Bt, H, W), dtype=f32, device=dev)
         # derived fields, written by the library
         self.rg = torch.zeros((W, Bt, H, K), dtype=f32, device=dev) if kind == "kda" else None
         self.ru = torch.zeros((W, Bt, H, V), dtype=f32, device=dev) if erase else None
@@ -76,10 +77,10 @@ class SketchSSMLayer:
         """The producer's side: the token's k, v, beta and log decay go into
         ring slot `slot` (default: the next slot of the window)."""
         s = self.n if slot is None else slot
-        self.rk[s].copy_(inp["k"])
-        self.rv[s].copy_(inp["v"])
-        self.rbeta[s].copy_(inp["beta"])
-        self.rla[s].copy_(inp["log_decay"])
+        self.rk[:, :, s].copy_(inp["k"])
+        self.rv[:, :, s].copy_(inp["v"])
+        self.rbeta[:, :, s].copy_(inp["beta"])
+        self.rla[:, :, s].copy_(inp["log_decay"])
 
     def read(self, q: torch.Tensor, out: torch.Tensor | None = None) -> torch.Tensor:
         """One decode token whose inputs already sit in ring slot n: a non-flush

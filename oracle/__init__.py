@@ -48,6 +48,7 @@ class _Cfg(ctypes.Structure):
         ("W", ctypes.c_int32),
         ("T", ctypes.c_int32),
         ("round_storage", ctypes.c_int32),
+        ("sketch_bf16", ctypes.c_int32),
     ]
 
 
@@ -144,7 +145,7 @@ def recurrence(kind, S_init, q, k, v, beta, log_decay, lib=None):
     keep = [_f32(x) for x in (S_init, q, k, v, beta, log_decay)]
     o, op = _out((T, n, V))
     S, Sp = _out((n, V, K))
-    cfg = _Cfg(KINDS[kind], n, K, V, 0, 1, T, 0)
+    cfg = _Cfg(KINDS[kind], n, K, V, 0, 1, T, 0, 0)
     rc = lib.orc_recurrence(ctypes.byref(cfg), *[p for _, p in keep], op, Sp)
     if rc != 0:
         raise RuntimeError(f"orc_recurrence failed ({rc})")
@@ -167,12 +168,14 @@ class SketchResult:
 
 
 def sketchssm(kind, W, heads, omega, coef, S_init, q, k, v, beta, log_decay, round_storage=False,
-              diagnostics=True, lib=None):
+              diagnostics=True, lib=None, sketch_bf16=False):
     """SketchSSM inference (Algorithm 1) in fp64.
 
     heads: [n] int, head index of every item (selects Omega / C); omega
     [H][K][G]; coef [H][G][K].  G = 0 (omega.shape[2] == 0) disables the
-    sketch (o_state_hat is then 0 between flushes).
+    sketch (o_state_hat is then 0 between flushes).  round_storage stores the
+    state and the sketch as fp32; sketch_bf16 stores the sketch as bf16
+    (round to nearest, ties to even, through fp32), the paper's storage.
     """
     lib = lib or _load()
     n, K, V, T = _check_inputs(kind, S_init, q, k, v, beta, log_decay)
@@ -195,7 +198,7 @@ def sketchssm(kind, W, heads, omega, coef, S_init, q, k, v, beta, log_decay, rou
     ob, obp = _out((T, n, V), diagnostics)
     S, Sp = _out((n, V, K))
     U, Up = _out((n, V, G))
-    cfg = _Cfg(KINDS[kind], n, K, V, G, int(W), T, 1 if round_storage else 0)
+    cfg = _Cfg(KINDS[kind], n, K, V, G, int(W), T, 1 if round_storage else 0, 1 if sketch_bf16 else 0)
     rc = lib.orc_sketchssm(
         ctypes.byref(cfg),
         heads.ctypes.data_as(ctypes.POINTER(ctypes.c_int32)),

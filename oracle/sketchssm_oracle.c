@@ -21,10 +21,12 @@
  *     at a time, buffer outputs by applying M_j to each buffered key one token
  *     at a time (eq. m-reads), and flushes replay the buffered tokens one at a
  *     time through the update (eq. transition-update, Algorithm 1).
- *   - The only optional deviation from pure fp64 is `round_storage`, which
+ *   - The only optional deviations from pure fp64 are `round_storage`, which
  *     rounds the full state and the sketch to fp32 at the points where the
  *     method writes them back (the paper keeps the state in FP32 storage,
- *     Appendix "Detailed Evaluation Setup"); arithmetic stays fp64.
+ *     Appendix "Detailed Evaluation Setup"), and `sketch_bf16`, which rounds
+ *     the sketch to bf16 there instead (the paper's sketch storage, Appendix
+ *     "State Memory Traffic Reduction"); arithmetic stays fp64.
  *
  * Pins (see tests/test_oracle_pins.py): brute-force closed forms of the
  * recurrence on tiny inputs, the delta-rule retrieval invariant, the
@@ -50,6 +52,7 @@ typedef struct {
   int32_t W;             /* window: tokens applied per flush                */
   int32_t T;             /* decode steps                                    */
   int32_t round_storage; /* 1: state and sketch stored as fp32              */
+  int32_t sketch_bf16;   /* 1: sketch stored as bf16 (the paper's storage)  */
 } orc_cfg;
 
 /* Per-item views of the per-step inputs.  Step inputs are laid out
@@ -140,6 +143,30 @@ static void read_state(int K, int V, const double* S, const double* x, double* o
 static void round_f32(double* a, size_t n)
 {
   for (size_t i = 0; i < n; ++i) a[i] = (double)(float)a[i];
+}
+
+/* The paper stores the sketch in BF16 (8-bit significand): round the value
+ * to fp32 and then to bf16, to nearest with ties to even. */
+static double bf16_rne(double x)
+{
+  float f = (float)x;
+  uint32_t u;
+  memcpy(&u, &f, sizeof u);
+  if ((u & 0x7f800000u) != 0x7f800000u) { /* finite: add half an ulp of bf16, ties to even */
+    u += 0x7fffu + ((u >> 16) & 1u);
+    u &= 0xffff0000u;
+  }
+  memcpy(&f, &u, sizeof f);
+  return (double)f;
+}
+
+static void store_sketch(const orc_cfg* c, double* U, size_t n)
+{
+  if (c->sketch_bf16) {
+    for (size_t i = 0; i < n; ++i) U[i] = bf16_rne(U[i]);
+  } else if (c->round_storage) {
+    round_f32(U, n);
+  }
 }
 
 /* U = S^T Omega  (V x G), Omega is this head's K x G block. */
@@ -253,7 +280,7 @@ int orc_sketchssm(const orc_cfg* c, const int32_t* heads, const float* omega, co
     /* Initialise the sketch from the prefill state (Algorithm 1). */
     if (G > 0) {
       make_sketch(K, V, G, S0, Om, U);
-      if (c->round_storage) round_f32(U, (size_t)V * G);
+      store_sketch(c, U, (size_t)V * G);
     }
     int len = 0; /* tokens in the buffer B */
     double x[1024], y[1024], cvec[1024], ohat[1024], ostate[1024], obuf[1024];
@@ -306,7 +333,7 @@ int orc_sketchssm(const orc_cfg* c, const int32_t* heads, const float* omega, co
         read_state(K, V, S0, x, ostate);
         if (G > 0) {
           make_sketch(K, V, G, S0, Om, U);
-          if (c->round_storage) round_f32(U, (size_t)V * G);
+          store_sketch(c, U, (size_t)V * G);
         }
         for (int j = 0; j < V; ++j) {
           if (o) o[oi + j] = ostate[j];

@@ -83,7 +83,7 @@ MUTANTS = {
     "kda_channel_index": [("[((size_t)n * c->n_items + t->item) * c->K + kk]",
                            "[((size_t)n * c->n_items + t->item) * c->K + (c->K - 1 - kk)]")],
     "sketch_not_refreshed": [("        if (G > 0) {\n          make_sketch(K, V, G, S0, Om, U);\n"
-                              "          if (c->round_storage) round_f32(U, (size_t)V * G);\n        }\n"
+                              "          store_sketch(c, U, (size_t)V * G);\n        }\n"
                               "        for (int j = 0; j < V; ++j) {\n          if (o) o[oi + j] = ostate[j];",
                               "        for (int j = 0; j < V; ++j) {\n          if (o) o[oi + j] = ostate[j];")],
 }

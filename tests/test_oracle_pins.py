@@ -227,3 +227,36 @@ def test_storage_rounding_only_changes_state_at_fp32_level():
     rel = np.linalg.norm(rr.o - r.o) / np.linalg.norm(r.o)
     assert 0 < rel < 1e-6
     np.testing.assert_array_equal(rr.S_final, rr.S_final.astype(np.float32).astype(np.float64))
+
+
+def test_bf16_sketch_storage_is_round_to_nearest_even():
+    """The paper stores the sketch in BF16.  With that storage the oracle's
+    sketch after a flush is torch's bfloat16 rounding (nearest, ties to even)
+    of the fp32 sketch, and the flush leaves the state untouched by it."""
+    import torch
+
+    S0, q, k, v, beta, logd = tiny_inputs("gdn", n=3, K=8, V=6, T=8, seed=11)
+    heads = np.zeros(3, np.int32)
+    om, C = heads_omega(1, 8, 4, seed=5)
+    a = oracle.sketchssm("gdn", 4, heads, om, C, S0, q, k, v, beta, logd, round_storage=True)
+    b = oracle.sketchssm("gdn", 4, heads, om, C, S0, q, k, v, beta, logd, round_storage=True, sketch_bf16=True)
+    want = torch.from_numpy(a.U_final.astype(np.float32)).to(torch.bfloat16).to(torch.float64).numpy()
+    assert np.array_equal(b.U_final, want)
+    assert not np.array_equal(a.U_final, b.U_final)
+    assert np.array_equal(a.S_final, b.S_final)
+
+
+def test_bf16_sketch_is_the_one_read():
+    """r = K, Omega = C = I, one token in the window (scalar decay): the
+    sketch read is U (alpha_1 q) with U the bf16-rounded S_0^T (Sec. 3.3 read
+    with the paper's storage)."""
+    import torch
+
+    S0, q, k, v, beta, logd = tiny_inputs("mamba2", n=2, K=6, V=5, T=1, seed=3)
+    eye = np.broadcast_to(np.eye(6, dtype=np.float32), (1, 6, 6)).copy()
+    r = oracle.sketchssm("mamba2", 4, np.zeros(2, np.int32), eye, eye, S0, q, k, v, beta, logd,
+                         round_storage=True, sketch_bf16=True)
+    U = torch.from_numpy(S0.astype(np.float32)).to(torch.bfloat16).to(torch.float64).numpy()  # [n][V][K]
+    qt = np.exp(logd[0].astype(np.float64))[:, None] * q[0].astype(np.float64)
+    want = np.einsum("nvk,nk->nv", U, qt)
+    assert np.allclose(r.o_state_hat[0], want, rtol=1e-12, atol=1e-12)

@@ -46,6 +46,10 @@ def parse():
     p.add_argument("--rank", type=int, default=None)
     p.add_argument("--window", type=int, default=None)
     p.add_argument("--layers", type=int, default=4)
+    p.add_argument("--sketch", choices=("f32", "bf16"), default="f32",
+                   help="storage of the sketch U for the headline path (bf16: the paper's storage)")
+    p.add_argument("--no-paper-storage", action="store_true",
+                   help="skip the extra timed pass with the bf16 sketch beside an fp32 headline")
     p.add_argument("--no-full-read", action="store_true", help="skip the exact baseline path")
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--cpu-seconds", type=float, default=12.0, help="target CPU time of the oracle sample")
@@ -80,19 +84,19 @@ def main():
     warm = -(-args.warmup // W) * W
     L = args.layers
     io_bytes = 2 if wl.io == "bf16" else 4
-    shape = traffic.Shape(wl.kind, wl.dk, wl.dv, rank, W, io_bytes)
+    shape = traffic.Shape(wl.kind, wl.dk, wl.dv, rank, W, io_bytes, 2 if args.sketch == "bf16" else 4)
     items = wl.items
 
     om, C = inputs.omega(wl, rank)
     om_t, C_t = torch.as_tensor(om), torch.as_tensor(C)
     pool = [inputs.step_inputs(wl, t, dev) for t in range(W)]  # one window of resident inputs, reused
 
-    def make_layers(baseline):
+    def make_layers(baseline, sketch):
         layers = []
         for li in range(L):
             S = inputs.initial_state(wl, dev, seed=inputs.SEED + li)
             lay = SketchSSMLayer(wl.kind, wl.batch, wl.heads, wl.dk, wl.dv, rank, W, wl.io, dev,
-                                 baseline=baseline, S=S, omega=om_t, coef=C_t)
+                                 baseline=baseline, S=S, omega=om_t, coef=C_t, sketch=sketch)
             lay.init_sketch()
             for slot in range(W):  # the producer's writes: one window of tokens, resident in the ring
                 lay.write_token(pool[slot], slot)
@@ -117,8 +121,8 @@ def main():
         for lay in layers:
             lay.n = n_tokens % W
 
-    def timed(baseline):
-        layers = make_layers(baseline)
+    def timed(baseline, sketch=args.sketch):
+        layers = make_layers(baseline, sketch)
         stream = torch.cuda.current_stream()
         events = [(t % W, torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
                   for t in range(K_steps)]
@@ -138,23 +142,31 @@ def main():
         torch.cuda.empty_cache()
         return elapsed, per_n
 
+    def kernel_stats(per_n, sketch):
+        """Decode and flush figures from per-slot launch times (seconds)."""
+        sh = traffic.Shape(wl.kind, wl.dk, wl.dv, rank, W, io_bytes, 2 if sketch == "bf16" else 4)
+        dec_n = [n for n in per_n if n < W - 1]
+        dec_time = sum(sum(per_n[n]) for n in dec_n)
+        dec_launches = sum(len(per_n[n]) for n in dec_n)
+        dec_bytes = sum(traffic.decode_bytes(sh, n) * items * len(per_n[n]) for n in dec_n)
+        fl = per_n.get(W - 1, [])
+        fl_mean = sum(fl) / len(fl)
+        fl_bytes = traffic.flush_bytes(sh, W - 1) * items
+        flops = items * (2 * wl.dv * wl.dk * W * (2 if sh.erase else 1) + 2 * wl.dv * wl.dk * rank)
+        win = sum(sum(v) / len(v) for v in per_n.values())
+        return {"dec_mean": dec_time / dec_launches, "dec_bytes": dec_bytes / dec_launches,
+                "dec_gbps": dec_bytes / dec_time / 1e9, "fl_mean": fl_mean, "fl_bytes": fl_bytes,
+                "fl_gbps": fl_bytes / fl_mean / 1e9, "fl_tflops": flops / fl_mean / 1e12, "window": win,
+                "per_slot": {int(n): round(sum(v) / len(v) * 1e6, 2) for n, v in sorted(per_n.items()) if n < W - 1}}
+
     # ---- the SketchSSM path
     elapsed, per_n = timed(False)
     layer_steps = K_steps * L
     value = layer_steps / elapsed
-    dec_n = [n for n in per_n if n < W - 1]
-    traffic_rec = recorded_traffic("decode", wl, rank, W)
-    dec_time = sum(sum(per_n[n]) for n in dec_n)
-    dec_launches = sum(len(per_n[n]) for n in dec_n)
-    dec_bytes = sum(traffic.decode_bytes(shape, n) * items * len(per_n[n]) for n in dec_n)
-    dec_mean_s = dec_time / dec_launches
-    dec_bytes_per_launch = dec_bytes / dec_launches
-    dec_gbps = dec_bytes / dec_time / 1e9
-    fl = per_n.get(W - 1, [])
-    fl_mean_s = sum(fl) / len(fl)
-    fl_bytes = traffic.flush_bytes(shape, W - 1) * items
-    mfma_flops = items * (2 * wl.dv * wl.dk * W * (2 if shape.erase else 1) + 2 * wl.dv * wl.dk * rank)
-    window_s = sum(sum(v) / len(v) for v in per_n.values())
+    ks = kernel_stats(per_n, args.sketch)
+    traffic_rec = recorded_traffic("decode", wl, rank, W, args.sketch)
+    dec_mean_s, dec_bytes_per_launch, dec_gbps = ks["dec_mean"], ks["dec_bytes"], ks["dec_gbps"]
+    fl_mean_s, fl_bytes, window_s = ks["fl_mean"], ks["fl_bytes"], ks["window"]
 
     out = {
         "metric": METRIC,
@@ -170,7 +182,7 @@ def main():
         "dtype": "f32",
         "data": "synthetic",
         "config": {"workload": wl.name, "kind": wl.kind, "batch": wl.batch, "heads": wl.heads, "dk": wl.dk,
-                   "dv": wl.dv, "rank": rank, "window": W, "io": wl.io, "state": "f32", "sketch": "f32",
+                   "dv": wl.dv, "rank": rank, "window": W, "io": wl.io, "state": "f32", "sketch": args.sketch,
                    "layers_rotated": L},
         "roofline": {
             "kernel": "decode_kernel (sketchssm_decode)",
@@ -186,15 +198,27 @@ def main():
         "state_access_gbps": round(dec_gbps, 1),
         "kernels": {
             "decode": {"mean_us": round(dec_mean_s * 1e6, 2), "gbps": round(dec_gbps, 1),
-                       "per_slot_us": {int(n): round(sum(v) / len(v) * 1e6, 2) for n, v in sorted(per_n.items())
-                                       if n < W - 1}},
+                       "per_slot_us": ks["per_slot"]},
             "flush": {"mean_us": round(fl_mean_s * 1e6, 2), "bytes": fl_bytes,
-                      "gbps": round(fl_bytes / fl_mean_s / 1e9, 1),
-                      "mfma_tflops": round(mfma_flops / fl_mean_s / 1e12, 2), "mfma_peak_tflops": 157.3},
+                      "gbps": round(ks["fl_gbps"], 1),
+                      "mfma_tflops": round(ks["fl_tflops"], 2), "mfma_peak_tflops": 157.3},
             "window_us": round(window_s * 1e6, 1),
             "window_avg_steps_per_s": round(W / window_s, 1),
         },
     }
+
+    # ---- the paper's sketch storage (bf16 U) beside an fp32 headline, same inputs
+    if args.sketch == "f32" and not args.no_paper_storage:
+        e_p, per_p = timed(False, "bf16")
+        kp = kernel_stats(per_p, "bf16")
+        tr = recorded_traffic("decode", wl, rank, W, "bf16")
+        out["paper_storage"] = {
+            "sketch": "bf16", "value": round(layer_steps / e_p, 2), "unit": "steps/s",
+            "decode_mean_us": round(kp["dec_mean"] * 1e6, 2), "decode_bytes_per_launch": int(kp["dec_bytes"]),
+            "decode_gbps": round(kp["dec_gbps"], 1), "decode_frac": round(kp["dec_gbps"] / traffic.HBM_PEAK_GBPS, 4),
+            "decode_traffic": tr and tr["bytes_per_launch"],
+            "flush_mean_us": round(kp["fl_mean"] * 1e6, 2), "window_avg_steps_per_s": round(W / kp["window"], 1),
+        }
 
     # ---- the exact full-state-read baseline (same inputs; flush with rank 0)
     if not args.no_full_read:
@@ -237,7 +261,7 @@ def main():
     return 0
 
 
-def recorded_traffic(entry, wl, rank, W):
+def recorded_traffic(entry, wl, rank, W, sketch="f32"):
     """HBM bytes per launch of the `entry` kernel ("decode", ...) on this
     workload, from the FETCH_SIZE and WRITE_SIZE counter runs recorded under
     profiles/, each scaled by the factor a plain copy kernel's counters gave
@@ -251,7 +275,7 @@ def recorded_traffic(entry, wl, rank, W):
     with open(path) as f:
         table = json.load(f)
     unit = f"{entry}_{wl.kind}"
-    rec = table.get(f"{unit}:{wl.name}:r{rank}:w{W}")
+    rec = table.get(f"{unit}:{wl.name}:r{rank}:w{W}" + (":bf16" if sketch == "bf16" else ""))
     if rec is None or rec.get("digest") != hip_build.source_digest(unit):
         return None
     b = rec["fetch_kib"] * 1024 * rec["fetch_scale"] + rec["write_kib"] * 1024 * rec["write_scale"]

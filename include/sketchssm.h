@@ -18,11 +18,14 @@
  * Layout.  The paper writes S as K x V with o = S^T q; this library stores
  * its transpose, S[B][H][V][K] fp32 with K contiguous, so a row S[b][h][v][:]
  * is contiguous.  All other per-item tensors are [B][H][...] row-major with
- * the item index b*H + h.  The sketch is fp32 in 4-column panels,
- * U[B][H][r/4][V][4]: element (v, g) of the paper's V x r sketch (the output
- * of basis query g at value channel v) sits at U[b][h][g/4][v][g%4], so each
- * panel of the read is one contiguous, coalesced run.  Omega[H][K][r] and
- * the coefficient map coef[H][r][K] (C, shared by the batch) are fp32.
+ * the item index b*H + h.  The sketch is stored in panels of 16 bytes per
+ * value channel, U[B][H][r/P][V][P] with P = 4 columns (fp32) or P = 8
+ * (bf16, the paper's sketch storage; cfg.sketch_dtype): element (v, g) of
+ * the paper's V x r sketch (the output of basis query g at value channel v)
+ * sits at U[b][h][g/P][v][g%P], so each panel of the read is one contiguous,
+ * coalesced run.  A bf16 sketch is rounded from fp32 to nearest, ties to
+ * even.  Omega[H][K][r] and the coefficient map coef[H][r][K] (C, shared by
+ * the batch) are fp32.
  *
  * Memory.  Every pointer is a device pointer owned by the caller; the library
  * never allocates, frees or synchronises, keeps no per-call state and is
@@ -76,6 +79,7 @@ typedef struct {
   int32_t rank;     /* r sketch columns (the paper's G)                     */
   int32_t window;   /* W tokens per window = ring capacity                  */
   int32_t io_dtype; /* skssm_dtype of q, k, v and ring.k / ring.v           */
+  int32_t sketch_dtype; /* skssm_dtype of U (0 = fp32; BF16 halves its read) */
 } skssm_config;
 
 /* Replay buffer ("ring"): W slots per (b, h) item.  Slot s holds the s-th
@@ -140,12 +144,12 @@ typedef struct {
  * ring   read-only here: k, v, beta, log_decay of slots 0..n_buffered;
  *        g (KDA), u and bcoef (GDN, KDA) of slots 0..n_buffered-1.
  * q      [B][H][K] io_dtype, the current query.
- * U      [B][H][rank/4][V][4] fp32 output, panel layout (may be NULL when rank == 0).
+ * U      [B][H][rank/P][V][P] output in cfg.sketch_dtype, panel layout (may be NULL when rank == 0).
  * o      [B][H][V] fp32 output or NULL.
  * rank may be 0 here (no sketch: the flush of the exact baseline).
  */
 int sketchssm_update(const skssm_config* cfg, float* S, const float* omega, const skssm_ring* ring,
-                     int32_t n_buffered, const void* q, float* U, float* o, void* stream);
+                     int32_t n_buffered, const void* q, void* U, float* o, void* stream);
 
 /*
  * sketchssm_decode -- non-flush step (Algorithm 1, t < W) for the token in
@@ -154,12 +158,12 @@ int sketchssm_update(const skssm_config* cfg, float* S, const float* omega, cons
  *     c_t = C (e^{g_t} . q_t) - sum_{s<=t} a_{t,s} f_s        (eq. app-projected-query)
  *     o_t^buffer = sum_{s<=t} a_{t,s} u_s,  a_{t,s} = <exp(g_t - g_s) k_s, q_t>
  * (for MAMBA2 f_s = 0 and u_s = beta_s v_s, so c_t = e^{g_t} C q_t).  S is
- * never read.  U [B][H][rank/4][V][4] fp32 and coef [H][rank][K] fp32 (C;
+ * never read.  U [B][H][rank/P][V][P] (cfg.sketch_dtype) and coef [H][rank][K] fp32 (C;
  * Omega^T for the offline map of Sec. 4.1 at E0 = I) are read; for GDN/KDA
  * the derived fields of slot n_buffered (u, f, bcoef; KDA g) are written.
  * q [B][H][K] io_dtype; o [B][H][V] fp32.  rank must be > 0, window >= 2.
  */
-int sketchssm_decode(const skssm_config* cfg, const float* U, const float* coef, const skssm_ring* ring,
+int sketchssm_decode(const skssm_config* cfg, const void* U, const float* coef, const skssm_ring* ring,
                      int32_t n_buffered, const void* q, float* o, void* stream);
 
 /*

@@ -34,7 +34,7 @@ class SketchSSMError(RuntimeError):
 
 class Config(ctypes.Structure):
     _fields_ = [(name, ctypes.c_int32) for name in
-                ("kind", "batch", "heads", "dk", "dv", "rank", "window", "io_dtype")]
+                ("kind", "batch", "heads", "dk", "dv", "rank", "window", "io_dtype", "sketch_dtype")]
 
 
 class Ring(ctypes.Structure):
@@ -80,10 +80,13 @@ def ptr(x) -> int | None:
     return x.data_ptr()
 
 
-def make_config(kind, batch, heads, dk, dv, rank, window, io) -> Config:
+def _dtype(x) -> int:
+    return {"f32": F32, "bf16": BF16}[x] if isinstance(x, str) else int(x)
+
+
+def make_config(kind, batch, heads, dk, dv, rank, window, io, sketch="f32") -> Config:
     k = KIND_IDS[kind] if isinstance(kind, str) else int(kind)
-    d = {"f32": F32, "bf16": BF16}.get(io, io) if isinstance(io, str) else int(io)
-    return Config(k, batch, heads, dk, dv, rank, window, d)
+    return Config(k, batch, heads, dk, dv, rank, window, _dtype(io), _dtype(sketch))
 
 
 def make_ring(k=None, v=None, beta=None, log_decay=None, g=None, u=None, f=None, pi=None, bcoef=None) -> Ring:

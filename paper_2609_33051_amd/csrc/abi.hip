@@ -31,6 +31,8 @@ int check_shape(const skssm_config* c, bool need_rank, bool allow_rank0) {
   if (c->batch < 1 || c->heads < 1) return fail(SKSSM_EINVAL, "batch and heads must be >= 1");
   if ((int64_t)c->batch * c->heads > (int64_t)1 << 30) return fail(SKSSM_EINVAL, "batch*heads too large");
   if (c->io_dtype != SKSSM_F32 && c->io_dtype != SKSSM_BF16) return fail(SKSSM_EINVAL, "unknown io_dtype %d", c->io_dtype);
+  if (c->sketch_dtype != SKSSM_F32 && c->sketch_dtype != SKSSM_BF16)
+    return fail(SKSSM_EINVAL, "unknown sketch_dtype %d", c->sketch_dtype);
   if (c->window < 1 || c->window > 32) return fail(SKSSM_EUNSUPPORTED, "window %d outside 1..32", c->window);
   const bool kv_ok = (c->dk == 64 && c->dv == 64) || (c->dk == 128 && c->dv == 64) || (c->dk == 128 && c->dv == 128);
   if (!kv_ok) return fail(SKSSM_EUNSUPPORTED, "(dk, dv) = (%d, %d) not compiled", c->dk, c->dv);
@@ -113,7 +115,7 @@ const char* sketchssm_last_error(void) { return g_err; }
 int sketchssm_check_config(const skssm_config* cfg) { return check_shape(cfg, true, false); }
 
 int sketchssm_update(const skssm_config* cfg, float* S, const float* omega, const skssm_ring* ring,
-                     int32_t n_buffered, const void* q, float* U, float* o, void* stream) {
+                     int32_t n_buffered, const void* q, void* U, float* o, void* stream) {
   int rc = check_shape(cfg, true, true);
   if (rc) return rc;
   if (!S) return fail(SKSSM_EINVAL, "S is NULL");
@@ -154,14 +156,14 @@ int sketchssm_update(const skssm_config* cfg, float* S, const float* omega, cons
   }
   int r;
   switch (cfg->kind) {
-    case SKSSM_MAMBA2: r = skssm::run_update_mamba2(a, cfg->dk, cfg->dv, cfg->rank, cfg->io_dtype, stream); break;
-    case SKSSM_GDN: r = skssm::run_update_gdn(a, cfg->dk, cfg->dv, cfg->rank, cfg->io_dtype, stream); break;
-    default: r = skssm::run_update_kda(a, cfg->dk, cfg->dv, cfg->rank, cfg->io_dtype, stream); break;
+    case SKSSM_MAMBA2: r = skssm::run_update_mamba2(a, cfg->dk, cfg->dv, cfg->rank, cfg->io_dtype, cfg->sketch_dtype, stream); break;
+    case SKSSM_GDN: r = skssm::run_update_gdn(a, cfg->dk, cfg->dv, cfg->rank, cfg->io_dtype, cfg->sketch_dtype, stream); break;
+    default: r = skssm::run_update_kda(a, cfg->dk, cfg->dv, cfg->rank, cfg->io_dtype, cfg->sketch_dtype, stream); break;
   }
   return launched(r, "sketchssm_update");
 }
 
-int sketchssm_decode(const skssm_config* cfg, const float* U, const float* coef, const skssm_ring* ring,
+int sketchssm_decode(const skssm_config* cfg, const void* U, const float* coef, const skssm_ring* ring,
                      int32_t n_buffered, const void* q, float* o, void* stream) {
   int rc = check_shape(cfg, true, false);
   if (rc) return rc;
@@ -176,9 +178,9 @@ int sketchssm_decode(const skssm_config* cfg, const float* U, const float* coef,
   a.coef = coef;
   int r;
   switch (cfg->kind) {
-    case SKSSM_MAMBA2: r = skssm::run_decode_mamba2(a, cfg->dk, cfg->dv, cfg->rank, cfg->io_dtype, stream); break;
-    case SKSSM_GDN: r = skssm::run_decode_gdn(a, cfg->dk, cfg->dv, cfg->rank, cfg->io_dtype, stream); break;
-    default: r = skssm::run_decode_kda(a, cfg->dk, cfg->dv, cfg->rank, cfg->io_dtype, stream); break;
+    case SKSSM_MAMBA2: r = skssm::run_decode_mamba2(a, cfg->dk, cfg->dv, cfg->rank, cfg->io_dtype, cfg->sketch_dtype, stream); break;
+    case SKSSM_GDN: r = skssm::run_decode_gdn(a, cfg->dk, cfg->dv, cfg->rank, cfg->io_dtype, cfg->sketch_dtype, stream); break;
+    default: r = skssm::run_decode_kda(a, cfg->dk, cfg->dv, cfg->rank, cfg->io_dtype, cfg->sketch_dtype, stream); break;
   }
   return launched(r, "sketchssm_decode");
 }

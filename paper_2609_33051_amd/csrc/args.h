@@ -15,7 +15,7 @@ namespace skssm {
 struct DecodeArgs {
   int B, H, W, n;                 // batch, heads, window, slot of the current token
   const void* q;                  // [B][H][K] io, current query
-  const float* U;                 // [B][H][R/4][V][4]   (sketch read)
+  const void* U;                  // [B][H][R/P][V][P], P = 4 (fp32) or 8 (bf16)  (sketch read)
   const float* coef;              // [H][R][K]           (sketch read)
   const float* S;                 // [B][H][V][K]        (exact baseline)
   const void* rk;                 // ring [B][H][W][K] io      raw keys
@@ -43,20 +43,20 @@ struct UpdateArgs {
   const float* rg;                // KDA cumulative log decay, slots < n
   const float* ru;                // GDN/KDA pseudo-values, slots < n
   const float* rb;                // GDN/KDA erase couplings, slots < n
-  float* U;                       // [B][H][R/4][V][4] or NULL
+  void* U;                        // [B][H][R/P][V][P], P = 4 (fp32) or 8 (bf16), or NULL
   float* o;                       // [B][H][V] or NULL
 };
 
 // Host-side entry points of the per-family translation units.  Each returns
 // 0 after a launch, or -2 when the shape has no compiled kernel.
-int run_decode_mamba2(const DecodeArgs& a, int K, int V, int R, int io, void* stream);
-int run_decode_gdn(const DecodeArgs& a, int K, int V, int R, int io, void* stream);
-int run_decode_kda(const DecodeArgs& a, int K, int V, int R, int io, void* stream);
+int run_decode_mamba2(const DecodeArgs& a, int K, int V, int R, int io, int sk, void* stream);
+int run_decode_gdn(const DecodeArgs& a, int K, int V, int R, int io, int sk, void* stream);
+int run_decode_kda(const DecodeArgs& a, int K, int V, int R, int io, int sk, void* stream);
 int run_full_read_mamba2(const DecodeArgs& a, int K, int V, int io, void* stream);
 int run_full_read_gdn(const DecodeArgs& a, int K, int V, int io, void* stream);
 int run_full_read_kda(const DecodeArgs& a, int K, int V, int io, void* stream);
-int run_update_mamba2(const UpdateArgs& a, int K, int V, int R, int io, void* stream);
-int run_update_gdn(const UpdateArgs& a, int K, int V, int R, int io, void* stream);
-int run_update_kda(const UpdateArgs& a, int K, int V, int R, int io, void* stream);
+int run_update_mamba2(const UpdateArgs& a, int K, int V, int R, int io, int sk, void* stream);
+int run_update_gdn(const UpdateArgs& a, int K, int V, int R, int io, int sk, void* stream);
+int run_update_kda(const UpdateArgs& a, int K, int V, int R, int io, int sk, void* stream);
 
 }  // namespace skssm

@@ -245,14 +245,15 @@ __device__ __forceinline__ void append_derived(const DecodeArgs& a, size_t item,
   }
 }
 
-template <int KIND, int K, int V, int R, int WMAX, typename IO>
+template <int KIND, int K, int V, int R, int WMAX, typename IO, typename SK>
 __global__ __launch_bounds__(256) void decode_kernel(const DecodeArgs a) {
   using L = RowLoads<KIND, K, V, WMAX, IO>;
   constexpr bool ERASE = L::ERASE, CHAN = L::CHAN;
   constexpr int KPL = L::KPL, VR = L::VR, NG = L::NG, GD = L::GD;
   constexpr int VPL = V / 64;                    // value channels per lane (value layout)
   constexpr int RP = (R + 15) / 16;              // sketch components per lane (row layout)
-  constexpr int NP = R / 4;                      // 4-column sketch panels
+  constexpr int PW = 16 / (int)sizeof(SK);       // sketch columns per panel: 16 bytes per value
+  constexpr int NP = R / PW;                     // sketch panels
   constexpr int CP = K + 4;                      // padded LDS row pitch of C
   constexpr int KQ = K / 4;                      // channels each row covers in C x
   constexpr int WS = 2 * K + R + V + WMAX;       // per-wave LDS: x_q, x_k, c, o_buf, b row
@@ -270,7 +271,7 @@ __global__ __launch_bounds__(256) void decode_kernel(const DecodeArgs a) {
   const int b = (blockIdx.x / H) * 4 + wave;
   const bool valid = b < a.B;
   const size_t item = (size_t)(valid ? b : 0) * H + h;
-  const float* Ub = a.U + item * (size_t)V * R;
+  const SK* Ub = static_cast<const SK*>(a.U) + item * (size_t)V * R;
 
   // ---- C first, then every global load of this item
   constexpr int CQ = (R * K / 4 + 255) / 256;  // float4 of C per thread
@@ -283,7 +284,7 @@ __global__ __launch_bounds__(256) void decode_kernel(const DecodeArgs a) {
   compiler_fence();
   L r;
   float fs[ERASE ? NG : 1][RP];      // ring f of slot 4 gi + row, component col + 16 p
-  float4 Ur[VPL][UP];                // sketch panels (value layout)
+  Raw<SK, PW> Ur[VPL][UP];           // sketch panels (value layout)
   if (valid) {
     r.load(a, item, row, col);
     if constexpr (ERASE) {
@@ -305,7 +306,7 @@ __global__ __launch_bounds__(256) void decode_kernel(const DecodeArgs a) {
       for (int p = 0; p < NP; ++p)
 #pragma unroll
         for (int vv = 0; vv < VPL; ++vv)
-          Ur[vv][p] = reinterpret_cast<const float4*>(Ub)[(uint32_t)(p * V + lane + 64 * vv)];
+          Ur[vv][p].load(Ub + (uint32_t)((p * V + lane + 64 * vv) * PW));
     }
   }
 
@@ -405,11 +406,14 @@ __global__ __launch_bounds__(256) void decode_kernel(const DecodeArgs a) {
     float acc = ob_l[lane + 64 * vv];
 #pragma unroll
     for (int p = 0; p < NP; ++p) {
-      const float4 c4 = *reinterpret_cast<const float4*>(c_l + 4 * p);
-      float4 u4;
-      if constexpr (U_PRELOAD) u4 = Ur[vv][p];
-      else u4 = reinterpret_cast<const float4*>(Ub)[(uint32_t)(p * V + lane + 64 * vv)];
-      acc += u4.x * c4.x + u4.y * c4.y + u4.z * c4.z + u4.w * c4.w;
+      Raw<SK, PW> u;
+      if constexpr (U_PRELOAD) u = Ur[vv][p];
+      else u.load(Ub + (uint32_t)((p * V + lane + 64 * vv) * PW));
+#pragma unroll
+      for (int i = 0; i < PW; i += 4) {
+        const float4 c4 = *reinterpret_cast<const float4*>(c_l + PW * p + i);
+        acc += u.get(i) * c4.x + u.get(i + 1) * c4.y + u.get(i + 2) * c4.z + u.get(i + 3) * c4.w;
+      }
     }
     ob_g[lane + 64 * vv] = acc;
   }

@@ -40,6 +40,14 @@ template <> __device__ __forceinline__ void st_bits<float>(float* p, uint32_t of
 template <> __device__ __forceinline__ void st_bits<bf16_t>(bf16_t* p, uint32_t off, uint32_t x) {
   p[off] = (bf16_t)x;
 }
+// fp32 -> bf16 bits, round to nearest with ties to even (NaN payloads are
+// truncated, infinities kept).
+__device__ __forceinline__ uint32_t bf16_bits_rne(float x) {
+  uint32_t u = __float_as_uint(x);
+  if ((u & 0x7f800000u) != 0x7f800000u) u += 0x7fffu + ((u >> 16) & 1u);
+  return u >> 16;
+}
+
 template <typename IO> __device__ __forceinline__ float bits_f32(uint32_t x) {
   if constexpr (sizeof(IO) == 2) return bf16_lo(x);
   else return __uint_as_float(x);

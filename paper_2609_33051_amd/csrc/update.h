@@ -40,7 +40,7 @@ template <typename IO> __device__ __forceinline__ float load1(const IO* p);
 template <> __device__ __forceinline__ float load1<float>(const float* p) { return *p; }
 template <> __device__ __forceinline__ float load1<bf16_t>(const bf16_t* p) { return bf16_lo((uint32_t)*p); }
 
-template <int KIND, int K, int V, int R, int WMAX, typename IO>
+template <int KIND, int K, int V, int R, int WMAX, typename IO, typename SK>
 __global__ __launch_bounds__(256, 3) void update_kernel(const UpdateArgs a) {
   constexpr bool ERASE = KIND != MAMBA2;
   constexpr bool CHAN = KIND == KDA;
@@ -422,10 +422,18 @@ __global__ __launch_bounds__(256, 3) void update_kernel(const UpdateArgs a) {
                 w = (jj < R) ? om[(16 * kt + 4 * lg + i) * R + jj] : 0.f;
               acc = mfma4(w, xs[t][kt][i], acc);
             }
-          // 4-column panel 4 jt + lg of U[B][H][R/4][V][4]
-          if (16 * jt + 4 * lg < R)
-            reinterpret_cast<float4*>(a.U + item * (size_t)V * R)[(4 * jt + lg) * V + v] =
-                make_float4(acc[0], acc[1], acc[2], acc[3]);
+          // columns 16 jt + 4 lg .. +3 of value v; panels of 16 bytes per value:
+          // fp32 U[B][H][R/4][V][4], bf16 U[B][H][R/8][V][8]
+          if (16 * jt + 4 * lg < R) {
+            SK* Ui = static_cast<SK*>(a.U) + item * (size_t)V * R;
+            if constexpr (sizeof(SK) == 4) {
+              reinterpret_cast<float4*>(Ui)[(4 * jt + lg) * V + v] = make_float4(acc[0], acc[1], acc[2], acc[3]);
+            } else {
+              const uint2 w = make_uint2(bf16_bits_rne(acc[0]) | (bf16_bits_rne(acc[1]) << 16),
+                                         bf16_bits_rne(acc[2]) | (bf16_bits_rne(acc[3]) << 16));
+              reinterpret_cast<uint2*>(Ui)[((2 * jt + (lg >> 1)) * V + v) * 2 + (lg & 1)] = w;
+            }
+          }
         }
       }
     }

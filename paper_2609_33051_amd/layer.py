@@ -5,8 +5,9 @@ torch supplies device memory and the stream; every computation is a call
 into libsketchssm.so.  Buffers (caller-owned, as the ABI requires):
 
   S      [B][H][V][K]  fp32 full state (stored transposed: K contiguous)
-  U      [B][H][r/4][V][4] fp32 sketch U = S^T Omega in 4-column panels
-         (sketch_matrix() gives the [B][H][V][r] view)
+  U      [B][H][r/P][V][P] sketch U = S^T Omega in panels of 16 bytes per
+         value: P = 4 columns fp32, or P = 8 bf16 (sketch="bf16", the paper's
+         storage); sketch_matrix() gives the [B][H][V][r] fp32 view
   omega  [H][K][r]     fp32 sketching matrix, coef [H][r][K] its coefficient map
   ring   replay buffer of W slots per item:
          raw inputs k, v (io dtype), beta, log_decay ([..][K] for KDA), item-major
@@ -24,9 +25,9 @@ from . import binding as B
 class SketchSSMLayer:
     def __init__(self, kind: str, batch: int, heads: int, dk: int, dv: int, rank: int, window: int,
                  io: str = "bf16", device="cuda", baseline: bool = False, S: torch.Tensor | None = None,
-                 omega: torch.Tensor | None = None, coef: torch.Tensor | None = None):
+                 omega: torch.Tensor | None = None, coef: torch.Tensor | None = None, sketch: str = "f32"):
         self.kind, self.batch, self.heads, self.dk, self.dv = kind, batch, heads, dk, dv
-        self.rank, self.window, self.io, self.baseline = rank, window, io, baseline
+        self.rank, self.window, self.io, self.baseline, self.sketch = rank, window, io, baseline, sketch
         self.device = torch.device(device)
         iodt = torch.bfloat16 if io == "bf16" else torch.float32
         f32 = torch.float32
@@ -35,11 +36,13 @@ class SketchSSMLayer:
         dev = self.device
         self.S = S if S is not None else torch.zeros((Bt, H, V, K), dtype=f32, device=dev)
         r = 0 if baseline else rank
-        self.cfg = B.make_config(kind, Bt, H, K, V, r, W, io)
+        self.cfg = B.make_config(kind, Bt, H, K, V, r, W, io, sketch)
         if not baseline:
             self.omega = omega.to(dev).contiguous()
             self.coef = coef.to(dev).contiguous()
-            self.U = torch.zeros((Bt, H, rank // 4, V, 4), dtype=f32, device=dev)
+            P = 8 if sketch == "bf16" else 4
+            self.U = torch.zeros((Bt, H, rank // P, V, P), dtype=torch.bfloat16 if sketch == "bf16" else f32,
+                                 device=dev)
         else:
             self.omega = self.coef = self.U = None
         # raw inputs, written by the producer of each token
@@ -61,7 +64,7 @@ class SketchSSMLayer:
     def sketch_matrix(self) -> torch.Tensor:
         """The sketch as [B][H][V][r] (a copy; U itself is stored in panels)."""
         Bt, H, V, r = self.batch, self.heads, self.dv, self.rank
-        return self.U.permute(0, 1, 3, 2, 4).reshape(Bt, H, V, r)
+        return self.U.permute(0, 1, 3, 2, 4).reshape(Bt, H, V, r).float()
 
     @staticmethod
     def stream() -> int:

@@ -111,12 +111,15 @@ def main(argv=None):
     wl = inputs.WORKLOADS[a.workload]
     rank = wl.rank if a.rank is None else a.rank
     W = wl.window if a.window is None else a.window
-    shape = traffic.Shape(wl.kind, wl.dk, wl.dv, rank, W, 2 if wl.io == "bf16" else 4)
     items = wl.items
-    algo = {
-        "decode": sum(traffic.decode_bytes(shape, n) for n in range(W - 1)) / (W - 1) * items,
-        "full_read": sum(traffic.full_read_bytes(shape, n) for n in range(W - 1)) / (W - 1) * items,
-    }
+
+    def algo(entry, sketch):
+        sh = traffic.Shape(wl.kind, wl.dk, wl.dv, rank, W, 2 if wl.io == "bf16" else 4, 2 if sketch == "bf16" else 4)
+        if entry == "decode":
+            return sum(traffic.decode_bytes(sh, n) for n in range(W - 1)) / (W - 1) * items
+        if entry == "full_read":
+            return sum(traffic.full_read_bytes(sh, n) for n in range(W - 1)) / (W - 1) * items
+        return None
 
     stats = {}
     for r in _rows(a.trace, "_kernel_stats.csv"):
@@ -136,6 +139,11 @@ def main(argv=None):
             continue
         unit = f"{e}_{wl.kind}"
         digest = hip_build.source_digest(unit)
+        # sketch storage: the last template argument of decode/update (unsigned short = bf16)
+        targs = s[s.index("<") + 1:s.rindex(">")].split(", ")
+        sketch = "bf16" if (e != "full_read" and targs[-1] == "unsigned short") else "f32"
+        tag = ":bf16" if sketch == "bf16" else ""
+        ab = algo(e, sketch)
         fv, wv = fetch.get(s, []), write.get(s, [])
         lines = [
             f"# {s} on {a.workload} (rank {rank}, window {W})",
@@ -163,13 +171,13 @@ def main(argv=None):
                 f"    HBM bytes per launch (scaled): read {fm * 1024 * f_scale / 1e6:.2f} MB + "
                 f"write {wm * 1024 * w_scale / 1e6:.2f} MB = {hbm / 1e6:.2f} MB",
             ]
-            if e in algo:
-                lines.append(f"    algorithmic bytes per launch (mean over slots 0..{W - 2}): {algo[e] / 1e6:.2f} MB"
-                             f" -> measured / algorithmic = {hbm / algo[e]:.3f}")
-                table[f"{unit}:{a.workload}:r{rank}:w{W}"] = {
+            if ab is not None:
+                lines.append(f"    algorithmic bytes per launch (mean over slots 0..{W - 2}): {ab / 1e6:.2f} MB"
+                             f" -> measured / algorithmic = {hbm / ab:.3f}")
+                table[f"{unit}:{a.workload}:r{rank}:w{W}{tag}"] = {
                     "kernel": s, "digest": digest, "fetch_kib": round(fm, 1), "write_kib": round(wm, 1),
                     "fetch_scale": round(f_scale, 6), "write_scale": round(w_scale, 6),
-                    "dispatches": len(fv), "algorithmic_bytes": int(algo[e]),
+                    "dispatches": len(fv), "algorithmic_bytes": int(ab),
                 }
             elif not re.search(r"<\d+, \d+, \d+, 0,", s):
                 lines.append("    (initial-sketch and flush dispatches of this kernel are mixed in these means)")
@@ -178,6 +186,8 @@ def main(argv=None):
             if m:
                 lines += ["", "matrix cores (" + a.mfma_command + "):"] + m
         name = f"{e}_{a.workload}" + ("" if rank == wl.rank and W == wl.window else f"_r{rank}_w{W}")
+        if sketch == "bf16":
+            name += "_bf16sketch"
         if "<" in s and e == "update" and re.search(r"<\d+, \d+, \d+, 0,", s):
             name += "_rank0"
         with open(os.path.join(a.out, name + ".txt"), "w") as f:

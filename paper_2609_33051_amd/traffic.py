@@ -56,6 +56,7 @@ class Shape:
     rank: int
     window: int
     io_bytes: int  # 2 (bf16) or 4 (fp32)
+    sketch_bytes: int = 4  # U element: 4 (fp32) or 2 (bf16)
 
     @property
     def erase(self) -> bool:
@@ -96,9 +97,9 @@ def derived_write_bytes(s: Shape, n: int, baseline: bool = False) -> int:
 
 def decode_bytes(s: Shape, n: int) -> int:
     """Sketch read at slot n: the query, n earlier slots, the current slot, the
-    derived fields, U (fp32) and o."""
+    derived fields, U and o."""
     return (s.io_bytes * s.dk + n * slot_read_bytes(s) + current_read_bytes(s) + derived_write_bytes(s, n)
-            + 4 * s.dv * s.rank + 4 * s.dv)
+            + s.sketch_bytes * s.dv * s.rank + 4 * s.dv)
 
 
 def full_read_bytes(s: Shape, n: int) -> int:
@@ -119,12 +120,12 @@ def flush_bytes(s: Shape, n_buffered: int, rank: int | None = None) -> int:
         slot = s.io_bytes * (s.dk + s.dv) + 4 + 4
         bcoef = 0
     return (8 * s.dk * s.dv + n_buffered * slot + bcoef + current_read_bytes(s) + s.io_bytes * s.dk
-            + 4 * s.dv * r + 4 * s.dv)
+            + s.sketch_bytes * s.dv * r + 4 * s.dv)
 
 
 def init_bytes(s: Shape) -> int:
     """Sketch construction from S alone: S read + U write."""
-    return 4 * s.dk * s.dv + 4 * s.dv * s.rank
+    return 4 * s.dk * s.dv + s.sketch_bytes * s.dv * s.rank
 
 
 def window_bytes(s: Shape, baseline: bool = False) -> dict:

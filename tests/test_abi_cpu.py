@@ -64,9 +64,10 @@ ADDR = 1 << 20  # a 16-byte aligned fake address, never dereferenced (every case
 
 
 def cfg(**kw):
-    d = dict(kind="mamba2", batch=2, heads=4, dk=128, dv=64, rank=16, window=16, io="bf16")
+    d = dict(kind="mamba2", batch=2, heads=4, dk=128, dv=64, rank=16, window=16, io="bf16", sketch="f32")
     d.update(kw)
-    return B.make_config(d["kind"], d["batch"], d["heads"], d["dk"], d["dv"], d["rank"], d["window"], d["io"])
+    return B.make_config(d["kind"], d["batch"], d["heads"], d["dk"], d["dv"], d["rank"], d["window"], d["io"],
+                         d["sketch"])
 
 
 def good_ring(**kw):
@@ -105,6 +106,8 @@ class TestValidation:
         assert status(d, cfg(), None, ADDR, good_ring(), 0, ADDR, ADDR) == -1
         assert status(d, cfg(batch=0), ADDR, ADDR, good_ring(), 0, ADDR, ADDR) == -1
         assert status(d, cfg(io=5), ADDR, ADDR, good_ring(), 0, ADDR, ADDR) == -1
+        assert status(d, cfg(sketch=3), ADDR, ADDR, good_ring(), 0, ADDR, ADDR) == -1
+        assert "sketch_dtype" in B.sketchssm_last_error()
         assert "n_buffered" in B.sketchssm_status_string(-4)
 
     def test_update_rejections(self, lib):
@@ -118,6 +121,7 @@ class TestValidation:
         assert status(u, cfg(kind="kda", dv=128), ADDR, ADDR, good_ring(u=None), 15, ADDR, ADDR, ADDR) == -1
         assert status(u, cfg(), ADDR, ADDR, None, 15, ADDR, ADDR, ADDR) == -1  # ring needed when n > 0
         assert status(u, cfg(), ADDR, ADDR, good_ring(), 15, ADDR, ADDR, ADDR + 2) == -3
+        assert status(u, cfg(sketch=-1), ADDR, ADDR, good_ring(), 15, ADDR, ADDR, ADDR) == -1
 
     def test_full_read_rejections(self, lib):
         f = B.sketchssm_full_read_baseline

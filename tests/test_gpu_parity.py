@@ -27,14 +27,14 @@ def announce(msg):
     print(f"[case] {msg}", flush=True)
 
 
-def check(wl, window=None, rank=None, steps=None, sel=None, omega_coef=None, baseline=False):
+def check(wl, window=None, rank=None, steps=None, sel=None, omega_coef=None, baseline=False, sketch="f32"):
     window = wl.window if window is None else window
     rank = wl.rank if rank is None else rank
     announce(f"{wl.name} kind={wl.kind} B={wl.batch} H={wl.heads} K={wl.dk} V={wl.dv} r={rank} W={window} "
-             f"io={wl.io} baseline={baseline} sel={'all' if sel is None else len(sel)}")
+             f"io={wl.io} sketch={sketch} baseline={baseline} sel={'all' if sel is None else len(sel)}")
     run, layer, S_sel, heads, (om, C) = run_workload(wl, rank=rank, window=window, steps=steps, sel=sel,
-                                                     omega_coef=omega_coef, baseline=baseline)
-    ref = oracle_of(wl, run, S_sel, heads, om, C, window)
+                                                     omega_coef=omega_coef, baseline=baseline, sketch=sketch)
+    ref = oracle_of(wl, run, S_sel, heads, om, C, window, sketch=sketch)
     target = ref.o_exact_windowed if baseline else ref.o
     err = max_step_rel(run.o_gpu, target)
     n_items = wl.batch * wl.heads
@@ -44,7 +44,7 @@ def check(wl, window=None, rank=None, steps=None, sel=None, omega_coef=None, bas
     if not baseline:
         errU = rel_l2(to_np32(layer.sketch_matrix().reshape(n_items, wl.dv, rank)[idx]), ref.U_final)
     print(f"  max step rel-L2 {err:.3e}  state {errS:.3e}  sketch {errU:.3e}", flush=True)
-    tol = TOL[wl.io]
+    tol = TOL["bf16" if sketch == "bf16" else wl.io]  # a bf16 sketch is bf16 data
     assert err <= tol and errS <= tol and errU <= tol
     return run, ref, layer
 
@@ -182,3 +182,23 @@ def test_full_size_workload(name):
 def test_stress_workload(rank, window):
     wl = inputs.WORKLOADS["mamba2_b2048"]
     check(wl, rank=rank, window=window, steps=2 * window + 5, sel=sample_items(wl, 32))
+
+
+# --- the paper's sketch storage: U in bf16, rounded identically on both sides ----------------------
+@pytest.mark.parametrize("fam,K,V,rank,window,io", [
+    ("mamba2_form", 64, 64, 8, 8, "f32"),
+    ("mamba2", 128, 64, 16, 16, "bf16"),
+    ("gdn", 128, 128, 16, 16, "bf16"),
+    ("kda", 128, 128, 32, 8, "bf16"),
+    ("gdn", 64, 64, 32, 32, "f32"),
+])
+def test_bf16_sketch_small(fam, K, V, rank, window, io):
+    wl = inputs.tiny(fam, batch=5, heads=3, dk=K, dv=V, rank=rank, window=window, steps=2 * window + 3, io=io)
+    run, ref, layer = check(wl, sketch="bf16")
+    assert layer.U.dtype == torch.bfloat16
+
+
+@pytest.mark.parametrize("name", ["mamba2_b256", "gdn_b512", "kda_b512"])
+def test_bf16_sketch_full_size(name):
+    wl = inputs.WORKLOADS[name]
+    check(wl, sel=sample_items(wl), sketch="bf16")

@@ -51,6 +51,8 @@ def parse():
     p.add_argument("--no-paper-storage", action="store_true",
                    help="skip the extra timed pass with the bf16 sketch beside an fp32 headline")
     p.add_argument("--no-full-read", action="store_true", help="skip the exact baseline path")
+    p.add_argument("--no-standard", action="store_true",
+                   help="skip the Standard recurrence (window 1, no sketch: S read and written every token)")
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--cpu-seconds", type=float, default=12.0, help="target CPU time of the oracle sample")
     p.add_argument("--copy-calibration", action="store_true",
@@ -238,6 +240,47 @@ def main():
             "speedup_sketch_vs_full_read": round(value / (layer_steps / e_b), 3),
             "read_bytes_ratio": round(traffic.full_read_bytes(shape, 0) / traffic.decode_bytes(shape, 0), 3),
         }
+    # ---- Standard decoding: every token reads and writes the whole state (window 1, rank 0)
+    if not args.no_standard:
+        layers = []
+        for li in range(L):
+            S = inputs.initial_state(wl, dev, seed=inputs.SEED + li)
+            lay = SketchSSMLayer(wl.kind, wl.batch, wl.heads, wl.dk, wl.dv, 0, 1, wl.io, dev, baseline=True, S=S)
+            lay.write_token(pool[0], 0)
+            layers.append(lay)
+        plan = [lay.prepared_read(pool[0]["q"], 0) for lay in layers]
+        stream = torch.cuda.current_stream()
+        for _ in range(warm):
+            for call in plan:
+                call()
+        ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(K_steps)]
+        for e0, e1 in ev:
+            e0.record(stream)
+            e1.record(stream)
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for e0, e1 in ev:
+            e0.record(stream)
+            for call in plan:
+                call()
+            e1.record(stream)
+        torch.cuda.synchronize()
+        e_s = time.perf_counter() - t0
+        st_launch = sum(e0.elapsed_time(e1) for e0, e1 in ev) * 1e-3 / (K_steps * L)
+        sh1 = traffic.Shape(wl.kind, wl.dk, wl.dv, 0, 1, io_bytes)
+        st_bytes = traffic.flush_bytes(sh1, 0, 0) * items
+        std_value = layer_steps / e_s
+        out["standard"] = {
+            "value": round(std_value, 2), "unit": "steps/s", "launch_mean_us": round(st_launch * 1e6, 2),
+            "bytes_per_launch": st_bytes, "gbps": round(st_bytes / st_launch / 1e9, 1),
+            "frac": round(st_bytes / st_launch / 1e9 / traffic.HBM_PEAK_GBPS, 4),
+            "speedup_sketch_vs_standard": round(value / std_value, 3),
+        }
+        if "paper_storage" in out:
+            out["paper_storage"]["speedup_vs_standard"] = round(out["paper_storage"]["value"] / std_value, 3)
+        del layers, plan
+        torch.cuda.empty_cache()
+
     out["traffic_model"] = {
         "paper_R_G_bf16": round(traffic.paper_reduction(wl.dk, wl.dv, rank, W, 1 if shape.erase else 0), 3),
         "state_vs_sketch_read": round(wl.dk / rank, 3),

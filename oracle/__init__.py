@@ -49,6 +49,8 @@ class _Cfg(ctypes.Structure):
         ("T", ctypes.c_int32),
         ("round_storage", ctypes.c_int32),
         ("sketch_bf16", ctypes.c_int32),
+        ("pivots", ctypes.c_int32),
+        ("ridge", ctypes.c_float),
     ]
 
 
@@ -73,7 +75,7 @@ def _bind(lib):
     ip = ctypes.POINTER(ctypes.c_int32)
     lib.orc_recurrence.argtypes = [ctypes.POINTER(_Cfg), fp, fp, fp, fp, fp, fp, dp, dp]
     lib.orc_recurrence.restype = ctypes.c_int
-    lib.orc_sketchssm.argtypes = [ctypes.POINTER(_Cfg), ip, fp, fp, fp, fp, fp, fp, fp, fp, dp, dp, dp, dp, dp, dp]
+    lib.orc_sketchssm.argtypes = [ctypes.POINTER(_Cfg), ip, fp, fp, fp, fp, fp, fp, fp, fp, dp, dp, dp, dp, dp, dp, dp]
     lib.orc_sketchssm.restype = ctypes.c_int
     lib.orc_max_threads.restype = ctypes.c_int
     lib.orc_set_threads.argtypes = [ctypes.c_int]
@@ -160,6 +162,7 @@ class SketchResult:
     o_buf: np.ndarray        # [T][n][V] buffer term (0 at flushes)
     S_final: np.ndarray      # [n][V][K]
     U_final: np.ndarray      # [n][V][G]
+    coef_final: np.ndarray   # [n][G][K] the coefficient map in use at the end
 
     @property
     def o_exact_windowed(self) -> np.ndarray:
@@ -168,7 +171,7 @@ class SketchResult:
 
 
 def sketchssm(kind, W, heads, omega, coef, S_init, q, k, v, beta, log_decay, round_storage=False,
-              diagnostics=True, lib=None, sketch_bf16=False):
+              diagnostics=True, lib=None, sketch_bf16=False, pivots=0, ridge=0.1):
     """SketchSSM inference (Algorithm 1) in fp64.
 
     heads: [n] int, head index of every item (selects Omega / C); omega
@@ -176,6 +179,10 @@ def sketchssm(kind, W, heads, omega, coef, S_init, q, k, v, beta, log_decay, rou
     sketch (o_state_hat is then 0 between flushes).  round_storage stores the
     state and the sketch as fp32; sketch_bf16 stores the sketch as bf16
     (round to nearest, ties to even, through fp32), the paper's storage.
+    pivots > 0 replaces the given coef by the state-dependent coefficient map
+    with that many pivots and ridge term `ridge` (lambda), rebuilt from the
+    state at the start and at every flush; coef_final returns the map in use
+    at the end.
     """
     lib = lib or _load()
     n, K, V, T = _check_inputs(kind, S_init, q, k, v, beta, log_decay)
@@ -198,14 +205,16 @@ def sketchssm(kind, W, heads, omega, coef, S_init, q, k, v, beta, log_decay, rou
     ob, obp = _out((T, n, V), diagnostics)
     S, Sp = _out((n, V, K))
     U, Up = _out((n, V, G))
-    cfg = _Cfg(KINDS[kind], n, K, V, G, int(W), T, 1 if round_storage else 0, 1 if sketch_bf16 else 0)
+    Cf, Cfp = _out((n, G, K))
+    cfg = _Cfg(KINDS[kind], n, K, V, G, int(W), T, 1 if round_storage else 0, 1 if sketch_bf16 else 0,
+               int(pivots), float(ridge))
     rc = lib.orc_sketchssm(
         ctypes.byref(cfg),
         heads.ctypes.data_as(ctypes.POINTER(ctypes.c_int32)),
         keep_o[1], keep_c[1],
         *[p for _, p in keep],
-        op, ohp, osp, obp, Sp, Up,
+        op, ohp, osp, obp, Sp, Up, Cfp,
     )
     if rc != 0:
         raise RuntimeError(f"orc_sketchssm failed ({rc})")
-    return SketchResult(o, oh, os_, ob, S, U)
+    return SketchResult(o, oh, os_, ob, S, U, Cf)

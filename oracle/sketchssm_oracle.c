@@ -53,6 +53,8 @@ typedef struct {
   int32_t T;             /* decode steps                                    */
   int32_t round_storage; /* 1: state and sketch stored as fp32              */
   int32_t sketch_bf16;   /* 1: sketch stored as bf16 (the paper's storage)  */
+  int32_t pivots;        /* 0: the given map C; P > 0: state-dependent map  */
+  float ridge;           /* lambda of the state-dependent map               */
 } orc_cfg;
 
 /* Per-item views of the per-step inputs.  Step inputs are laid out
@@ -180,6 +182,167 @@ static void make_sketch(int K, int V, int G, const double* S, const float* omega
     }
 }
 
+/* ------------------------------------------------------------------------ */
+/* State-dependent coefficient map (Sec. 4.1, eq. m-coeff, solved with the   */
+/* ridge term and the low-rank-plus-diagonal state metric of the appendix    */
+/* "Low-Rank-Plus-Diagonal Approximation for the Coefficient Map"), in the   */
+/* paper's basis-aligned coordinates and order of steps:                     */
+/*   R       orthogonal K x K whose first G rows are Omega^T (Omega completed  */
+/*           by Gram-Schmidt over the unit vectors), J = first G coordinates */
+/*   S'      = R S,  mu = |S'|_F^2 / K (1 for a zero state),  H = S' S'^T/mu */
+/*   Q       orthonormal basis of the first p = min(G, P) columns of U       */
+/*           (Gram-Schmidt; a column dependent on the earlier ones is dropped)*/
+/*   L       = S' Q / sqrt(mu),  d_i = max(H_ii - |L_i|^2, 0)                */
+/*   Hhat    = L L^T + Diag(d)                                               */
+/*   c       = (J^T Hhat J + lambda I)^{-1} J^T Hhat x,  x = R q~            */
+/* so c = Cm q~ with Cm = (J^T Hhat J + lambda I)^{-1} J^T Hhat R (G x K),    */
+/* solved directly by Gaussian elimination with partial pivoting.            */
+/* ------------------------------------------------------------------------ */
+typedef struct {
+  double *R, *Sp, *H, *Q, *L, *d, *Hh, *A, *B;
+} orc_cmap_work;
+
+static int cmap_work_alloc(orc_cmap_work* w, int K, int V, int G)
+{
+  w->R = (double*)malloc(sizeof(double) * (size_t)K * K);
+  w->Sp = (double*)malloc(sizeof(double) * (size_t)K * V);
+  w->H = (double*)malloc(sizeof(double) * (size_t)K * K);
+  w->Q = (double*)malloc(sizeof(double) * (size_t)V * (G > 0 ? G : 1));
+  w->L = (double*)malloc(sizeof(double) * (size_t)K * (G > 0 ? G : 1));
+  w->d = (double*)malloc(sizeof(double) * (size_t)K);
+  w->Hh = (double*)malloc(sizeof(double) * (size_t)K * K);
+  w->A = (double*)malloc(sizeof(double) * (size_t)G * G + 1);
+  w->B = (double*)malloc(sizeof(double) * (size_t)G * K + 1);
+  return w->R && w->Sp && w->H && w->Q && w->L && w->d && w->Hh && w->A && w->B;
+}
+
+static void cmap_work_free(orc_cmap_work* w)
+{
+  free(w->R); free(w->Sp); free(w->H); free(w->Q); free(w->L); free(w->d); free(w->Hh); free(w->A); free(w->B);
+}
+
+/* Orthonormalise column vector x (length n, stride 1) against the m rows
+ * basis[0..m-1] (each length n); returns 1 and normalises x when it has a
+ * part outside their span, 0 when it is dependent on them. */
+static int gram_schmidt(double* x, const double* basis, int m, int n, double scale)
+{
+  for (int pass = 0; pass < 2; ++pass) /* twice, for a clean orthogonalisation */
+    for (int r = 0; r < m; ++r) {
+      double dot = 0.0;
+      for (int i = 0; i < n; ++i) dot += basis[(size_t)r * n + i] * x[i];
+      for (int i = 0; i < n; ++i) x[i] -= dot * basis[(size_t)r * n + i];
+    }
+  double nrm = 0.0;
+  for (int i = 0; i < n; ++i) nrm += x[i] * x[i];
+  nrm = sqrt(nrm);
+  if (!(nrm > 1e-12 * scale)) return 0;
+  for (int i = 0; i < n; ++i) x[i] /= nrm;
+  return 1;
+}
+
+static void coef_map(const orc_cfg* c, int K, int V, int G, const double* S, const float* Om, const double* U,
+                     double* Cm, orc_cmap_work* w)
+{
+  const int P = c->pivots, p = G < P ? G : P;
+  const double lambda = (double)c->ridge;
+  /* R: rows 0..G-1 = the columns of Omega, then unit vectors outside their span */
+  int m = 0;
+  double x[1024];
+  for (int g = 0; g < G; ++g) {
+    for (int kk = 0; kk < K; ++kk) x[kk] = (double)Om[(size_t)kk * G + g];
+    if (gram_schmidt(x, w->R, m, K, 1.0)) memcpy(w->R + (size_t)m++ * K, x, sizeof(double) * K);
+  }
+  for (int e = 0; e < K && m < K; ++e) {
+    for (int kk = 0; kk < K; ++kk) x[kk] = (kk == e) ? 1.0 : 0.0;
+    if (gram_schmidt(x, w->R, m, K, 1.0)) memcpy(w->R + (size_t)m++ * K, x, sizeof(double) * K);
+  }
+  /* S' = R S, mu, H */
+  double fro = 0.0;
+  for (int i = 0; i < K; ++i)
+    for (int j = 0; j < V; ++j) {
+      double acc = 0.0;
+      for (int kk = 0; kk < K; ++kk) acc += w->R[(size_t)i * K + kk] * S[(size_t)kk * V + j];
+      w->Sp[(size_t)i * V + j] = acc;
+      fro += acc * acc;
+    }
+  const double mu = fro > 0.0 ? fro / K : 1.0;
+  for (int i = 0; i < K; ++i)
+    for (int i2 = 0; i2 < K; ++i2) {
+      double acc = 0.0;
+      for (int j = 0; j < V; ++j) acc += w->Sp[(size_t)i * V + j] * w->Sp[(size_t)i2 * V + j];
+      w->H[(size_t)i * K + i2] = acc / mu;
+    }
+  /* Q: the first p columns of U, orthonormalised (stored as rows of length V) */
+  int pq = 0;
+  for (int a = 0; a < p; ++a) {
+    double nrm = 0.0;
+    for (int j = 0; j < V; ++j) {
+      x[j] = U[(size_t)j * G + a];
+      nrm += x[j] * x[j];
+    }
+    if (nrm > 0.0 && gram_schmidt(x, w->Q, pq, V, sqrt(nrm))) memcpy(w->Q + (size_t)pq++ * V, x, sizeof(double) * V);
+  }
+  /* L = S' Q / sqrt(mu) (K x pq), d, Hhat */
+  const double rs = 1.0 / sqrt(mu);
+  for (int i = 0; i < K; ++i)
+    for (int a = 0; a < pq; ++a) {
+      double acc = 0.0;
+      for (int j = 0; j < V; ++j) acc += w->Sp[(size_t)i * V + j] * w->Q[(size_t)a * V + j];
+      w->L[(size_t)i * pq + a] = acc * rs;
+    }
+  for (int i = 0; i < K; ++i) {
+    double l2 = 0.0;
+    for (int a = 0; a < pq; ++a) l2 += w->L[(size_t)i * pq + a] * w->L[(size_t)i * pq + a];
+    const double r = w->H[(size_t)i * K + i] - l2;
+    w->d[i] = r > 0.0 ? r : 0.0;
+  }
+  for (int i = 0; i < K; ++i)
+    for (int i2 = 0; i2 < K; ++i2) {
+      double acc = (i == i2) ? w->d[i] : 0.0;
+      for (int a = 0; a < pq; ++a) acc += w->L[(size_t)i * pq + a] * w->L[(size_t)i2 * pq + a];
+      w->Hh[(size_t)i * K + i2] = acc;
+    }
+  /* A = J^T Hhat J + lambda I (G x G);  B = J^T Hhat R (G x K) */
+  for (int g = 0; g < G; ++g) {
+    for (int g2 = 0; g2 < G; ++g2) w->A[(size_t)g * G + g2] = w->Hh[(size_t)g * K + g2] + (g == g2 ? lambda : 0.0);
+    for (int kk = 0; kk < K; ++kk) {
+      double acc = 0.0;
+      for (int i = 0; i < K; ++i) acc += w->Hh[(size_t)g * K + i] * w->R[(size_t)i * K + kk];
+      w->B[(size_t)g * K + kk] = acc;
+    }
+  }
+  /* Cm = A^{-1} B: Gaussian elimination with partial pivoting on [A | B] */
+  for (int col = 0; col < G; ++col) {
+    int piv = col;
+    for (int r = col + 1; r < G; ++r)
+      if (fabs(w->A[(size_t)r * G + col]) > fabs(w->A[(size_t)piv * G + col])) piv = r;
+    if (piv != col) {
+      for (int j = 0; j < G; ++j) {
+        const double t = w->A[(size_t)col * G + j];
+        w->A[(size_t)col * G + j] = w->A[(size_t)piv * G + j];
+        w->A[(size_t)piv * G + j] = t;
+      }
+      for (int j = 0; j < K; ++j) {
+        const double t = w->B[(size_t)col * K + j];
+        w->B[(size_t)col * K + j] = w->B[(size_t)piv * K + j];
+        w->B[(size_t)piv * K + j] = t;
+      }
+    }
+    const double inv = 1.0 / w->A[(size_t)col * G + col];
+    for (int r = 0; r < G; ++r) {
+      if (r == col) continue;
+      const double f = w->A[(size_t)r * G + col] * inv;
+      if (f == 0.0) continue;
+      for (int j = col; j < G; ++j) w->A[(size_t)r * G + j] -= f * w->A[(size_t)col * G + j];
+      for (int j = 0; j < K; ++j) w->B[(size_t)r * K + j] -= f * w->B[(size_t)col * K + j];
+    }
+  }
+  for (int g = 0; g < G; ++g) {
+    const double inv = 1.0 / w->A[(size_t)g * G + g];
+    for (int kk = 0; kk < K; ++kk) Cm[(size_t)g * K + kk] = w->B[(size_t)g * K + kk] * inv;
+  }
+}
+
 static void load_state(int K, int V, const float* S_vk, double* S)
 {
   for (int j = 0; j < V; ++j)
@@ -249,13 +412,17 @@ int orc_recurrence(const orc_cfg* c, const float* S_init, const float* q, const 
 /*   o_buf        [T][n][V]  buffer term (0 at flushes)                      */
 /*   S_final      [n][V][K]  the full state after the last flush             */
 /*   U_final      [n][V][G]  the sketch after the last flush                 */
+/*   coef_final   [n][G][K]  the coefficient map in use after the last flush */
+/* With c->pivots > 0 the map is state-dependent: built from the state and   */
+/* its (unrounded) sketch at the start and at every flush (coef_map above);  */
+/* otherwise it is the given C of the item's head.                           */
 /* The exact windowed output (what a full-state read would give) is         */
 /* o_state + o_buf at every step.                                           */
 /* ------------------------------------------------------------------------ */
 int orc_sketchssm(const orc_cfg* c, const int32_t* heads, const float* omega, const float* coef,
                   const float* S_init, const float* q, const float* k, const float* v, const float* beta,
                   const float* log_decay, double* o, double* o_state_hat, double* o_state, double* o_buf,
-                  double* S_final, double* U_final)
+                  double* S_final, double* U_final, double* coef_final)
 {
   if (!c || c->K <= 0 || c->V <= 0 || c->n_items <= 0 || c->T < 0 || c->W < 1 || c->G < 0) return -1;
   if (c->K > 1024 || c->V > 1024 || c->G > 1024) return -1;
@@ -268,6 +435,13 @@ int orc_sketchssm(const orc_cfg* c, const int32_t* heads, const float* omega, co
     const float* Cm = coef ? coef + (size_t)h * G * K : NULL;
     double* S0 = (double*)malloc(sizeof(double) * (size_t)K * V);
     double* U = (double*)malloc(sizeof(double) * ((size_t)V * (G > 0 ? G : 1)));
+    const int statedep = c->pivots > 0 && G > 0;
+    double* Cmi = statedep ? (double*)malloc(sizeof(double) * (size_t)G * K) : NULL;
+    orc_cmap_work cw = {0};
+    if (statedep && (!Cmi || !cmap_work_alloc(&cw, K, V, G))) {
+#pragma omp atomic write
+      err = -2;
+    }
     double* tmp = (double*)malloc(sizeof(double) * (size_t)(K + V));
     int* buf = (int*)malloc(sizeof(int) * (size_t)W);
     if (!S0 || !U || !tmp || !buf) {
@@ -280,6 +454,7 @@ int orc_sketchssm(const orc_cfg* c, const int32_t* heads, const float* omega, co
     /* Initialise the sketch from the prefill state (Algorithm 1). */
     if (G > 0) {
       make_sketch(K, V, G, S0, Om, U);
+      if (statedep && Cmi && cw.R) coef_map(c, K, V, G, S0, Om, U, Cmi, &cw);
       store_sketch(c, U, (size_t)V * G);
     }
     int len = 0; /* tokens in the buffer B */
@@ -298,7 +473,8 @@ int orc_sketchssm(const orc_cfg* c, const int32_t* heads, const float* omega, co
         if (G > 0) {
           for (int g = 0; g < G; ++g) {
             double acc = 0.0;
-            for (int kk = 0; kk < K; ++kk) acc += (double)Cm[(size_t)g * K + kk] * x[kk];
+            for (int kk = 0; kk < K; ++kk)
+              acc += (Cmi ? Cmi[(size_t)g * K + kk] : (double)Cm[(size_t)g * K + kk]) * x[kk];
             cvec[g] = acc;
           }
           for (int j = 0; j < V; ++j) {
@@ -333,6 +509,7 @@ int orc_sketchssm(const orc_cfg* c, const int32_t* heads, const float* omega, co
         read_state(K, V, S0, x, ostate);
         if (G > 0) {
           make_sketch(K, V, G, S0, Om, U);
+          if (statedep && Cmi && cw.R) coef_map(c, K, V, G, S0, Om, U, Cmi, &cw);
           store_sketch(c, U, (size_t)V * G);
         }
         for (int j = 0; j < V; ++j) {
@@ -346,6 +523,12 @@ int orc_sketchssm(const orc_cfg* c, const int32_t* heads, const float* omega, co
     }
     if (S_final) store_state(K, V, S0, S_final + (size_t)i * V * K);
     if (U_final && G > 0) memcpy(U_final + (size_t)i * V * G, U, sizeof(double) * (size_t)V * G);
+    if (coef_final && G > 0) {
+      for (size_t e = 0; e < (size_t)G * K; ++e)
+        coef_final[(size_t)i * G * K + e] = Cmi ? Cmi[e] : (double)Cm[e];
+    }
+    if (statedep) cmap_work_free(&cw);
+    free(Cmi);
     free(S0); free(U); free(tmp); free(buf);
   }
   return err;

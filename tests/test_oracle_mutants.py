@@ -43,6 +43,22 @@ def pins_hold(lib) -> bool:
     r = oracle.sketchssm("mamba2", W, np.zeros(n, np.int32), om, C, S0, q_in, k, v, beta, logd, lib=lib)
     if not np.allclose(r.o_state_hat, r.o_state, rtol=1e-6, atol=1e-6):
         return False
+    # the state-dependent coefficient map
+    from test_oracle_pins import coef_map_of, exact_ridge_map, low_rank_state
+    Sl = low_rank_state(2, 6, 8, 2, seed=2)
+    oml = heads_omega(1, 8, 5, seed=21)[0]
+    if not np.allclose(coef_map_of(Sl, oml, 2, 0.1, lib=lib), exact_ridge_map(Sl, oml, 0.1), rtol=1e-6, atol=1e-7):
+        return False
+    Sg = np.random.default_rng(12).standard_normal((2, 6, 8)).astype(np.float32)
+    omg = heads_omega(1, 8, 6, seed=7)[0]
+    perm = np.array([1, 0, 5, 2, 4, 3])
+    if not np.allclose(coef_map_of(Sg, np.ascontiguousarray(omg[:, :, perm]), 2, 0.1, lib=lib),
+                       coef_map_of(Sg, omg, 2, 0.1, lib=lib)[:, perm], rtol=1e-6, atol=1e-7):
+        return False
+    eye = np.eye(5, dtype=np.float32)[None]
+    Si = np.random.default_rng(4).standard_normal((2, 7, 5)).astype(np.float32)
+    if not np.allclose(coef_map_of(Si, eye, 3, 1e-9, lib=lib), np.broadcast_to(np.eye(5), (2, 5, 5)), atol=1e-6):
+        return False
     # the sketch must be refreshed from the updated state at each flush
     r = oracle.sketchssm("mamba2", 2, np.zeros(n, np.int32), om, C, S0, q_in, k, v, beta, logd, lib=lib)
     Uref = np.einsum("nvk,kg->nvg", r.S_final, om[0].astype(np.float64))
@@ -52,6 +68,11 @@ def pins_hold(lib) -> bool:
 
 
 MUTANTS = {
+    "coef_ridge_dropped": [("w->A[(size_t)g * G + g2] = w->Hh[(size_t)g * K + g2] + (g == g2 ? lambda : 0.0);",
+                            "w->A[(size_t)g * G + g2] = w->Hh[(size_t)g * K + g2];")],
+    "coef_metric_not_normalised": [("      w->H[(size_t)i * K + i2] = acc / mu;", "      w->H[(size_t)i * K + i2] = acc;")],
+    "coef_pivots_from_last_columns": [("      x[j] = U[(size_t)j * G + a];", "      x[j] = U[(size_t)j * G + (G - 1 - a)];")],
+    "coef_diagonal_dropped": [("      double acc = (i == i2) ? w->d[i] : 0.0;", "      double acc = 0.0;")],
     "erase_sign": [("S[(size_t)kk * V + j] -= beta * (double)k[kk] * tmpV[j];",
                     "S[(size_t)kk * V + j] += beta * (double)k[kk] * tmpV[j];")],
     "erase_before_decay_in_update": [
@@ -76,13 +97,14 @@ MUTANTS = {
     "buffer_drops_beta": [("const double w = tok_beta(&t, buf[s]) * a;", "const double w = a;")],
     "flush_drops_last_token": [("for (int s = 0; s < len; ++s) update_state(&t, buf[s], S0, tmp);",
                                 "for (int s = 0; s < len - 1; ++s) update_state(&t, buf[s], S0, tmp);")],
-    "coefficient_map_transposed": [("acc += (double)Cm[(size_t)g * K + kk] * x[kk];",
-                                    "acc += (double)Cm[(size_t)kk * G + g] * x[kk];")],
+    "coefficient_map_transposed": [("acc += (Cmi ? Cmi[(size_t)g * K + kk] : (double)Cm[(size_t)g * K + kk]) * x[kk];",
+                                    "acc += (Cmi ? Cmi[(size_t)g * K + kk] : (double)Cm[(size_t)kk * G + g]) * x[kk];")],
     "sketch_omega_transposed": [("acc += S[(size_t)kk * V + j] * (double)omega[(size_t)kk * G + g];",
                                  "acc += S[(size_t)kk * V + j] * (double)omega[(size_t)g * K + kk];")],
     "kda_channel_index": [("[((size_t)n * c->n_items + t->item) * c->K + kk]",
                            "[((size_t)n * c->n_items + t->item) * c->K + (c->K - 1 - kk)]")],
     "sketch_not_refreshed": [("        if (G > 0) {\n          make_sketch(K, V, G, S0, Om, U);\n"
+                              "          if (statedep && Cmi && cw.R) coef_map(c, K, V, G, S0, Om, U, Cmi, &cw);\n"
                               "          store_sketch(c, U, (size_t)V * G);\n        }\n"
                               "        for (int j = 0; j < V; ++j) {\n          if (o) o[oi + j] = ostate[j];",
                               "        for (int j = 0; j < V; ++j) {\n          if (o) o[oi + j] = ostate[j];")],

@@ -260,3 +260,98 @@ def test_bf16_sketch_is_the_one_read():
     qt = np.exp(logd[0].astype(np.float64))[:, None] * q[0].astype(np.float64)
     want = np.einsum("nvk,nk->nv", U, qt)
     assert np.allclose(r.o_state_hat[0], want, rtol=1e-12, atol=1e-12)
+
+
+# --- the state-dependent coefficient map (Sec. 4.1 eq. m-coeff; low-rank-plus-diagonal metric) ------
+def coef_map_of(S_vk, om, pivots, ridge, lib=None):
+    """The oracle's coefficient map for the states S_vk [n][V][K] (no flush:
+    the map is the one built from the initial state)."""
+    n, V, K = S_vk.shape
+    G = om.shape[2]
+    rng = np.random.default_rng(0)
+    q = rng.standard_normal((1, n, K)).astype(np.float32)
+    z = np.zeros((1, n, K), np.float32)
+    r = oracle.sketchssm("mamba2", 4, np.zeros(n, np.int32), om, np.ascontiguousarray(om.transpose(0, 2, 1)),
+                         S_vk.astype(np.float32), q, z, np.zeros((1, n, V), np.float32), np.zeros((1, n), np.float32),
+                         np.zeros((1, n), np.float32), pivots=pivots, ridge=ridge, lib=lib)
+    return r.coef_final
+
+
+def low_rank_state(n, V, K, rank, seed):
+    rng = np.random.default_rng(seed)
+    return np.einsum("nvr,nkr->nvk", rng.standard_normal((n, V, rank)), rng.standard_normal((n, K, rank))).astype(np.float32)
+
+
+def exact_ridge_map(S_vk, om, ridge):
+    """(U^T U / mu + lambda I)^{-1} U^T S^T / mu with U = S^T Omega: the ridge
+    solution under the exact state metric, solved by numpy."""
+    X = S_vk.astype(np.float64)
+    Om = om[0].astype(np.float64)
+    out = []
+    for Xi in X:
+        U = Xi @ Om
+        mu = (Xi ** 2).sum() / Xi.shape[1]
+        out.append(np.linalg.solve(U.T @ U / mu + ridge * np.eye(U.shape[1]), U.T @ Xi / mu))
+    return np.stack(out)
+
+
+@pytest.mark.parametrize("pivots,rank", [(2, 2), (4, 3), (4, 4)])
+def test_coef_map_is_the_exact_ridge_map_when_pivots_span_the_state(pivots, rank):
+    """When S^T lies in the span of the first p sketch columns, the pivot
+    metric reproduces the state metric (L L^T = H, d = 0), so the map is the
+    ridge solution of eq. m-coeff under the exact metric."""
+    K, V, G = 8, 6, 5
+    S = low_rank_state(3, V, K, rank, seed=rank)
+    om = heads_omega(1, K, G, seed=21)[0]
+    got = coef_map_of(S, om, pivots, 0.1)
+    # Omega is orthonormal to fp32 precision only; the oracle's basis completion
+    # re-orthonormalises it, which moves the map at the 1e-8 level
+    assert np.allclose(got, exact_ridge_map(S, om, 0.1), rtol=1e-6, atol=1e-7)
+
+
+def test_coef_map_is_invariant_to_value_rotation_and_state_scale():
+    """The metric H = S' S'^T / mu sees S only through S S^T and its norm, and
+    Q spans the same value subspace after a rotation: the map must not move."""
+    K, V, G = 7, 5, 4
+    rng = np.random.default_rng(8)
+    S = rng.standard_normal((2, V, K)).astype(np.float32)
+    O, _ = np.linalg.qr(rng.standard_normal((V, V)))
+    om = heads_omega(1, K, G, seed=3)[0]
+    base = coef_map_of(S, om, 2, 0.1)
+    rot = coef_map_of(np.einsum("uv,nvk->nuk", O, S.astype(np.float64)).astype(np.float32), om, 2, 0.1)
+    scaled = coef_map_of((S * 8.0).astype(np.float32), om, 2, 0.1)
+    assert np.allclose(rot, base, rtol=1e-5, atol=1e-6)   # the rotated state is rounded to fp32
+    assert np.allclose(scaled, base, rtol=1e-12, atol=1e-12)
+
+
+def test_coef_map_with_a_full_basis_tends_to_the_identity():
+    """Omega = I (G = K): the ridge solve is (Hhat + lambda I)^{-1} Hhat, the
+    identity as lambda -> 0, so the sketch read becomes exact."""
+    K, V = 5, 7
+    rng = np.random.default_rng(4)
+    S = rng.standard_normal((2, V, K)).astype(np.float32)
+    eye = np.eye(K, dtype=np.float32)[None]
+    got = coef_map_of(S, eye, 3, 1e-9)
+    assert np.allclose(got, np.broadcast_to(np.eye(K), got.shape), atol=1e-6)
+
+
+def test_coef_map_of_a_zero_state_is_zero():
+    """A zero state: mu = 1, no pivot columns, H = 0, so c = 0."""
+    om = heads_omega(1, 6, 3, seed=2)[0]
+    assert np.array_equal(coef_map_of(np.zeros((2, 4, 6), np.float32), om, 4, 0.1), np.zeros((2, 3, 6)))
+
+
+def test_coef_map_pivots_are_the_leading_sketch_columns():
+    """Q spans the first p sketch columns: reordering the other columns of
+    Omega (or the first p among themselves) reorders the rows of the map and
+    changes nothing else."""
+    K, V, G, p = 8, 6, 6, 2
+    rng = np.random.default_rng(12)
+    S = rng.standard_normal((2, V, K)).astype(np.float32)
+    om = heads_omega(1, K, G, seed=7)[0]
+    base = coef_map_of(S, om, p, 0.1)
+    perm = np.array([1, 0, 5, 2, 4, 3])
+    moved = coef_map_of(S, np.ascontiguousarray(om[:, :, perm]), p, 0.1)
+    assert np.allclose(moved, base[:, perm], rtol=1e-6, atol=1e-7)  # Omega orthonormal to fp32 only
+    other = np.array([2, 0, 1, 3, 4, 5])  # a different pair leads: the map must change
+    assert not np.allclose(coef_map_of(S, np.ascontiguousarray(om[:, :, other]), p, 0.1), base[:, other], atol=1e-6)

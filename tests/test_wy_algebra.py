@@ -91,3 +91,4 @@ def test_rank_w_flush(kind, W):
     Wv = np.stack([u[s] - X0 @ pis[s] for s in range(W)], axis=1)        # V x W
     XW = X0 * np.exp(g[-1])[None, :] + Wv @ L
     np.testing.assert_allclose(XW, S.T, atol=1e-12)
+

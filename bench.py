@@ -48,8 +48,10 @@ def parse():
     p.add_argument("--layers", type=int, default=4)
     p.add_argument("--sketch", choices=("f32", "bf16"), default="f32",
                    help="storage of the sketch U for the headline path (bf16: the paper's storage)")
+    p.add_argument("--pivots", type=int, choices=(0, 4), default=0,
+                   help="coefficient map of the headline path: 0 = offline (C = Omega^T), 4 = state-dependent")
     p.add_argument("--no-paper-storage", action="store_true",
-                   help="skip the extra timed pass with the bf16 sketch beside an fp32 headline")
+                   help="skip the extra timed passes with the paper's storage and method beside the headline")
     p.add_argument("--no-full-read", action="store_true", help="skip the exact baseline path")
     p.add_argument("--no-standard", action="store_true",
                    help="skip the Standard recurrence (window 1, no sketch: S read and written every token)")
@@ -86,19 +88,19 @@ def main():
     warm = -(-args.warmup // W) * W
     L = args.layers
     io_bytes = 2 if wl.io == "bf16" else 4
-    shape = traffic.Shape(wl.kind, wl.dk, wl.dv, rank, W, io_bytes, 2 if args.sketch == "bf16" else 4)
+    shape = traffic.Shape(wl.kind, wl.dk, wl.dv, rank, W, io_bytes, 2 if args.sketch == "bf16" else 4, args.pivots)
     items = wl.items
 
     om, C = inputs.omega(wl, rank)
     om_t, C_t = torch.as_tensor(om), torch.as_tensor(C)
     pool = [inputs.step_inputs(wl, t, dev) for t in range(W)]  # one window of resident inputs, reused
 
-    def make_layers(baseline, sketch):
+    def make_layers(baseline, sketch, pivots):
         layers = []
         for li in range(L):
             S = inputs.initial_state(wl, dev, seed=inputs.SEED + li)
             lay = SketchSSMLayer(wl.kind, wl.batch, wl.heads, wl.dk, wl.dv, rank, W, wl.io, dev,
-                                 baseline=baseline, S=S, omega=om_t, coef=C_t, sketch=sketch)
+                                 baseline=baseline, S=S, omega=om_t, coef=C_t, sketch=sketch, pivots=pivots)
             lay.init_sketch()
             for slot in range(W):  # the producer's writes: one window of tokens, resident in the ring
                 lay.write_token(pool[slot], slot)
@@ -123,8 +125,8 @@ def main():
         for lay in layers:
             lay.n = n_tokens % W
 
-    def timed(baseline, sketch=args.sketch):
-        layers = make_layers(baseline, sketch)
+    def timed(baseline, sketch=args.sketch, pivots=args.pivots):
+        layers = make_layers(baseline, sketch, pivots)
         stream = torch.cuda.current_stream()
         events = [(t % W, torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
                   for t in range(K_steps)]
@@ -144,9 +146,9 @@ def main():
         torch.cuda.empty_cache()
         return elapsed, per_n
 
-    def kernel_stats(per_n, sketch):
+    def kernel_stats(per_n, sketch, pivots):
         """Decode and flush figures from per-slot launch times (seconds)."""
-        sh = traffic.Shape(wl.kind, wl.dk, wl.dv, rank, W, io_bytes, 2 if sketch == "bf16" else 4)
+        sh = traffic.Shape(wl.kind, wl.dk, wl.dv, rank, W, io_bytes, 2 if sketch == "bf16" else 4, pivots)
         dec_n = [n for n in per_n if n < W - 1]
         dec_time = sum(sum(per_n[n]) for n in dec_n)
         dec_launches = sum(len(per_n[n]) for n in dec_n)
@@ -165,8 +167,8 @@ def main():
     elapsed, per_n = timed(False)
     layer_steps = K_steps * L
     value = layer_steps / elapsed
-    ks = kernel_stats(per_n, args.sketch)
-    traffic_rec = recorded_traffic("decode", wl, rank, W, args.sketch)
+    ks = kernel_stats(per_n, args.sketch, args.pivots)
+    traffic_rec = recorded_traffic("decode", wl, rank, W, args.sketch, args.pivots)
     dec_mean_s, dec_bytes_per_launch, dec_gbps = ks["dec_mean"], ks["dec_bytes"], ks["dec_gbps"]
     fl_mean_s, fl_bytes, window_s = ks["fl_mean"], ks["fl_bytes"], ks["window"]
 
@@ -185,6 +187,7 @@ def main():
         "data": "synthetic",
         "config": {"workload": wl.name, "kind": wl.kind, "batch": wl.batch, "heads": wl.heads, "dk": wl.dk,
                    "dv": wl.dv, "rank": rank, "window": W, "io": wl.io, "state": "f32", "sketch": args.sketch,
+                   "pivots": args.pivots,
                    "layers_rotated": L},
         "roofline": {
             "kernel": "decode_kernel (sketchssm_decode)",
@@ -209,18 +212,21 @@ def main():
         },
     }
 
-    # ---- the paper's sketch storage (bf16 U) beside an fp32 headline, same inputs
-    if args.sketch == "f32" and not args.no_paper_storage:
-        e_p, per_p = timed(False, "bf16")
-        kp = kernel_stats(per_p, "bf16")
-        tr = recorded_traffic("decode", wl, rank, W, "bf16")
-        out["paper_storage"] = {
-            "sketch": "bf16", "value": round(layer_steps / e_p, 2), "unit": "steps/s",
-            "decode_mean_us": round(kp["dec_mean"] * 1e6, 2), "decode_bytes_per_launch": int(kp["dec_bytes"]),
-            "decode_gbps": round(kp["dec_gbps"], 1), "decode_frac": round(kp["dec_gbps"] / traffic.HBM_PEAK_GBPS, 4),
-            "decode_traffic": tr and tr["bytes_per_launch"],
-            "flush_mean_us": round(kp["fl_mean"] * 1e6, 2), "window_avg_steps_per_s": round(W / kp["window"], 1),
-        }
+    # ---- beside an offline-map fp32 headline, same inputs: the paper's sketch
+    # storage (bf16 U), and its method (bf16 U with the state-dependent map)
+    if args.sketch == "f32" and args.pivots == 0 and not args.no_paper_storage:
+        for key, sk_, pv in (("paper_storage", "bf16", 0), ("paper_method", "bf16", 4)):
+            e_p, per_p = timed(False, sk_, pv)
+            kp = kernel_stats(per_p, sk_, pv)
+            tr = recorded_traffic("decode", wl, rank, W, sk_, pv)
+            out[key] = {
+                "sketch": sk_, "pivots": pv, "value": round(layer_steps / e_p, 2), "unit": "steps/s",
+                "decode_mean_us": round(kp["dec_mean"] * 1e6, 2), "decode_bytes_per_launch": int(kp["dec_bytes"]),
+                "decode_gbps": round(kp["dec_gbps"], 1),
+                "decode_frac": round(kp["dec_gbps"] / traffic.HBM_PEAK_GBPS, 4),
+                "decode_traffic": tr and tr["bytes_per_launch"],
+                "flush_mean_us": round(kp["fl_mean"] * 1e6, 2), "window_avg_steps_per_s": round(W / kp["window"], 1),
+            }
 
     # ---- the exact full-state-read baseline (same inputs; flush with rank 0)
     if not args.no_full_read:
@@ -276,8 +282,9 @@ def main():
             "frac": round(st_bytes / st_launch / 1e9 / traffic.HBM_PEAK_GBPS, 4),
             "speedup_sketch_vs_standard": round(value / std_value, 3),
         }
-        if "paper_storage" in out:
-            out["paper_storage"]["speedup_vs_standard"] = round(out["paper_storage"]["value"] / std_value, 3)
+        for key in ("paper_storage", "paper_method"):
+            if key in out:
+                out[key]["speedup_vs_standard"] = round(out[key]["value"] / std_value, 3)
         del layers, plan
         torch.cuda.empty_cache()
 
@@ -304,7 +311,7 @@ def main():
     return 0
 
 
-def recorded_traffic(entry, wl, rank, W, sketch="f32"):
+def recorded_traffic(entry, wl, rank, W, sketch="f32", pivots=0):
     """HBM bytes per launch of the `entry` kernel ("decode", ...) on this
     workload, from the FETCH_SIZE and WRITE_SIZE counter runs recorded under
     profiles/, each scaled by the factor a plain copy kernel's counters gave
@@ -318,7 +325,8 @@ def recorded_traffic(entry, wl, rank, W, sketch="f32"):
     with open(path) as f:
         table = json.load(f)
     unit = f"{entry}_{wl.kind}"
-    rec = table.get(f"{unit}:{wl.name}:r{rank}:w{W}" + (":bf16" if sketch == "bf16" else ""))
+    rec = table.get(f"{unit}:{wl.name}:r{rank}:w{W}" + (":bf16" if sketch == "bf16" else "")
+                    + (f":p{pivots}" if pivots else ""))
     if rec is None or rec.get("digest") != hip_build.source_digest(unit):
         return None
     b = rec["fetch_kib"] * 1024 * rec["fetch_scale"] + rec["write_kib"] * 1024 * rec["write_scale"]

@@ -80,6 +80,10 @@ typedef struct {
   int32_t window;   /* W tokens per window = ring capacity                  */
   int32_t io_dtype; /* skssm_dtype of q, k, v and ring.k / ring.v           */
   int32_t sketch_dtype; /* skssm_dtype of U (0 = fp32; BF16 halves its read) */
+  int32_t pivots;   /* 0: the coefficient map is `coef` (offline, shared per head);
+                       4: state-dependent map with P = 4 pivots, rebuilt from the
+                       state by every sketchssm_update into `cmap` (rank 8..32)   */
+  float ridge;      /* lambda of the state-dependent map (the paper uses 0.1)     */
 } skssm_config;
 
 /* Replay buffer ("ring"): W slots per (b, h) item.  Slot s holds the s-th
@@ -145,11 +149,17 @@ typedef struct {
  *        g (KDA), u and bcoef (GDN, KDA) of slots 0..n_buffered-1.
  * q      [B][H][K] io_dtype, the current query.
  * U      [B][H][rank/P][V][P] output in cfg.sketch_dtype, panel layout (may be NULL when rank == 0).
+ * cmap   cfg.pivots = 4: [B][H][4K + 4 rank + rank^2] fp32 output, the
+ *        state-dependent coefficient map of Sec. 4.1 (eq. m-coeff with the
+ *        ridge term and the P = 4 low-rank-plus-diagonal state metric of the
+ *        appendix on the coefficient map), built from S_W and U and stored
+ *        factored as M [4][K], F1 [rank][4], F2 [rank][rank] with
+ *        C = F1 M + F2 Omega^T; ignored (may be NULL) when pivots = 0.
  * o      [B][H][V] fp32 output or NULL.
  * rank may be 0 here (no sketch: the flush of the exact baseline).
  */
 int sketchssm_update(const skssm_config* cfg, float* S, const float* omega, const skssm_ring* ring,
-                     int32_t n_buffered, const void* q, void* U, float* o, void* stream);
+                     int32_t n_buffered, const void* q, void* U, float* cmap, float* o, void* stream);
 
 /*
  * sketchssm_decode -- non-flush step (Algorithm 1, t < W) for the token in
@@ -161,10 +171,13 @@ int sketchssm_update(const skssm_config* cfg, float* S, const float* omega, cons
  * never read.  U [B][H][rank/P][V][P] (cfg.sketch_dtype) and coef [H][rank][K] fp32 (C;
  * Omega^T for the offline map of Sec. 4.1 at E0 = I) are read; for GDN/KDA
  * the derived fields of slot n_buffered (u, f, bcoef; KDA g) are written.
- * q [B][H][K] io_dtype; o [B][H][V] fp32.  rank must be > 0, window >= 2.
+ * With cfg.pivots = 4 the map is the state-dependent one that the last
+ * sketchssm_update wrote to cmap, C = F1 M + F2 coef, and coef must then be
+ * Omega^T.  q [B][H][K] io_dtype; o [B][H][V] fp32.  rank must be > 0,
+ * window >= 2.
  */
-int sketchssm_decode(const skssm_config* cfg, const void* U, const float* coef, const skssm_ring* ring,
-                     int32_t n_buffered, const void* q, float* o, void* stream);
+int sketchssm_decode(const skssm_config* cfg, const void* U, const float* coef, const float* cmap,
+                     const skssm_ring* ring, int32_t n_buffered, const void* q, float* o, void* stream);
 
 /*
  * sketchssm_full_read_baseline -- exact non-flush step that reads all of S

@@ -34,7 +34,8 @@ class SketchSSMError(RuntimeError):
 
 class Config(ctypes.Structure):
     _fields_ = [(name, ctypes.c_int32) for name in
-                ("kind", "batch", "heads", "dk", "dv", "rank", "window", "io_dtype", "sketch_dtype")]
+                ("kind", "batch", "heads", "dk", "dv", "rank", "window", "io_dtype", "sketch_dtype", "pivots")] + [
+                   ("ridge", ctypes.c_float)]
 
 
 class Ring(ctypes.Structure):
@@ -57,8 +58,8 @@ def load(path: str | None = None):
     P = ctypes.c_void_p
     cfgp = ctypes.POINTER(Config)
     ringp = ctypes.POINTER(Ring)
-    lib.sketchssm_update.argtypes = [cfgp, P, P, ringp, ctypes.c_int32, P, P, P, P]
-    lib.sketchssm_decode.argtypes = [cfgp, P, P, ringp, ctypes.c_int32, P, P, P]
+    lib.sketchssm_update.argtypes = [cfgp, P, P, ringp, ctypes.c_int32, P, P, P, P, P]
+    lib.sketchssm_decode.argtypes = [cfgp, P, P, P, ringp, ctypes.c_int32, P, P, P]
     lib.sketchssm_full_read_baseline.argtypes = [cfgp, P, ringp, ctypes.c_int32, P, P, P]
     for f in ("sketchssm_update", "sketchssm_decode", "sketchssm_full_read_baseline", "sketchssm_check_config"):
         getattr(lib, f).restype = ctypes.c_int
@@ -84,9 +85,15 @@ def _dtype(x) -> int:
     return {"f32": F32, "bf16": BF16}[x] if isinstance(x, str) else int(x)
 
 
-def make_config(kind, batch, heads, dk, dv, rank, window, io, sketch="f32") -> Config:
+def make_config(kind, batch, heads, dk, dv, rank, window, io, sketch="f32", pivots=0, ridge=0.1) -> Config:
     k = KIND_IDS[kind] if isinstance(kind, str) else int(kind)
-    return Config(k, batch, heads, dk, dv, rank, window, _dtype(io), _dtype(sketch))
+    return Config(k, batch, heads, dk, dv, rank, window, _dtype(io), _dtype(sketch), int(pivots), float(ridge))
+
+
+def cmap_width(cfg: Config) -> int:
+    """Floats per item of the state-dependent coefficient map (M, F1, F2)."""
+    p, K, r = cfg.pivots, cfg.dk, cfg.rank
+    return p * K + r * p + r * r if p else 0
 
 
 def make_ring(k=None, v=None, beta=None, log_decay=None, g=None, u=None, f=None, pi=None, bcoef=None) -> Ring:
@@ -120,17 +127,18 @@ def _vp(x):
     return None if p is None else ctypes.c_void_p(p)
 
 
-def prepare_update(cfg: Config, S, omega, ring: Ring | None, n_buffered: int, q, U, o, stream=None) -> Prepared:
+def prepare_update(cfg: Config, S, omega, ring: Ring | None, n_buffered: int, q, U, o, stream=None,
+                   cmap=None) -> Prepared:
     lib = load()
     args = (ctypes.byref(cfg), _vp(S), _vp(omega), ctypes.byref(ring) if ring else None, ctypes.c_int32(n_buffered),
-            _vp(q), _vp(U), _vp(o), _vp(stream))
+            _vp(q), _vp(U), _vp(cmap), _vp(o), _vp(stream))
     return Prepared(lib.sketchssm_update, args, (cfg, ring))
 
 
-def prepare_decode(cfg: Config, U, coef, ring: Ring, n_buffered: int, q, o, stream=None) -> Prepared:
+def prepare_decode(cfg: Config, U, coef, ring: Ring, n_buffered: int, q, o, stream=None, cmap=None) -> Prepared:
     lib = load()
-    args = (ctypes.byref(cfg), _vp(U), _vp(coef), ctypes.byref(ring), ctypes.c_int32(n_buffered), _vp(q), _vp(o),
-            _vp(stream))
+    args = (ctypes.byref(cfg), _vp(U), _vp(coef), _vp(cmap), ctypes.byref(ring), ctypes.c_int32(n_buffered), _vp(q),
+            _vp(o), _vp(stream))
     return Prepared(lib.sketchssm_decode, args, (cfg, ring))
 
 
@@ -140,15 +148,15 @@ def prepare_full_read_baseline(cfg: Config, S, ring: Ring, n_buffered: int, q, o
     return Prepared(lib.sketchssm_full_read_baseline, args, (cfg, ring))
 
 
-def sketchssm_update(cfg: Config, S, omega, ring: Ring | None, n_buffered: int, q, U, o, stream=None):
+def sketchssm_update(cfg: Config, S, omega, ring: Ring | None, n_buffered: int, q, U, o, stream=None, cmap=None):
     lib = load()
     _check(lib.sketchssm_update(ctypes.byref(cfg), ptr(S), ptr(omega), ctypes.byref(ring) if ring else None,
-                                int(n_buffered), ptr(q), ptr(U), ptr(o), stream))
+                                int(n_buffered), ptr(q), ptr(U), ptr(cmap), ptr(o), stream))
 
 
-def sketchssm_decode(cfg: Config, U, coef, ring: Ring, n_buffered: int, q, o, stream=None):
+def sketchssm_decode(cfg: Config, U, coef, ring: Ring, n_buffered: int, q, o, stream=None, cmap=None):
     lib = load()
-    _check(lib.sketchssm_decode(ctypes.byref(cfg), ptr(U), ptr(coef), ctypes.byref(ring) if ring else None,
+    _check(lib.sketchssm_decode(ctypes.byref(cfg), ptr(U), ptr(coef), ptr(cmap), ctypes.byref(ring) if ring else None,
                                 int(n_buffered), ptr(q), ptr(o), stream))
 
 

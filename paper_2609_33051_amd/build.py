@@ -44,11 +44,13 @@ KERNEL_HEADERS = {"decode": "decode.h", "full_read": "decode.h", "update": "upda
 
 def unit_sources(unit: str) -> list[str]:
     """The files whose text decides the machine code of one unit's kernels
-    (unit = "decode_mamba2", "update_gdn", ...): the unit, the shared device
-    and argument headers, the launch table and the kernel's own header."""
+    (unit = "decode_mamba2", "update_gdn", ...): its translation units (the
+    dispatcher and one per shape), the shared device and argument headers,
+    the launch table and the kernel's own header."""
     entry = unit.rsplit("_", 1)[0]
     names = ["device.h", "args.h", "dispatch.h", KERNEL_HEADERS[entry]]
-    return [os.path.join(CSRC, "units", unit + ".hip")] + [os.path.join(CSRC, n) for n in names]
+    units = sorted(glob.glob(os.path.join(CSRC, "units", unit + ".hip")) + glob.glob(os.path.join(CSRC, "units", unit + "_*.hip")))
+    return units + [os.path.join(CSRC, n) for n in names]
 
 
 def source_digest(unit: str) -> str:

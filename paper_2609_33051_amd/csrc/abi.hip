@@ -33,6 +33,8 @@ int check_shape(const skssm_config* c, bool need_rank, bool allow_rank0) {
   if (c->io_dtype != SKSSM_F32 && c->io_dtype != SKSSM_BF16) return fail(SKSSM_EINVAL, "unknown io_dtype %d", c->io_dtype);
   if (c->sketch_dtype != SKSSM_F32 && c->sketch_dtype != SKSSM_BF16)
     return fail(SKSSM_EINVAL, "unknown sketch_dtype %d", c->sketch_dtype);
+  if (c->pivots != 0 && c->pivots != 4) return fail(SKSSM_EUNSUPPORTED, "pivots %d: 0 or 4 are compiled", c->pivots);
+  if (c->pivots && !(c->ridge >= 0.f && c->ridge < 1e30f)) return fail(SKSSM_EINVAL, "ridge must be finite and >= 0");
   if (c->window < 1 || c->window > 32) return fail(SKSSM_EUNSUPPORTED, "window %d outside 1..32", c->window);
   const bool kv_ok = (c->dk == 64 && c->dv == 64) || (c->dk == 128 && c->dv == 64) || (c->dk == 128 && c->dv == 128);
   if (!kv_ok) return fail(SKSSM_EUNSUPPORTED, "(dk, dv) = (%d, %d) not compiled", c->dk, c->dv);
@@ -115,9 +117,14 @@ const char* sketchssm_last_error(void) { return g_err; }
 int sketchssm_check_config(const skssm_config* cfg) { return check_shape(cfg, true, false); }
 
 int sketchssm_update(const skssm_config* cfg, float* S, const float* omega, const skssm_ring* ring,
-                     int32_t n_buffered, const void* q, void* U, float* o, void* stream) {
+                     int32_t n_buffered, const void* q, void* U, float* cmap, float* o, void* stream) {
   int rc = check_shape(cfg, true, true);
   if (rc) return rc;
+  if (cfg->pivots) {
+    if (cfg->rank < 8 || cfg->rank > 32) return fail(SKSSM_EUNSUPPORTED, "pivot maps need rank 8..32");
+    if (!cmap) return fail(SKSSM_EINVAL, "cmap is required when pivots > 0");
+    if (!aligned(cmap)) return fail(SKSSM_EALIGN, "cmap not aligned");
+  }
   if (!S) return fail(SKSSM_EINVAL, "S is NULL");
   if (!aligned(S)) return fail(SKSSM_EALIGN, "S not aligned");
   if (cfg->rank > 0) {
@@ -133,6 +140,8 @@ int sketchssm_update(const skssm_config* cfg, float* S, const float* omega, cons
   a.S = S;
   a.omega = omega;
   a.U = cfg->rank > 0 ? U : nullptr;
+  a.cmap = cfg->pivots ? cmap : nullptr;
+  a.ridge = cfg->ridge;
   if (q) {
     if (n_buffered < 0 || n_buffered > cfg->window - 1)
       return fail(SKSSM_ESTATE, "n_buffered %d outside 0..%d", n_buffered, cfg->window - 1);
@@ -156,17 +165,22 @@ int sketchssm_update(const skssm_config* cfg, float* S, const float* omega, cons
   }
   int r;
   switch (cfg->kind) {
-    case SKSSM_MAMBA2: r = skssm::run_update_mamba2(a, cfg->dk, cfg->dv, cfg->rank, cfg->io_dtype, cfg->sketch_dtype, stream); break;
-    case SKSSM_GDN: r = skssm::run_update_gdn(a, cfg->dk, cfg->dv, cfg->rank, cfg->io_dtype, cfg->sketch_dtype, stream); break;
-    default: r = skssm::run_update_kda(a, cfg->dk, cfg->dv, cfg->rank, cfg->io_dtype, cfg->sketch_dtype, stream); break;
+    case SKSSM_MAMBA2: r = skssm::run_update_mamba2(a, cfg->dk, cfg->dv, cfg->rank, cfg->io_dtype, cfg->sketch_dtype, cfg->pivots, stream); break;
+    case SKSSM_GDN: r = skssm::run_update_gdn(a, cfg->dk, cfg->dv, cfg->rank, cfg->io_dtype, cfg->sketch_dtype, cfg->pivots, stream); break;
+    default: r = skssm::run_update_kda(a, cfg->dk, cfg->dv, cfg->rank, cfg->io_dtype, cfg->sketch_dtype, cfg->pivots, stream); break;
   }
   return launched(r, "sketchssm_update");
 }
 
-int sketchssm_decode(const skssm_config* cfg, const void* U, const float* coef, const skssm_ring* ring,
-                     int32_t n_buffered, const void* q, float* o, void* stream) {
+int sketchssm_decode(const skssm_config* cfg, const void* U, const float* coef, const float* cmap,
+                     const skssm_ring* ring, int32_t n_buffered, const void* q, float* o, void* stream) {
   int rc = check_shape(cfg, true, false);
   if (rc) return rc;
+  if (cfg->pivots) {
+    if (cfg->rank < 8 || cfg->rank > 32) return fail(SKSSM_EUNSUPPORTED, "pivot maps need rank 8..32");
+    if (!cmap) return fail(SKSSM_EINVAL, "cmap is required when pivots > 0");
+    if (!aligned(cmap)) return fail(SKSSM_EALIGN, "cmap not aligned");
+  }
   if (cfg->window < 2) return fail(SKSSM_EINVAL, "decode needs window >= 2 (window 1 flushes every token)");
   if (n_buffered < 0 || n_buffered > cfg->window - 2)
     return fail(SKSSM_ESTATE, "n_buffered %d outside 0..%d", n_buffered, cfg->window - 2);
@@ -176,11 +190,12 @@ int sketchssm_decode(const skssm_config* cfg, const void* U, const float* coef, 
   skssm::DecodeArgs a = decode_args(cfg, ring, n_buffered, q, o);
   a.U = U;
   a.coef = coef;
+  a.cmap = cfg->pivots ? cmap : nullptr;
   int r;
   switch (cfg->kind) {
-    case SKSSM_MAMBA2: r = skssm::run_decode_mamba2(a, cfg->dk, cfg->dv, cfg->rank, cfg->io_dtype, cfg->sketch_dtype, stream); break;
-    case SKSSM_GDN: r = skssm::run_decode_gdn(a, cfg->dk, cfg->dv, cfg->rank, cfg->io_dtype, cfg->sketch_dtype, stream); break;
-    default: r = skssm::run_decode_kda(a, cfg->dk, cfg->dv, cfg->rank, cfg->io_dtype, cfg->sketch_dtype, stream); break;
+    case SKSSM_MAMBA2: r = skssm::run_decode_mamba2(a, cfg->dk, cfg->dv, cfg->rank, cfg->io_dtype, cfg->sketch_dtype, cfg->pivots, stream); break;
+    case SKSSM_GDN: r = skssm::run_decode_gdn(a, cfg->dk, cfg->dv, cfg->rank, cfg->io_dtype, cfg->sketch_dtype, cfg->pivots, stream); break;
+    default: r = skssm::run_decode_kda(a, cfg->dk, cfg->dv, cfg->rank, cfg->io_dtype, cfg->sketch_dtype, cfg->pivots, stream); break;
   }
   return launched(r, "sketchssm_decode");
 }

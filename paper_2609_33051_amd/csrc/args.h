@@ -16,7 +16,8 @@ struct DecodeArgs {
   int B, H, W, n;                 // batch, heads, window, slot of the current token
   const void* q;                  // [B][H][K] io, current query
   const void* U;                  // [B][H][R/P][V][P], P = 4 (fp32) or 8 (bf16)  (sketch read)
-  const float* coef;              // [H][R][K]           (sketch read)
+  const float* coef;              // [H][R][K]           (sketch read; Omega^T with a pivot map)
+  const float* cmap;              // [B][H][4K + 4R + R*R] pivot map factors M, F1, F2 (or NULL)
   const float* S;                 // [B][H][V][K]        (exact baseline)
   const void* rk;                 // ring [B][H][W][K] io      raw keys
   const void* rv;                 // ring [B][H][W][V] io      raw values
@@ -44,19 +45,21 @@ struct UpdateArgs {
   const float* ru;                // GDN/KDA pseudo-values, slots < n
   const float* rb;                // GDN/KDA erase couplings, slots < n
   void* U;                        // [B][H][R/P][V][P], P = 4 (fp32) or 8 (bf16), or NULL
+  float* cmap;                    // [B][H][4K + 4R + R*R] state-dependent coefficient map (pivots), or NULL
+  float ridge;                    // its lambda
   float* o;                       // [B][H][V] or NULL
 };
 
 // Host-side entry points of the per-family translation units.  Each returns
 // 0 after a launch, or -2 when the shape has no compiled kernel.
-int run_decode_mamba2(const DecodeArgs& a, int K, int V, int R, int io, int sk, void* stream);
-int run_decode_gdn(const DecodeArgs& a, int K, int V, int R, int io, int sk, void* stream);
-int run_decode_kda(const DecodeArgs& a, int K, int V, int R, int io, int sk, void* stream);
+int run_decode_mamba2(const DecodeArgs& a, int K, int V, int R, int io, int sk, int piv, void* stream);
+int run_decode_gdn(const DecodeArgs& a, int K, int V, int R, int io, int sk, int piv, void* stream);
+int run_decode_kda(const DecodeArgs& a, int K, int V, int R, int io, int sk, int piv, void* stream);
 int run_full_read_mamba2(const DecodeArgs& a, int K, int V, int io, void* stream);
 int run_full_read_gdn(const DecodeArgs& a, int K, int V, int io, void* stream);
 int run_full_read_kda(const DecodeArgs& a, int K, int V, int io, void* stream);
-int run_update_mamba2(const UpdateArgs& a, int K, int V, int R, int io, int sk, void* stream);
-int run_update_gdn(const UpdateArgs& a, int K, int V, int R, int io, int sk, void* stream);
-int run_update_kda(const UpdateArgs& a, int K, int V, int R, int io, int sk, void* stream);
+int run_update_mamba2(const UpdateArgs& a, int K, int V, int R, int io, int sk, int piv, void* stream);
+int run_update_gdn(const UpdateArgs& a, int K, int V, int R, int io, int sk, int piv, void* stream);
+int run_update_kda(const UpdateArgs& a, int K, int V, int R, int io, int sk, int piv, void* stream);
 
 }  // namespace skssm

@@ -245,7 +245,7 @@ __device__ __forceinline__ void append_derived(const DecodeArgs& a, size_t item,
   }
 }
 
-template <int KIND, int K, int V, int R, int WMAX, typename IO, typename SK>
+template <int KIND, int K, int V, int R, int WMAX, typename IO, typename SK, int P>
 __global__ __launch_bounds__(256) void decode_kernel(const DecodeArgs a) {
   using L = RowLoads<KIND, K, V, WMAX, IO>;
   constexpr bool ERASE = L::ERASE, CHAN = L::CHAN;
@@ -354,7 +354,7 @@ __global__ __launch_bounds__(256) void decode_kernel(const DecodeArgs a) {
   }
   wave_lds_sync();
   const float eg = CHAN ? 1.f : fast_exp(gt[0]);
-  float cfin[RP], ft[RP];
+  float cfin[RP], ft[RP], sqv[RP], skv[RP];
 #pragma unroll
   for (int p = 0; p < RP; ++p) {
     const int j = col + 16 * p;
@@ -374,9 +374,71 @@ __global__ __launch_bounds__(256) void decode_kernel(const DecodeArgs a) {
         }
       }
     }
-    sq = cross_row_sum(sq);
+    sqv[p] = cross_row_sum(sq);
+    skv[p] = ERASE ? cross_row_sum(sk) : 0.f;
+  }
+  if constexpr (P > 0) {
+    // state-dependent map C = F1 M + F2 Omega^T (coef holds Omega^T): C x =
+    // F1 (M x) + F2 (Omega^T x) for x = e^g . q and x = e^g . k
+    static_assert(P == 4 && R <= 32, "pivot maps: P = 4, rank up to 32");
+    const float* cm = a.cmap + item * (size_t)(P * K + R * P + R * R);
+    constexpr int CW = K / 16;                      // channels per lane of M x
+    const int pa = col >> 2, ch = ((col & 3) + 4 * row) * CW;
+    Vec<CW> mr;
+    mr.load(cm + pa * K + ch);
+    float mq = 0.f, mk = 0.f;
+#pragma unroll
+    for (int m = 0; m < CW; ++m) {
+      mq += mr.e[m] * xq_l[ch + m];
+      if constexpr (ERASE) mk += mr.e[m] * xk_l[ch + m];
+    }
+    mq = cross_row_sum(quad_sum(mq));               // lanes with col / 4 = a hold (M x)[a]
+    if constexpr (ERASE) mk = cross_row_sum(quad_sum(mk));
+    float mqa[P], mka[P];
+#pragma unroll
+    for (int x = 0; x < P; ++x) {
+      mqa[x] = lane_bcast(mq, 4 * x);
+      mka[x] = ERASE ? lane_bcast(mk, 4 * x) : 0.f;
+    }
+    wave_lds_sync();                                // x_q, x_k are read; reuse them for Omega^T x
+    if (row == 0) {
+#pragma unroll
+      for (int p = 0; p < RP; ++p) {
+        const int j = col + 16 * p;
+        if (j < R) {
+          xq_l[j] = sqv[p];
+          if constexpr (ERASE) xk_l[j] = skv[p];
+        }
+      }
+    }
+    wave_lds_sync();
+    constexpr int HQ = R / 4;                       // F2 columns per row of lanes
+#pragma unroll
+    for (int p = 0; p < RP; ++p) {
+      const int j = col + 16 * p;
+      float cq = 0.f, ck = 0.f;
+      if (j < R) {
+        Vec<HQ> f2;
+        f2.load(cm + P * K + R * P + j * R + row * HQ);
+#pragma unroll
+        for (int m = 0; m < HQ; ++m) {
+          cq += f2.e[m] * xq_l[row * HQ + m];
+          if constexpr (ERASE) ck += f2.e[m] * xk_l[row * HQ + m];
+        }
+        if (row == 0) {
+          const float4 f1 = *reinterpret_cast<const float4*>(cm + P * K + j * P);
+          cq += f1.x * mqa[0] + f1.y * mqa[1] + f1.z * mqa[2] + f1.w * mqa[3];
+          if constexpr (ERASE) ck += f1.x * mka[0] + f1.y * mka[1] + f1.z * mka[2] + f1.w * mka[3];
+        }
+      }
+      sqv[p] = cross_row_sum(cq);
+      if constexpr (ERASE) skv[p] = cross_row_sum(ck);
+    }
+  }
+#pragma unroll
+  for (int p = 0; p < RP; ++p) {
+    const float sq = sqv[p], sk = skv[p];
     if constexpr (ERASE) {
-      sk = cross_row_sum(sk);
       float sb = 0.f, sa = 0.f;
 #pragma unroll
       for (int gi = 0; gi < NG; ++gi) {

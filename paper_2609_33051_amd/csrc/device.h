@@ -165,6 +165,13 @@ __device__ __forceinline__ float row_sum16(float x) {
 }
 
 // Sum over the 4 rows (lanes l, l^16, l^32, l^48); every lane receives it.
+// Sum over a quad of lanes (lane & ~3 .. lane | 3).
+__device__ __forceinline__ float quad_sum(float x) {
+  x += dpp<0xB1>(x);  // quad_perm [1,0,3,2]
+  x += dpp<0x4E>(x);  // quad_perm [2,3,0,1]
+  return x;
+}
+
 __device__ __forceinline__ float cross_row_sum(float x) {
   x += __shfl_xor(x, 16);
   x += __shfl_xor(x, 32);

@@ -13,10 +13,10 @@ namespace skssm {
 
 constexpr int kUnsupported = -2;
 
-template <int KIND, int K, int V, int R, int WM, typename IO, typename SK>
+template <int KIND, int K, int V, int R, int WM, typename IO, typename SK, int P>
 int launch_decode(const DecodeArgs& a, hipStream_t s) {
   const unsigned tiles = (unsigned)((a.B + 3) / 4);
-  hipLaunchKernelGGL((decode_kernel<KIND, K, V, R, WM, IO, SK>), dim3((unsigned)a.H * tiles), dim3(256), 0, s, a);
+  hipLaunchKernelGGL((decode_kernel<KIND, K, V, R, WM, IO, SK, P>), dim3((unsigned)a.H * tiles), dim3(256), 0, s, a);
   return 0;
 }
 
@@ -27,41 +27,50 @@ int launch_full_read(const DecodeArgs& a, hipStream_t s) {
   return 0;
 }
 
-template <int KIND, int K, int V, int R, int WM, typename IO, typename SK>
+template <int KIND, int K, int V, int R, int WM, typename IO, typename SK, int P>
 int launch_update(const UpdateArgs& a, hipStream_t s) {
   const size_t items = (size_t)a.B * a.H;
-  hipLaunchKernelGGL((update_kernel<KIND, K, V, R, WM, IO, SK>), dim3((unsigned)items), dim3(256), 0, s, a);
+  hipLaunchKernelGGL((update_kernel<KIND, K, V, R, WM, IO, SK, P>), dim3((unsigned)items), dim3(256), 0, s, a);
   return 0;
 }
 
-template <int KIND, int K, int V, int R, int WM>
+// Pivot maps (P = 4) are compiled for ranks 8..32; piv selects them.
+template <int R> constexpr bool kPivotRank = R >= 8 && R <= 32;
+
+template <int KIND, int K, int V, int R, int WM, int P>
 int decode_t(const DecodeArgs& a, int io, int sk, hipStream_t s) {
-  if (io) return sk ? launch_decode<KIND, K, V, R, WM, bf16_t, bf16_t>(a, s) : launch_decode<KIND, K, V, R, WM, bf16_t, float>(a, s);
-  return sk ? launch_decode<KIND, K, V, R, WM, float, bf16_t>(a, s) : launch_decode<KIND, K, V, R, WM, float, float>(a, s);
+  if (io) return sk ? launch_decode<KIND, K, V, R, WM, bf16_t, bf16_t, P>(a, s) : launch_decode<KIND, K, V, R, WM, bf16_t, float, P>(a, s);
+  return sk ? launch_decode<KIND, K, V, R, WM, float, bf16_t, P>(a, s) : launch_decode<KIND, K, V, R, WM, float, float, P>(a, s);
 }
 
 template <int KIND, int K, int V, int R>
-int decode_w(const DecodeArgs& a, int io, int sk, hipStream_t s) {
-  return a.W <= 16 ? decode_t<KIND, K, V, R, 16>(a, io, sk, s) : decode_t<KIND, K, V, R, 32>(a, io, sk, s);
+int decode_w(const DecodeArgs& a, int io, int sk, int piv, hipStream_t s) {
+  if constexpr (kPivotRank<R>) {
+    if (piv) return a.W <= 16 ? decode_t<KIND, K, V, R, 16, 4>(a, io, sk, s) : decode_t<KIND, K, V, R, 32, 4>(a, io, sk, s);
+  } else {
+    if (piv) return kUnsupported;
+  }
+  return a.W <= 16 ? decode_t<KIND, K, V, R, 16, 0>(a, io, sk, s) : decode_t<KIND, K, V, R, 32, 0>(a, io, sk, s);
 }
 
+// One (kind, K, V) shape; explicitly instantiated in its own translation unit.
 template <int KIND, int K, int V>
-int decode_r(const DecodeArgs& a, int R, int io, int sk, hipStream_t s) {
+int decode_r(const DecodeArgs& a, int R, int io, int sk, int piv, hipStream_t s) {
   switch (R) {
-    case 8: return decode_w<KIND, K, V, 8>(a, io, sk, s);
-    case 16: return decode_w<KIND, K, V, 16>(a, io, sk, s);
-    case 32: return decode_w<KIND, K, V, 32>(a, io, sk, s);
-    case K: return decode_w<KIND, K, V, K>(a, io, sk, s);
+    case 8: return decode_w<KIND, K, V, 8>(a, io, sk, piv, s);
+    case 16: return decode_w<KIND, K, V, 16>(a, io, sk, piv, s);
+    case 32: return decode_w<KIND, K, V, 32>(a, io, sk, piv, s);
+    case K: return decode_w<KIND, K, V, K>(a, io, sk, piv, s);
     default: return kUnsupported;
   }
 }
 
 template <int KIND>
-int run_decode(const DecodeArgs& a, int K, int V, int R, int io, int sk, void* stream) {
+int run_decode(const DecodeArgs& a, int K, int V, int R, int io, int sk, int piv, void* stream) {
   hipStream_t s = static_cast<hipStream_t>(stream);
-  if (K == 64 && V == 64) return decode_r<KIND, 64, 64>(a, R, io, sk, s);
-  if (K == 128 && V == 64) return decode_r<KIND, 128, 64>(a, R, io, sk, s);
-  if (K == 128 && V == 128) return decode_r<KIND, 128, 128>(a, R, io, sk, s);
+  if (K == 64 && V == 64) return decode_r<KIND, 64, 64>(a, R, io, sk, piv, s);
+  if (K == 128 && V == 64) return decode_r<KIND, 128, 64>(a, R, io, sk, piv, s);
+  if (K == 128 && V == 128) return decode_r<KIND, 128, 128>(a, R, io, sk, piv, s);
   return kUnsupported;
 }
 
@@ -81,39 +90,45 @@ int run_full_read(const DecodeArgs& a, int K, int V, int io, void* stream) {
   return kUnsupported;
 }
 
-template <int KIND, int K, int V, int R, int WM>
+template <int KIND, int K, int V, int R, int WM, int P>
 int update_t(const UpdateArgs& a, int io, int sk, hipStream_t s) {
   if constexpr (R == 0) {  // no sketch: its dtype does not matter
-    return io ? launch_update<KIND, K, V, 0, WM, bf16_t, float>(a, s) : launch_update<KIND, K, V, 0, WM, float, float>(a, s);
+    return io ? launch_update<KIND, K, V, 0, WM, bf16_t, float, 0>(a, s) : launch_update<KIND, K, V, 0, WM, float, float, 0>(a, s);
   } else {
-    if (io) return sk ? launch_update<KIND, K, V, R, WM, bf16_t, bf16_t>(a, s) : launch_update<KIND, K, V, R, WM, bf16_t, float>(a, s);
-    return sk ? launch_update<KIND, K, V, R, WM, float, bf16_t>(a, s) : launch_update<KIND, K, V, R, WM, float, float>(a, s);
+    if (io) return sk ? launch_update<KIND, K, V, R, WM, bf16_t, bf16_t, P>(a, s) : launch_update<KIND, K, V, R, WM, bf16_t, float, P>(a, s);
+    return sk ? launch_update<KIND, K, V, R, WM, float, bf16_t, P>(a, s) : launch_update<KIND, K, V, R, WM, float, float, P>(a, s);
   }
 }
 
 template <int KIND, int K, int V, int R>
-int update_w(const UpdateArgs& a, int io, int sk, hipStream_t s) {
-  return a.W <= 16 ? update_t<KIND, K, V, R, 16>(a, io, sk, s) : update_t<KIND, K, V, R, 32>(a, io, sk, s);
+int update_w(const UpdateArgs& a, int io, int sk, int piv, hipStream_t s) {
+  if constexpr (kPivotRank<R>) {
+    if (piv) return a.W <= 16 ? update_t<KIND, K, V, R, 16, 4>(a, io, sk, s) : update_t<KIND, K, V, R, 32, 4>(a, io, sk, s);
+  } else {
+    if (piv) return kUnsupported;
+  }
+  return a.W <= 16 ? update_t<KIND, K, V, R, 16, 0>(a, io, sk, s) : update_t<KIND, K, V, R, 32, 0>(a, io, sk, s);
 }
 
+// One (kind, K, V) shape; explicitly instantiated in its own translation unit.
 template <int KIND, int K, int V>
-int update_r(const UpdateArgs& a, int R, int io, int sk, hipStream_t s) {
+int update_r(const UpdateArgs& a, int R, int io, int sk, int piv, hipStream_t s) {
   switch (R) {
-    case 0: return update_w<KIND, K, V, 0>(a, io, sk, s);
-    case 8: return update_w<KIND, K, V, 8>(a, io, sk, s);
-    case 16: return update_w<KIND, K, V, 16>(a, io, sk, s);
-    case 32: return update_w<KIND, K, V, 32>(a, io, sk, s);
-    case K: return update_w<KIND, K, V, K>(a, io, sk, s);
+    case 0: return update_w<KIND, K, V, 0>(a, io, sk, piv, s);
+    case 8: return update_w<KIND, K, V, 8>(a, io, sk, piv, s);
+    case 16: return update_w<KIND, K, V, 16>(a, io, sk, piv, s);
+    case 32: return update_w<KIND, K, V, 32>(a, io, sk, piv, s);
+    case K: return update_w<KIND, K, V, K>(a, io, sk, piv, s);
     default: return kUnsupported;
   }
 }
 
 template <int KIND>
-int run_update(const UpdateArgs& a, int K, int V, int R, int io, int sk, void* stream) {
+int run_update(const UpdateArgs& a, int K, int V, int R, int io, int sk, int piv, void* stream) {
   hipStream_t s = static_cast<hipStream_t>(stream);
-  if (K == 64 && V == 64) return update_r<KIND, 64, 64>(a, R, io, sk, s);
-  if (K == 128 && V == 64) return update_r<KIND, 128, 64>(a, R, io, sk, s);
-  if (K == 128 && V == 128) return update_r<KIND, 128, 128>(a, R, io, sk, s);
+  if (K == 64 && V == 64) return update_r<KIND, 64, 64>(a, R, io, sk, piv, s);
+  if (K == 128 && V == 64) return update_r<KIND, 128, 64>(a, R, io, sk, piv, s);
+  if (K == 128 && V == 128) return update_r<KIND, 128, 128>(a, R, io, sk, piv, s);
   return kUnsupported;
 }
 

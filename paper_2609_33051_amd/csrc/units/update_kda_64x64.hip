@@ -1,0 +1,5 @@
+// Instantiations: flush / initial sketch, kda, K = 64, V = 64.
+#include "../dispatch.h"
+namespace skssm {
+template int update_r<KDA, 64, 64>(const UpdateArgs&, int, int, int, int, hipStream_t);
+}  // namespace skssm

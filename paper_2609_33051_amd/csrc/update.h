@@ -40,7 +40,219 @@ template <typename IO> __device__ __forceinline__ float load1(const IO* p);
 template <> __device__ __forceinline__ float load1<float>(const float* p) { return *p; }
 template <> __device__ __forceinline__ float load1<bf16_t>(const bf16_t* p) { return bf16_lo((uint32_t)*p); }
 
-template <int KIND, int K, int V, int R, int WMAX, typename IO, typename SK>
+// The state-dependent coefficient map (Sec. 4.1, eq. m-coeff with the ridge
+// term and the low-rank-plus-diagonal metric of the appendix on the P = 4
+// pivot approximation), from the partial sums the tiles left behind:
+//   mu   = |S|_F^2 / K (1 for a zero state)
+//   U_p  = the first P sketch columns,  U_p^T U_p = R^T R (Cholesky; a column
+//          dependent on the earlier ones is dropped: its row of R^{-1} is 0)
+//   L_G  = U^T U_p R^{-1} / sqrt(mu)             (G x P; Q = U_p R^{-1})
+//   M    = R^{-T} U_p^T S^T / sqrt(mu)           (P x K, i.e. Q^T S^T / sqrt(mu))
+//   d    = max(diag(U^T U) / mu - |L_G rows|^2, 0),  D = d + lambda
+//   T    = I + L_G^T D^{-1} L_G                  (Woodbury: only T is inverted)
+//   F1   = D^{-1} L_G T^{-1}  (= A^{-1} L_G),  F2 = A^{-1} Diag(d),
+//   A^{-1} = D^{-1} - D^{-1} L_G T^{-1} L_G^T D^{-1}
+// so the map is C = F1 M + F2 Omega^T.  Stored per item as M [P][K], F1
+// [G][P], F2 [G][G] (fp32).  Every thread of the workgroup calls this.
+template <int K, int R, int P, int MT, int RT, int LSZ, int USZ>
+__device__ __forceinline__ void coef_map_tail(const UpdateArgs& a, size_t item, int wave, int lane, int tid,
+                                              const floatx4 (&nacc)[MT], const float (&gpart)[RT][4][5], float msq,
+                                              float* Ls, float* Us, float* cmS) {
+  static_assert(LSZ >= 4 * K * P && USZ >= 4 * R * 5, "staging buffers too small for the map's partial sums");
+  const int lr = lane & 15, lg = lane >> 4;
+  // this wave's Gram partials summed over its 16 value lanes
+  float gs[RT][4][5];
+#pragma unroll
+  for (int jt = 0; jt < RT; ++jt)
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int e = 0; e < 5; ++e) gs[jt][i][e] = row_sum16(gpart[jt][i][e]);
+  msq = wave_sum(msq);
+  lds_barrier();  // every wave is done with the window staging (Ls, Us), reused below
+  float* cmN = Ls;  // [wave][K][P]
+  float* cmG = Us;  // [wave][R][5]
+  if (lg == 0) {
+#pragma unroll
+    for (int kt = 0; kt < MT; ++kt)
+      *reinterpret_cast<float4*>(&cmN[(wave * K + 16 * kt + lr) * P]) = make_float4(nacc[kt][0], nacc[kt][1], nacc[kt][2], nacc[kt][3]);
+  }
+  if (lr == 0) {
+#pragma unroll
+    for (int jt = 0; jt < RT; ++jt)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int j = 16 * jt + 4 * lg + i;
+        if (j < R) {
+#pragma unroll
+          for (int e = 0; e < 5; ++e) cmG[(wave * R + j) * 5 + e] = gs[jt][i][e];
+        }
+      }
+  }
+  if (lane == 0) cmS[wave] = msq;
+  lds_barrier();
+
+  const size_t CMW = (size_t)P * K + R * P + R * R;
+  float* cm = a.cmap + item * CMW;
+  if (wave == 0) {
+    const float fro = cmS[0] + cmS[1] + cmS[2] + cmS[3];
+    const float mu = fro > 0.f ? fro / K : 1.f;
+    const float rs = 1.f / sqrtf(mu);
+    // pivot Gram, Cholesky with dropping, R^{-1} (all lanes, uniform)
+    float Gp[P][P], Rm[P][P], Ri[P][P];
+#pragma unroll
+    for (int x = 0; x < P; ++x)
+#pragma unroll
+      for (int y = 0; y < P; ++y) {
+        Gp[x][y] = cmG[(0 * R + x) * 5 + y] + cmG[(1 * R + x) * 5 + y] + cmG[(2 * R + x) * 5 + y] + cmG[(3 * R + x) * 5 + y];
+        Rm[x][y] = 0.f;
+        Ri[x][y] = 0.f;
+      }
+#pragma unroll
+    for (int x = 0; x < P; ++x) {
+      float sd = Gp[x][x];
+#pragma unroll
+      for (int b = 0; b < x; ++b) sd -= Rm[b][x] * Rm[b][x];
+      if (Gp[x][x] > 0.f && sd > 1e-6f * Gp[x][x]) {
+        const float rxx = sqrtf(sd);
+        Rm[x][x] = rxx;
+#pragma unroll
+        for (int y = x + 1; y < P; ++y) {
+          float e = Gp[x][y];
+#pragma unroll
+          for (int b = 0; b < x; ++b) e -= Rm[b][x] * Rm[b][y];
+          Rm[x][y] = e / rxx;
+        }
+      }
+    }
+#pragma unroll
+    for (int x = 0; x < P; ++x) {
+      if (Rm[x][x] > 0.f) Ri[x][x] = 1.f / Rm[x][x];
+#pragma unroll
+      for (int y = x + 1; y < P; ++y) {
+        if (Rm[y][y] > 0.f) {
+          float e = 0.f;
+#pragma unroll
+          for (int b = x; b < y; ++b) e += Ri[x][b] * Rm[b][y];
+          Ri[x][y] = -e / Rm[y][y];
+        }
+      }
+    }
+    // lane g < R: row g of L_G, d, D^{-1}
+    const int g = lane;
+    float LG[P] = {}, dg = 0.f, dinv = 0.f;
+    if (g < R) {
+      float Bg[P], diag = 0.f;
+#pragma unroll
+      for (int b = 0; b < P; ++b)
+        Bg[b] = cmG[(0 * R + g) * 5 + b] + cmG[(1 * R + g) * 5 + b] + cmG[(2 * R + g) * 5 + b] + cmG[(3 * R + g) * 5 + b];
+      diag = cmG[(0 * R + g) * 5 + 4] + cmG[(1 * R + g) * 5 + 4] + cmG[(2 * R + g) * 5 + 4] + cmG[(3 * R + g) * 5 + 4];
+      float l2 = 0.f;
+#pragma unroll
+      for (int c = 0; c < P; ++c) {
+        float e = 0.f;
+#pragma unroll
+        for (int b = 0; b < P; ++b) e += Bg[b] * Ri[b][c];
+        LG[c] = e * rs;
+        l2 += LG[c] * LG[c];
+      }
+      dg = fmaxf(diag / mu - l2, 0.f);
+      dinv = 1.f / (dg + a.ridge);
+    }
+    // T = I + L_G^T D^{-1} L_G (sum over the lanes g), then its inverse
+    float Tm[P][P];
+#pragma unroll
+    for (int x = 0; x < P; ++x)
+#pragma unroll
+      for (int y = x; y < P; ++y) {
+        const float e = wave_sum(LG[x] * dinv * LG[y]);
+        Tm[x][y] = e + (x == y ? 1.f : 0.f);
+        Tm[y][x] = Tm[x][y];
+      }
+    float Ti[P][P];
+#pragma unroll
+    for (int x = 0; x < P; ++x)
+#pragma unroll
+      for (int y = 0; y < P; ++y) Ti[x][y] = (x == y) ? 1.f : 0.f;
+#pragma unroll
+    for (int c = 0; c < P; ++c) {  // Gauss-Jordan on the SPD T (pivots >= 1)
+      const float inv = 1.f / Tm[c][c];
+#pragma unroll
+      for (int y = 0; y < P; ++y) {
+        Tm[c][y] *= inv;
+        Ti[c][y] *= inv;
+      }
+#pragma unroll
+      for (int x = 0; x < P; ++x) {
+        if (x == c) continue;
+        const float f = Tm[x][c];
+#pragma unroll
+        for (int y = 0; y < P; ++y) {
+          Tm[x][y] -= f * Tm[c][y];
+          Ti[x][y] -= f * Ti[c][y];
+        }
+      }
+    }
+    // F1 row g, and the factors the F2 rows need from every g
+    float F1[P];
+#pragma unroll
+    for (int c = 0; c < P; ++c) {
+      float e = 0.f;
+#pragma unroll
+      for (int b = 0; b < P; ++b) e += LG[b] * Ti[b][c];
+      F1[c] = dinv * e;
+    }
+    float* sL = cmS + 8 + 16;  // [R][P] L_G, then [R] w = D^{-1} d
+    if (g < R) {
+#pragma unroll
+      for (int c = 0; c < P; ++c) sL[g * P + c] = LG[c];
+      sL[R * P + g] = dinv * dg;
+    }
+    if (lane == 0) {
+#pragma unroll
+      for (int x = 0; x < P; ++x)
+#pragma unroll
+        for (int y = 0; y < P; ++y) cmS[8 + x * P + y] = Ri[x][y] * rs;
+    }
+    wave_lds_sync();
+    if (g < R) {
+      *reinterpret_cast<float4*>(cm + P * K + g * P) = make_float4(F1[0], F1[1], F1[2], F1[3]);
+      float* F2 = cm + P * K + R * P + g * R;
+#pragma unroll 4
+      for (int hq = 0; hq < R; hq += 4) {
+        float o4[4];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+          const int hh = hq + u;
+          float e = 0.f;
+#pragma unroll
+          for (int c = 0; c < P; ++c) e += F1[c] * sL[hh * P + c];
+          const float w = sL[R * P + hh];
+          o4[u] = (hh == g ? w : 0.f) - e * w;
+        }
+        *reinterpret_cast<float4*>(F2 + hq) = make_float4(o4[0], o4[1], o4[2], o4[3]);
+      }
+    }
+  }
+  lds_barrier();
+  // M = R^{-T} N^T / sqrt(mu): thread k sums the four waves' N rows
+  if (tid < K) {
+    const int k = tid;
+    float Nk[P];
+#pragma unroll
+    for (int b = 0; b < P; ++b)
+      Nk[b] = cmN[(0 * K + k) * P + b] + cmN[(1 * K + k) * P + b] + cmN[(2 * K + k) * P + b] + cmN[(3 * K + k) * P + b];
+#pragma unroll
+    for (int x = 0; x < P; ++x) {
+      float e = 0.f;
+#pragma unroll
+      for (int b = 0; b < P; ++b) e += cmS[8 + b * P + x] * Nk[b];
+      cm[x * K + k] = e;
+    }
+  }
+}
+
+template <int KIND, int K, int V, int R, int WMAX, typename IO, typename SK, int P>
 __global__ __launch_bounds__(256, 3) void update_kernel(const UpdateArgs a) {
   constexpr bool ERASE = KIND != MAMBA2;
   constexpr bool CHAN = KIND == KDA;
@@ -87,6 +299,28 @@ __global__ __launch_bounds__(256, 3) void update_kernel(const UpdateArgs a) {
   constexpr int OQ = OM_LDS ? (K * R / 4 + 255) / 256 : 1;  // float4 of Omega per thread
   __shared__ __align__(16) float OmL[OM_LDS ? K * OPJ : 4];
   const bool want_U = R > 0 && a.U != nullptr;
+
+  // state-dependent coefficient map (P > 0 pivots): per-wave scratch for the
+  // block transposes of N = S U_p and for the first P sketch columns, and the
+  // small factors shared by the workgroup
+  static_assert(P == 0 || (P == 4 && R >= 8 && R <= 32), "pivot maps: P = 4, rank 8..32");
+  constexpr int XP = 20;                                        // row pitch of a transposed 16 x 16 block
+  __shared__ __align__(16) float cmX[P > 0 ? 4 * 16 * XP : 4];  // [wave][16 values][16 keys]
+  __shared__ __align__(16) float cmU[P > 0 ? 4 * 16 * 4 : 4];   // [wave][16 values][P]
+  __shared__ __align__(16) float cmS[P > 0 ? 8 + 16 + 5 * R : 4];  // mu parts, R^{-1}/sqrt(mu), L_G and w
+  floatx4 nacc[P > 0 ? MT : 1];    // N^T (rows a = 4 lg + i), per k tile, this wave's values
+  float gpart[P > 0 ? RT : 1][4][5];  // sketch Gram: U[v][j] U[v][a] (a < 4) and U[v][j]^2, this lane's values
+  float msq = 0.f;                 // this lane's share of |S|_F^2
+  if constexpr (P > 0) {
+#pragma unroll
+    for (int kt = 0; kt < MT; ++kt) nacc[kt] = floatx4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int jt = 0; jt < RT; ++jt)
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int e = 0; e < 5; ++e) gpart[jt][i][e] = 0.f;
+  }
 
   // ---- every small load first (window, query, couplings, Omega), then the
   // state: the staged values reach LDS while the state read is still in flight
@@ -407,6 +641,8 @@ __global__ __launch_bounds__(256, 3) void update_kernel(const UpdateArgs a) {
     if constexpr (R > 0) {
       if (want_U) {
         const float* om = a.omega + (size_t)h * K * R;
+        float4 up4 = make_float4(0.f, 0.f, 0.f, 0.f);  // U[v][0..3] (state-dependent map)
+        float aop[4] = {0.f, 0.f, 0.f, 0.f};            // U_p^T as the A operand of N^T = U_p^T X
 #pragma unroll
         for (int jt = 0; jt < RT; ++jt) {
           const int jj = 16 * jt + lr;
@@ -422,6 +658,27 @@ __global__ __launch_bounds__(256, 3) void update_kernel(const UpdateArgs a) {
                 w = (jj < R) ? om[(16 * kt + 4 * lg + i) * R + jj] : 0.f;
               acc = mfma4(w, xs[t][kt][i], acc);
             }
+          if constexpr (P > 0) {
+            // Gram partials of the sketch against its first P columns, which lane
+            // (lr, lg = 0) holds for this tile's 16 values after the jt = 0 product
+            if (jt == 0) {
+              float* cu = cmU + wave * 64;
+              wave_lds_sync();
+              if (lg == 0) *reinterpret_cast<float4*>(&cu[lr * 4]) = make_float4(acc[0], acc[1], acc[2], acc[3]);
+              wave_lds_sync();
+              up4 = *reinterpret_cast<const float4*>(&cu[lr * 4]);
+#pragma unroll
+              for (int st = 0; st < 4; ++st) aop[st] = (lr < 4) ? cu[(4 * st + lg) * 4 + lr] : 0.f;
+            }
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+              gpart[jt][i][0] += acc[i] * up4.x;
+              gpart[jt][i][1] += acc[i] * up4.y;
+              gpart[jt][i][2] += acc[i] * up4.z;
+              gpart[jt][i][3] += acc[i] * up4.w;
+              gpart[jt][i][4] += acc[i] * acc[i];
+            }
+          }
           // columns 16 jt + 4 lg .. +3 of value v; panels of 16 bytes per value:
           // fp32 U[B][H][R/4][V][4], bf16 U[B][H][R/8][V][8]
           if (16 * jt + 4 * lg < R) {
@@ -435,6 +692,23 @@ __global__ __launch_bounds__(256, 3) void update_kernel(const UpdateArgs a) {
             }
           }
         }
+        if constexpr (P > 0) {
+          // N^T = U_p^T X over this tile's 16 values on the matrix cores: each 16 x 16
+          // block of X goes through LDS so that the value index becomes the
+          // contraction index (lane group), then four 16x16x4 steps
+          float* cx = cmX + wave * 16 * XP;
+#pragma unroll
+          for (int kt = 0; kt < MT; ++kt) {
+            wave_lds_sync();
+            *reinterpret_cast<float4*>(&cx[lr * XP + 4 * lg]) =
+                make_float4(xs[t][kt][0], xs[t][kt][1], xs[t][kt][2], xs[t][kt][3]);
+            wave_lds_sync();
+#pragma unroll
+            for (int st = 0; st < 4; ++st) nacc[kt] = mfma4(aop[st], cx[(4 * st + lg) * XP + lr], nacc[kt]);
+#pragma unroll
+            for (int i = 0; i < 4; ++i) msq += xs[t][kt][i] * xs[t][kt][i];
+          }
+        }
       }
     }
     if (flush) {
@@ -443,6 +717,10 @@ __global__ __launch_bounds__(256, 3) void update_kernel(const UpdateArgs a) {
       for (int kt = 0; kt < MT; ++kt)
         *reinterpret_cast<float4*>(dst + 16 * kt) = make_float4(xs[t][kt][0], xs[t][kt][1], xs[t][kt][2], xs[t][kt][3]);
     }
+  }
+
+  if constexpr (P > 0) {
+    if (want_U) coef_map_tail<K, R, P, MT, RT, SP * LP, SP * UP>(a, item, wave, lane, tid, nacc, gpart, msq, Ls, Us, cmS);
   }
 }
 

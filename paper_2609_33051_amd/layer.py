@@ -9,6 +9,8 @@ into libsketchssm.so.  Buffers (caller-owned, as the ABI requires):
          value: P = 4 columns fp32, or P = 8 bf16 (sketch="bf16", the paper's
          storage); sketch_matrix() gives the [B][H][V][r] fp32 view
   omega  [H][K][r]     fp32 sketching matrix, coef [H][r][K] its coefficient map
+         (Omega^T, the offline map; with pivots = 4 the map is state-dependent,
+         C = F1 M + F2 coef, rebuilt at every flush into cmap [B][H][4K+4r+r^2])
   ring   replay buffer of W slots per item:
          raw inputs k, v (io dtype), beta, log_decay ([..][K] for KDA), item-major
          [B][H][W][...], written into slot n by the token's producer (write_token);
@@ -25,9 +27,11 @@ from . import binding as B
 class SketchSSMLayer:
     def __init__(self, kind: str, batch: int, heads: int, dk: int, dv: int, rank: int, window: int,
                  io: str = "bf16", device="cuda", baseline: bool = False, S: torch.Tensor | None = None,
-                 omega: torch.Tensor | None = None, coef: torch.Tensor | None = None, sketch: str = "f32"):
+                 omega: torch.Tensor | None = None, coef: torch.Tensor | None = None, sketch: str = "f32",
+                 pivots: int = 0, ridge: float = 0.1):
         self.kind, self.batch, self.heads, self.dk, self.dv = kind, batch, heads, dk, dv
         self.rank, self.window, self.io, self.baseline, self.sketch = rank, window, io, baseline, sketch
+        self.pivots = 0 if baseline else pivots
         self.device = torch.device(device)
         iodt = torch.bfloat16 if io == "bf16" else torch.float32
         f32 = torch.float32
@@ -36,7 +40,7 @@ class SketchSSMLayer:
         dev = self.device
         self.S = S if S is not None else torch.zeros((Bt, H, V, K), dtype=f32, device=dev)
         r = 0 if baseline else rank
-        self.cfg = B.make_config(kind, Bt, H, K, V, r, W, io, sketch)
+        self.cfg = B.make_config(kind, Bt, H, K, V, r, W, io, sketch, self.pivots, ridge)
         if not baseline:
             self.omega = omega.to(dev).contiguous()
             self.coef = coef.to(dev).contiguous()
@@ -45,6 +49,9 @@ class SketchSSMLayer:
                                  device=dev)
         else:
             self.omega = self.coef = self.U = None
+        # state-dependent coefficient map (M, F1, F2 per item), written by every update
+        cw = B.cmap_width(self.cfg)
+        self.cmap = torch.zeros((Bt, H, cw), dtype=f32, device=dev) if cw else None
         # raw inputs, written by the producer of each token
         self.rk = torch.zeros((Bt, H, W, K), dtype=iodt, device=dev)
         self.rv = torch.zeros((Bt, H, W, V), dtype=iodt, device=dev)
@@ -74,7 +81,7 @@ class SketchSSMLayer:
         """U = S^T Omega from S alone (after prefill); empties the window."""
         self.n = 0
         if not self.baseline:
-            B.sketchssm_update(self.cfg, self.S, self.omega, None, 0, None, self.U, None, self.stream())
+            B.sketchssm_update(self.cfg, self.S, self.omega, None, 0, None, self.U, None, self.stream(), cmap=self.cmap)
 
     def write_token(self, inp: dict, slot: int | None = None):
         """The producer's side: the token's k, v, beta and log decay go into
@@ -91,13 +98,14 @@ class SketchSSMLayer:
         open, the flush on its W-th token."""
         o = self.o if out is None else out
         if self.n == self.window - 1:
-            B.sketchssm_update(self.cfg, self.S, self.omega, self.ring, self.n, q, self.U, o, self.stream())
+            B.sketchssm_update(self.cfg, self.S, self.omega, self.ring, self.n, q, self.U, o, self.stream(),
+                               cmap=self.cmap)
             self.n = 0
         elif self.baseline:
             B.sketchssm_full_read_baseline(self.cfg, self.S, self.ring, self.n, q, o, self.stream())
             self.n += 1
         else:
-            B.sketchssm_decode(self.cfg, self.U, self.coef, self.ring, self.n, q, o, self.stream())
+            B.sketchssm_decode(self.cfg, self.U, self.coef, self.ring, self.n, q, o, self.stream(), cmap=self.cmap)
             self.n += 1
         return o
 
@@ -109,10 +117,10 @@ class SketchSSMLayer:
         o = self.o if out is None else out
         st = self.stream()
         if n == self.window - 1:
-            return B.prepare_update(self.cfg, self.S, self.omega, self.ring, n, q, self.U, o, st)
+            return B.prepare_update(self.cfg, self.S, self.omega, self.ring, n, q, self.U, o, st, cmap=self.cmap)
         if self.baseline:
             return B.prepare_full_read_baseline(self.cfg, self.S, self.ring, n, q, o, st)
-        return B.prepare_decode(self.cfg, self.U, self.coef, self.ring, n, q, o, st)
+        return B.prepare_decode(self.cfg, self.U, self.coef, self.ring, n, q, o, st, cmap=self.cmap)
 
     def step(self, inp: dict, out: torch.Tensor | None = None) -> torch.Tensor:
         """write_token + read."""

@@ -113,8 +113,9 @@ def main(argv=None):
     W = wl.window if a.window is None else a.window
     items = wl.items
 
-    def algo(entry, sketch):
-        sh = traffic.Shape(wl.kind, wl.dk, wl.dv, rank, W, 2 if wl.io == "bf16" else 4, 2 if sketch == "bf16" else 4)
+    def algo(entry, sketch, pivots):
+        sh = traffic.Shape(wl.kind, wl.dk, wl.dv, rank, W, 2 if wl.io == "bf16" else 4, 2 if sketch == "bf16" else 4,
+                           pivots)
         if entry == "decode":
             return sum(traffic.decode_bytes(sh, n) for n in range(W - 1)) / (W - 1) * items
         if entry == "full_read":
@@ -141,9 +142,11 @@ def main(argv=None):
         digest = hip_build.source_digest(unit)
         # sketch storage: the last template argument of decode/update (unsigned short = bf16)
         targs = s[s.index("<") + 1:s.rindex(">")].split(", ")
-        sketch = "bf16" if (e != "full_read" and targs[-1] == "unsigned short") else "f32"
-        tag = ":bf16" if sketch == "bf16" else ""
-        ab = algo(e, sketch)
+        # template arguments of decode/update: ..., io, sketch, pivots
+        sketch = "bf16" if (e != "full_read" and targs[-2] == "unsigned short") else "f32"
+        pivots = int(targs[-1]) if e != "full_read" else 0
+        tag = (":bf16" if sketch == "bf16" else "") + (f":p{pivots}" if pivots else "")
+        ab = algo(e, sketch, pivots)
         fv, wv = fetch.get(s, []), write.get(s, [])
         lines = [
             f"# {s} on {a.workload} (rank {rank}, window {W})",
@@ -188,6 +191,8 @@ def main(argv=None):
         name = f"{e}_{a.workload}" + ("" if rank == wl.rank and W == wl.window else f"_r{rank}_w{W}")
         if sketch == "bf16":
             name += "_bf16sketch"
+        if pivots:
+            name += f"_pivots{pivots}"
         if "<" in s and e == "update" and re.search(r"<\d+, \d+, \d+, 0,", s):
             name += "_rank0"
         with open(os.path.join(a.out, name + ".txt"), "w") as f:

@@ -57,10 +57,17 @@ class Shape:
     window: int
     io_bytes: int  # 2 (bf16) or 4 (fp32)
     sketch_bytes: int = 4  # U element: 4 (fp32) or 2 (bf16)
+    pivots: int = 0        # state-dependent coefficient map with this many pivots (0: offline map)
 
     @property
     def erase(self) -> bool:
         return self.kind in ("gdn", "kda")
+
+    @property
+    def cmap_bytes(self) -> int:
+        """The per-item factors of a state-dependent map: M [P][K], F1 [r][P], F2 [r][r], fp32."""
+        p = self.pivots
+        return 4 * (p * self.dk + self.rank * p + self.rank * self.rank) if p else 0
 
     @property
     def decay_bytes(self) -> int:
@@ -97,9 +104,9 @@ def derived_write_bytes(s: Shape, n: int, baseline: bool = False) -> int:
 
 def decode_bytes(s: Shape, n: int) -> int:
     """Sketch read at slot n: the query, n earlier slots, the current slot, the
-    derived fields, U and o."""
+    derived fields, U, the state-dependent map's factors (if any) and o."""
     return (s.io_bytes * s.dk + n * slot_read_bytes(s) + current_read_bytes(s) + derived_write_bytes(s, n)
-            + s.sketch_bytes * s.dv * s.rank + 4 * s.dv)
+            + s.sketch_bytes * s.dv * s.rank + s.cmap_bytes + 4 * s.dv)
 
 
 def full_read_bytes(s: Shape, n: int) -> int:
@@ -120,7 +127,7 @@ def flush_bytes(s: Shape, n_buffered: int, rank: int | None = None) -> int:
         slot = s.io_bytes * (s.dk + s.dv) + 4 + 4
         bcoef = 0
     return (8 * s.dk * s.dv + n_buffered * slot + bcoef + current_read_bytes(s) + s.io_bytes * s.dk
-            + s.sketch_bytes * s.dv * r + 4 * s.dv)
+            + s.sketch_bytes * s.dv * r + (s.cmap_bytes if r else 0) + 4 * s.dv)
 
 
 def init_bytes(s: Shape) -> int:

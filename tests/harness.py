@@ -31,7 +31,7 @@ class Run:
 
 
 def run_workload(wl, rank=None, window=None, steps=None, omega_coef=None, sel=None, baseline=False,
-                 device="cuda", seed=inputs.SEED, S0=None, keep_layer=False, sketch="f32"):
+                 device="cuda", seed=inputs.SEED, S0=None, keep_layer=False, sketch="f32", pivots=0):
     """Run `steps` decode tokens of workload `wl` on the GPU.
 
     sel: flat item indices (b*H + h) whose outputs and inputs are kept for the
@@ -47,7 +47,8 @@ def run_workload(wl, rank=None, window=None, steps=None, omega_coef=None, sel=No
     sel_t = None if sel is None else torch.as_tensor(sel, device=device, dtype=torch.long)
     S_sel = to_np32(S.reshape(n_items, wl.dv, wl.dk) if sel is None else S.reshape(n_items, wl.dv, wl.dk)[sel_t])
     layer = SketchSSMLayer(wl.kind, wl.batch, wl.heads, wl.dk, wl.dv, rank, window, wl.io, device,
-                           baseline=baseline, S=S, omega=torch.as_tensor(om), coef=torch.as_tensor(C), sketch=sketch)
+                           baseline=baseline, S=S, omega=torch.as_tensor(om), coef=torch.as_tensor(C), sketch=sketch,
+                           pivots=pivots)
     layer.init_sketch()
     run = Run()
     for t in range(steps):
@@ -63,7 +64,7 @@ def run_workload(wl, rank=None, window=None, steps=None, omega_coef=None, sel=No
     return run, layer, S_sel, heads.astype(np.int32), (om, C)
 
 
-def oracle_of(wl, run, S_sel, heads, om, C, window=None, sketch="f32"):
+def oracle_of(wl, run, S_sel, heads, om, C, window=None, sketch="f32", pivots=0):
     window = wl.window if window is None else window
     q = np.stack(run.inp["q"])
     k = np.stack(run.inp["k"])
@@ -71,7 +72,7 @@ def oracle_of(wl, run, S_sel, heads, om, C, window=None, sketch="f32"):
     beta = np.stack(run.inp["beta"])
     logd = np.stack(run.inp["log_decay"])
     return oracle.sketchssm(wl.kind, window, heads, om, C, S_sel, q, k, v, beta, logd, round_storage=True,
-                            sketch_bf16=(sketch == "bf16"))
+                            sketch_bf16=(sketch == "bf16"), pivots=pivots, ridge=0.1)
 
 
 def max_step_rel(o_gpu_list, o_ref):

@@ -64,10 +64,11 @@ ADDR = 1 << 20  # a 16-byte aligned fake address, never dereferenced (every case
 
 
 def cfg(**kw):
-    d = dict(kind="mamba2", batch=2, heads=4, dk=128, dv=64, rank=16, window=16, io="bf16", sketch="f32")
+    d = dict(kind="mamba2", batch=2, heads=4, dk=128, dv=64, rank=16, window=16, io="bf16", sketch="f32", pivots=0,
+             ridge=0.1)
     d.update(kw)
     return B.make_config(d["kind"], d["batch"], d["heads"], d["dk"], d["dv"], d["rank"], d["window"], d["io"],
-                         d["sketch"])
+                         d["sketch"], d["pivots"], d["ridge"])
 
 
 def good_ring(**kw):
@@ -108,6 +109,13 @@ class TestValidation:
         assert status(d, cfg(io=5), ADDR, ADDR, good_ring(), 0, ADDR, ADDR) == -1
         assert status(d, cfg(sketch=3), ADDR, ADDR, good_ring(), 0, ADDR, ADDR) == -1
         assert "sketch_dtype" in B.sketchssm_last_error()
+        # state-dependent coefficient map: P = 4 only, rank 8..32, a 16-byte aligned cmap, ridge >= 0
+        assert status(d, cfg(pivots=3), ADDR, ADDR, good_ring(), 0, ADDR, ADDR) == -2
+        assert status(d, cfg(pivots=4, rank=128), ADDR, ADDR, good_ring(), 0, ADDR, ADDR) == -2
+        assert status(d, cfg(pivots=4), ADDR, ADDR, good_ring(), 0, ADDR, ADDR) == -1  # no cmap
+        assert status(lambda *x: B.sketchssm_decode(*x, cmap=ADDR + 4), cfg(pivots=4), ADDR, ADDR, good_ring(), 0,
+                      ADDR, ADDR) == -3
+        assert status(d, cfg(pivots=4, ridge=-1.0), ADDR, ADDR, good_ring(), 0, ADDR, ADDR) == -1
         assert "n_buffered" in B.sketchssm_status_string(-4)
 
     def test_update_rejections(self, lib):
@@ -122,6 +130,8 @@ class TestValidation:
         assert status(u, cfg(), ADDR, ADDR, None, 15, ADDR, ADDR, ADDR) == -1  # ring needed when n > 0
         assert status(u, cfg(), ADDR, ADDR, good_ring(), 15, ADDR, ADDR, ADDR + 2) == -3
         assert status(u, cfg(sketch=-1), ADDR, ADDR, good_ring(), 15, ADDR, ADDR, ADDR) == -1
+        assert status(u, cfg(pivots=4), ADDR, ADDR, good_ring(), 15, ADDR, ADDR, ADDR) == -1  # no cmap
+        assert status(u, cfg(pivots=4, rank=0), ADDR, None, good_ring(), 15, ADDR, None, ADDR) == -2
 
     def test_full_read_rejections(self, lib):
         f = B.sketchssm_full_read_baseline

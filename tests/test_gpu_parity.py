@@ -27,14 +27,15 @@ def announce(msg):
     print(f"[case] {msg}", flush=True)
 
 
-def check(wl, window=None, rank=None, steps=None, sel=None, omega_coef=None, baseline=False, sketch="f32"):
+def check(wl, window=None, rank=None, steps=None, sel=None, omega_coef=None, baseline=False, sketch="f32", pivots=0):
     window = wl.window if window is None else window
     rank = wl.rank if rank is None else rank
     announce(f"{wl.name} kind={wl.kind} B={wl.batch} H={wl.heads} K={wl.dk} V={wl.dv} r={rank} W={window} "
-             f"io={wl.io} sketch={sketch} baseline={baseline} sel={'all' if sel is None else len(sel)}")
+             f"io={wl.io} sketch={sketch} pivots={pivots} baseline={baseline} sel={'all' if sel is None else len(sel)}")
     run, layer, S_sel, heads, (om, C) = run_workload(wl, rank=rank, window=window, steps=steps, sel=sel,
-                                                     omega_coef=omega_coef, baseline=baseline, sketch=sketch)
-    ref = oracle_of(wl, run, S_sel, heads, om, C, window, sketch=sketch)
+                                                     omega_coef=omega_coef, baseline=baseline, sketch=sketch,
+                                                     pivots=pivots)
+    ref = oracle_of(wl, run, S_sel, heads, om, C, window, sketch=sketch, pivots=pivots)
     target = ref.o_exact_windowed if baseline else ref.o
     err = max_step_rel(run.o_gpu, target)
     n_items = wl.batch * wl.heads
@@ -202,3 +203,23 @@ def test_bf16_sketch_small(fam, K, V, rank, window, io):
 def test_bf16_sketch_full_size(name):
     wl = inputs.WORKLOADS[name]
     check(wl, sel=sample_items(wl), sketch="bf16")
+
+
+# --- the state-dependent coefficient map (4 pivots, lambda = 0.1), rebuilt at every flush ---------
+@pytest.mark.parametrize("fam,K,V,rank,window,io,sketch", [
+    ("mamba2_form", 64, 64, 8, 8, "f32", "f32"),
+    ("mamba2", 128, 64, 16, 16, "bf16", "f32"),
+    ("gdn", 128, 128, 16, 16, "bf16", "f32"),
+    ("kda", 128, 128, 32, 8, "bf16", "f32"),
+    ("gdn", 64, 64, 32, 32, "f32", "f32"),
+    ("mamba2", 128, 64, 16, 16, "bf16", "bf16"),
+])
+def test_pivot_map_small(fam, K, V, rank, window, io, sketch):
+    wl = inputs.tiny(fam, batch=5, heads=3, dk=K, dv=V, rank=rank, window=window, steps=2 * window + 3, io=io)
+    check(wl, sketch=sketch, pivots=4)
+
+
+@pytest.mark.parametrize("name", ["mamba2_b256", "gdn_b512", "kda_b512"])
+def test_pivot_map_full_size(name):
+    wl = inputs.WORKLOADS[name]
+    check(wl, sel=sample_items(wl), pivots=4)

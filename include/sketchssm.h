@@ -92,7 +92,7 @@ typedef struct {
  *     read here, are item-major, field[B][H][W][...]: the window of an item
  *     is one contiguous block, so a read fetches four consecutive slots per
  *     load instruction and the flush stages the window in one sweep;
- *   - derived fields (g, u, f, pi, bcoef), written by each read for its own
+ *   - derived fields (f, pi, bcoef), written by each read for its own
  *     slot, are slot-major, field[W][B][H][...]: one step's writes for all
  *     items form one contiguous region of whole cache lines.
  *
@@ -102,26 +102,26 @@ typedef struct {
  * v = x_t, beta = dt and log_decay = dt * A_h (Sec. 3.2, M_t = D_t); the
  * query C_t is passed to each call.
  *
- * The library derives and stores the remaining fields when a token is read
- * for the first time (Appendix C), so later reads are parallel reductions
- * over slots:
- *   g      KDA: window-local cumulative log decay g_s = sum_{j<=s} log alpha_j
- *          (scalar decays rebuild it from log_decay on the fly), so every
- *          decay ratio is exp(g_t - g_s) <= 1, never a division;
+ * Every read rebuilds the window-local cumulative log decays
+ * g_s = sum_{j<=s} log alpha_j from log_decay (per channel for KDA), so every
+ * decay ratio is exp(g_t - g_s) <= 1, never a division.  The library derives
+ * and stores the remaining fields when a token is read for the first time
+ * (Appendix C), so later reads are parallel reductions over slots:
  *   bcoef  b_{s,j} = <exp(g_s - g_j) k_j, k_s>, j < s      (erase couplings);
- *   u      pseudo-values u_s = beta_s (v_s - sum_{j<s} b_{s,j} u_j), which
- *          carry the erase into the buffer output sum_s a_{t,s} u_s;
  *   f      projected erase factors f_s = C pi_s in R^r (eq. wyread), read by
  *          sketchssm_decode;
  *   pi     erase factors pi_s in R^K (eq. wy), read by the exact baseline.
+ * The pseudo-values u_s = beta_s (v_s - sum_{j<s} b_{s,j} u_j) that carry the
+ * erase into the buffer output are never stored: with T = I + Diag(beta) B
+ * unit lower triangular, sum_s a_{t,s} u_s = sum_j alpha_j beta_j v_j where
+ * T^T alpha = a_{t,.}, solved by each read from the couplings and the raw
+ * values; the flush forms u_s itself.
  * Unused fields may be NULL. */
 typedef struct {
   const void* k;          /* [B][H][W][K] io_dtype raw keys (producer)              all kinds */
   const void* v;          /* [B][H][W][V] io_dtype raw values (producer)            all kinds */
   const float* beta;      /* [B][H][W] write gates (producer)                       all kinds */
   const float* log_decay; /* [B][H][W] (MAMBA2, GDN) or [B][H][W][K] (KDA), <= 0 (producer) */
-  float* g;               /* [W][B][H][K] cumulative log decay                      KDA       */
-  float* u;               /* [W][B][H][V] pseudo-values                             GDN, KDA  */
   float* f;               /* [W][B][H][rank] projected erase factors   GDN, KDA (sketch read) */
   float* pi;              /* [W][B][H][K] erase factors                GDN, KDA (baseline)    */
   float* bcoef;           /* [W][B][H][W]: slot s holds b_{s,j}, j < s             GDN, KDA  */

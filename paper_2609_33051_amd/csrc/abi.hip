@@ -53,13 +53,9 @@ int check_ring(const skssm_config* c, const skssm_ring* r, bool derived_f, bool 
   if (!r->k || !r->v || !r->beta || !r->log_decay) return fail(SKSSM_EINVAL, "ring k/v/beta/log_decay is NULL");
   if (!aligned(r->k) || !aligned(r->v) || !aligned(r->beta) || !aligned(r->log_decay))
     return fail(SKSSM_EALIGN, "ring input field not 16-byte aligned");
-  if (c->kind == SKSSM_KDA) {
-    if (!r->g) return fail(SKSSM_EINVAL, "ring g is NULL (KDA)");
-    if (!aligned(r->g)) return fail(SKSSM_EALIGN, "ring g not aligned");
-  }
   if (c->kind != SKSSM_MAMBA2) {
-    if (!r->u || !r->bcoef) return fail(SKSSM_EINVAL, "ring u/bcoef is NULL (GDN/KDA)");
-    if (!aligned(r->u) || !aligned(r->bcoef)) return fail(SKSSM_EALIGN, "ring u/bcoef not aligned");
+    if (!r->bcoef) return fail(SKSSM_EINVAL, "ring bcoef is NULL (GDN/KDA)");
+    if (!aligned(r->bcoef)) return fail(SKSSM_EALIGN, "ring bcoef not aligned");
     if (derived_f && !r->f) return fail(SKSSM_EINVAL, "ring f is NULL (GDN/KDA sketch read)");
     if (derived_f && !aligned(r->f)) return fail(SKSSM_EALIGN, "ring f not aligned");
     if (derived_pi && !r->pi) return fail(SKSSM_EINVAL, "ring pi is NULL (GDN/KDA baseline)");
@@ -87,8 +83,6 @@ skssm::DecodeArgs decode_args(const skssm_config* c, const skssm_ring* r, int32_
   a.rv = r->v;
   a.rbeta = r->beta;
   a.rla = r->log_decay;
-  a.rg = r->g;
-  a.ru = r->u;
   a.rf = r->f;
   a.rpi = r->pi;
   a.rb = r->bcoef;
@@ -153,8 +147,6 @@ int sketchssm_update(const skssm_config* cfg, float* S, const float* omega, cons
     a.rv = ring->v;
     a.rbeta = ring->beta;
     a.rla = ring->log_decay;
-    a.rg = ring->g;
-    a.ru = ring->u;
     a.rb = ring->bcoef;
     a.o = o;
   } else {

@@ -23,8 +23,6 @@ struct DecodeArgs {
   const void* rv;                 // ring [B][H][W][V] io      raw values
   const float* rbeta;             // ring [B][H][W]            write gates
   const float* rla;               // ring [B][H][W] or [..][K] log decays
-  float* rg;                      // ring [W][B][H][K]  cumulative log decay (KDA)
-  float* ru;                      // ring [W][B][H][V]  pseudo-values (GDN/KDA)
   float* rf;                      // ring [W][B][H][R]  projected erase factors (GDN/KDA sketch read)
   float* rpi;                     // ring [W][B][H][K]  erase factors (GDN/KDA baseline)
   float* rb;                      // ring [W][B][H][W]  erase couplings (GDN/KDA)
@@ -41,8 +39,6 @@ struct UpdateArgs {
   const void* rv;
   const float* rbeta;
   const float* rla;
-  const float* rg;                // KDA cumulative log decay, slots < n
-  const float* ru;                // GDN/KDA pseudo-values, slots < n
   const float* rb;                // GDN/KDA erase couplings, slots < n
   void* U;                        // [B][H][R/P][V][P], P = 4 (fp32) or 8 (bf16), or NULL
   float* cmap;                    // [B][H][4K + 4R + R*R] state-dependent coefficient map (pivots), or NULL

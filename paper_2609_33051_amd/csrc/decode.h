@@ -50,12 +50,11 @@ struct RowLoads {
   Raw<IO, VR> v_raw;                  // current value (same in every row)
   float beta_t;
   float la[GD];                       // log alpha_t
-  float gprev[GD];                    // g_{t-1} (KDA: loaded; scalar decay: rebuilt)
+  float gprev[GD];                    // g_{t-1}, rebuilt from the ring's log alphas
   Raw<IO, KPL> ks[NG];                // ring keys of slot 4 gi + row, s < n
-  float gs[NG][GD];                   // cumulative log decay of slot 4 gi + row
-  Raw<IO, VR> vs[ERASE ? 1 : NG];     // ring raw values (Mamba-2)
-  float bs[ERASE ? 1 : NG];           // ring beta (Mamba-2)
-  Vec<VR> us[ERASE ? NG : 1];         // ring pseudo-values (GDN, KDA)
+  float gs[NG][GD];                   // log alpha, then cumulative log decay, of slot 4 gi + row
+  Raw<IO, VR> vs[NG];                 // ring raw values
+  float bs[NG];                       // ring beta
 
   // `item` is wave-uniform.  Slot s of a raw ring field (k, v, beta, log
   // alpha) of width w sits at field + (item * W + s) * w, the W slots of an
@@ -75,58 +74,67 @@ struct RowLoads {
       t.load(a.rla + cur * K + koff);
 #pragma unroll
       for (int m = 0; m < KPL; ++m) la[m] = t.e[m];
-#pragma unroll
-      for (int m = 0; m < KPL; ++m) gprev[m] = 0.f;
-      if (n > 0) {
-        Vec<KPL> g;
-        g.load(a.rg + ((size_t)(n - 1) * NI + item) * K + koff);
-#pragma unroll
-        for (int m = 0; m < KPL; ++m) gprev[m] = g.e[m];
-      }
     } else {
       la[0] = a.rla[cur];
     }
+#pragma unroll
+    for (int m = 0; m < GD; ++m) gprev[m] = 0.f;
     const size_t rowslot = item * W + row;           // slot `row` of this item (raw fields)
-    const size_t rowder = (size_t)row * NI + item;   // the same slot in the derived fields
 #pragma unroll
     for (int gi = 0; gi < NG; ++gi) {
       const int s = 4 * gi + row;
       const size_t si = rowslot + 4 * gi;
-      const size_t sd = rowder + (size_t)(4 * gi) * NI;
       ks[gi].zero();
+      vs[gi].zero();
+      bs[gi] = 0.f;
 #pragma unroll
       for (int m = 0; m < GD; ++m) gs[gi][m] = 0.f;
-      if constexpr (ERASE) {
-#pragma unroll
-        for (int m = 0; m < VR; ++m) us[gi].e[m] = 0.f;
-      } else {
-        vs[gi].zero();
-        bs[gi] = 0.f;
-      }
       if (4 * gi < n && s < n) {
         ks[gi].load(static_cast<const IO*>(a.rk) + si * K + koff);
+        vs[gi].load(static_cast<const IO*>(a.rv) + si * V + voff);
+        bs[gi] = a.rbeta[si];
+        // log alpha_s for now; made cumulative in prefix_decay()
         if constexpr (CHAN) {
           Vec<KPL> t;
-          t.load(a.rg + sd * K + koff);
+          t.load(a.rla + si * K + koff);
 #pragma unroll
           for (int m = 0; m < KPL; ++m) gs[gi][m] = t.e[m];
         } else {
-          gs[gi][0] = a.rla[si];  // log alpha_s for now; made cumulative in prefix_decay()
-        }
-        if constexpr (ERASE) {
-          us[gi].load(a.ru + sd * V + voff);
-        } else {
-          vs[gi].load(static_cast<const IO*>(a.rv) + si * V + voff);
-          bs[gi] = a.rbeta[si];
+          gs[gi][0] = a.rla[si];
         }
       }
     }
   }
 
-  // Scalar decay: turn the per-slot log alphas into cumulative log decays
-  // g_s = sum_{j<=s} log alpha_j (slots in order), and g_{t-1}.
+  // Turn the per-slot log alphas into cumulative log decays
+  // g_s = sum_{j<=s} log alpha_j (slots in order), and g_{t-1}.  Slots >= n
+  // hold zeros, so sums over whole groups are sums over the window.
   __device__ __forceinline__ void prefix_decay(int n, int row) {
-    if constexpr (!CHAN) {
+    if constexpr (CHAN) {
+      // per channel: inclusive scan over the 4 rows of a group (lanes 16
+      // apart), then the running total of earlier groups
+      float tot[KPL];
+#pragma unroll
+      for (int m = 0; m < KPL; ++m) tot[m] = 0.f;
+#pragma unroll
+      for (int gi = 0; gi < NG; ++gi) {
+        if (4 * gi < n) {
+#pragma unroll
+          for (int m = 0; m < KPL; ++m) {
+            const float x = gs[gi][m];
+            const float u1 = __shfl_up(x, 16);
+            const float y = x + (row >= 1 ? u1 : 0.f);
+            const float u2 = __shfl_up(y, 32);
+            const float z = y + (row >= 2 ? u2 : 0.f);
+            const float grp = __shfl(z, (threadIdx.x & 15) + 48);
+            gs[gi][m] = tot[m] + z;
+            tot[m] += grp;
+          }
+        }
+      }
+#pragma unroll
+      for (int m = 0; m < KPL; ++m) gprev[m] = tot[m];
+    } else {
       float tot = 0.f;
 #pragma unroll
       for (int gi = 0; gi < NG; ++gi) {
@@ -184,22 +192,72 @@ __device__ __forceinline__ void slot_dots(const L& r, int n, int row, const floa
   }
 }
 
-// Buffer term and current pseudo-value in the row layout (every row ends
-// with the full sums): ut = u_t, ob = sum_{s<=t} a_{t,s} u_s.
+// Coefficients of the buffer term on the raw values (GDN/KDA).  The
+// pseudo-values solve T u = beta . v with T = I + Diag(beta) B unit lower
+// triangular (B_{s,j} = b_{s,j}, j < s < n), so
+//   sum_{s<n} a_{t,s} u_s = sum_j alpha_j beta_j v_j,   T^T alpha = a_{t,.}
+//   sum_{j<n} b_{t,j} u_j = sum_j gamma_j beta_j v_j,   T^T gamma = b_{t,.}
+// and no pseudo-value is stored or read.  Lane j < n carries alpha_j and
+// gamma_j through the back substitution (s = n-1 .. 1, lanes j < s subtract
+// beta_s b_{s,j} x_s); b_{s,j} comes from the stored coupling rows.  Returns
+// ca = alpha . beta and cg = gamma . beta in the row layout (slot 4 gi + row).
+// sc: 3 WMAX floats of the wave's LDS scratch.
 template <class L>
-__device__ __forceinline__ void buffer_term(const L& r, const float (&av)[L::NG], const float (&bv)[L::NG],
+__device__ __forceinline__ void erase_coefs(const DecodeArgs& a, size_t item, int lane, int row, int col,
+                                            const L& r, const float (&av)[L::NG], const float (&bv)[L::NG], float* sc,
+                                            float (&ca)[L::NG], float (&cg)[L::NG]) {
+  constexpr int NG = L::NG, WM = 4 * NG;
+  const int n = a.n;
+  if (col == 0) {
+#pragma unroll
+    for (int gi = 0; gi < NG; ++gi) {
+      sc[4 * gi + row] = av[gi];
+      sc[WM + 4 * gi + row] = bv[gi];
+      sc[2 * WM + 4 * gi + row] = r.bs[gi];
+    }
+  }
+  const size_t NI = (size_t)a.B * a.H;
+  float bcol[WM];  // b_{s, lane} for lane < s < n
+#pragma unroll
+  for (int s = 0; s < WM; ++s) bcol[s] = (lane < s && s < n) ? a.rb[((size_t)s * NI + item) * a.W + lane] : 0.f;
+  wave_lds_sync();
+  float al = 0.f, gl = 0.f, bl = 0.f;
+  if (lane < n) {
+    al = sc[lane];
+    gl = sc[WM + lane];
+    bl = sc[2 * WM + lane];
+  }
+#pragma unroll
+  for (int s = WM - 1; s >= 1; --s) {
+    if (s < n) {
+      const float w = lane_bcast(bl, s) * bcol[s];
+      al -= w * lane_bcast(al, s);
+      gl -= w * lane_bcast(gl, s);
+    }
+  }
+  const float cal = al * bl, cgl = gl * bl;
+#pragma unroll
+  for (int gi = 0; gi < NG; ++gi) {
+    ca[gi] = __shfl(cal, 4 * gi + row);
+    cg[gi] = __shfl(cgl, 4 * gi + row);
+  }
+}
+
+// Buffer term and current pseudo-value in the row layout (every row ends
+// with the full sums), from per-slot coefficients on the raw values:
+// ob = sum_s ca_s v_s + a_{t,t} u_t and u_t = beta_t (v_t - sum_s cg_s v_s)
+// (Mamba-2: ca_s = a_{t,s} beta_s, no cg, u_t = beta_t v_t).
+template <class L>
+__device__ __forceinline__ void buffer_term(const L& r, const float (&ca)[L::NG], const float (&cg)[L::NG],
                                             float at, float (&ut)[L::VR], float (&ob)[L::VR]) {
 #pragma unroll
   for (int m = 0; m < L::VR; ++m) {
     float sa = 0.f, sb = 0.f;
 #pragma unroll
     for (int gi = 0; gi < L::NG; ++gi) {
-      if constexpr (L::ERASE) {
-        sa += av[gi] * r.us[gi].e[m];
-        sb += bv[gi] * r.us[gi].e[m];
-      } else {
-        sa += av[gi] * r.bs[gi] * r.vs[gi].get(m);
-      }
+      const float x = r.vs[gi].get(m);
+      sa += ca[gi] * x;
+      if constexpr (L::ERASE) sb += cg[gi] * x;
     }
     sa = cross_row_sum(sa);
     if constexpr (L::ERASE) {
@@ -212,28 +270,31 @@ __device__ __forceinline__ void buffer_term(const L& r, const float (&av)[L::NG]
   }
 }
 
-// Store the derived fields of the token at ring slot n (GDN/KDA: u_t and the
-// coupling row b_{t,.}; KDA: g_t).  Mamba-2 derives nothing.
+// Per-slot coefficients of the buffer term for any kind (see erase_coefs).
+template <class L>
+__device__ __forceinline__ void buffer_coefs(const DecodeArgs& a, size_t item, int lane, int row, int col,
+                                             const L& r, const float (&av)[L::NG], const float (&bv)[L::NG],
+                                             float* sc, float (&ca)[L::NG], float (&cg)[L::NG]) {
+  if constexpr (L::ERASE) {
+    erase_coefs<L>(a, item, lane, row, col, r, av, bv, sc, ca, cg);
+  } else {
+#pragma unroll
+    for (int gi = 0; gi < L::NG; ++gi) {
+      ca[gi] = av[gi] * r.bs[gi];
+      cg[gi] = 0.f;
+    }
+  }
+}
+
+// Store the coupling row b_{t,.} of the token at ring slot n (GDN/KDA) for
+// later reads and the flush.  Mamba-2 derives nothing.
 template <class L>
 __device__ __forceinline__ void append_derived(const DecodeArgs& a, size_t item, int row, int col, int lane,
-                                               const float (&gt)[L::GD], const float (&ut)[L::VR],
                                                const float (&bv)[L::NG], float* b_l) {
-  constexpr int K = L::KPL * 16, V = L::VR * 16, KPL = L::KPL, VR = L::VR, NG = L::NG;
+  constexpr int NG = L::NG;
   if constexpr (L::ERASE) {
     const int n = a.n, W = a.W;
     const size_t sl = (size_t)n * a.B * a.H + item;
-    if (row == 0) {
-      if constexpr (L::CHAN) {
-        Vec<KPL> t;
-#pragma unroll
-        for (int m = 0; m < KPL; ++m) t.e[m] = gt[m];
-        t.store(a.rg + sl * K + col * KPL);
-      }
-      Vec<VR> t;
-#pragma unroll
-      for (int m = 0; m < VR; ++m) t.e[m] = ut[m];
-      t.store(a.ru + sl * V + col * VR);
-    }
     // b_{t,s}, s < n: gather through LDS, then one contiguous store of the row
     if (col == 0) {
 #pragma unroll
@@ -256,7 +317,7 @@ __global__ __launch_bounds__(256) void decode_kernel(const DecodeArgs a) {
   constexpr int NP = R / PW;                     // sketch panels
   constexpr int CP = K + 4;                      // padded LDS row pitch of C
   constexpr int KQ = K / 4;                      // channels each row covers in C x
-  constexpr int WS = 2 * K + R + V + WMAX;       // per-wave LDS: x_q, x_k, c, o_buf, b row
+  constexpr int WS = 2 * K + R + V + 4 * WMAX;   // per-wave LDS: x_q, x_k, c, o_buf, b row, erase solve
   constexpr bool U_PRELOAD = R <= 32;
   constexpr int UP = U_PRELOAD ? NP : 1;
 
@@ -338,8 +399,10 @@ __global__ __launch_bounds__(256) void decode_kernel(const DecodeArgs a) {
 
   float av[NG], bv[NG], at;
   slot_dots(r, n, row, qv, kv, gt, av, bv, at);
+  float ca[NG], cg[NG];
+  buffer_coefs<L>(a, item, lane, row, col, r, av, bv, b_l + WMAX, ca, cg);
   float ut[VR], ob[VR];
-  buffer_term(r, av, bv, at, ut, ob);
+  buffer_term(r, ca, cg, at, ut, ob);
 
   // ---- C (e^{g_t} . q_t) and C (e^{g_t} . k_t): each row covers K/4 channels
   if (row == 0) {
@@ -481,7 +544,7 @@ __global__ __launch_bounds__(256) void decode_kernel(const DecodeArgs a) {
   }
 
   // ---- derived fields of the token at ring slot n
-  append_derived<L>(a, item, row, col, lane, gt, ut, bv, b_l);
+  append_derived<L>(a, item, row, col, lane, bv, b_l);
   if constexpr (ERASE) {
     if (row == 0) {
       const size_t sl = (size_t)n * a.B * H + item;
@@ -498,7 +561,7 @@ __global__ __launch_bounds__(256) void full_read_kernel(const DecodeArgs a) {
   constexpr bool ERASE = L::ERASE, CHAN = L::CHAN;
   constexpr int KPL = L::KPL, VR = L::VR, NG = L::NG, GD = L::GD;
   constexpr int VPL = V / 64;
-  constexpr int WS = 2 * V + WMAX;   // per-wave LDS: o^state, o_buf, b row
+  constexpr int WS = 2 * V + 4 * WMAX;  // per-wave LDS: o^state, o_buf, b row, erase solve
 
   __shared__ __align__(16) float wscr[4 * WS];
 
@@ -548,8 +611,10 @@ __global__ __launch_bounds__(256) void full_read_kernel(const DecodeArgs a) {
 
   float av[NG], bv[NG], at;
   slot_dots(r, n, row, qv, kv, gt, av, bv, at);
+  float ca[NG], cg[NG];
+  buffer_coefs<L>(a, item, lane, row, col, r, av, bv, b_l + WMAX, ca, cg);
   float ut[VR], ob[VR];
-  buffer_term(r, av, bv, at, ut, ob);
+  buffer_term(r, ca, cg, at, ut, ob);
 
   // ---- effective query q~_t and erase factor pi_t (row layout, all rows equal)
   float qe[KPL], pit[KPL];
@@ -595,7 +660,7 @@ __global__ __launch_bounds__(256) void full_read_kernel(const DecodeArgs a) {
 #pragma unroll
   for (int vv = 0; vv < VPL; ++vv) ob_g[lane + 64 * vv] = os_l[lane + 64 * vv] + ob_l[lane + 64 * vv];
 
-  append_derived<L>(a, item, row, col, lane, gt, ut, bv, b_l);
+  append_derived<L>(a, item, row, col, lane, bv, b_l);
   if constexpr (ERASE) {
     if (row == 0) {
       Vec<KPL> t;

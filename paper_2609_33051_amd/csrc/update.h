@@ -328,27 +328,38 @@ __global__ __launch_bounds__(256, 3) void update_kernel(const UpdateArgs a) {
   float bsv[SP], gsv[SP];               // beta_s and (scalar decay) g_s, wave-uniform
   float gk[CHAN ? SP : 1];              // KDA: g_s of channel tid
   Raw<IO, KPL> kr[NG / 4];              // ring keys, row layout (slot 4 (wave + 4 gq) + row)
-  Vec<ERASE ? VR : 1> ur[NG / 4];       // GDN/KDA: pseudo-values u_s (s < n)
-  Raw<IO, VR> vr[NG / 4];               // raw values (Mamba-2: all slots; GDN/KDA: slot n)
+  Raw<IO, VR> vr[NG / 4];               // raw values
   float qv = 0.f;
   constexpr int BQ = ERASE ? (SP * SP + 255) / 256 : 1;
   float bv[BQ];
   Vec<4> omv[OQ];
   if (flush) {
+    // every slot load is issued before any is used: slots past n re-read slot
+    // n (in bounds) and are masked afterwards, so no load waits on a branch
+    float lav[CHAN ? 1 : SP];
+#pragma unroll
+    for (int s = 0; s < SP; ++s) {
+      const size_t si = item * W + (s < n ? s : n);
+      bsv[s] = a.rbeta[si];
+      if constexpr (!CHAN) lav[s] = a.rla[si];
+    }
+    if constexpr (CHAN) {
+      if (tid < K) {
+#pragma unroll
+        for (int s = 0; s < SP; ++s) gk[s] = a.rla[(item * W + (s < n ? s : n)) * K + tid];
+      }
+    }
     {
-      float acc = 0.f;
+      float acc = 0.f;  // g_s: running sum of the window's log alphas
 #pragma unroll
       for (int s = 0; s < SP; ++s) {
-        bsv[s] = 0.f;
-        gsv[s] = 0.f;
-        if (s <= n) {
-          const size_t si = item * W + s;
-          bsv[s] = a.rbeta[si];
-          if constexpr (!CHAN) {
-            acc += a.rla[si];
-            gsv[s] = acc;
-          }
+        if constexpr (!CHAN) {
+          acc += s <= n ? lav[s] : 0.f;
+          gsv[s] = s <= n ? acc : 0.f;
+        } else {
+          gsv[s] = 0.f;
         }
+        bsv[s] = s <= n ? bsv[s] : 0.f;
       }
     }
 #pragma unroll
@@ -358,30 +369,13 @@ __global__ __launch_bounds__(256, 3) void update_kernel(const UpdateArgs a) {
         bn = bsv[s];
       }
     if constexpr (!CHAN) egn = fast_exp(gn);
-    if constexpr (CHAN) {
-      if (tid < K) {
-#pragma unroll
-        for (int s = 0; s < SP; ++s) {
-          gk[s] = 0.f;
-          if (s <= n) {
-            const size_t si = item * W + s;
-            const size_t sd = (size_t)s * NI + item;
-            gk[s] = (s < n) ? a.rg[sd * K + tid] : ((n > 0 ? a.rg[(sd - NI) * K + tid] : 0.f) + a.rla[si * K + tid]);
-          }
-        }
-      }
-    }
 #pragma unroll
     for (int gq = 0; gq < NG / 4; ++gq) {
       const int s = 4 * (wave + 4 * gq) + row;
       const size_t si = item * W + s;
       if (s <= n) {
         kr[gq].load(static_cast<const IO*>(a.rk) + si * K + col * KPL);
-        if (ERASE && s < n) {
-          if constexpr (ERASE) ur[gq].load(a.ru + ((size_t)s * NI + item) * V + col * VR);
-        } else {
-          vr[gq].load(static_cast<const IO*>(a.rv) + si * V + col * VR);
-        }
+        vr[gq].load(static_cast<const IO*>(a.rv) + si * V + col * VR);
       }
     }
     if (tid < K) qv = load1<IO>(static_cast<const IO*>(a.q) + item * K + tid);
@@ -448,14 +442,9 @@ __global__ __launch_bounds__(256, 3) void update_kernel(const UpdateArgs a) {
       if (s <= n) {
 #pragma unroll
         for (int m = 0; m < KPL; ++m) ksv[m] = kr[gq].get(m);
-        if (ERASE && s < n) {
-          if constexpr (ERASE) {
-#pragma unroll
-            for (int m = 0; m < VR; ++m) vsv[m] = ur[gq].e[m];
-          }
-        } else {
-          // raw value: Mamba-2 scales it into c_s beta_s v_s; GDN/KDA keep v_n
-          // in row n until u_n is formed
+        {
+          // raw value: Mamba-2 scales it into c_s beta_s v_s; GDN/KDA keep it
+          // until the pseudo-values are formed
           float sc = 1.f;
           if constexpr (!ERASE) {
             // select this row's slot from the wave-uniform tables (compile-time indices only)
@@ -502,12 +491,22 @@ __global__ __launch_bounds__(256, 3) void update_kernel(const UpdateArgs a) {
   if (flush) {
     if constexpr (ERASE) {
       // ---- channel work: thread tid owns channel k = tid.  Ls holds raw keys.
+      // The pseudo-values of slots before n need only the stored couplings,
+      // so the waves that own no channel form them meanwhile.
+      static_assert(K + V <= 256, "channel waves and value waves must be disjoint");
       float pi[SP], kn = 0.f;
       if (tid < K) {
         const int kk = tid;
         kn = Ls[n * LP + kk];
         float gnk = gn;
         if constexpr (CHAN) {
+          // g_s of channel tid: running sum of the window's log alphas
+          float acc = 0.f;
+#pragma unroll
+          for (int s = 0; s < SP; ++s) {
+            acc += s <= n ? gk[s] : 0.f;
+            gk[s] = s <= n ? acc : 0.f;
+          }
 #pragma unroll
           for (int s = 0; s < SP; ++s)
             if (s == n) gnk = gk[s];
@@ -539,12 +538,28 @@ __global__ __launch_bounds__(256, 3) void update_kernel(const UpdateArgs a) {
           for (int s = 0; s < SP; ++s)
             if (s < n) Ls[s * LP + kk] *= fast_exp(gnk - gk[s]);
         }
+      } else if (tid >= 256 - V) {
+        // pseudo-values u_s = beta_s (v_s - sum_{j<s} b_{s,j} u_j), s < n, in
+        // place over the raw values (thread owns value channel v)
+        const int v = tid - (256 - V);
+        float uv[SP];
+#pragma unroll
+        for (int s = 0; s < SP; ++s) {
+          uv[s] = 0.f;
+          if (s < n) {
+            float acc = Us[s * UP + v];
+#pragma unroll
+            for (int j = 0; j < s; ++j) acc -= Bs[s * SP + j] * uv[j];
+            uv[s] = bsv[s] * acc;
+            Us[s * UP + v] = uv[s];
+          }
+        }
       }
       lds_barrier();
-      // ---- the current token: u_n and pi_n need b_{n,j} from every wave
+      // ---- slot n: row n of the couplings comes from every wave's partial sums
       if (tid < V) {
         const int v = tid;
-        float acc = Us[n * UP + v];  // raw v_n
+        float acc = Us[n * UP + v];
 #pragma unroll
         for (int j = 0; j < SP; ++j) {
           if (j < n) {
@@ -554,7 +569,7 @@ __global__ __launch_bounds__(256, 3) void update_kernel(const UpdateArgs a) {
             acc -= bj * Us[j * UP + v];
           }
         }
-        Us[n * UP + v] = bn * acc;  // u_n
+        Us[n * UP + v] = bn * acc;
       }
       if (tid < K) {
         const int kk = tid;

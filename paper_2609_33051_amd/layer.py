@@ -58,13 +58,11 @@ class SketchSSMLayer:
         self.rbeta = torch.zeros((Bt, H, W), dtype=f32, device=dev)
         self.rla = torch.zeros((Bt, H, W, K) if kind == "kda" else (Bt, H, W), dtype=f32, device=dev)
         # derived fields, written by the library
-        self.rg = torch.zeros((W, Bt, H, K), dtype=f32, device=dev) if kind == "kda" else None
-        self.ru = torch.zeros((W, Bt, H, V), dtype=f32, device=dev) if erase else None
         self.rb = torch.zeros((W, Bt, H, W), dtype=f32, device=dev) if erase else None
         self.rf = torch.zeros((W, Bt, H, rank), dtype=f32, device=dev) if (erase and not baseline) else None
         self.rpi = torch.zeros((W, Bt, H, K), dtype=f32, device=dev) if (erase and baseline) else None
-        self.ring = B.make_ring(k=self.rk, v=self.rv, beta=self.rbeta, log_decay=self.rla, g=self.rg,
-                                u=self.ru, f=self.rf, pi=self.rpi, bcoef=self.rb)
+        self.ring = B.make_ring(k=self.rk, v=self.rv, beta=self.rbeta, log_decay=self.rla, f=self.rf,
+                                pi=self.rpi, bcoef=self.rb)
         self.o = torch.zeros((Bt, H, V), dtype=f32, device=dev)
         self.n = 0  # slot of the next token in the current window
 

@@ -78,14 +78,20 @@ class Shape:
 def slot_read_bytes(s: Shape, baseline: bool = False) -> int:
     """What a non-flush read takes from each earlier slot of the ring.
 
-    Mamba-2: raw key and value, beta, log decay.
-    GDN/KDA: raw key, pseudo-value u (fp32), the projected erase vector f
-    (r fp32, sketch read) or erase factor pi (K fp32, exact baseline), and the
-    log decay (GDN) or cumulative log decay (KDA, K fp32)."""
+    Every kind: raw key and value, beta, log decay (K fp32 for KDA).
+    GDN/KDA also: the projected erase vector f (r fp32, sketch read) or the
+    erase factor pi (K fp32, exact baseline).  (The pseudo-values are solved
+    from the raw values and the couplings, not stored.)"""
+    raw = s.io_bytes * (s.dk + s.dv) + 4 + s.decay_bytes
     if not s.erase:
-        return s.io_bytes * (s.dk + s.dv) + 4 + 4
-    extra = 4 * s.dk if baseline else 4 * s.rank
-    return s.io_bytes * s.dk + 4 * s.dv + extra + s.decay_bytes
+        return raw
+    return raw + (4 * s.dk if baseline else 4 * s.rank)
+
+
+def coupling_read_bytes(s: Shape, n: int) -> int:
+    """GDN/KDA: the stored coupling rows b_{s,.} of the n earlier slots
+    (slot s holds s of them), read to solve for the buffer coefficients."""
+    return 2 * n * (n - 1) if s.erase else 0
 
 
 def current_read_bytes(s: Shape) -> int:
@@ -94,38 +100,35 @@ def current_read_bytes(s: Shape) -> int:
 
 
 def derived_write_bytes(s: Shape, n: int, baseline: bool = False) -> int:
-    """Fields a read derives and stores for slot n: GDN/KDA u, f (or pi), the
-    coupling row b_{n,.}; KDA the cumulative log decay.  Mamba-2: none."""
+    """Fields a read derives and stores for slot n: GDN/KDA f (or pi) and the
+    coupling row b_{n,.}.  Mamba-2: none."""
     if not s.erase:
         return 0
     extra = 4 * s.dk if baseline else 4 * s.rank
-    return 4 * s.dv + extra + 4 * n + (4 * s.dk if s.kind == "kda" else 0)
+    return extra + 4 * n
 
 
 def decode_bytes(s: Shape, n: int) -> int:
     """Sketch read at slot n: the query, n earlier slots, the current slot, the
     derived fields, U, the state-dependent map's factors (if any) and o."""
-    return (s.io_bytes * s.dk + n * slot_read_bytes(s) + current_read_bytes(s) + derived_write_bytes(s, n)
-            + s.sketch_bytes * s.dv * s.rank + s.cmap_bytes + 4 * s.dv)
+    return (s.io_bytes * s.dk + n * slot_read_bytes(s) + current_read_bytes(s) + coupling_read_bytes(s, n)
+            + derived_write_bytes(s, n) + s.sketch_bytes * s.dv * s.rank + s.cmap_bytes + 4 * s.dv)
 
 
 def full_read_bytes(s: Shape, n: int) -> int:
     """Exact full-state read at slot n: as decode with S (4KV) in place of U."""
-    return (s.io_bytes * s.dk + n * slot_read_bytes(s, True) + current_read_bytes(s)
+    return (s.io_bytes * s.dk + n * slot_read_bytes(s, True) + current_read_bytes(s) + coupling_read_bytes(s, n)
             + derived_write_bytes(s, n, True) + 4 * s.dk * s.dv + 4 * s.dv)
 
 
 def flush_bytes(s: Shape, n_buffered: int, rank: int | None = None) -> int:
     """Flush of the token in slot n_buffered: S read + write, the earlier
-    slots (k, u or v, beta, decay) and their coupling rows, the current slot,
-    the query, the sketch write (rank columns) and o."""
+    slots (raw k, v, beta, log decay) and their coupling rows, the current
+    slot, the query, the sketch write (rank columns), the state-dependent
+    map's factors (if any) and o."""
     r = s.rank if rank is None else rank
-    if s.erase:
-        slot = s.io_bytes * s.dk + 4 * s.dv + 4 + s.decay_bytes
-        bcoef = 4 * n_buffered * (n_buffered - 1) // 2
-    else:
-        slot = s.io_bytes * (s.dk + s.dv) + 4 + 4
-        bcoef = 0
+    slot = s.io_bytes * (s.dk + s.dv) + 4 + s.decay_bytes
+    bcoef = 4 * n_buffered * (n_buffered - 1) // 2 if s.erase else 0
     return (8 * s.dk * s.dv + n_buffered * slot + bcoef + current_read_bytes(s) + s.io_bytes * s.dk
             + s.sketch_bytes * s.dv * r + (s.cmap_bytes if r else 0) + 4 * s.dv)
 

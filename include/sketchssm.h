@@ -92,7 +92,7 @@ typedef struct {
  *     read here, are item-major, field[B][H][W][...]: the window of an item
  *     is one contiguous block, so a read fetches four consecutive slots per
  *     load instruction and the flush stages the window in one sweep;
- *   - derived fields (f, pi, bcoef), written by each read for its own
+ *   - derived fields (f, pi, tinv), written by each read for its own
  *     slot, are slot-major, field[W][B][H][...]: one step's writes for all
  *     items form one contiguous region of whole cache lines.
  *
@@ -106,16 +106,22 @@ typedef struct {
  * g_s = sum_{j<=s} log alpha_j from log_decay (per channel for KDA), so every
  * decay ratio is exp(g_t - g_s) <= 1, never a division.  The library derives
  * and stores the remaining fields when a token is read for the first time
- * (Appendix C), so later reads are parallel reductions over slots:
- *   bcoef  b_{s,j} = <exp(g_s - g_j) k_j, k_s>, j < s      (erase couplings);
+ * (the WY appendix), so later reads are parallel reductions over slots.
+ * With the couplings of eq. wy, b_{s,j} = <exp(g_s - g_j) k_j, k_s> (j < s),
+ * T = I + Diag(beta) B is unit lower triangular; the erase factors are
+ * pi = T^{-1} (beta . e^g . k) and the pseudo-values that carry the erase
+ * into the buffer output are u = T^{-1} (beta . v) (stacked over slots).
+ *   tinv   row s of T^{-1}: entries j < s (the unit diagonal is implicit).
+ *          Row s is -beta_s gamma^T with gamma = T^{-T} b_{s,.}, which the
+ *          read of token s computes anyway;
  *   f      projected erase factors f_s = C pi_s in R^r (eq. wyread), read by
  *          sketchssm_decode;
  *   pi     erase factors pi_s in R^K (eq. wy), read by the exact baseline.
- * The pseudo-values u_s = beta_s (v_s - sum_{j<s} b_{s,j} u_j) that carry the
- * erase into the buffer output are never stored: with T = I + Diag(beta) B
- * unit lower triangular, sum_s a_{t,s} u_s = sum_j alpha_j beta_j v_j where
- * T^T alpha = a_{t,.}, solved by each read from the couplings and the raw
- * values; the flush forms u_s itself.
+ * u is never stored: sum_s a_{t,s} u_s = sum_j alpha_j beta_j v_j with
+ * alpha = T^{-T} a_{t,.}, one product with the stored rows per read; the
+ * flush forms u itself.  Entries of tinv at or above the diagonal, and rows
+ * of slots not yet read in this window, are never used (the ring needs no
+ * clearing).
  * Unused fields may be NULL. */
 typedef struct {
   const void* k;          /* [B][H][W][K] io_dtype raw keys (producer)              all kinds */
@@ -124,7 +130,7 @@ typedef struct {
   const float* log_decay; /* [B][H][W] (MAMBA2, GDN) or [B][H][W][K] (KDA), <= 0 (producer) */
   float* f;               /* [W][B][H][rank] projected erase factors   GDN, KDA (sketch read) */
   float* pi;              /* [W][B][H][K] erase factors                GDN, KDA (baseline)    */
-  float* bcoef;           /* [W][B][H][W]: slot s holds b_{s,j}, j < s             GDN, KDA  */
+  float* tinv;            /* [W][B][H][W]: slot s holds (T^{-1})_{s,j}, j < s      GDN, KDA  */
 } skssm_ring;
 
 /*
@@ -146,7 +152,7 @@ typedef struct {
  * S      [B][H][V][K] fp32, read and (q != NULL) written in place.
  * omega  [H][K][rank] fp32 (may be NULL when rank == 0).
  * ring   read-only here: k, v, beta, log_decay of slots 0..n_buffered;
- *        g (KDA), u and bcoef (GDN, KDA) of slots 0..n_buffered-1.
+ *        tinv (GDN, KDA) of slots 0..n_buffered-1.
  * q      [B][H][K] io_dtype, the current query.
  * U      [B][H][rank/P][V][P] output in cfg.sketch_dtype, panel layout (may be NULL when rank == 0).
  * cmap   cfg.pivots = 4: [B][H][4K + 4 rank + rank^2] fp32 output, the
@@ -170,7 +176,7 @@ int sketchssm_update(const skssm_config* cfg, float* S, const float* omega, cons
  * (for MAMBA2 f_s = 0 and u_s = beta_s v_s, so c_t = e^{g_t} C q_t).  S is
  * never read.  U [B][H][rank/P][V][P] (cfg.sketch_dtype) and coef [H][rank][K] fp32 (C;
  * Omega^T for the offline map of Sec. 4.1 at E0 = I) are read; for GDN/KDA
- * the derived fields of slot n_buffered (u, f, bcoef; KDA g) are written.
+ * the derived fields of slot n_buffered (f, tinv) are written.
  * With cfg.pivots = 4 the map is the state-dependent one that the last
  * sketchssm_update wrote to cmap, C = F1 M + F2 coef, and coef must then be
  * Omega^T.  q [B][H][K] io_dtype; o [B][H][V] fp32.  rank must be > 0,
@@ -185,7 +191,7 @@ int sketchssm_decode(const skssm_config* cfg, const void* U, const float* coef, 
  *     o = S_0^T q~_t + o_t^buffer,  q~_t = e^{g_t} . q_t - sum_{s<=t} a_{t,s} pi_s
  * (eq. m-reads with the effective query of eq. app-effective-query-wy), for
  * the token in ring slot n_buffered (0..W-2).  For GDN/KDA the derived fields
- * of that slot (u, pi, bcoef; KDA g) are written.  S [B][H][V][K] is only
+ * of that slot (pi, tinv) are written.  S [B][H][V][K] is only
  * read.  Flushes of this path use sketchssm_update with rank = 0.
  * cfg->rank is ignored.
  */

@@ -40,7 +40,7 @@ class Config(ctypes.Structure):
 
 class Ring(ctypes.Structure):
     _fields_ = [(name, ctypes.c_void_p) for name in
-                ("k", "v", "beta", "log_decay", "f", "pi", "bcoef")]
+                ("k", "v", "beta", "log_decay", "f", "pi", "tinv")]
 
 
 _lib = None
@@ -96,8 +96,8 @@ def cmap_width(cfg: Config) -> int:
     return p * K + r * p + r * r if p else 0
 
 
-def make_ring(k=None, v=None, beta=None, log_decay=None, f=None, pi=None, bcoef=None) -> Ring:
-    return Ring(ptr(k), ptr(v), ptr(beta), ptr(log_decay), ptr(f), ptr(pi), ptr(bcoef))
+def make_ring(k=None, v=None, beta=None, log_decay=None, f=None, pi=None, tinv=None) -> Ring:
+    return Ring(ptr(k), ptr(v), ptr(beta), ptr(log_decay), ptr(f), ptr(pi), ptr(tinv))
 
 
 def _check(rc: int):

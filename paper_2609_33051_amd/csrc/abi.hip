@@ -54,8 +54,8 @@ int check_ring(const skssm_config* c, const skssm_ring* r, bool derived_f, bool 
   if (!aligned(r->k) || !aligned(r->v) || !aligned(r->beta) || !aligned(r->log_decay))
     return fail(SKSSM_EALIGN, "ring input field not 16-byte aligned");
   if (c->kind != SKSSM_MAMBA2) {
-    if (!r->bcoef) return fail(SKSSM_EINVAL, "ring bcoef is NULL (GDN/KDA)");
-    if (!aligned(r->bcoef)) return fail(SKSSM_EALIGN, "ring bcoef not aligned");
+    if (!r->tinv) return fail(SKSSM_EINVAL, "ring tinv is NULL (GDN/KDA)");
+    if (!aligned(r->tinv)) return fail(SKSSM_EALIGN, "ring tinv not aligned");
     if (derived_f && !r->f) return fail(SKSSM_EINVAL, "ring f is NULL (GDN/KDA sketch read)");
     if (derived_f && !aligned(r->f)) return fail(SKSSM_EALIGN, "ring f not aligned");
     if (derived_pi && !r->pi) return fail(SKSSM_EINVAL, "ring pi is NULL (GDN/KDA baseline)");
@@ -85,7 +85,7 @@ skssm::DecodeArgs decode_args(const skssm_config* c, const skssm_ring* r, int32_
   a.rla = r->log_decay;
   a.rf = r->f;
   a.rpi = r->pi;
-  a.rb = r->bcoef;
+  a.rt = r->tinv;
   a.o = o;
   return a;
 }
@@ -147,7 +147,7 @@ int sketchssm_update(const skssm_config* cfg, float* S, const float* omega, cons
     a.rv = ring->v;
     a.rbeta = ring->beta;
     a.rla = ring->log_decay;
-    a.rb = ring->bcoef;
+    a.rt = ring->tinv;
     a.o = o;
   } else {
     if (n_buffered != 0) return fail(SKSSM_ESTATE, "sketch-only update needs n_buffered = 0");

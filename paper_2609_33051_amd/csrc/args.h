@@ -25,7 +25,7 @@ struct DecodeArgs {
   const float* rla;               // ring [B][H][W] or [..][K] log decays
   float* rf;                      // ring [W][B][H][R]  projected erase factors (GDN/KDA sketch read)
   float* rpi;                     // ring [W][B][H][K]  erase factors (GDN/KDA baseline)
-  float* rb;                      // ring [W][B][H][W]  erase couplings (GDN/KDA)
+  float* rt;                      // ring [W][B][H][W]  rows of T^{-1} (GDN/KDA)
   float* o;                       // [B][H][V]
 };
 
@@ -39,7 +39,7 @@ struct UpdateArgs {
   const void* rv;
   const float* rbeta;
   const float* rla;
-  const float* rb;                // GDN/KDA erase couplings, slots < n
+  const float* rt;                // GDN/KDA rows of T^{-1}, slots < n
   void* U;                        // [B][H][R/P][V][P], P = 4 (fp32) or 8 (bf16), or NULL
   float* cmap;                    // [B][H][4K + 4R + R*R] state-dependent coefficient map (pivots), or NULL
   float ridge;                    // its lambda

@@ -45,6 +45,7 @@ struct RowLoads {
   static constexpr int VR = V / 16;   // value channels per lane
   static constexpr int NG = WMAX / 4; // groups of four slots
   static constexpr int GD = CHAN ? KPL : 1;
+  static constexpr int JP = (WMAX + 15) / 16;  // columns of T^{-1} per lane: j = col + 16 p
 
   Raw<IO, KPL> q_raw, k_raw;          // current query and key (same in every row)
   Raw<IO, VR> v_raw;                  // current value (same in every row)
@@ -55,14 +56,30 @@ struct RowLoads {
   float gs[NG][GD];                   // log alpha, then cumulative log decay, of slot 4 gi + row
   Raw<IO, VR> vs[NG];                 // ring raw values
   float bs[NG];                       // ring beta
+  float tv[ERASE ? NG : 1][JP];       // ring (T^{-1})_{s,j}, s = 4 gi + row, j = col + 16 p (unmasked)
 
   // `item` is wave-uniform.  Slot s of a raw ring field (k, v, beta, log
   // alpha) of width w sits at field + (item * W + s) * w, the W slots of an
-  // item contiguous; slot s of a derived field (g, u, f, pi, b) at
+  // item contiguous; slot s of a derived field (f, pi, rows of T^{-1}) at
   // field + (s * B*H + item) * w, one slot of all items contiguous.
   __device__ __forceinline__ void load(const DecodeArgs& a, size_t item, int row, int col) {
     const int n = a.n;
     const size_t W = (size_t)a.W, NI = (size_t)a.B * a.H;
+    if constexpr (ERASE) {
+      // rows of T^{-1}: issued first and without branches (row and column
+      // clamped into the ring, masked below), so they share the first wait
+      const int smax = n > 0 ? n - 1 : 0;
+#pragma unroll
+      for (int gi = 0; gi < NG; ++gi) {
+        const int s = 4 * gi + row;
+        const size_t rs = ((size_t)(s < smax ? s : smax) * NI + item) * W;
+#pragma unroll
+        for (int p = 0; p < JP; ++p) {
+          const int j = col + 16 * p;
+          tv[gi][p] = a.rt[rs + (size_t)(j < a.W ? j : a.W - 1)];
+        }
+      }
+    }
     const uint32_t koff = (uint32_t)(col * KPL), voff = (uint32_t)(col * VR);
     const size_t cur = item * W + n;                 // slot n of this item (raw fields)
     q_raw.load(static_cast<const IO*>(a.q) + item * K + koff);
@@ -110,46 +127,25 @@ struct RowLoads {
   // g_s = sum_{j<=s} log alpha_j (slots in order), and g_{t-1}.  Slots >= n
   // hold zeros, so sums over whole groups are sums over the window.
   __device__ __forceinline__ void prefix_decay(int n, int row) {
-    if constexpr (CHAN) {
-      // per channel: inclusive scan over the 4 rows of a group (lanes 16
-      // apart), then the running total of earlier groups
-      float tot[KPL];
+    // per channel (KDA) or per slot: inclusive scan over the 4 rows of a
+    // group (rows_scan), then the running total of the earlier groups
+    float tot[GD];
 #pragma unroll
-      for (int m = 0; m < KPL; ++m) tot[m] = 0.f;
+    for (int m = 0; m < GD; ++m) tot[m] = 0.f;
 #pragma unroll
-      for (int gi = 0; gi < NG; ++gi) {
-        if (4 * gi < n) {
+    for (int gi = 0; gi < NG; ++gi) {
+      if (4 * gi < n) {
 #pragma unroll
-          for (int m = 0; m < KPL; ++m) {
-            const float x = gs[gi][m];
-            const float u1 = __shfl_up(x, 16);
-            const float y = x + (row >= 1 ? u1 : 0.f);
-            const float u2 = __shfl_up(y, 32);
-            const float z = y + (row >= 2 ? u2 : 0.f);
-            const float grp = __shfl(z, (threadIdx.x & 15) + 48);
-            gs[gi][m] = tot[m] + z;
-            tot[m] += grp;
-          }
+        for (int m = 0; m < GD; ++m) {
+          float grp;
+          const float z = rows_scan(gs[gi][m], row, grp);
+          gs[gi][m] = tot[m] + z;
+          tot[m] += grp;
         }
       }
-#pragma unroll
-      for (int m = 0; m < KPL; ++m) gprev[m] = tot[m];
-    } else {
-      float tot = 0.f;
-#pragma unroll
-      for (int gi = 0; gi < NG; ++gi) {
-        if (4 * gi < n) {
-          const float x = gs[gi][0];
-          const float p0 = tot + lane_bcast(x, 0);
-          const float p1 = p0 + lane_bcast(x, 16);
-          const float p2 = p1 + lane_bcast(x, 32);
-          const float p3 = p2 + lane_bcast(x, 48);
-          gs[gi][0] = row == 0 ? p0 : row == 1 ? p1 : row == 2 ? p2 : p3;
-          tot = p3;  // log alphas of slots >= n are zero
-        }
-      }
-      gprev[0] = tot;
     }
+#pragma unroll
+    for (int m = 0; m < GD; ++m) gprev[m] = tot[m];
   }
 };
 
@@ -192,54 +188,58 @@ __device__ __forceinline__ void slot_dots(const L& r, int n, int row, const floa
   }
 }
 
-// Coefficients of the buffer term on the raw values (GDN/KDA).  The
-// pseudo-values solve T u = beta . v with T = I + Diag(beta) B unit lower
-// triangular (B_{s,j} = b_{s,j}, j < s < n), so
-//   sum_{s<n} a_{t,s} u_s = sum_j alpha_j beta_j v_j,   T^T alpha = a_{t,.}
-//   sum_{j<n} b_{t,j} u_j = sum_j gamma_j beta_j v_j,   T^T gamma = b_{t,.}
-// and no pseudo-value is stored or read.  Lane j < n carries alpha_j and
-// gamma_j through the back substitution (s = n-1 .. 1, lanes j < s subtract
-// beta_s b_{s,j} x_s); b_{s,j} comes from the stored coupling rows.  Returns
-// ca = alpha . beta and cg = gamma . beta in the row layout (slot 4 gi + row).
-// sc: 3 WMAX floats of the wave's LDS scratch.
+// Coefficients of the buffer term on the raw values (GDN/KDA).  With the
+// couplings B_{s,j} = b_{s,j} (j < s) of eq. wy, T = I + Diag(beta) B is unit
+// lower triangular and the pseudo-values are u = T^{-1} (beta . v), so
+//   sum_{s<n} a_{t,s} u_s = sum_j alpha_j beta_j v_j,   alpha = T^{-T} a_{t,.}
+//   sum_{j<n} b_{t,j} u_j = sum_j gamma_j beta_j v_j,   gamma = T^{-T} b_{t,.}
+// The ring holds the rows of T^{-1}, so both are products with stored rows:
+// lane (row, col) multiplies (T^{-1})_{s,j} (s = 4 gi + row, j = col + 16 p)
+// by a_s and b_s and the 4 rows are summed, leaving alpha_j and gamma_j in
+// column j.  A pass through LDS (sc: 2 WMAX floats) returns them to the row
+// layout as ca = alpha . beta and cg = gamma . beta (slot 4 gi + row);
+// gcol keeps gamma_j in column j for the new row of T^{-1}.
 template <class L>
-__device__ __forceinline__ void erase_coefs(const DecodeArgs& a, size_t item, int lane, int row, int col,
-                                            const L& r, const float (&av)[L::NG], const float (&bv)[L::NG], float* sc,
-                                            float (&ca)[L::NG], float (&cg)[L::NG]) {
-  constexpr int NG = L::NG, WM = 4 * NG;
-  const int n = a.n;
-  if (col == 0) {
+__device__ __forceinline__ void erase_coefs(int n, int row, int col, const L& r, const float (&av)[L::NG],
+                                            const float (&bv)[L::NG], float* sc, float (&ca)[L::NG],
+                                            float (&cg)[L::NG], float (&gcol)[L::JP]) {
+  constexpr int NG = L::NG, JP = L::JP, WM = 4 * NG;
+  float acol[JP];
+#pragma unroll
+  for (int p = 0; p < JP; ++p) {
+    const int j = col + 16 * p;
+    float pa = 0.f, pg = 0.f;
 #pragma unroll
     for (int gi = 0; gi < NG; ++gi) {
-      sc[4 * gi + row] = av[gi];
-      sc[WM + 4 * gi + row] = bv[gi];
-      sc[2 * WM + 4 * gi + row] = r.bs[gi];
+      const int s = 4 * gi + row;
+      // selected, never multiplied away: entries past row n-1 or on and
+      // above the diagonal are stale ring contents (slots >= n have a_s = b_s = 0)
+      const float t = (s < n && j < s) ? r.tv[gi][p] : (j == s ? 1.f : 0.f);
+      pa += t * av[gi];
+      pg += t * bv[gi];
+    }
+    acol[p] = cross_row_sum(pa);
+    gcol[p] = cross_row_sum(pg);
+  }
+  // column j -> slot j = 4 gi + row: sc[(j % 4) NG + j / 4], so a lane reads its NG values contiguously
+  if (row == 0) {
+#pragma unroll
+    for (int p = 0; p < JP; ++p) {
+      const int j = col + 16 * p;
+      if (j < WM) {
+        sc[(j & 3) * NG + (j >> 2)] = acol[p];
+        sc[WM + (j & 3) * NG + (j >> 2)] = gcol[p];
+      }
     }
   }
-  const size_t NI = (size_t)a.B * a.H;
-  float bcol[WM];  // b_{s, lane} for lane < s < n
-#pragma unroll
-  for (int s = 0; s < WM; ++s) bcol[s] = (lane < s && s < n) ? a.rb[((size_t)s * NI + item) * a.W + lane] : 0.f;
   wave_lds_sync();
-  float al = 0.f, gl = 0.f, bl = 0.f;
-  if (lane < n) {
-    al = sc[lane];
-    gl = sc[WM + lane];
-    bl = sc[2 * WM + lane];
-  }
-#pragma unroll
-  for (int s = WM - 1; s >= 1; --s) {
-    if (s < n) {
-      const float w = lane_bcast(bl, s) * bcol[s];
-      al -= w * lane_bcast(al, s);
-      gl -= w * lane_bcast(gl, s);
-    }
-  }
-  const float cal = al * bl, cgl = gl * bl;
+  Vec<NG> va, vg;
+  va.load(sc + row * NG);
+  vg.load(sc + WM + row * NG);
 #pragma unroll
   for (int gi = 0; gi < NG; ++gi) {
-    ca[gi] = __shfl(cal, 4 * gi + row);
-    cg[gi] = __shfl(cgl, 4 * gi + row);
+    ca[gi] = va.e[gi] * r.bs[gi];
+    cg[gi] = vg.e[gi] * r.bs[gi];
   }
 }
 
@@ -272,37 +272,39 @@ __device__ __forceinline__ void buffer_term(const L& r, const float (&ca)[L::NG]
 
 // Per-slot coefficients of the buffer term for any kind (see erase_coefs).
 template <class L>
-__device__ __forceinline__ void buffer_coefs(const DecodeArgs& a, size_t item, int lane, int row, int col,
-                                             const L& r, const float (&av)[L::NG], const float (&bv)[L::NG],
-                                             float* sc, float (&ca)[L::NG], float (&cg)[L::NG]) {
+__device__ __forceinline__ void buffer_coefs(int n, int row, int col, const L& r, const float (&av)[L::NG],
+                                             const float (&bv)[L::NG], float* sc, float (&ca)[L::NG],
+                                             float (&cg)[L::NG], float (&gcol)[L::JP]) {
   if constexpr (L::ERASE) {
-    erase_coefs<L>(a, item, lane, row, col, r, av, bv, sc, ca, cg);
+    erase_coefs<L>(n, row, col, r, av, bv, sc, ca, cg, gcol);
   } else {
 #pragma unroll
     for (int gi = 0; gi < L::NG; ++gi) {
       ca[gi] = av[gi] * r.bs[gi];
       cg[gi] = 0.f;
     }
+#pragma unroll
+    for (int p = 0; p < L::JP; ++p) gcol[p] = 0.f;
   }
 }
 
-// Store the coupling row b_{t,.} of the token at ring slot n (GDN/KDA) for
-// later reads and the flush.  Mamba-2 derives nothing.
+// Row n of T^{-1} for the token at ring slot n (GDN/KDA), stored for later
+// reads and the flush: (T^{-1})_{n,j} = -beta_n gamma_j, j < n, because row n
+// of T T^{-1} = I reads (T^{-1})_{n,.} = -beta_n b_{n,.} T^{-1}.  Mamba-2
+// derives nothing.
 template <class L>
-__device__ __forceinline__ void append_derived(const DecodeArgs& a, size_t item, int row, int col, int lane,
-                                               const float (&bv)[L::NG], float* b_l) {
-  constexpr int NG = L::NG;
+__device__ __forceinline__ void append_derived(const DecodeArgs& a, size_t item, int row, int col,
+                                               const L& r, const float (&gcol)[L::JP]) {
   if constexpr (L::ERASE) {
-    const int n = a.n, W = a.W;
-    const size_t sl = (size_t)n * a.B * a.H + item;
-    // b_{t,s}, s < n: gather through LDS, then one contiguous store of the row
-    if (col == 0) {
+    const int n = a.n;
+    if (row == 0) {
+      float* dst = a.rt + ((size_t)n * a.B * a.H + item) * a.W;
 #pragma unroll
-      for (int gi = 0; gi < NG; ++gi)
-        if (4 * gi < n) b_l[4 * gi + row] = bv[gi];
+      for (int p = 0; p < L::JP; ++p) {
+        const int j = col + 16 * p;
+        if (j < n) dst[j] = -r.beta_t * gcol[p];
+      }
     }
-    wave_lds_sync();
-    if (lane < n) a.rb[sl * W + lane] = b_l[lane];
   }
 }
 
@@ -317,7 +319,7 @@ __global__ __launch_bounds__(256) void decode_kernel(const DecodeArgs a) {
   constexpr int NP = R / PW;                     // sketch panels
   constexpr int CP = K + 4;                      // padded LDS row pitch of C
   constexpr int KQ = K / 4;                      // channels each row covers in C x
-  constexpr int WS = 2 * K + R + V + 4 * WMAX;   // per-wave LDS: x_q, x_k, c, o_buf, b row, erase solve
+  constexpr int WS = 2 * K + R + V + 2 * WMAX;   // per-wave LDS: x_q, x_k, c, o_buf, alpha/gamma transposition
   constexpr bool U_PRELOAD = R <= 32;
   constexpr int UP = U_PRELOAD ? NP : 1;
 
@@ -399,8 +401,8 @@ __global__ __launch_bounds__(256) void decode_kernel(const DecodeArgs a) {
 
   float av[NG], bv[NG], at;
   slot_dots(r, n, row, qv, kv, gt, av, bv, at);
-  float ca[NG], cg[NG];
-  buffer_coefs<L>(a, item, lane, row, col, r, av, bv, b_l + WMAX, ca, cg);
+  float ca[NG], cg[NG], gcol[L::JP];
+  buffer_coefs<L>(n, row, col, r, av, bv, b_l, ca, cg, gcol);
   float ut[VR], ob[VR];
   buffer_term(r, ca, cg, at, ut, ob);
 
@@ -544,7 +546,7 @@ __global__ __launch_bounds__(256) void decode_kernel(const DecodeArgs a) {
   }
 
   // ---- derived fields of the token at ring slot n
-  append_derived<L>(a, item, row, col, lane, bv, b_l);
+  append_derived<L>(a, item, row, col, r, gcol);
   if constexpr (ERASE) {
     if (row == 0) {
       const size_t sl = (size_t)n * a.B * H + item;
@@ -561,7 +563,7 @@ __global__ __launch_bounds__(256) void full_read_kernel(const DecodeArgs a) {
   constexpr bool ERASE = L::ERASE, CHAN = L::CHAN;
   constexpr int KPL = L::KPL, VR = L::VR, NG = L::NG, GD = L::GD;
   constexpr int VPL = V / 64;
-  constexpr int WS = 2 * V + 4 * WMAX;  // per-wave LDS: o^state, o_buf, b row, erase solve
+  constexpr int WS = 2 * V + 2 * WMAX;  // per-wave LDS: o^state, o_buf, alpha/gamma transposition
 
   __shared__ __align__(16) float wscr[4 * WS];
 
@@ -611,8 +613,8 @@ __global__ __launch_bounds__(256) void full_read_kernel(const DecodeArgs a) {
 
   float av[NG], bv[NG], at;
   slot_dots(r, n, row, qv, kv, gt, av, bv, at);
-  float ca[NG], cg[NG];
-  buffer_coefs<L>(a, item, lane, row, col, r, av, bv, b_l + WMAX, ca, cg);
+  float ca[NG], cg[NG], gcol[L::JP];
+  buffer_coefs<L>(n, row, col, r, av, bv, b_l, ca, cg, gcol);
   float ut[VR], ob[VR];
   buffer_term(r, ca, cg, at, ut, ob);
 
@@ -660,7 +662,7 @@ __global__ __launch_bounds__(256) void full_read_kernel(const DecodeArgs a) {
 #pragma unroll
   for (int vv = 0; vv < VPL; ++vv) ob_g[lane + 64 * vv] = os_l[lane + 64 * vv] + ob_l[lane + 64 * vv];
 
-  append_derived<L>(a, item, row, col, lane, bv, b_l);
+  append_derived<L>(a, item, row, col, r, gcol);
   if constexpr (ERASE) {
     if (row == 0) {
       Vec<KPL> t;

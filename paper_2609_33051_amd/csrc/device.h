@@ -164,7 +164,6 @@ __device__ __forceinline__ float row_sum16(float x) {
   return x;
 }
 
-// Sum over the 4 rows (lanes l, l^16, l^32, l^48); every lane receives it.
 // Sum over a quad of lanes (lane & ~3 .. lane | 3).
 __device__ __forceinline__ float quad_sum(float x) {
   x += dpp<0xB1>(x);  // quad_perm [1,0,3,2]
@@ -172,10 +171,33 @@ __device__ __forceinline__ float quad_sum(float x) {
   return x;
 }
 
-__device__ __forceinline__ float cross_row_sum(float x) {
-  x += __shfl_xor(x, 16);
-  x += __shfl_xor(x, 32);
-  return x;
+// The row exchanges are gfx950's permlane swaps: swapping a register with a
+// copy of itself leaves the partner row's value in one of the two results,
+// so a pair sum is one swap and one add (no LDS round trip).
+__device__ __forceinline__ float pair_rows_sum(float x) {  // rows (0,1) and (2,3)
+  const auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
+__device__ __forceinline__ float half_waves_sum(float x) {  // lanes l and l ^ 32
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
+
+// Sum over the 4 rows (lanes l, l^16, l^32, l^48); every lane receives it.
+__device__ __forceinline__ float cross_row_sum(float x) { return half_waves_sum(pair_rows_sum(x)); }
+
+// Inclusive scan over the 4 rows (row r receives x_0 + ... + x_r of its
+// column) and the total of all four rows.
+__device__ __forceinline__ float rows_scan(float x, int row, float& total) {
+  const auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  // r[0] holds the even row of the pair, r[1] the odd one, in both rows of the pair
+  const float ev = __uint_as_float(r[0]), od = __uint_as_float(r[1]);
+  const float pair = ev + od;
+  const float in_pair = (row & 1) ? pair : ev;
+  const auto h = __builtin_amdgcn_permlane32_swap(__float_as_uint(pair), __float_as_uint(pair), false, false);
+  const float lo = __uint_as_float(h[0]), hi = __uint_as_float(h[1]);  // pair totals of rows 0-1 and 2-3
+  total = lo + hi;
+  return in_pair + (row >= 2 ? lo : 0.f);
 }
 
 __device__ __forceinline__ float wave_sum(float x) { return cross_row_sum(row_sum16(x)); }

@@ -5,6 +5,9 @@
 // cumulative log decays g_s and c_s = exp(g_n - g_s):
 //   L[s]   = exp(g_n - g_s) . k_s                  (left factors l_s(W), Appendix C.1)
 //   pi_s   = beta_s (e^{g_s} . k_s - sum_{j<s} b_{s,j} pi_j)           (eq. wy)
+//          = sum_{j<=s} (T^{-1})_{s,j} beta_j e^{g_j} . k_j,  T = I + Diag(beta) B
+//            (rows s < n of T^{-1} come from the ring; row n's couplings
+//            b_{n,j} are formed here)
 //   w_s    = u_s - X_0 pi_s                         (true write vectors; Mamba-2: beta_s v_s)
 //   X_W    = X_0 Diag(e^{g_n}) + sum_s w_s L[s]^T   (eq. update in rank-(n+1) form)
 //   o_W    = X_W q_W,   U = X_W Omega
@@ -273,7 +276,7 @@ __global__ __launch_bounds__(256, 3) void update_kernel(const UpdateArgs a) {
   __shared__ __align__(16) float Ls[SP * LP];                 // keys k_s (KDA: then L[s]), [s][k]
   __shared__ __align__(16) float PiT[ERASE ? K * PP : 4];     // Pi^T[k][s]
   __shared__ __align__(16) float Us[SP * UP];                 // c_s beta_s v_s (Mamba-2) or u_s
-  __shared__ float Bs[ERASE ? SP * SP : 1];                   // b_{s,j}
+  __shared__ float Bs[ERASE ? SP * SP : 1];                   // (T^{-1})_{s,j}, j < s < n
   __shared__ float bpart[ERASE ? KW * SP : 1];                // partial sums of b_{n,j}
   __shared__ __align__(16) float qs[K];
   __shared__ __align__(16) float ds[CHAN ? K : 4];            // e^{g_n} per channel (KDA)
@@ -322,7 +325,7 @@ __global__ __launch_bounds__(256, 3) void update_kernel(const UpdateArgs a) {
         for (int e = 0; e < 5; ++e) gpart[jt][i][e] = 0.f;
   }
 
-  // ---- every small load first (window, query, couplings, Omega), then the
+  // ---- every small load first (window, query, rows of T^{-1}, Omega), then the
   // state: the staged values reach LDS while the state read is still in flight
   float egn = 1.f, gn = 0.f, bn = 0.f;  // e^{g_n} (scalar decay), g_n, beta_n
   float bsv[SP], gsv[SP];               // beta_s and (scalar decay) g_s, wave-uniform
@@ -384,7 +387,7 @@ __global__ __launch_bounds__(256, 3) void update_kernel(const UpdateArgs a) {
       for (int c = 0; c < BQ; ++c) {
         const int idx = tid + 256 * c;
         const int s = idx / SP, j = idx % SP;
-        bv[c] = (idx < SP * SP && s < n && j < s) ? a.rb[((size_t)s * NI + item) * W + j] : 0.f;
+        bv[c] = (idx < SP * SP && s < n && j < s) ? a.rt[((size_t)s * NI + item) * W + j] : 0.f;
       }
     }
   }
@@ -491,7 +494,7 @@ __global__ __launch_bounds__(256, 3) void update_kernel(const UpdateArgs a) {
   if (flush) {
     if constexpr (ERASE) {
       // ---- channel work: thread tid owns channel k = tid.  Ls holds raw keys.
-      // The pseudo-values of slots before n need only the stored couplings,
+      // The pseudo-values of slots before n need only the stored rows of T^{-1},
       // so the waves that own no channel form them meanwhile.
       static_assert(K + V <= 256, "channel waves and value waves must be disjoint");
       float pi[SP], kn = 0.f;
@@ -511,15 +514,19 @@ __global__ __launch_bounds__(256, 3) void update_kernel(const UpdateArgs a) {
           for (int s = 0; s < SP; ++s)
             if (s == n) gnk = gk[s];
         }
-        // erase factors pi_s, s < n, by forward substitution over the stored couplings
+        // erase factors pi_s = sum_{j<=s} (T^{-1})_{s,j} beta_j e^{g_j} k_j, s < n
+        // (eq. wy with T^{-1} from the ring): independent sums, no recursion
+        float xk[SP];
+#pragma unroll
+        for (int s = 0; s < SP; ++s) xk[s] = s < n ? bsv[s] * fast_exp(CHAN ? gk[s] : gsv[s]) * Ls[s * LP + kk] : 0.f;
 #pragma unroll
         for (int s = 0; s < SP; ++s) {
           pi[s] = 0.f;
           if (s < n) {
-            float acc = fast_exp(CHAN ? gk[s] : gsv[s]) * Ls[s * LP + kk];
+            float acc = xk[s];
 #pragma unroll
-            for (int j = 0; j < s; ++j) acc -= Bs[s * SP + j] * pi[j];
-            pi[s] = bsv[s] * acc;
+            for (int j = 0; j < s; ++j) acc += Bs[s * SP + j] * xk[j];
+            pi[s] = acc;
           }
         }
         // b_{n,s} = <exp(g_n - g_s) . k_s, k_n>: partial sums over this wave's channels
@@ -539,19 +546,19 @@ __global__ __launch_bounds__(256, 3) void update_kernel(const UpdateArgs a) {
             if (s < n) Ls[s * LP + kk] *= fast_exp(gnk - gk[s]);
         }
       } else if (tid >= 256 - V) {
-        // pseudo-values u_s = beta_s (v_s - sum_{j<s} b_{s,j} u_j), s < n, in
+        // pseudo-values u_s = sum_{j<=s} (T^{-1})_{s,j} beta_j v_j, s < n, in
         // place over the raw values (thread owns value channel v)
         const int v = tid - (256 - V);
-        float uv[SP];
+        float xv[SP];
+#pragma unroll
+        for (int s = 0; s < SP; ++s) xv[s] = s < n ? bsv[s] * Us[s * UP + v] : 0.f;
 #pragma unroll
         for (int s = 0; s < SP; ++s) {
-          uv[s] = 0.f;
           if (s < n) {
-            float acc = Us[s * UP + v];
+            float acc = xv[s];
 #pragma unroll
-            for (int j = 0; j < s; ++j) acc -= Bs[s * SP + j] * uv[j];
-            uv[s] = bsv[s] * acc;
-            Us[s * UP + v] = uv[s];
+            for (int j = 0; j < s; ++j) acc += Bs[s * SP + j] * xv[j];
+            Us[s * UP + v] = acc;
           }
         }
       }

@@ -14,7 +14,7 @@ into libsketchssm.so.  Buffers (caller-owned, as the ABI requires):
   ring   replay buffer of W slots per item:
          raw inputs k, v (io dtype), beta, log_decay ([..][K] for KDA), item-major
          [B][H][W][...], written into slot n by the token's producer (write_token);
-         derived fields, slot-major [W][B][H][...]: g (KDA), u, bcoef (GDN/KDA),
+         derived fields, slot-major [W][B][H][...]: rows of T^{-1} (GDN/KDA),
          f (sketch read) or pi (baseline).
 """
 from __future__ import annotations
@@ -58,11 +58,11 @@ class SketchSSMLayer:
         self.rbeta = torch.zeros((Bt, H, W), dtype=f32, device=dev)
         self.rla = torch.zeros((Bt, H, W, K) if kind == "kda" else (Bt, H, W), dtype=f32, device=dev)
         # derived fields, written by the library
-        self.rb = torch.zeros((W, Bt, H, W), dtype=f32, device=dev) if erase else None
+        self.rt = torch.zeros((W, Bt, H, W), dtype=f32, device=dev) if erase else None
         self.rf = torch.zeros((W, Bt, H, rank), dtype=f32, device=dev) if (erase and not baseline) else None
         self.rpi = torch.zeros((W, Bt, H, K), dtype=f32, device=dev) if (erase and baseline) else None
         self.ring = B.make_ring(k=self.rk, v=self.rv, beta=self.rbeta, log_decay=self.rla, f=self.rf,
-                                pi=self.rpi, bcoef=self.rb)
+                                pi=self.rpi, tinv=self.rt)
         self.o = torch.zeros((Bt, H, V), dtype=f32, device=dev)
         self.n = 0  # slot of the next token in the current window
 

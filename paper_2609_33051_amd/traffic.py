@@ -81,16 +81,17 @@ def slot_read_bytes(s: Shape, baseline: bool = False) -> int:
     Every kind: raw key and value, beta, log decay (K fp32 for KDA).
     GDN/KDA also: the projected erase vector f (r fp32, sketch read) or the
     erase factor pi (K fp32, exact baseline).  (The pseudo-values are solved
-    from the raw values and the couplings, not stored.)"""
+    from the raw values and the stored rows of T^{-1}, not stored.)"""
     raw = s.io_bytes * (s.dk + s.dv) + 4 + s.decay_bytes
     if not s.erase:
         return raw
     return raw + (4 * s.dk if baseline else 4 * s.rank)
 
 
-def coupling_read_bytes(s: Shape, n: int) -> int:
-    """GDN/KDA: the stored coupling rows b_{s,.} of the n earlier slots
-    (slot s holds s of them), read to solve for the buffer coefficients."""
+def tinv_read_bytes(s: Shape, n: int) -> int:
+    """GDN/KDA: the stored rows of T^{-1} (T = I + Diag(beta) B, B the
+    couplings of eq. wy) of the n earlier slots (slot s holds s entries),
+    which turn the buffer term into sums over the raw values."""
     return 2 * n * (n - 1) if s.erase else 0
 
 
@@ -100,8 +101,8 @@ def current_read_bytes(s: Shape) -> int:
 
 
 def derived_write_bytes(s: Shape, n: int, baseline: bool = False) -> int:
-    """Fields a read derives and stores for slot n: GDN/KDA f (or pi) and the
-    coupling row b_{n,.}.  Mamba-2: none."""
+    """Fields a read derives and stores for slot n: GDN/KDA f (or pi) and row
+    n of T^{-1} (n entries).  Mamba-2: none."""
     if not s.erase:
         return 0
     extra = 4 * s.dk if baseline else 4 * s.rank
@@ -111,25 +112,25 @@ def derived_write_bytes(s: Shape, n: int, baseline: bool = False) -> int:
 def decode_bytes(s: Shape, n: int) -> int:
     """Sketch read at slot n: the query, n earlier slots, the current slot, the
     derived fields, U, the state-dependent map's factors (if any) and o."""
-    return (s.io_bytes * s.dk + n * slot_read_bytes(s) + current_read_bytes(s) + coupling_read_bytes(s, n)
+    return (s.io_bytes * s.dk + n * slot_read_bytes(s) + current_read_bytes(s) + tinv_read_bytes(s, n)
             + derived_write_bytes(s, n) + s.sketch_bytes * s.dv * s.rank + s.cmap_bytes + 4 * s.dv)
 
 
 def full_read_bytes(s: Shape, n: int) -> int:
     """Exact full-state read at slot n: as decode with S (4KV) in place of U."""
-    return (s.io_bytes * s.dk + n * slot_read_bytes(s, True) + current_read_bytes(s) + coupling_read_bytes(s, n)
+    return (s.io_bytes * s.dk + n * slot_read_bytes(s, True) + current_read_bytes(s) + tinv_read_bytes(s, n)
             + derived_write_bytes(s, n, True) + 4 * s.dk * s.dv + 4 * s.dv)
 
 
 def flush_bytes(s: Shape, n_buffered: int, rank: int | None = None) -> int:
     """Flush of the token in slot n_buffered: S read + write, the earlier
-    slots (raw k, v, beta, log decay) and their coupling rows, the current
+    slots (raw k, v, beta, log decay) and their rows of T^{-1}, the current
     slot, the query, the sketch write (rank columns), the state-dependent
     map's factors (if any) and o."""
     r = s.rank if rank is None else rank
     slot = s.io_bytes * (s.dk + s.dv) + 4 + s.decay_bytes
-    bcoef = 4 * n_buffered * (n_buffered - 1) // 2 if s.erase else 0
-    return (8 * s.dk * s.dv + n_buffered * slot + bcoef + current_read_bytes(s) + s.io_bytes * s.dk
+    tinv = 4 * n_buffered * (n_buffered - 1) // 2 if s.erase else 0
+    return (8 * s.dk * s.dv + n_buffered * slot + tinv + current_read_bytes(s) + s.io_bytes * s.dk
             + s.sketch_bytes * s.dv * r + (s.cmap_bytes if r else 0) + 4 * s.dv)
 
 

@@ -72,7 +72,7 @@ def cfg(**kw):
 
 
 def good_ring(**kw):
-    d = dict(k=ADDR, v=ADDR, beta=ADDR, log_decay=ADDR, f=ADDR, pi=ADDR, bcoef=ADDR)
+    d = dict(k=ADDR, v=ADDR, beta=ADDR, log_decay=ADDR, f=ADDR, pi=ADDR, tinv=ADDR)
     d.update(kw)
     return B.make_ring(**d)
 
@@ -101,7 +101,7 @@ class TestValidation:
         assert status(d, cfg(), ADDR, ADDR, good_ring(), 0, ADDR + 8, ADDR) == -3
         assert status(d, cfg(), ADDR, ADDR, good_ring(v=None), 0, ADDR, ADDR) == -1
         assert status(d, cfg(), ADDR, ADDR, good_ring(log_decay=ADDR + 4), 0, ADDR, ADDR) == -3
-        assert status(d, cfg(kind="kda", dv=128), ADDR, ADDR, good_ring(bcoef=None), 0, ADDR, ADDR) == -1
+        assert status(d, cfg(kind="kda", dv=128), ADDR, ADDR, good_ring(tinv=None), 0, ADDR, ADDR) == -1
         assert status(d, cfg(), ADDR, ADDR, good_ring(), 0, None, ADDR) == -1
         assert status(d, cfg(kind="gdn", dv=128), ADDR, ADDR, good_ring(f=None), 0, ADDR, ADDR) == -1
         assert status(d, cfg(), None, ADDR, good_ring(), 0, ADDR, ADDR) == -1
@@ -126,7 +126,7 @@ class TestValidation:
         assert status(u, cfg(rank=0), ADDR, None, None, 0, None, None, None) == -1   # sketch-only needs rank
         assert status(u, cfg(), None, ADDR, good_ring(), 15, ADDR, ADDR, ADDR) == -1
         assert status(u, cfg(), ADDR, None, good_ring(), 15, ADDR, ADDR, ADDR) == -1
-        assert status(u, cfg(kind="kda", dv=128), ADDR, ADDR, good_ring(bcoef=None), 15, ADDR, ADDR, ADDR) == -1
+        assert status(u, cfg(kind="kda", dv=128), ADDR, ADDR, good_ring(tinv=None), 15, ADDR, ADDR, ADDR) == -1
         assert status(u, cfg(), ADDR, ADDR, None, 15, ADDR, ADDR, ADDR) == -1  # ring needed when n > 0
         assert status(u, cfg(), ADDR, ADDR, good_ring(), 15, ADDR, ADDR, ADDR + 2) == -3
         assert status(u, cfg(sketch=-1), ADDR, ADDR, good_ring(), 15, ADDR, ADDR, ADDR) == -1

@@ -47,5 +47,5 @@ def test_algorithmic_bytes_gdn_decode():
     # slot 0: q 256, current k, v 512 + beta 4 + log decay 4, derived f 64, U 8 KiB, o 512
     assert traffic.decode_bytes(s, 0) == 256 + 520 + 64 + 8192 + 512
     # each earlier slot adds raw k, v 512 + beta 4 + log decay 4 + f 64 = 584; from 2 to 3 earlier
-    # slots the coupling reads grow from 1 + 0 to 2 + 1 + 0 values (8 B) and the stored row by 4 B
+    # slots the T^{-1} row reads grow from 1 + 0 to 2 + 1 + 0 values (8 B) and the stored row by 4 B
     assert traffic.decode_bytes(s, 3) - traffic.decode_bytes(s, 2) == 584 + 8 + 4

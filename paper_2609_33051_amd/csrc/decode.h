@@ -82,13 +82,13 @@ struct RowLoads {
     }
     const uint32_t koff = (uint32_t)(col * KPL), voff = (uint32_t)(col * VR);
     const size_t cur = item * W + n;                 // slot n of this item (raw fields)
-    q_raw.load(static_cast<const IO*>(a.q) + item * K + koff);
-    k_raw.load(static_cast<const IO*>(a.rk) + cur * K + koff);
-    v_raw.load(static_cast<const IO*>(a.rv) + cur * V + voff);
+    q_raw.load_nt(static_cast<const IO*>(a.q) + item * K + koff);
+    k_raw.load_nt(static_cast<const IO*>(a.rk) + cur * K + koff);
+    v_raw.load_nt(static_cast<const IO*>(a.rv) + cur * V + voff);
     beta_t = a.rbeta[cur];
     if constexpr (CHAN) {
       Vec<KPL> t;
-      t.load(a.rla + cur * K + koff);
+      t.load_nt(a.rla + cur * K + koff);
 #pragma unroll
       for (int m = 0; m < KPL; ++m) la[m] = t.e[m];
     } else {
@@ -107,13 +107,13 @@ struct RowLoads {
 #pragma unroll
       for (int m = 0; m < GD; ++m) gs[gi][m] = 0.f;
       if (4 * gi < n && s < n) {
-        ks[gi].load(static_cast<const IO*>(a.rk) + si * K + koff);
-        vs[gi].load(static_cast<const IO*>(a.rv) + si * V + voff);
+        ks[gi].load_nt(static_cast<const IO*>(a.rk) + si * K + koff);
+        vs[gi].load_nt(static_cast<const IO*>(a.rv) + si * V + voff);
         bs[gi] = a.rbeta[si];
         // log alpha_s for now; made cumulative in prefix_decay()
         if constexpr (CHAN) {
           Vec<KPL> t;
-          t.load(a.rla + si * K + koff);
+          t.load_nt(a.rla + si * K + koff);
 #pragma unroll
           for (int m = 0; m < KPL; ++m) gs[gi][m] = t.e[m];
         } else {
@@ -369,7 +369,7 @@ __global__ __launch_bounds__(256) void decode_kernel(const DecodeArgs a) {
       for (int p = 0; p < NP; ++p)
 #pragma unroll
         for (int vv = 0; vv < VPL; ++vv)
-          Ur[vv][p].load(Ub + (uint32_t)((p * V + lane + 64 * vv) * PW));
+          Ur[vv][p].load_nt(Ub + (uint32_t)((p * V + lane + 64 * vv) * PW));
     }
   }
 
@@ -450,7 +450,7 @@ __global__ __launch_bounds__(256) void decode_kernel(const DecodeArgs a) {
     constexpr int CW = K / 16;                      // channels per lane of M x
     const int pa = col >> 2, ch = ((col & 3) + 4 * row) * CW;
     Vec<CW> mr;
-    mr.load(cm + pa * K + ch);
+    mr.load_nt(cm + pa * K + ch);
     float mq = 0.f, mk = 0.f;
 #pragma unroll
     for (int m = 0; m < CW; ++m) {
@@ -484,7 +484,7 @@ __global__ __launch_bounds__(256) void decode_kernel(const DecodeArgs a) {
       float cq = 0.f, ck = 0.f;
       if (j < R) {
         Vec<HQ> f2;
-        f2.load(cm + P * K + R * P + j * R + row * HQ);
+        f2.load_nt(cm + P * K + R * P + j * R + row * HQ);
 #pragma unroll
         for (int m = 0; m < HQ; ++m) {
           cq += f2.e[m] * xq_l[row * HQ + m];
@@ -535,7 +535,7 @@ __global__ __launch_bounds__(256) void decode_kernel(const DecodeArgs a) {
     for (int p = 0; p < NP; ++p) {
       Raw<SK, PW> u;
       if constexpr (U_PRELOAD) u = Ur[vv][p];
-      else u.load(Ub + (uint32_t)((p * V + lane + 64 * vv) * PW));
+      else u.load_nt(Ub + (uint32_t)((p * V + lane + 64 * vv) * PW));
 #pragma unroll
       for (int i = 0; i < PW; i += 4) {
         const float4 c4 = *reinterpret_cast<const float4*>(c_l + PW * p + i);

@@ -22,6 +22,8 @@ Reported (one JSON line):
                  bytes per launch / mean launch time from HIP events recorded
                  on the launch stream, against the 8 TB/s HBM peak
   kernels        the same for the flush and the window-averaged figures
+  ragged         a per-head rank table over the same storage width (seeded,
+                 with dense-fallback heads read exactly beside the sketch read)
   full_read      the exact full-state-read (ReplaySSM-style) baseline path
   cpu_baseline   the CPU oracle timed on a bounded sample of the same
                  workload on the host cores, scaled to steps/s per layer
@@ -53,6 +55,8 @@ def parse():
     p.add_argument("--no-paper-storage", action="store_true",
                    help="skip the extra timed passes with the paper's storage and method beside the headline")
     p.add_argument("--no-full-read", action="store_true", help="skip the exact baseline path")
+    p.add_argument("--no-ragged", action="store_true",
+                   help="skip the pass with a per-head rank table (seeded, with dense-fallback heads)")
     p.add_argument("--no-standard", action="store_true",
                    help="skip the Standard recurrence (window 1, no sketch: S read and written every token)")
     p.add_argument("--no-cpu-baseline", action="store_true")
@@ -95,12 +99,13 @@ def main():
     om_t, C_t = torch.as_tensor(om), torch.as_tensor(C)
     pool = [inputs.step_inputs(wl, t, dev) for t in range(W)]  # one window of resident inputs, reused
 
-    def make_layers(baseline, sketch, pivots):
+    def make_layers(baseline, sketch, pivots, head_ranks=None):
         layers = []
         for li in range(L):
             S = inputs.initial_state(wl, dev, seed=inputs.SEED + li)
             lay = SketchSSMLayer(wl.kind, wl.batch, wl.heads, wl.dk, wl.dv, rank, W, wl.io, dev,
-                                 baseline=baseline, S=S, omega=om_t, coef=C_t, sketch=sketch, pivots=pivots)
+                                 baseline=baseline, S=S, omega=om_t, coef=C_t, sketch=sketch, pivots=pivots,
+                                 head_ranks=head_ranks)
             lay.init_sketch()
             for slot in range(W):  # the producer's writes: one window of tokens, resident in the ring
                 lay.write_token(pool[slot], slot)
@@ -125,8 +130,8 @@ def main():
         for lay in layers:
             lay.n = n_tokens % W
 
-    def timed(baseline, sketch=args.sketch, pivots=args.pivots):
-        layers = make_layers(baseline, sketch, pivots)
+    def timed(baseline, sketch=args.sketch, pivots=args.pivots, head_ranks=None):
+        layers = make_layers(baseline, sketch, pivots, head_ranks)
         stream = torch.cuda.current_stream()
         events = [(t % W, torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
                   for t in range(K_steps)]
@@ -227,6 +232,31 @@ def main():
                 "decode_traffic": tr and tr["bytes_per_launch"],
                 "flush_mean_us": round(kp["fl_mean"] * 1e6, 2), "window_avg_steps_per_s": round(W / kp["window"], 1),
             }
+
+    # ---- a per-head rank table (Sec. 4.2) over the same storage width: a
+    # seeded synthetic allocation with dense-fallback heads, whose non-flush
+    # reads are exact full-state reads issued beside the sketch read
+    if not args.no_ragged and rank in (8, 16, 32) and wl.heads <= 256:
+        ranks = inputs.ragged_ranks(wl)
+        e_r, per_r = timed(False, args.sketch, args.pivots, head_ranks=ranks)
+        rd_n = [n for n in per_r if n < W - 1]
+        rd_time = sum(sum(per_r[n]) for n in rd_n)
+        rd_launch = rd_time / sum(len(per_r[n]) for n in rd_n)
+        rd_bytes = sum(traffic.ragged_decode_bytes(shape, n, ranks) * wl.batch * len(per_r[n]) for n in rd_n)
+        rf = per_r.get(W - 1, [])
+        rf_mean = sum(rf) / len(rf)
+        win_r = sum(sum(v) / len(v) for v in per_r.values())
+        out["ragged"] = {
+            "head_ranks": ranks, "dense_heads": sum(1 for g in ranks if g == 0),
+            "mean_rank": round(sum(ranks) / len(ranks), 3), "value": round(layer_steps / e_r, 2), "unit": "steps/s",
+            "read_mean_us": round(rd_launch * 1e6, 2),
+            "read_bytes_per_step": int(rd_bytes / sum(len(per_r[n]) for n in rd_n)),
+            "read_gbps": round(rd_bytes / rd_time / 1e9, 1),
+            "read_frac": round(rd_bytes / rd_time / 1e9 / traffic.HBM_PEAK_GBPS, 4),
+            "flush_mean_us": round(rf_mean * 1e6, 2),
+            "flush_gbps": round(traffic.ragged_flush_bytes(shape, W - 1, ranks) * wl.batch / rf_mean / 1e9, 1),
+            "window_avg_steps_per_s": round(W / win_r, 1),
+        }
 
     # ---- the exact full-state-read baseline (same inputs; flush with rank 0)
     if not args.no_full_read:

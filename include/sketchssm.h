@@ -84,6 +84,21 @@ typedef struct {
                        4: state-dependent map with P = 4 pivots, rebuilt from the
                        state by every sketchssm_update into `cmap` (rank 8..32)   */
   float ridge;      /* lambda of the state-dependent map (the paper uses 0.1)     */
+  const int32_t* head_rank; /* per-head rank table (host memory, read during the call),
+                       or NULL: every head has rank `rank`.  With a table (the
+                       allocation of Sec. 4.2 and the allocation appendix), entry h
+                       is head h's rank G_h in 0..rank, and `rank` (8, 16 or 32) is
+                       the storage width: U, omega, coef, f and cmap keep the layouts
+                       of width `rank`, a head uses its first G_h columns (U panels
+                       up to the next whole panel; the tail of a partly used panel
+                       is written as zeros), and the unused panels, f entries and map
+                       rows are neither read nor written.  G_h = 0 is a dense-fallback
+                       head: it keeps the full state; sketchssm_decode reads its state
+                       exactly (as sketchssm_full_read_baseline does, in the same
+                       launch) and its flush writes no sketch.  heads <= 256;
+                       omega's columns past G_h are ignored.
+                       sketchssm_full_read_baseline reads every head exactly and
+                       ignores the table (after validating it).                  */
 } skssm_config;
 
 /* Replay buffer ("ring"): W slots per (b, h) item.  Slot s holds the s-th
@@ -169,20 +184,25 @@ int sketchssm_update(const skssm_config* cfg, float* S, const float* omega, cons
 
 /*
  * sketchssm_decode -- non-flush step (Algorithm 1, t < W) for the token in
- * ring slot n_buffered (0..W-2):
+ * ring slot n_buffered (0..W-2), every head of the layer:
  *     o = U c_t + o_t^buffer,
  *     c_t = C (e^{g_t} . q_t) - sum_{s<=t} a_{t,s} f_s        (eq. app-projected-query)
  *     o_t^buffer = sum_{s<=t} a_{t,s} u_s,  a_{t,s} = <exp(g_t - g_s) k_s, q_t>
- * (for MAMBA2 f_s = 0 and u_s = beta_s v_s, so c_t = e^{g_t} C q_t).  S is
- * never read.  U [B][H][rank/P][V][P] (cfg.sketch_dtype) and coef [H][rank][K] fp32 (C;
- * Omega^T for the offline map of Sec. 4.1 at E0 = I) are read; for GDN/KDA
- * the derived fields of slot n_buffered (f, tinv) are written.
+ * (for MAMBA2 f_s = 0 and u_s = beta_s v_s, so c_t = e^{g_t} C q_t).  The
+ * state of a sketched head is never read.  U [B][H][rank/P][V][P]
+ * (cfg.sketch_dtype) and coef [H][rank][K] fp32 (C; Omega^T for the offline
+ * map of Sec. 4.1 at E0 = I) are read; for GDN/KDA the derived fields of slot
+ * n_buffered (f, tinv) are written.
+ * S [B][H][V][K] fp32 is read only for the dense-fallback heads of a per-head
+ * rank table (cfg.head_rank entries 0), whose output is the exact read of
+ * sketchssm_full_read_baseline (their slot gets pi instead of f, so ring.pi
+ * is then required); S may be NULL when no head is dense.
  * With cfg.pivots = 4 the map is the state-dependent one that the last
  * sketchssm_update wrote to cmap, C = F1 M + F2 coef, and coef must then be
  * Omega^T.  q [B][H][K] io_dtype; o [B][H][V] fp32.  rank must be > 0,
  * window >= 2.
  */
-int sketchssm_decode(const skssm_config* cfg, const void* U, const float* coef, const float* cmap,
+int sketchssm_decode(const skssm_config* cfg, const void* U, const float* coef, const float* cmap, const float* S,
                      const skssm_ring* ring, int32_t n_buffered, const void* q, float* o, void* stream);
 
 /*

@@ -35,7 +35,7 @@ class SketchSSMError(RuntimeError):
 class Config(ctypes.Structure):
     _fields_ = [(name, ctypes.c_int32) for name in
                 ("kind", "batch", "heads", "dk", "dv", "rank", "window", "io_dtype", "sketch_dtype", "pivots")] + [
-                   ("ridge", ctypes.c_float)]
+                   ("ridge", ctypes.c_float), ("head_rank", ctypes.POINTER(ctypes.c_int32))]
 
 
 class Ring(ctypes.Structure):
@@ -59,7 +59,7 @@ def load(path: str | None = None):
     cfgp = ctypes.POINTER(Config)
     ringp = ctypes.POINTER(Ring)
     lib.sketchssm_update.argtypes = [cfgp, P, P, ringp, ctypes.c_int32, P, P, P, P, P]
-    lib.sketchssm_decode.argtypes = [cfgp, P, P, P, ringp, ctypes.c_int32, P, P, P]
+    lib.sketchssm_decode.argtypes = [cfgp, P, P, P, P, ringp, ctypes.c_int32, P, P, P]
     lib.sketchssm_full_read_baseline.argtypes = [cfgp, P, ringp, ctypes.c_int32, P, P, P]
     for f in ("sketchssm_update", "sketchssm_decode", "sketchssm_full_read_baseline", "sketchssm_check_config"):
         getattr(lib, f).restype = ctypes.c_int
@@ -85,9 +85,26 @@ def _dtype(x) -> int:
     return {"f32": F32, "bf16": BF16}[x] if isinstance(x, str) else int(x)
 
 
-def make_config(kind, batch, heads, dk, dv, rank, window, io, sketch="f32", pivots=0, ridge=0.1) -> Config:
+def make_config(kind, batch, heads, dk, dv, rank, window, io, sketch="f32", pivots=0, ridge=0.1,
+                head_ranks=None) -> Config:
+    """head_ranks: optional per-head rank table (H ints, 0 = dense fallback);
+    `rank` is then the storage width.  The table is copied into host memory
+    owned by the returned Config."""
     k = KIND_IDS[kind] if isinstance(kind, str) else int(kind)
-    return Config(k, batch, heads, dk, dv, rank, window, _dtype(io), _dtype(sketch), int(pivots), float(ridge))
+    cfg = Config(k, batch, heads, dk, dv, rank, window, _dtype(io), _dtype(sketch), int(pivots), float(ridge), None)
+    if head_ranks is not None:
+        vals = [int(x) for x in head_ranks]
+        if len(vals) != heads:
+            raise ValueError(f"head_ranks has {len(vals)} entries for {heads} heads")
+        arr = (ctypes.c_int32 * heads)(*vals)
+        cfg.head_rank = ctypes.cast(arr, ctypes.POINTER(ctypes.c_int32))
+        cfg._head_rank_storage = arr
+    return cfg
+
+
+def head_ranks(cfg: Config) -> list[int] | None:
+    """The per-head rank table of a Config, or None."""
+    return None if not cfg.head_rank else [cfg.head_rank[h] for h in range(cfg.heads)]
 
 
 def cmap_width(cfg: Config) -> int:
@@ -135,10 +152,11 @@ def prepare_update(cfg: Config, S, omega, ring: Ring | None, n_buffered: int, q,
     return Prepared(lib.sketchssm_update, args, (cfg, ring))
 
 
-def prepare_decode(cfg: Config, U, coef, ring: Ring, n_buffered: int, q, o, stream=None, cmap=None) -> Prepared:
+def prepare_decode(cfg: Config, U, coef, ring: Ring, n_buffered: int, q, o, stream=None, cmap=None,
+                   S=None) -> Prepared:
     lib = load()
-    args = (ctypes.byref(cfg), _vp(U), _vp(coef), _vp(cmap), ctypes.byref(ring), ctypes.c_int32(n_buffered), _vp(q),
-            _vp(o), _vp(stream))
+    args = (ctypes.byref(cfg), _vp(U), _vp(coef), _vp(cmap), _vp(S), ctypes.byref(ring), ctypes.c_int32(n_buffered),
+            _vp(q), _vp(o), _vp(stream))
     return Prepared(lib.sketchssm_decode, args, (cfg, ring))
 
 
@@ -154,10 +172,10 @@ def sketchssm_update(cfg: Config, S, omega, ring: Ring | None, n_buffered: int, 
                                 int(n_buffered), ptr(q), ptr(U), ptr(cmap), ptr(o), stream))
 
 
-def sketchssm_decode(cfg: Config, U, coef, ring: Ring, n_buffered: int, q, o, stream=None, cmap=None):
+def sketchssm_decode(cfg: Config, U, coef, ring: Ring, n_buffered: int, q, o, stream=None, cmap=None, S=None):
     lib = load()
-    _check(lib.sketchssm_decode(ctypes.byref(cfg), ptr(U), ptr(coef), ptr(cmap), ctypes.byref(ring) if ring else None,
-                                int(n_buffered), ptr(q), ptr(o), stream))
+    _check(lib.sketchssm_decode(ctypes.byref(cfg), ptr(U), ptr(coef), ptr(cmap), ptr(S),
+                                ctypes.byref(ring) if ring else None, int(n_buffered), ptr(q), ptr(o), stream))
 
 
 def sketchssm_full_read_baseline(cfg: Config, S, ring: Ring, n_buffered: int, q, o, stream=None):

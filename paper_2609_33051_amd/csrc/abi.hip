@@ -64,6 +64,49 @@ int check_ring(const skssm_config* c, const skssm_ring* r, bool derived_f, bool 
   return SKSSM_OK;
 }
 
+// Per-head rank table (cfg->head_rank): validated here and copied into the
+// kernel arguments.  Counts the dense-fallback and the sketched heads.
+struct Ranks {
+  int ragged = 0, dense = 0, sketched = 0;
+  uint8_t h[skssm::kMaxRaggedHeads] = {};
+  uint8_t order[skssm::kMaxRaggedHeads] = {};  // dense heads first, then the sketched ones
+};
+
+int check_ranks(const skssm_config* c, Ranks& rk) {
+  rk = Ranks{};
+  if (!c->head_rank) {
+    rk.sketched = c->heads;
+    return SKSSM_OK;
+  }
+  if (c->heads > skssm::kMaxRaggedHeads)
+    return fail(SKSSM_EUNSUPPORTED, "a per-head rank table supports at most %d heads", skssm::kMaxRaggedHeads);
+  if (c->rank != 8 && c->rank != 16 && c->rank != 32)
+    return fail(SKSSM_EUNSUPPORTED, "with a per-head rank table, rank (the storage width) must be 8, 16 or 32");
+  for (int h = 0; h < c->heads; ++h) {
+    const int32_t g = c->head_rank[h];
+    if (g < 0 || g > c->rank) return fail(SKSSM_EINVAL, "head_rank[%d] = %d outside 0..%d", h, g, c->rank);
+    rk.h[h] = (uint8_t)g;
+    if (g == 0) ++rk.dense; else ++rk.sketched;
+  }
+  int d = 0, k = rk.dense;
+  for (int h = 0; h < c->heads; ++h) rk.order[rk.h[h] == 0 ? d++ : k++] = (uint8_t)h;
+  rk.ragged = 1;
+  return SKSSM_OK;
+}
+
+// The decode launches the dense heads' workgroups first: each reads a whole
+// state and takes several times as long as a sketch read, so starting them
+// early keeps them from trailing the launch.
+void put_order(skssm::DecodeArgs& a, const Ranks& rk) {
+  a.ndense = rk.dense;
+  for (int h = 0; h < skssm::kMaxRaggedHeads; ++h) a.hlist[h] = rk.order[h];
+}
+
+template <class A> void put_ranks(A& a, const Ranks& rk) {
+  a.ragged = rk.ragged;
+  for (int h = 0; h < skssm::kMaxRaggedHeads; ++h) a.hrank[h] = rk.h[h];
+}
+
 int launched(int rc, const char* what) {
   if (rc == -2) return fail(SKSSM_EUNSUPPORTED, "%s: no kernel compiled for this shape", what);
   const hipError_t e = hipGetLastError();
@@ -114,6 +157,8 @@ int sketchssm_update(const skssm_config* cfg, float* S, const float* omega, cons
                      int32_t n_buffered, const void* q, void* U, float* cmap, float* o, void* stream) {
   int rc = check_shape(cfg, true, true);
   if (rc) return rc;
+  Ranks rk;
+  if ((rc = check_ranks(cfg, rk))) return rc;
   if (cfg->pivots) {
     if (cfg->rank < 8 || cfg->rank > 32) return fail(SKSSM_EUNSUPPORTED, "pivot maps need rank 8..32");
     if (!cmap) return fail(SKSSM_EINVAL, "cmap is required when pivots > 0");
@@ -131,6 +176,7 @@ int sketchssm_update(const skssm_config* cfg, float* S, const float* omega, cons
   a.H = cfg->heads;
   a.W = cfg->window;
   a.n = n_buffered;
+  put_ranks(a, rk);
   a.S = S;
   a.omega = omega;
   a.U = cfg->rank > 0 ? U : nullptr;
@@ -154,6 +200,10 @@ int sketchssm_update(const skssm_config* cfg, float* S, const float* omega, cons
     if (cfg->rank == 0 || !U) return fail(SKSSM_EINVAL, "sketch-only update needs rank > 0 and U");
     a.nt = 0;
     a.o = nullptr;
+    if (rk.sketched == 0) {  // every head is dense: no sketch to build
+      g_err[0] = '\0';
+      return SKSSM_OK;
+    }
   }
   int r;
   switch (cfg->kind) {
@@ -164,10 +214,12 @@ int sketchssm_update(const skssm_config* cfg, float* S, const float* omega, cons
   return launched(r, "sketchssm_update");
 }
 
-int sketchssm_decode(const skssm_config* cfg, const void* U, const float* coef, const float* cmap,
+int sketchssm_decode(const skssm_config* cfg, const void* U, const float* coef, const float* cmap, const float* S,
                      const skssm_ring* ring, int32_t n_buffered, const void* q, float* o, void* stream) {
   int rc = check_shape(cfg, true, false);
   if (rc) return rc;
+  Ranks rk;
+  if ((rc = check_ranks(cfg, rk))) return rc;
   if (cfg->pivots) {
     if (cfg->rank < 8 || cfg->rank > 32) return fail(SKSSM_EUNSUPPORTED, "pivot maps need rank 8..32");
     if (!cmap) return fail(SKSSM_EINVAL, "cmap is required when pivots > 0");
@@ -178,8 +230,15 @@ int sketchssm_decode(const skssm_config* cfg, const void* U, const float* coef, 
     return fail(SKSSM_ESTATE, "n_buffered %d outside 0..%d", n_buffered, cfg->window - 2);
   if (!U || !coef || !o || !q) return fail(SKSSM_EINVAL, "U, coef, q and o are required");
   if (!aligned(U) || !aligned(coef) || !aligned(o) || !aligned(q)) return fail(SKSSM_EALIGN, "U/coef/q/o not aligned");
-  if ((rc = check_ring(cfg, ring, true, false))) return rc;
+  if (rk.dense) {  // dense-fallback heads read the state (and keep pi in the ring)
+    if (!S) return fail(SKSSM_EINVAL, "S is required when the rank table has dense-fallback heads");
+    if (!aligned(S)) return fail(SKSSM_EALIGN, "S not aligned");
+  }
+  if ((rc = check_ring(cfg, ring, rk.sketched > 0, rk.dense > 0))) return rc;
   skssm::DecodeArgs a = decode_args(cfg, ring, n_buffered, q, o);
+  put_ranks(a, rk);
+  put_order(a, rk);
+  a.S = rk.dense ? S : nullptr;
   a.U = U;
   a.coef = coef;
   a.cmap = cfg->pivots ? cmap : nullptr;
@@ -196,6 +255,8 @@ int sketchssm_full_read_baseline(const skssm_config* cfg, const float* S, const 
                                  int32_t n_buffered, const void* q, float* o, void* stream) {
   int rc = check_shape(cfg, false, false);
   if (rc) return rc;
+  Ranks rk;
+  if ((rc = check_ranks(cfg, rk))) return rc;
   if (cfg->window < 2) return fail(SKSSM_EINVAL, "baseline read needs window >= 2");
   if (n_buffered < 0 || n_buffered > cfg->window - 2)
     return fail(SKSSM_ESTATE, "n_buffered %d outside 0..%d", n_buffered, cfg->window - 2);

@@ -308,276 +308,19 @@ __device__ __forceinline__ void append_derived(const DecodeArgs& a, size_t item,
   }
 }
 
-template <int KIND, int K, int V, int R, int WMAX, typename IO, typename SK, int P>
-__global__ __launch_bounds__(256) void decode_kernel(const DecodeArgs a) {
-  using L = RowLoads<KIND, K, V, WMAX, IO>;
-  constexpr bool ERASE = L::ERASE, CHAN = L::CHAN;
-  constexpr int KPL = L::KPL, VR = L::VR, NG = L::NG, GD = L::GD;
-  constexpr int VPL = V / 64;                    // value channels per lane (value layout)
-  constexpr int RP = (R + 15) / 16;              // sketch components per lane (row layout)
-  constexpr int PW = 16 / (int)sizeof(SK);       // sketch columns per panel: 16 bytes per value
-  constexpr int NP = R / PW;                     // sketch panels
-  constexpr int CP = K + 4;                      // padded LDS row pitch of C
-  constexpr int KQ = K / 4;                      // channels each row covers in C x
-  constexpr int WS = 2 * K + R + V + 2 * WMAX;   // per-wave LDS: x_q, x_k, c, o_buf, alpha/gamma transposition
-  constexpr bool U_PRELOAD = R <= 32;
-  constexpr int UP = U_PRELOAD ? NP : 1;
-
-  __shared__ __align__(16) float c_lds[R * CP];
-  __shared__ __align__(16) float wscr[4 * WS];
-
-  const int tid = threadIdx.x, lane = tid & 63;
-  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const int row = lane >> 4, col = lane & 15;
-  const int H = a.H, n = a.n;
-  const int h = blockIdx.x % H;
-  const int b = (blockIdx.x / H) * 4 + wave;
-  const bool valid = b < a.B;
-  const size_t item = (size_t)(valid ? b : 0) * H + h;
-  const SK* Ub = static_cast<const SK*>(a.U) + item * (size_t)V * R;
-
-  // ---- C first, then every global load of this item
-  constexpr int CQ = (R * K / 4 + 255) / 256;  // float4 of C per thread
-  Vec<4> cv[CQ];
-#pragma unroll
-  for (int c = 0; c < CQ; ++c) {
-    const int i = tid + 256 * c;
-    if (CQ * 256 == R * K / 4 || i < R * K / 4) cv[c].load(a.coef + (size_t)h * R * K + 4 * i);
-  }
-  compiler_fence();
-  L r;
-  float fs[ERASE ? NG : 1][RP];      // ring f of slot 4 gi + row, component col + 16 p
-  Raw<SK, PW> Ur[VPL][UP];           // sketch panels (value layout)
-  if (valid) {
-    r.load(a, item, row, col);
-    if constexpr (ERASE) {
-      const size_t NI = (size_t)a.B * H;
-      const size_t rowder = (size_t)row * NI + item;
-#pragma unroll
-      for (int gi = 0; gi < NG; ++gi) {
-        const int s = 4 * gi + row;
-        const float* fp = a.rf + (rowder + (size_t)(4 * gi) * NI) * R;
-#pragma unroll
-        for (int p = 0; p < RP; ++p) {
-          const int j = col + 16 * p;
-          fs[gi][p] = (4 * gi < n && s < n && j < R) ? fp[j] : 0.f;
-        }
-      }
-    }
-    if constexpr (U_PRELOAD) {
-#pragma unroll
-      for (int p = 0; p < NP; ++p)
-#pragma unroll
-        for (int vv = 0; vv < VPL; ++vv)
-          Ur[vv][p].load_nt(Ub + (uint32_t)((p * V + lane + 64 * vv) * PW));
-    }
-  }
-
-  // ---- this head's coefficient map C (R x K) into LDS; its loads were issued
-  // first, so the LDS-only barrier leaves the item's own loads in flight
-#pragma unroll
-  for (int c = 0; c < CQ; ++c) {
-    const int i = tid + 256 * c;
-    if (CQ * 256 == R * K / 4 || i < R * K / 4) cv[c].store(&c_lds[((4 * i) / K) * CP + (4 * i) % K]);
-  }
-  lds_barrier();
-  if (!valid) return;
-
-  float* xq_l = wscr + wave * WS;
-  float* xk_l = xq_l + K;
-  float* c_l = xq_l + 2 * K;
-  float* ob_l = c_l + R;
-  float* b_l = ob_l + V;
-
-  r.prefix_decay(n, row);
-  float qv[KPL], kv[KPL], gt[GD];
-#pragma unroll
-  for (int m = 0; m < KPL; ++m) {
-    qv[m] = r.q_raw.get(m);
-    kv[m] = r.k_raw.get(m);
-  }
-#pragma unroll
-  for (int m = 0; m < GD; ++m) gt[m] = r.gprev[m] + r.la[m];
-
-  float av[NG], bv[NG], at;
-  slot_dots(r, n, row, qv, kv, gt, av, bv, at);
-  float ca[NG], cg[NG], gcol[L::JP];
-  buffer_coefs<L>(n, row, col, r, av, bv, b_l, ca, cg, gcol);
-  float ut[VR], ob[VR];
-  buffer_term(r, ca, cg, at, ut, ob);
-
-  // ---- C (e^{g_t} . q_t) and C (e^{g_t} . k_t): each row covers K/4 channels
-  if (row == 0) {
-#pragma unroll
-    for (int m = 0; m < KPL; ++m) {
-      const float e = CHAN ? fast_exp(gt[m]) : 1.f;
-      xq_l[col * KPL + m] = e * qv[m];
-      if constexpr (ERASE) xk_l[col * KPL + m] = e * kv[m];
-    }
-#pragma unroll
-    for (int m = 0; m < VR; ++m) ob_l[col * VR + m] = ob[m];
-  }
-  wave_lds_sync();
-  const float eg = CHAN ? 1.f : fast_exp(gt[0]);
-  float cfin[RP], ft[RP], sqv[RP], skv[RP];
-#pragma unroll
-  for (int p = 0; p < RP; ++p) {
-    const int j = col + 16 * p;
-    float sq = 0.f, sk = 0.f;
-    if (j < R) {
-      const float* cr = c_lds + j * CP + row * KQ;
-      const float* xqr = xq_l + row * KQ;
-      const float* xkr = xk_l + row * KQ;
-#pragma unroll
-      for (int m = 0; m < KQ; m += 4) {
-        const float4 cc = *reinterpret_cast<const float4*>(cr + m);
-        const float4 xx = *reinterpret_cast<const float4*>(xqr + m);
-        sq += cc.x * xx.x + cc.y * xx.y + cc.z * xx.z + cc.w * xx.w;
-        if constexpr (ERASE) {
-          const float4 yy = *reinterpret_cast<const float4*>(xkr + m);
-          sk += cc.x * yy.x + cc.y * yy.y + cc.z * yy.z + cc.w * yy.w;
-        }
-      }
-    }
-    sqv[p] = cross_row_sum(sq);
-    skv[p] = ERASE ? cross_row_sum(sk) : 0.f;
-  }
-  if constexpr (P > 0) {
-    // state-dependent map C = F1 M + F2 Omega^T (coef holds Omega^T): C x =
-    // F1 (M x) + F2 (Omega^T x) for x = e^g . q and x = e^g . k
-    static_assert(P == 4 && R <= 32, "pivot maps: P = 4, rank up to 32");
-    const float* cm = a.cmap + item * (size_t)(P * K + R * P + R * R);
-    constexpr int CW = K / 16;                      // channels per lane of M x
-    const int pa = col >> 2, ch = ((col & 3) + 4 * row) * CW;
-    Vec<CW> mr;
-    mr.load_nt(cm + pa * K + ch);
-    float mq = 0.f, mk = 0.f;
-#pragma unroll
-    for (int m = 0; m < CW; ++m) {
-      mq += mr.e[m] * xq_l[ch + m];
-      if constexpr (ERASE) mk += mr.e[m] * xk_l[ch + m];
-    }
-    mq = cross_row_sum(quad_sum(mq));               // lanes with col / 4 = a hold (M x)[a]
-    if constexpr (ERASE) mk = cross_row_sum(quad_sum(mk));
-    float mqa[P], mka[P];
-#pragma unroll
-    for (int x = 0; x < P; ++x) {
-      mqa[x] = lane_bcast(mq, 4 * x);
-      mka[x] = ERASE ? lane_bcast(mk, 4 * x) : 0.f;
-    }
-    wave_lds_sync();                                // x_q, x_k are read; reuse them for Omega^T x
-    if (row == 0) {
-#pragma unroll
-      for (int p = 0; p < RP; ++p) {
-        const int j = col + 16 * p;
-        if (j < R) {
-          xq_l[j] = sqv[p];
-          if constexpr (ERASE) xk_l[j] = skv[p];
-        }
-      }
-    }
-    wave_lds_sync();
-    constexpr int HQ = R / 4;                       // F2 columns per row of lanes
-#pragma unroll
-    for (int p = 0; p < RP; ++p) {
-      const int j = col + 16 * p;
-      float cq = 0.f, ck = 0.f;
-      if (j < R) {
-        Vec<HQ> f2;
-        f2.load_nt(cm + P * K + R * P + j * R + row * HQ);
-#pragma unroll
-        for (int m = 0; m < HQ; ++m) {
-          cq += f2.e[m] * xq_l[row * HQ + m];
-          if constexpr (ERASE) ck += f2.e[m] * xk_l[row * HQ + m];
-        }
-        if (row == 0) {
-          const float4 f1 = *reinterpret_cast<const float4*>(cm + P * K + j * P);
-          cq += f1.x * mqa[0] + f1.y * mqa[1] + f1.z * mqa[2] + f1.w * mqa[3];
-          if constexpr (ERASE) ck += f1.x * mka[0] + f1.y * mka[1] + f1.z * mka[2] + f1.w * mka[3];
-        }
-      }
-      sqv[p] = cross_row_sum(cq);
-      if constexpr (ERASE) skv[p] = cross_row_sum(ck);
-    }
-  }
-#pragma unroll
-  for (int p = 0; p < RP; ++p) {
-    const float sq = sqv[p], sk = skv[p];
-    if constexpr (ERASE) {
-      float sb = 0.f, sa = 0.f;
-#pragma unroll
-      for (int gi = 0; gi < NG; ++gi) {
-        sb += bv[gi] * fs[gi][p];
-        sa += av[gi] * fs[gi][p];
-      }
-      sb = cross_row_sum(sb);
-      sa = cross_row_sum(sa);
-      ft[p] = r.beta_t * (eg * sk - sb);
-      cfin[p] = eg * sq - sa - at * ft[p];
-    } else {
-      ft[p] = 0.f;
-      cfin[p] = eg * sq;
-    }
-  }
-  if (row == 0) {
-#pragma unroll
-    for (int p = 0; p < RP; ++p)
-      if (col + 16 * p < R) c_l[col + 16 * p] = cfin[p];
-  }
-  wave_lds_sync();
-
-  // ---- o = U c + buffer term  (value layout)
-  float* ob_g = a.o + item * V;
-#pragma unroll
-  for (int vv = 0; vv < VPL; ++vv) {
-    float acc = ob_l[lane + 64 * vv];
-#pragma unroll
-    for (int p = 0; p < NP; ++p) {
-      Raw<SK, PW> u;
-      if constexpr (U_PRELOAD) u = Ur[vv][p];
-      else u.load_nt(Ub + (uint32_t)((p * V + lane + 64 * vv) * PW));
-#pragma unroll
-      for (int i = 0; i < PW; i += 4) {
-        const float4 c4 = *reinterpret_cast<const float4*>(c_l + PW * p + i);
-        acc += u.get(i) * c4.x + u.get(i + 1) * c4.y + u.get(i + 2) * c4.z + u.get(i + 3) * c4.w;
-      }
-    }
-    ob_g[lane + 64 * vv] = acc;
-  }
-
-  // ---- derived fields of the token at ring slot n
-  append_derived<L>(a, item, row, col, r, gcol);
-  if constexpr (ERASE) {
-    if (row == 0) {
-      const size_t sl = (size_t)n * a.B * H + item;
-#pragma unroll
-      for (int p = 0; p < RP; ++p)
-        if (col + 16 * p < R) a.rf[sl * R + col + 16 * p] = ft[p];
-    }
-  }
-}
-
+// The exact full-state read of one item by one wave (no workgroup barrier):
+//   o = S_0^T q~_t + o_t^buffer,  q~_t = e^{g_t} . q_t - sum_s a_{t,s} pi_s
+// (eq. app-effective-query-wy), storing pi_t and row n of T^{-1} for the
+// token.  ws: the wave's 2V + 2 WMAX floats of LDS.
 template <int KIND, int K, int V, int WMAX, typename IO>
-__global__ __launch_bounds__(256) void full_read_kernel(const DecodeArgs a) {
+__device__ __forceinline__ void full_read_item(const DecodeArgs& a, size_t item, int lane, float* ws) {
   using L = RowLoads<KIND, K, V, WMAX, IO>;
   constexpr bool ERASE = L::ERASE, CHAN = L::CHAN;
   constexpr int KPL = L::KPL, VR = L::VR, NG = L::NG, GD = L::GD;
   constexpr int VPL = V / 64;
-  constexpr int WS = 2 * V + 2 * WMAX;  // per-wave LDS: o^state, o_buf, alpha/gamma transposition
-
-  __shared__ __align__(16) float wscr[4 * WS];
-
-  const int tid = threadIdx.x, lane = tid & 63;
-  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int row = lane >> 4, col = lane & 15;
   const int n = a.n;
   const size_t NI = (size_t)a.B * a.H;
-  // XCD x runs a contiguous share of the items (neighbouring items share the
-  // cache lines of the per-slot scalars); plain order when the grid does not split
-  const uint32_t G = gridDim.x, wg = blockIdx.x;
-  const uint32_t lwg = (G % 8 == 0) ? (wg % 8) * (G / 8) + wg / 8 : wg;
-  const size_t item = (size_t)lwg * 4 + wave;
-  if (item >= NI) return;  // wave-uniform; no block barrier in this kernel
   const uint32_t koff = (uint32_t)(col * KPL);
 
   L r;
@@ -597,7 +340,7 @@ __global__ __launch_bounds__(256) void full_read_kernel(const DecodeArgs a) {
     }
   }
 
-  float* os_l = wscr + wave * WS;
+  float* os_l = ws;
   float* ob_l = os_l + V;
   float* b_l = ob_l + V;
 
@@ -671,6 +414,302 @@ __global__ __launch_bounds__(256) void full_read_kernel(const DecodeArgs a) {
       t.store(a.rpi + ((size_t)n * NI + item) * K + koff);
     }
   }
+}
+
+template <int KIND, int K, int V, int R, int WMAX, typename IO, typename SK, int P>
+__global__ __launch_bounds__(256) void decode_kernel(const DecodeArgs a) {
+  using L = RowLoads<KIND, K, V, WMAX, IO>;
+  constexpr bool ERASE = L::ERASE, CHAN = L::CHAN;
+  constexpr int KPL = L::KPL, VR = L::VR, NG = L::NG, GD = L::GD;
+  constexpr int VPL = V / 64;                    // value channels per lane (value layout)
+  constexpr int RP = (R + 15) / 16;              // sketch components per lane (row layout)
+  constexpr int PW = 16 / (int)sizeof(SK);       // sketch columns per panel: 16 bytes per value
+  constexpr int NP = R / PW;                     // sketch panels
+  constexpr int CP = K + 4;                      // padded LDS row pitch of C
+  constexpr int KQ = K / 4;                      // channels each row covers in C x
+  constexpr int WS = 2 * K + R + V + 2 * WMAX;   // per-wave LDS: x_q, x_k, c, o_buf, alpha/gamma transposition
+  constexpr bool U_PRELOAD = R <= 32;
+  constexpr int UP = U_PRELOAD ? NP : 1;
+
+  __shared__ __align__(16) float c_lds[R * CP];
+  __shared__ __align__(16) float wscr[4 * WS];
+
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int row = lane >> 4, col = lane & 15;
+  const int H = a.H, n = a.n;
+  // workgroup -> (head, batch tile): head fastest; with a per-head rank table
+  // the dense heads' workgroups come first, in the head order hlist
+  int h = blockIdx.x % H, tile = blockIdx.x / H;
+  if (a.ragged) {
+    const int T = gridDim.x / H, nd = a.ndense, w = blockIdx.x;
+    if (w < nd * T) {
+      h = a.hlist[w % nd];
+      tile = w / nd;
+    } else {
+      const int ns = H - nd, w2 = w - nd * T;
+      h = a.hlist[nd + w2 % ns];
+      tile = w2 / ns;
+    }
+  }
+  const int b = tile * 4 + wave;
+  const bool valid = b < a.B;
+  const size_t item = (size_t)(valid ? b : 0) * H + h;
+  const SK* Ub = static_cast<const SK*>(a.U) + item * (size_t)V * R;
+  // this head's rank: its first rh sketch columns, coefficient rows and f
+  // entries are used; a dense-fallback head (rh = 0) is read elsewhere
+  const int rh = a.ragged ? (int)a.hrank[h] : R;
+  if (rh == 0) {
+    // dense-fallback head: the exact full-state read of its items, one per
+    // wave (the whole workgroup shares the head and takes this branch, so no
+    // barrier is skipped)
+    static_assert(WS >= 2 * V + 2 * WMAX, "per-wave LDS too small for the full read");
+    if (valid) full_read_item<KIND, K, V, WMAX, IO>(a, item, lane, wscr + wave * WS);
+    return;
+  }
+
+  // ---- C first, then every global load of this item
+  constexpr int CQ = (R * K / 4 + 255) / 256;  // float4 of C per thread
+  Vec<4> cv[CQ];
+#pragma unroll
+  for (int c = 0; c < CQ; ++c) {
+    const int i = tid + 256 * c;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) cv[c].e[e] = 0.f;
+    if ((CQ * 256 == R * K / 4 || i < R * K / 4) && (4 * i) / K < rh) cv[c].load(a.coef + (size_t)h * R * K + 4 * i);
+  }
+  compiler_fence();
+  L r;
+  float fs[ERASE ? NG : 1][RP];      // ring f of slot 4 gi + row, component col + 16 p
+  Raw<SK, PW> Ur[VPL][UP];           // sketch panels (value layout)
+  if (valid) {
+    r.load(a, item, row, col);
+    if constexpr (ERASE) {
+      const size_t NI = (size_t)a.B * H;
+      const size_t rowder = (size_t)row * NI + item;
+#pragma unroll
+      for (int gi = 0; gi < NG; ++gi) {
+        const int s = 4 * gi + row;
+        const float* fp = a.rf + (rowder + (size_t)(4 * gi) * NI) * R;
+#pragma unroll
+        for (int p = 0; p < RP; ++p) {
+          const int j = col + 16 * p;
+          fs[gi][p] = (4 * gi < n && s < n && j < rh) ? fp[j] : 0.f;
+        }
+      }
+    }
+    if constexpr (U_PRELOAD) {
+#pragma unroll
+      for (int p = 0; p < NP; ++p)
+#pragma unroll
+        for (int vv = 0; vv < VPL; ++vv) {
+          Ur[vv][p].zero();
+          if (p * PW < rh) Ur[vv][p].load_nt(Ub + (uint32_t)((p * V + lane + 64 * vv) * PW));
+        }
+    }
+  }
+
+  // ---- this head's coefficient map C (R x K) into LDS; its loads were issued
+  // first, so the LDS-only barrier leaves the item's own loads in flight
+#pragma unroll
+  for (int c = 0; c < CQ; ++c) {
+    const int i = tid + 256 * c;
+    if (CQ * 256 == R * K / 4 || i < R * K / 4) cv[c].store(&c_lds[((4 * i) / K) * CP + (4 * i) % K]);
+  }
+  lds_barrier();
+  if (!valid) return;
+
+  float* xq_l = wscr + wave * WS;
+  float* xk_l = xq_l + K;
+  float* c_l = xq_l + 2 * K;
+  float* ob_l = c_l + R;
+  float* b_l = ob_l + V;
+
+  r.prefix_decay(n, row);
+  float qv[KPL], kv[KPL], gt[GD];
+#pragma unroll
+  for (int m = 0; m < KPL; ++m) {
+    qv[m] = r.q_raw.get(m);
+    kv[m] = r.k_raw.get(m);
+  }
+#pragma unroll
+  for (int m = 0; m < GD; ++m) gt[m] = r.gprev[m] + r.la[m];
+
+  float av[NG], bv[NG], at;
+  slot_dots(r, n, row, qv, kv, gt, av, bv, at);
+  float ca[NG], cg[NG], gcol[L::JP];
+  buffer_coefs<L>(n, row, col, r, av, bv, b_l, ca, cg, gcol);
+  float ut[VR], ob[VR];
+  buffer_term(r, ca, cg, at, ut, ob);
+
+  // ---- C (e^{g_t} . q_t) and C (e^{g_t} . k_t): each row covers K/4 channels
+  if (row == 0) {
+#pragma unroll
+    for (int m = 0; m < KPL; ++m) {
+      const float e = CHAN ? fast_exp(gt[m]) : 1.f;
+      xq_l[col * KPL + m] = e * qv[m];
+      if constexpr (ERASE) xk_l[col * KPL + m] = e * kv[m];
+    }
+#pragma unroll
+    for (int m = 0; m < VR; ++m) ob_l[col * VR + m] = ob[m];
+  }
+  wave_lds_sync();
+  const float eg = CHAN ? 1.f : fast_exp(gt[0]);
+  float cfin[RP], ft[RP], sqv[RP], skv[RP];
+#pragma unroll
+  for (int p = 0; p < RP; ++p) {
+    const int j = col + 16 * p;
+    float sq = 0.f, sk = 0.f;
+    if (j < rh) {
+      const float* cr = c_lds + j * CP + row * KQ;
+      const float* xqr = xq_l + row * KQ;
+      const float* xkr = xk_l + row * KQ;
+#pragma unroll
+      for (int m = 0; m < KQ; m += 4) {
+        const float4 cc = *reinterpret_cast<const float4*>(cr + m);
+        const float4 xx = *reinterpret_cast<const float4*>(xqr + m);
+        sq += cc.x * xx.x + cc.y * xx.y + cc.z * xx.z + cc.w * xx.w;
+        if constexpr (ERASE) {
+          const float4 yy = *reinterpret_cast<const float4*>(xkr + m);
+          sk += cc.x * yy.x + cc.y * yy.y + cc.z * yy.z + cc.w * yy.w;
+        }
+      }
+    }
+    sqv[p] = cross_row_sum(sq);
+    skv[p] = ERASE ? cross_row_sum(sk) : 0.f;
+  }
+  if constexpr (P > 0) {
+    // state-dependent map C = F1 M + F2 Omega^T (coef holds Omega^T): C x =
+    // F1 (M x) + F2 (Omega^T x) for x = e^g . q and x = e^g . k
+    static_assert(P == 4 && R <= 32, "pivot maps: P = 4, rank up to 32");
+    const float* cm = a.cmap + item * (size_t)(P * K + R * P + R * R);
+    constexpr int CW = K / 16;                      // channels per lane of M x
+    const int pa = col >> 2, ch = ((col & 3) + 4 * row) * CW;
+    Vec<CW> mr;
+    mr.load_nt(cm + pa * K + ch);
+    float mq = 0.f, mk = 0.f;
+#pragma unroll
+    for (int m = 0; m < CW; ++m) {
+      mq += mr.e[m] * xq_l[ch + m];
+      if constexpr (ERASE) mk += mr.e[m] * xk_l[ch + m];
+    }
+    mq = cross_row_sum(quad_sum(mq));               // lanes with col / 4 = a hold (M x)[a]
+    if constexpr (ERASE) mk = cross_row_sum(quad_sum(mk));
+    float mqa[P], mka[P];
+#pragma unroll
+    for (int x = 0; x < P; ++x) {
+      mqa[x] = lane_bcast(mq, 4 * x);
+      mka[x] = ERASE ? lane_bcast(mk, 4 * x) : 0.f;
+    }
+    wave_lds_sync();                                // x_q, x_k are read; reuse them for Omega^T x
+    if (row == 0) {
+#pragma unroll
+      for (int p = 0; p < RP; ++p) {
+        const int j = col + 16 * p;
+        if (j < R) {
+          xq_l[j] = sqv[p];
+          if constexpr (ERASE) xk_l[j] = skv[p];
+        }
+      }
+    }
+    wave_lds_sync();
+    constexpr int HQ = R / 4;                       // F2 columns per row of lanes
+#pragma unroll
+    for (int p = 0; p < RP; ++p) {
+      const int j = col + 16 * p;
+      float cq = 0.f, ck = 0.f;
+      if (j < rh) {  // rows and columns of F2 past the head's rank are zero and not read
+        Vec<HQ> f2;
+#pragma unroll
+        for (int m = 0; m < HQ; ++m) f2.e[m] = 0.f;
+        if (row * HQ < rh) f2.load_nt(cm + P * K + R * P + j * R + row * HQ);
+#pragma unroll
+        for (int m = 0; m < HQ; ++m) {
+          cq += f2.e[m] * xq_l[row * HQ + m];
+          if constexpr (ERASE) ck += f2.e[m] * xk_l[row * HQ + m];
+        }
+        if (row == 0) {
+          const float4 f1 = *reinterpret_cast<const float4*>(cm + P * K + j * P);
+          cq += f1.x * mqa[0] + f1.y * mqa[1] + f1.z * mqa[2] + f1.w * mqa[3];
+          if constexpr (ERASE) ck += f1.x * mka[0] + f1.y * mka[1] + f1.z * mka[2] + f1.w * mka[3];
+        }
+      }
+      sqv[p] = cross_row_sum(cq);
+      if constexpr (ERASE) skv[p] = cross_row_sum(ck);
+    }
+  }
+#pragma unroll
+  for (int p = 0; p < RP; ++p) {
+    const float sq = sqv[p], sk = skv[p];
+    if constexpr (ERASE) {
+      float sb = 0.f, sa = 0.f;
+#pragma unroll
+      for (int gi = 0; gi < NG; ++gi) {
+        sb += bv[gi] * fs[gi][p];
+        sa += av[gi] * fs[gi][p];
+      }
+      sb = cross_row_sum(sb);
+      sa = cross_row_sum(sa);
+      ft[p] = r.beta_t * (eg * sk - sb);
+      cfin[p] = eg * sq - sa - at * ft[p];
+    } else {
+      ft[p] = 0.f;
+      cfin[p] = eg * sq;
+    }
+  }
+  if (row == 0) {
+#pragma unroll
+    for (int p = 0; p < RP; ++p)
+      if (col + 16 * p < R) c_l[col + 16 * p] = cfin[p];
+  }
+  wave_lds_sync();
+
+  // ---- o = U c + buffer term  (value layout)
+  float* ob_g = a.o + item * V;
+#pragma unroll
+  for (int vv = 0; vv < VPL; ++vv) {
+    float acc = ob_l[lane + 64 * vv];
+#pragma unroll
+    for (int p = 0; p < NP; ++p) {
+      if (p * PW >= rh) break;  // panels past this head's rank are not stored
+      Raw<SK, PW> u;
+      if constexpr (U_PRELOAD) u = Ur[vv][p];
+      else u.load_nt(Ub + (uint32_t)((p * V + lane + 64 * vv) * PW));
+#pragma unroll
+      for (int i = 0; i < PW; i += 4) {
+        const float4 c4 = *reinterpret_cast<const float4*>(c_l + PW * p + i);
+        acc += u.get(i) * c4.x + u.get(i + 1) * c4.y + u.get(i + 2) * c4.z + u.get(i + 3) * c4.w;
+      }
+    }
+    ob_g[lane + 64 * vv] = acc;
+  }
+
+  // ---- derived fields of the token at ring slot n
+  append_derived<L>(a, item, row, col, r, gcol);
+  if constexpr (ERASE) {
+    if (row == 0) {
+      const size_t sl = (size_t)n * a.B * H + item;
+#pragma unroll
+      for (int p = 0; p < RP; ++p)
+        if (col + 16 * p < rh) a.rf[sl * R + col + 16 * p] = ft[p];
+    }
+  }
+}
+
+template <int KIND, int K, int V, int WMAX, typename IO>
+__global__ __launch_bounds__(256) void full_read_kernel(const DecodeArgs a) {
+  constexpr int WS = 2 * V + 2 * WMAX;  // per-wave LDS: o^state, o_buf, alpha/gamma transposition
+  __shared__ __align__(16) float wscr[4 * WS];
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const size_t NI = (size_t)a.B * a.H;
+  // XCD x runs a contiguous share of the items (neighbouring items share the
+  // cache lines of the per-slot scalars); plain order when the grid does not split
+  const uint32_t G = gridDim.x, wg = blockIdx.x;
+  const uint32_t lwg = (G % 8 == 0) ? (wg % 8) * (G / 8) + wg / 8 : wg;
+  const size_t item = (size_t)lwg * 4 + wave;
+  if (item >= NI) return;  // wave-uniform; no block barrier in this kernel
+  full_read_item<KIND, K, V, WMAX, IO>(a, item, lane, wscr + wave * WS);
 }
 
 }  // namespace skssm

@@ -301,7 +301,11 @@ __global__ __launch_bounds__(256, 3) void update_kernel(const UpdateArgs a) {
   constexpr int OPJ = 16 * RT + 4;
   constexpr int OQ = OM_LDS ? (K * R / 4 + 255) / 256 : 1;  // float4 of Omega per thread
   __shared__ __align__(16) float OmL[OM_LDS ? K * OPJ : 4];
-  const bool want_U = R > 0 && a.U != nullptr;
+  // this head's rank (per-head rank table): the sketch uses Omega's first rh
+  // columns (the rest are zeroed in LDS, so U's columns past rh come out 0 and
+  // the state-dependent map's rows past rh too); rh = 0: a dense-fallback head
+  const int rh = a.ragged ? (int)a.hrank[h] : R;
+  const bool want_U = R > 0 && a.U != nullptr && rh > 0;
 
   // state-dependent coefficient map (P > 0 pivots): per-wave scratch for the
   // block transposes of N = S U_p and for the first P sketch columns, and the
@@ -396,7 +400,9 @@ __global__ __launch_bounds__(256, 3) void update_kernel(const UpdateArgs a) {
 #pragma unroll
       for (int c = 0; c < OQ; ++c) {
         const int i = tid + 256 * c;
-        if (i < K * R / 4) omv[c].load(a.omega + (size_t)h * K * R + 4 * i);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) omv[c].e[e] = 0.f;
+        if (i < K * R / 4 && 4 * (i % (R / 4)) < rh) omv[c].load(a.omega + (size_t)h * K * R + 4 * i);
       }
     }
   }
@@ -423,8 +429,13 @@ __global__ __launch_bounds__(256, 3) void update_kernel(const UpdateArgs a) {
 #pragma unroll
       for (int c = 0; c < OQ; ++c) {
         const int i = tid + 256 * c;
-        if (i < K * R / 4)
-          omv[c].store(&OmL[(i / (R / 4)) * OPJ + 4 * (i % (R / 4))]);
+        if (i < K * R / 4) {
+          Vec<4> w = omv[c];
+#pragma unroll
+          for (int e = 0; e < 4; ++e)
+            if (4 * (i % (R / 4)) + e >= rh) w.e[e] = 0.f;
+          w.store(&OmL[(i / (R / 4)) * OPJ + 4 * (i % (R / 4))]);
+        }
       }
       if constexpr (R < 16 * RT) {  // zero columns R..16 RT-1
         constexpr int ZQ = (16 * RT - R) / 4;
@@ -703,7 +714,10 @@ __global__ __launch_bounds__(256, 3) void update_kernel(const UpdateArgs a) {
           }
           // columns 16 jt + 4 lg .. +3 of value v; panels of 16 bytes per value:
           // fp32 U[B][H][R/4][V][4], bf16 U[B][H][R/8][V][8]
-          if (16 * jt + 4 * lg < R) {
+          // (panels past this head's rank are not stored; the tail of its last
+          // panel holds zeros)
+          constexpr int PWU = 16 / (int)sizeof(SK);
+          if (16 * jt + 4 * lg < R && ((16 * jt + 4 * lg) / PWU) * PWU < rh) {
             SK* Ui = static_cast<SK*>(a.U) + item * (size_t)V * R;
             if constexpr (sizeof(SK) == 4) {
               reinterpret_cast<float4*>(Ui)[(4 * jt + lg) * V + v] = make_float4(acc[0], acc[1], acc[2], acc[3]);

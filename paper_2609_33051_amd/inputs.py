@@ -179,3 +179,17 @@ def tiny(family: str, batch=2, heads=3, dk=64, dv=64, rank=8, window=8, steps=24
     """A small workload of any family, for parity cases the oracle finishes quickly."""
     return Workload(name or f"tiny_{family}_{dk}x{dv}_r{rank}_w{window}_{io}", family, batch, heads, dk, dv,
                     rank, window, steps, io)
+
+
+def ragged_ranks(wl: Workload, seed: int = SEED) -> list[int]:
+    """A seeded per-head rank table for workload `wl` with storage width
+    wl.rank, shaped like the allocations of Sec. 4.2 (a spread of ranks from
+    1 to the width, and a small share of dense-fallback heads): one head in
+    ten (at least one) is dense (rank 0); the others draw their rank
+    uniformly from 1..wl.rank.  (No calibration data is used.)"""
+    rng = np.random.default_rng(_seed(wl.name, "head_ranks", 0, seed))
+    H = wl.heads
+    ranks = rng.integers(1, wl.rank + 1, size=H)
+    dense = rng.choice(H, size=max(1, H // 10), replace=False)
+    ranks[dense] = 0
+    return [int(x) for x in ranks]

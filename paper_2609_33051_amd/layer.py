@@ -16,6 +16,10 @@ into libsketchssm.so.  Buffers (caller-owned, as the ABI requires):
          [B][H][W][...], written into slot n by the token's producer (write_token);
          derived fields, slot-major [W][B][H][...]: rows of T^{-1} (GDN/KDA),
          f (sketch read) or pi (baseline).
+  head_ranks  optional per-head rank table (allocation of Sec. 4.2): head h
+         uses the first head_ranks[h] columns of the rank-r storage; 0 keeps the
+         head dense (the sketch read reads its state exactly, in the same
+         launch; the ring then holds both f and pi).
 """
 from __future__ import annotations
 
@@ -28,7 +32,7 @@ class SketchSSMLayer:
     def __init__(self, kind: str, batch: int, heads: int, dk: int, dv: int, rank: int, window: int,
                  io: str = "bf16", device="cuda", baseline: bool = False, S: torch.Tensor | None = None,
                  omega: torch.Tensor | None = None, coef: torch.Tensor | None = None, sketch: str = "f32",
-                 pivots: int = 0, ridge: float = 0.1):
+                 pivots: int = 0, ridge: float = 0.1, head_ranks=None):
         self.kind, self.batch, self.heads, self.dk, self.dv = kind, batch, heads, dk, dv
         self.rank, self.window, self.io, self.baseline, self.sketch = rank, window, io, baseline, sketch
         self.pivots = 0 if baseline else pivots
@@ -40,7 +44,9 @@ class SketchSSMLayer:
         dev = self.device
         self.S = S if S is not None else torch.zeros((Bt, H, V, K), dtype=f32, device=dev)
         r = 0 if baseline else rank
-        self.cfg = B.make_config(kind, Bt, H, K, V, r, W, io, sketch, self.pivots, ridge)
+        self.head_ranks = None if (baseline or head_ranks is None) else [int(x) for x in head_ranks]
+        self.dense_heads = 0 if self.head_ranks is None else sum(1 for x in self.head_ranks if x == 0)
+        self.cfg = B.make_config(kind, Bt, H, K, V, r, W, io, sketch, self.pivots, ridge, head_ranks=self.head_ranks)
         if not baseline:
             self.omega = omega.to(dev).contiguous()
             self.coef = coef.to(dev).contiguous()
@@ -60,7 +66,8 @@ class SketchSSMLayer:
         # derived fields, written by the library
         self.rt = torch.zeros((W, Bt, H, W), dtype=f32, device=dev) if erase else None
         self.rf = torch.zeros((W, Bt, H, rank), dtype=f32, device=dev) if (erase and not baseline) else None
-        self.rpi = torch.zeros((W, Bt, H, K), dtype=f32, device=dev) if (erase and baseline) else None
+        self.rpi = (torch.zeros((W, Bt, H, K), dtype=f32, device=dev)
+                    if (erase and (baseline or self.dense_heads)) else None)
         self.ring = B.make_ring(k=self.rk, v=self.rv, beta=self.rbeta, log_decay=self.rla, f=self.rf,
                                 pi=self.rpi, tinv=self.rt)
         self.o = torch.zeros((Bt, H, V), dtype=f32, device=dev)
@@ -103,7 +110,8 @@ class SketchSSMLayer:
             B.sketchssm_full_read_baseline(self.cfg, self.S, self.ring, self.n, q, o, self.stream())
             self.n += 1
         else:
-            B.sketchssm_decode(self.cfg, self.U, self.coef, self.ring, self.n, q, o, self.stream(), cmap=self.cmap)
+            B.sketchssm_decode(self.cfg, self.U, self.coef, self.ring, self.n, q, o, self.stream(), cmap=self.cmap,
+                               S=self.S if self.dense_heads else None)
             self.n += 1
         return o
 
@@ -118,7 +126,8 @@ class SketchSSMLayer:
             return B.prepare_update(self.cfg, self.S, self.omega, self.ring, n, q, self.U, o, st, cmap=self.cmap)
         if self.baseline:
             return B.prepare_full_read_baseline(self.cfg, self.S, self.ring, n, q, o, st)
-        return B.prepare_decode(self.cfg, self.U, self.coef, self.ring, n, q, o, st, cmap=self.cmap)
+        return B.prepare_decode(self.cfg, self.U, self.coef, self.ring, n, q, o, st, cmap=self.cmap,
+                                S=self.S if self.dense_heads else None)
 
     def step(self, inp: dict, out: torch.Tensor | None = None) -> torch.Tensor:
         """write_token + read."""

@@ -18,7 +18,7 @@ These are the numerators of the reported HBM roofline fractions.
 """
 from __future__ import annotations
 
-from dataclasses import dataclass
+from dataclasses import dataclass, replace
 
 HBM_PEAK_GBPS = 8000.0  # MI355X HBM3E, published peak
 
@@ -146,3 +146,31 @@ def window_bytes(s: Shape, baseline: bool = False) -> dict:
     fl = flush_bytes(s, W - 1, 0 if baseline else None)
     return {"nonflush": reads, "flush": fl, "total": sum(reads) + fl,
             "nonflush_mean": (sum(reads) / len(reads)) if reads else 0.0}
+
+
+def panel_cols(s: Shape, g: int) -> int:
+    """Sketch columns a rank-g head stores: whole panels of 16 bytes per value."""
+    P = 16 // s.sketch_bytes
+    return -(-g // P) * P
+
+
+def ragged_decode_bytes(s: Shape, n: int, ranks) -> int:
+    """Non-flush read at slot n of one batch row (all heads) under a per-head
+    rank table with storage width s.rank: a sketched head (g > 0) moves the
+    decode bytes of rank g (its U up to the next whole panel); a dense head
+    (g = 0) moves the exact full-read bytes."""
+    tot = 0
+    for g in ranks:
+        if g == 0:
+            tot += full_read_bytes(s, n)
+        else:
+            sg = replace(s, rank=g)
+            tot += decode_bytes(sg, n) + s.sketch_bytes * s.dv * (panel_cols(s, g) - g)
+    return tot
+
+
+def ragged_flush_bytes(s: Shape, n_buffered: int, ranks) -> int:
+    """Flush of one batch row under a per-head rank table: each head's state
+    read and write, its sketch columns (whole panels; none for a dense head)
+    and, with a state-dependent map, the full-width factors."""
+    return sum(flush_bytes(s, n_buffered, panel_cols(s, g) if g else 0) for g in ranks)

@@ -31,7 +31,7 @@ class Run:
 
 
 def run_workload(wl, rank=None, window=None, steps=None, omega_coef=None, sel=None, baseline=False,
-                 device="cuda", seed=inputs.SEED, S0=None, keep_layer=False, sketch="f32", pivots=0):
+                 device="cuda", seed=inputs.SEED, S0=None, keep_layer=False, sketch="f32", pivots=0, head_ranks=None):
     """Run `steps` decode tokens of workload `wl` on the GPU.
 
     sel: flat item indices (b*H + h) whose outputs and inputs are kept for the
@@ -48,7 +48,7 @@ def run_workload(wl, rank=None, window=None, steps=None, omega_coef=None, sel=No
     S_sel = to_np32(S.reshape(n_items, wl.dv, wl.dk) if sel is None else S.reshape(n_items, wl.dv, wl.dk)[sel_t])
     layer = SketchSSMLayer(wl.kind, wl.batch, wl.heads, wl.dk, wl.dv, rank, window, wl.io, device,
                            baseline=baseline, S=S, omega=torch.as_tensor(om), coef=torch.as_tensor(C), sketch=sketch,
-                           pivots=pivots)
+                           pivots=pivots, head_ranks=head_ranks)
     layer.init_sketch()
     run = Run()
     for t in range(steps):

@@ -65,10 +65,10 @@ ADDR = 1 << 20  # a 16-byte aligned fake address, never dereferenced (every case
 
 def cfg(**kw):
     d = dict(kind="mamba2", batch=2, heads=4, dk=128, dv=64, rank=16, window=16, io="bf16", sketch="f32", pivots=0,
-             ridge=0.1)
+             ridge=0.1, head_ranks=None)
     d.update(kw)
     return B.make_config(d["kind"], d["batch"], d["heads"], d["dk"], d["dv"], d["rank"], d["window"], d["io"],
-                         d["sketch"], d["pivots"], d["ridge"])
+                         d["sketch"], d["pivots"], d["ridge"], head_ranks=d["head_ranks"])
 
 
 def good_ring(**kw):
@@ -141,6 +141,39 @@ class TestValidation:
         assert status(f, cfg(), None, good_ring(), 0, ADDR, ADDR) == -1
         assert status(f, cfg(dv=32), ADDR, good_ring(), 0, ADDR, ADDR) == -2
 
+    def test_head_rank_table(self, lib):
+        """Per-head rank tables are validated on the host; calls with nothing to
+        do for their path return OK without a launch."""
+        d, f, u = B.sketchssm_decode, B.sketchssm_full_read_baseline, B.sketchssm_update
+        ok = [16, 0, 5, 8]
+        assert status(d, cfg(head_ranks=[16, 0, 17, 8]), ADDR, ADDR, good_ring(), 0, ADDR, ADDR) == -1
+        assert "head_rank[2]" in B.sketchssm_last_error()
+        assert status(d, cfg(head_ranks=[16, -1, 4, 8]), ADDR, ADDR, good_ring(), 0, ADDR, ADDR) == -1
+        assert status(d, cfg(rank=128, head_ranks=ok), ADDR, ADDR, good_ring(), 0, ADDR, ADDR) == -2
+        assert status(u, cfg(rank=0, head_ranks=[0, 0, 0, 0]), ADDR, None, good_ring(), 15, ADDR, None, ADDR) == -2
+        assert status(f, cfg(rank=0, head_ranks=[0, 0, 0, 0]), ADDR, good_ring(), 0, ADDR, ADDR) == -2
+        many = 300
+        assert status(d, cfg(heads=many, head_ranks=[8] * many), ADDR, ADDR, good_ring(), 0, ADDR, ADDR) == -2
+        # dense-fallback heads are read from S by the decode: S (and, GDN/KDA, ring pi) required
+        assert status(d, cfg(head_ranks=[0, 4, 0, 0]), ADDR, ADDR, good_ring(), 0, ADDR, ADDR) == -1
+        assert "dense-fallback" in B.sketchssm_last_error()
+        assert status(lambda *x: d(*x, S=ADDR + 4), cfg(head_ranks=[0, 4, 0, 0]), ADDR, ADDR, good_ring(), 0,
+                      ADDR, ADDR) == -3
+        assert status(lambda *x: d(*x, S=ADDR), cfg(kind="gdn", dv=128, head_ranks=[0, 4, 0, 0]), ADDR, ADDR,
+                      good_ring(pi=None), 0, ADDR, ADDR) == -1
+        # a sketch-only update with every head dense has nothing to build: OK without a launch
+        assert status(u, cfg(head_ranks=[0, 0, 0, 0]), ADDR, ADDR, None, 0, None, ADDR, None) == 0
+        # the rest of the validation still applies with a table
+        assert status(d, cfg(head_ranks=[0, 0, 0, 0]), ADDR, ADDR, good_ring(), 15, ADDR, ADDR) == -4
+
 
 def check_config_ok(lib):
     return B.sketchssm_check_config(cfg()) == 0 and B.sketchssm_check_config(cfg(rank=5)) == -2
+
+
+def test_head_rank_table_marshalling():
+    c = B.make_config("gdn", 2, 3, 128, 128, 16, 16, "bf16", head_ranks=[16, 0, 7])
+    assert B.head_ranks(c) == [16, 0, 7]
+    assert B.head_ranks(B.make_config("gdn", 2, 3, 128, 128, 16, 16, "bf16")) is None
+    with pytest.raises(ValueError):
+        B.make_config("gdn", 2, 3, 128, 128, 16, 16, "bf16", head_ranks=[16, 0])

@@ -1,0 +1,118 @@
+"""GPU parity of per-head rank tables (the rank allocation of Sec. 4.2 and the
+allocation appendix): heads of one layer with different sketch ranks, and
+dense-fallback heads (rank 0) that keep exact full-state reads.
+
+Each head is checked on its own against the CPU oracle run for that head
+alone: a sketched head of rank G_h against the oracle's rank-G_h method with
+the first G_h columns of the head's Omega (and its state-dependent map with
+min(4, G_h) pivots), a dense head against the exact windowed read.  The
+storage keeps the layer's full width; the tail of a head's last sketch panel
+must hold exact zeros, and panels past it are never written.  Bars as in the
+uniform-rank parity tests.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2609_33051_amd import inputs
+from harness import max_step_rel, rel_l2, run_workload, to_np32
+
+pytestmark = pytest.mark.gpu
+
+TOL = {"f32": 1e-5, "bf16": 2e-3}
+
+
+def check_ragged(wl, head_ranks, window=None, steps=None, sketch="f32", pivots=0, sel=None):
+    window = wl.window if window is None else window
+    print(f"[case] ragged {wl.name} kind={wl.kind} B={wl.batch} H={wl.heads} K={wl.dk} V={wl.dv} r={wl.rank} "
+          f"W={window} io={wl.io} sketch={sketch} pivots={pivots} ranks={head_ranks} "
+          f"sel={'all' if sel is None else len(sel)}", flush=True)
+    run, layer, S_sel, heads, (om, C) = run_workload(wl, window=window, steps=steps, sel=sel, sketch=sketch,
+                                                     pivots=pivots, head_ranks=head_ranks)
+    n_items = wl.batch * wl.heads
+    items = np.arange(n_items) if sel is None else np.asarray(sel)
+    q, k, v, beta, logd = (np.stack(run.inp[x]) for x in ("q", "k", "v", "beta", "log_decay"))
+    o_gpu = np.stack(run.o_gpu)
+    S_gpu = to_np32(layer.S.reshape(n_items, wl.dv, wl.dk))[items]
+    U_gpu = to_np32(layer.sketch_matrix().reshape(n_items, wl.dv, wl.rank))[items]
+    tol = TOL["bf16" if sketch == "bf16" else wl.io]
+    P = 8 if sketch == "bf16" else 4
+    worst = 0.0
+    for h in range(wl.heads):
+        m = heads == h
+        if not m.any():
+            continue
+        g = head_ranks[h]
+        hz = np.zeros(int(m.sum()), np.int32)
+        om_h = om[h:h + 1, :, :max(g, 1)] if g else om[h:h + 1]
+        C_h = C[h:h + 1, :max(g, 1), :] if g else C[h:h + 1]
+        ref = oracle.sketchssm(wl.kind, window, hz, np.ascontiguousarray(om_h), np.ascontiguousarray(C_h), S_sel[m],
+                               q[:, m], k[:, m], v[:, m], beta[:, m], logd[:, m], round_storage=True,
+                               sketch_bf16=(sketch == "bf16"), pivots=pivots if g else 0, ridge=0.1)
+        target = ref.o if g else ref.o_exact_windowed
+        err = max_step_rel(list(o_gpu[:, m]), target)
+        errS = rel_l2(S_gpu[m], ref.S_final)
+        errU = rel_l2(U_gpu[m][:, :, :g], ref.U_final) if g else 0.0
+        print(f"  head {h} rank {g}: max step rel-L2 {err:.3e}  state {errS:.3e}  sketch {errU:.3e}", flush=True)
+        assert err <= tol and errS <= tol and errU <= tol, f"head {h} rank {g}"
+        # columns past the head's rank: zeros in its last panel, untouched (still zero) beyond
+        if g < wl.rank:
+            assert np.all(U_gpu[m][:, :, g:] == 0.0), f"head {h}: sketch columns past rank {g} not zero"
+        worst = max(worst, err)
+    return worst, layer
+
+
+@pytest.mark.parametrize("fam,K,V,rank,window,io,ranks", [
+    ("mamba2", 128, 64, 16, 8, "bf16", [16, 0, 5, 8]),
+    ("gdn", 128, 128, 16, 8, "bf16", [12, 0, 16, 3]),
+    ("kda", 128, 128, 32, 8, "bf16", [32, 7, 0, 20]),
+    ("mamba2_form", 64, 64, 8, 8, "f32", [1, 8, 0, 4]),
+    ("gdn", 64, 64, 32, 16, "f32", [0, 31, 9, 2]),
+])
+def test_ragged_small(fam, K, V, rank, window, io, ranks):
+    wl = inputs.tiny(fam, batch=5, heads=len(ranks), dk=K, dv=V, rank=rank, window=window, steps=2 * window + 3,
+                     io=io)
+    check_ragged(wl, ranks)
+
+
+@pytest.mark.parametrize("fam,rank,ranks,sketch", [
+    ("mamba2", 16, [16, 0, 5, 8], "f32"),
+    ("gdn", 16, [12, 0, 16, 3], "bf16"),
+    ("kda", 32, [32, 7, 0, 20], "f32"),
+])
+def test_ragged_pivot_map(fam, rank, ranks, sketch):
+    V = 64 if fam == "mamba2" else 128
+    wl = inputs.tiny(fam, batch=5, heads=len(ranks), dk=128, dv=V, rank=rank, window=8, steps=19, io="bf16")
+    check_ragged(wl, ranks, sketch=sketch, pivots=4)
+
+
+def test_ragged_all_dense_and_all_sketched():
+    """Tables with no sketched head (only full reads) and with no dense head."""
+    wl = inputs.tiny("gdn", batch=4, heads=3, dk=128, dv=128, rank=16, window=8, steps=11, io="bf16")
+    check_ragged(wl, [0, 0, 0])
+    check_ragged(wl, [16, 4, 9])
+
+
+def test_ragged_full_rank_table_matches_uniform():
+    """A table that gives every head the full width reproduces the uniform
+    rank call bitwise."""
+    wl = inputs.tiny("kda", batch=6, heads=2, dk=128, dv=128, rank=16, window=8, steps=12, io="bf16")
+    print("[case] ragged table [16, 16] vs uniform rank 16 (kda)", flush=True)
+    a, la, _, _, _ = run_workload(wl, head_ranks=[16, 16])
+    b, lb, _, _, _ = run_workload(wl)
+    for x, y in zip(a.o_gpu, b.o_gpu):
+        assert np.array_equal(x, y)
+    assert torch.equal(la.S, lb.S) and torch.equal(la.U, lb.U)
+
+
+@pytest.mark.parametrize("name", ["gdn_b512", "kda_b512"])
+def test_ragged_full_size(name):
+    """The paper-shape workloads with a mixed table (about a tenth of the heads
+    dense), sampled items, in the launch configuration the benchmark times."""
+    wl = inputs.WORKLOADS[name]
+    ranks = inputs.ragged_ranks(wl)
+    rng = np.random.default_rng(11)
+    items = wl.batch * wl.heads
+    sel = np.unique(np.concatenate([[0, items - 1], rng.choice(items, size=48, replace=False)]))
+    check_ragged(wl, ranks, steps=wl.window + 5, sel=sel)

@@ -49,3 +49,18 @@ def test_algorithmic_bytes_gdn_decode():
     # each earlier slot adds raw k, v 512 + beta 4 + log decay 4 + f 64 = 584; from 2 to 3 earlier
     # slots the T^{-1} row reads grow from 1 + 0 to 2 + 1 + 0 values (8 B) and the stored row by 4 B
     assert traffic.decode_bytes(s, 3) - traffic.decode_bytes(s, 2) == 584 + 8 + 4
+
+
+def test_ragged_bytes_reduce_to_the_uniform_and_dense_cases():
+    T = traffic
+    s = T.Shape("gdn", 128, 128, 16, 16, 2)
+    for n in (0, 5, 14):
+        # a full-width table is the uniform sketch read; an all-dense one the exact full read
+        assert T.ragged_decode_bytes(s, n, [16, 16, 16]) == 3 * T.decode_bytes(s, n)
+        assert T.ragged_decode_bytes(s, n, [0, 0]) == 2 * T.full_read_bytes(s, n)
+        # a rank-5 head stores two fp32 panels (8 columns) of U and 5 f entries per slot
+        sg = T.Shape("gdn", 128, 128, 5, 16, 2)
+        assert T.ragged_decode_bytes(s, n, [5]) == T.decode_bytes(sg, n) + 4 * 128 * 3
+    assert T.panel_cols(s, 5) == 8 and T.panel_cols(T.Shape("gdn", 128, 128, 16, 16, 2, 2), 5) == 8
+    assert T.panel_cols(T.Shape("gdn", 128, 128, 16, 16, 2, 2), 9) == 16
+    assert T.ragged_flush_bytes(s, 15, [16, 0]) == T.flush_bytes(s, 15) + T.flush_bytes(s, 15, 0)

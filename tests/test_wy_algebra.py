@@ -92,3 +92,40 @@ def test_rank_w_flush(kind, W):
     XW = X0 * np.exp(g[-1])[None, :] + Wv @ L
     np.testing.assert_allclose(XW, S.T, atol=1e-12)
 
+
+
+@pytest.mark.parametrize("kind,seed", [("gdn", 0), ("kda", 1), ("gdn", 2)])
+def test_inverse_rows_replace_the_recursions(kind, seed):
+    """The ring stores rows of T^{-1}, T = I + Diag(beta) B with the couplings
+    B_{s,j} = b_{s,j} (j < s) of eq. wy.  Each read computes gamma = T^{-T} b_t
+    and stores row t as -beta_t gamma; the stored rows must be T^{-1} (an
+    explicit inverse), and products with them must give the pseudo-values,
+    the erase factors and the buffer term that the recursions define."""
+    k, q, v, beta, logd, S0, C = make(kind, K=7, V=5, W=9, seed=seed)
+    W, K = k.shape
+    g = np.cumsum(logd, axis=0)
+    Bc = np.zeros((W, W))
+    for t in range(W):
+        for j in range(t):
+            Bc[t, j] = np.sum(np.exp(g[t] - g[j]) * k[j] * k[t])
+    T = np.eye(W) + np.diag(beta) @ Bc
+    Tinv = np.zeros((W, W))                       # rows as the reads append them
+    for t in range(W):
+        Tinv[t, t] = 1.0
+        if t:
+            gamma = Tinv[:t, :t].T @ Bc[t, :t]        # T_{<t}^{-T} b_t
+            Tinv[t, :t] = -beta[t] * gamma
+    np.testing.assert_allclose(Tinv, np.linalg.inv(T), atol=1e-12)
+    # recursions of eq. wy (pi) and of the pseudo-values (u)
+    u, pis = [], []
+    for t in range(W):
+        u.append(beta[t] * (v[t] - sum(Bc[t, j] * u[j] for j in range(t))))
+        pis.append(beta[t] * (np.exp(g[t]) * k[t] - sum(Bc[t, j] * pis[j] for j in range(t))))
+    np.testing.assert_allclose(Tinv @ (beta[:, None] * v), np.array(u), atol=1e-12)
+    np.testing.assert_allclose(Tinv @ (beta[:, None] * np.exp(g) * k), np.array(pis), atol=1e-12)
+    # a read at slot n: sum_s a_s u_s = sum_j alpha_j beta_j v_j with alpha = T^{-T} a
+    for n in range(1, W):
+        a = np.array([np.sum(np.exp(g[n] - g[s]) * k[s] * q[n]) for s in range(n)])
+        alpha = Tinv[:n, :n].T @ a
+        np.testing.assert_allclose(sum(a[s] * u[s] for s in range(n)),
+                                   (alpha * beta[:n]) @ v[:n], atol=1e-12)

@@ -275,12 +275,13 @@ __global__ __launch_bounds__(256, 3) void update_kernel(const UpdateArgs a) {
 
   __shared__ __align__(16) float Ls[SP * LP];                 // keys k_s (KDA: then L[s]), [s][k]
   __shared__ __align__(16) float PiT[ERASE ? K * PP : 4];     // Pi^T[k][s]
-  __shared__ __align__(16) float Us[SP * UP];                 // c_s beta_s v_s (Mamba-2) or u_s
+  __shared__ __align__(16) float Us[SP * UP];                 // raw v_s (Mamba-2) or u_s
   __shared__ float Bs[ERASE ? SP * SP : 1];                   // (T^{-1})_{s,j}, j < s < n
   __shared__ float bpart[ERASE ? KW * SP : 1];                // partial sums of b_{n,j}
   __shared__ __align__(16) float qs[K];
   __shared__ __align__(16) float ds[CHAN ? K : 4];            // e^{g_n} per channel (KDA)
-  __shared__ float csc[SP];                                   // c_s (scalar decay)
+  __shared__ float csc[SP];                                   // c_s = e^{g_n - g_s} (scalar decay)
+  __shared__ float bsl[SP], gsl[SP];                          // beta_s, g_s (0 past slot n)
 
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -331,8 +332,8 @@ __global__ __launch_bounds__(256, 3) void update_kernel(const UpdateArgs a) {
 
   // ---- every small load first (window, query, rows of T^{-1}, Omega), then the
   // state: the staged values reach LDS while the state read is still in flight
-  float egn = 1.f, gn = 0.f, bn = 0.f;  // e^{g_n} (scalar decay), g_n, beta_n
-  float bsv[SP], gsv[SP];               // beta_s and (scalar decay) g_s, wave-uniform
+  float egn = 1.f, gn = 0.f, bn = 0.f;  // e^{g_n} (scalar decay), g_n, beta_n (from LDS after the staging)
+  float bl = 0.f, ll = 0.f;             // wave 0, lane s: beta_s and (scalar decay) log alpha_s
   float gk[CHAN ? SP : 1];              // KDA: g_s of channel tid
   Raw<IO, KPL> kr[NG / 4];              // ring keys, row layout (slot 4 (wave + 4 gq) + row)
   Raw<IO, VR> vr[NG / 4];               // raw values
@@ -341,14 +342,13 @@ __global__ __launch_bounds__(256, 3) void update_kernel(const UpdateArgs a) {
   float bv[BQ];
   Vec<4> omv[OQ];
   if (flush) {
-    // every slot load is issued before any is used: slots past n re-read slot
-    // n (in bounds) and are masked afterwards, so no load waits on a branch
-    float lav[CHAN ? 1 : SP];
-#pragma unroll
-    for (int s = 0; s < SP; ++s) {
-      const size_t si = item * W + (s < n ? s : n);
-      bsv[s] = a.rbeta[si];
-      if constexpr (!CHAN) lav[s] = a.rla[si];
+    // per-slot scalars: lane s of wave 0 loads slot s; every slot load is
+    // issued before any is used (slots past n re-read slot n, in bounds, and
+    // are masked afterwards), so no load waits on a branch
+    if (tid < SP) {
+      const size_t si = item * W + (tid < n ? tid : n);
+      bl = a.rbeta[si];
+      if constexpr (!CHAN) ll = a.rla[si];
     }
     if constexpr (CHAN) {
       if (tid < K) {
@@ -356,26 +356,6 @@ __global__ __launch_bounds__(256, 3) void update_kernel(const UpdateArgs a) {
         for (int s = 0; s < SP; ++s) gk[s] = a.rla[(item * W + (s < n ? s : n)) * K + tid];
       }
     }
-    {
-      float acc = 0.f;  // g_s: running sum of the window's log alphas
-#pragma unroll
-      for (int s = 0; s < SP; ++s) {
-        if constexpr (!CHAN) {
-          acc += s <= n ? lav[s] : 0.f;
-          gsv[s] = s <= n ? acc : 0.f;
-        } else {
-          gsv[s] = 0.f;
-        }
-        bsv[s] = s <= n ? bsv[s] : 0.f;
-      }
-    }
-#pragma unroll
-    for (int s = 0; s < SP; ++s)
-      if (s == n) {
-        gn = gsv[s];
-        bn = bsv[s];
-      }
-    if constexpr (!CHAN) egn = fast_exp(gn);
 #pragma unroll
     for (int gq = 0; gq < NG / 4; ++gq) {
       const int s = 4 * (wave + 4 * gq) + row;
@@ -456,24 +436,9 @@ __global__ __launch_bounds__(256, 3) void update_kernel(const UpdateArgs a) {
       if (s <= n) {
 #pragma unroll
         for (int m = 0; m < KPL; ++m) ksv[m] = kr[gq].get(m);
-        {
-          // raw value: Mamba-2 scales it into c_s beta_s v_s; GDN/KDA keep it
-          // until the pseudo-values are formed
-          float sc = 1.f;
-          if constexpr (!ERASE) {
-            // select this row's slot from the wave-uniform tables (compile-time indices only)
-            float gs = 0.f, bs = 0.f;
+        // raw values (Mamba-2 scales them by beta_s c_s where they are used)
 #pragma unroll
-            for (int j = 0; j < SP; ++j)
-              if (j == s) {
-                gs = gsv[j];
-                bs = bsv[j];
-              }
-            sc = bs * fast_exp(gn - gs);
-          }
-#pragma unroll
-          for (int m = 0; m < VR; ++m) vsv[m] = sc * vr[gq].get(m);
-        }
+        for (int m = 0; m < VR; ++m) vsv[m] = vr[gq].get(m);
       }
 #pragma unroll
       for (int m = 0; m < KPL; m += 4)
@@ -483,13 +448,22 @@ __global__ __launch_bounds__(256, 3) void update_kernel(const UpdateArgs a) {
         *reinterpret_cast<float4*>(&Us[s * UP + col * VR + m]) = make_float4(vsv[m], vsv[m + 1], vsv[m + 2], vsv[m + 3]);
     }
     if (tid < K) qs[tid] = qv;
-    if constexpr (!CHAN) {
-      if (tid < SP) {
-        float c = 0.f;
+    if (tid < 64) {
+      // wave 0: beta_s, g_s = sum_{j<=s} log alpha_j (inclusive scan over the
+      // lanes) and c_s = e^{g_n - g_s}, slots past n zero
+      const int sl = tid;
+      const bool live = sl <= n && sl < SP;
+      float g = (!CHAN && live) ? ll : 0.f;
 #pragma unroll
-        for (int j = 0; j < SP; ++j)
-          if (j == tid && j <= n) c = fast_exp(gn - gsv[j]);
-        csc[tid] = c;
+      for (int d = 1; d < SP; d <<= 1) {
+        const float u = __shfl_up(g, d);
+        if (sl >= d) g += u;
+      }
+      const float gnn = __shfl(g, n);
+      if (sl < SP) {
+        bsl[sl] = live ? bl : 0.f;
+        gsl[sl] = live ? g : 0.f;
+        if constexpr (!CHAN) csc[sl] = live ? fast_exp(gnn - g) : 0.f;
       }
     }
     if constexpr (ERASE) {
@@ -501,6 +475,11 @@ __global__ __launch_bounds__(256, 3) void update_kernel(const UpdateArgs a) {
     }
   }
   lds_barrier();
+  if (flush) {  // the current slot's scalars, for every thread
+    gn = gsl[n];
+    bn = bsl[n];
+    if constexpr (!CHAN) egn = fast_exp(gn);
+  }
 
   if (flush) {
     if constexpr (ERASE) {
@@ -529,7 +508,7 @@ __global__ __launch_bounds__(256, 3) void update_kernel(const UpdateArgs a) {
         // (eq. wy with T^{-1} from the ring): independent sums, no recursion
         float xk[SP];
 #pragma unroll
-        for (int s = 0; s < SP; ++s) xk[s] = s < n ? bsv[s] * fast_exp(CHAN ? gk[s] : gsv[s]) * Ls[s * LP + kk] : 0.f;
+        for (int s = 0; s < SP; ++s) xk[s] = s < n ? bsl[s] * fast_exp(CHAN ? gk[s] : gsl[s]) * Ls[s * LP + kk] : 0.f;
 #pragma unroll
         for (int s = 0; s < SP; ++s) {
           pi[s] = 0.f;
@@ -562,7 +541,7 @@ __global__ __launch_bounds__(256, 3) void update_kernel(const UpdateArgs a) {
         const int v = tid - (256 - V);
         float xv[SP];
 #pragma unroll
-        for (int s = 0; s < SP; ++s) xv[s] = s < n ? bsv[s] * Us[s * UP + v] : 0.f;
+        for (int s = 0; s < SP; ++s) xv[s] = s < n ? bsl[s] * Us[s * UP + v] : 0.f;
 #pragma unroll
         for (int s = 0; s < SP; ++s) {
           if (s < n) {
@@ -643,7 +622,8 @@ __global__ __launch_bounds__(256, 3) void update_kernel(const UpdateArgs a) {
         for (int i = 0; i < 4; ++i) {
           const int s = 16 * st + 4 * lg + i;
           float w = Us[s * UP + v] - acc[i];
-          if constexpr (ERASE && !CHAN) w *= csc[s];  // GDN: c_s w_s
+          if constexpr (!ERASE) w *= bsl[s] * csc[s];     // Mamba-2: c_s beta_s v_s
+          if constexpr (ERASE && !CHAN) w *= csc[s];      // GDN: c_s w_s
           wv[st][i] = w;
         }
       }

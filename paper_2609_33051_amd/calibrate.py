@@ -256,3 +256,41 @@ def allocate(scores, tau_sk: float, full_cost: float, budget: float, iters: int 
 def allocation_budget(n_heads: int, mean_rank: float, tau_sk: float) -> float:
     """B = N Gbar tau_sk."""
     return n_heads * mean_rank * tau_sk
+
+
+@dataclass
+class LayerCalibration:
+    omega: np.ndarray      # [H][K][width] fp32, each head's leading `width` basis columns
+    coef: np.ndarray       # [H][width][K] fp32, the offline map of the full width
+    head_ranks: list       # per head: rank 1..width, or 0 = dense fallback
+    allocation: Allocation
+    scores: np.ndarray     # [H][width] the per-rank scores the allocation used
+
+
+def calibrate_layer(states, queries, width: int, mean_rank: float, W: int, erase: bool, grads=None,
+                    ) -> LayerCalibration:
+    """One layer's offline calibration in the decode path's layouts.
+
+    states [H][N][V][K] (stored S^T), queries [H][N][K] (effective queries),
+    grads [H][N][V] (output gradients) or None (then the gradient-free score
+    eps(G) of the allocation appendix is used).  The basis of each head is its
+    Omega* = E0^{-1/2} P_width; its columns are E0-orthonormal, so the
+    offline map of the first g columns is the first g rows of the stored map,
+    which is what a per-head rank table uses.  The allocation chooses, per
+    head, a rank in 1..min(G*, width) or the full state under the budget
+    H mean_rank tau_sk."""
+    X = np.asarray(states, np.float64)
+    q = np.asarray(queries, np.float64)
+    H, _, V, K = X.shape
+    A = min(max_rank(K, V, W, erase), width)
+    omegas = np.zeros((H, K, width))
+    coefs = np.zeros((H, width, K))
+    scores = np.zeros((H, A))
+    for h in range(H):
+        b = offline_basis(X[h], q[h], width)
+        omegas[h], coefs[h] = b.omega, b.coef
+        eps, J = rank_scores(X[h], q[h], b.omega, None if grads is None else grads[h])
+        scores[h] = (eps if J is None else J)[1:A + 1]
+    tau = tau_sketch(K, V, W, erase)
+    al = allocate(scores, tau, 4.0 * K * V, allocation_budget(H, mean_rank, tau))
+    return LayerCalibration(omegas.astype(np.float32), coefs.astype(np.float32), al.ranks, al, scores)

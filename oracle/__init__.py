@@ -51,6 +51,7 @@ class _Cfg(ctypes.Structure):
         ("sketch_bf16", ctypes.c_int32),
         ("pivots", ctypes.c_int32),
         ("ridge", ctypes.c_float),
+        ("paper_path", ctypes.c_int32),
     ]
 
 
@@ -171,14 +172,18 @@ class SketchResult:
 
 
 def sketchssm(kind, W, heads, omega, coef, S_init, q, k, v, beta, log_decay, round_storage=False,
-              diagnostics=True, lib=None, sketch_bf16=False, pivots=0, ridge=0.1):
+              diagnostics=True, lib=None, sketch_bf16=False, pivots=0, ridge=0.1, paper_path=False):
     """SketchSSM inference (Algorithm 1) in fp64.
 
     heads: [n] int, head index of every item (selects Omega / C); omega
     [H][K][G]; coef [H][G][K].  G = 0 (omega.shape[2] == 0) disables the
     sketch (o_state_hat is then 0 between flushes).  round_storage stores the
     state and the sketch as fp32; sketch_bf16 stores the sketch as bf16
-    (round to nearest, ties to even, through fp32), the paper's storage.
+    (round to nearest, ties to even, through fp32), the paper's storage, and
+    with it the projected erase factors f_s and the state-dependent map's
+    factors.  paper_path computes the coefficients through f_s (eq. wyread,
+    app-projected-query) and the map through its Woodbury factors (implied by
+    sketch_bf16; without rounding it equals the direct forms).
     pivots > 0 replaces the given coef by the state-dependent coefficient map
     with that many pivots and ridge term `ridge` (lambda), rebuilt from the
     state at the start and at every flush; coef_final returns the map in use
@@ -207,7 +212,7 @@ def sketchssm(kind, W, heads, omega, coef, S_init, q, k, v, beta, log_decay, rou
     U, Up = _out((n, V, G))
     Cf, Cfp = _out((n, G, K))
     cfg = _Cfg(KINDS[kind], n, K, V, G, int(W), T, 1 if round_storage else 0, 1 if sketch_bf16 else 0,
-               int(pivots), float(ridge))
+               int(pivots), float(ridge), 1 if paper_path else 0)
     rc = lib.orc_sketchssm(
         ctypes.byref(cfg),
         heads.ctypes.data_as(ctypes.POINTER(ctypes.c_int32)),

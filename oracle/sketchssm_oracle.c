@@ -25,8 +25,12 @@
  *     rounds the full state and the sketch to fp32 at the points where the
  *     method writes them back (the paper keeps the state in FP32 storage,
  *     Appendix "Detailed Evaluation Setup"), and `sketch_bf16`, which rounds
- *     the sketch to bf16 there instead (the paper's sketch storage, Appendix
- *     "State Memory Traffic Reduction"); arithmetic stays fp64.
+ *     to bf16 what the paper stores in BF16 (Appendix "State Memory Traffic
+ *     Reduction"): the sketch, the projected erase factors f_s and the
+ *     coefficient map; arithmetic stays fp64.  Those f_s and the map's factors
+ *     only exist on the `paper_path` (the paper's coefficient-space forms),
+ *     which bf16 storage therefore selects; without rounding it equals the
+ *     direct forms (pinned).
  *
  * Pins (see tests/test_oracle_pins.py): brute-force closed forms of the
  * recurrence on tiny inputs, the delta-rule retrieval invariant, the
@@ -52,9 +56,16 @@ typedef struct {
   int32_t W;             /* window: tokens applied per flush                */
   int32_t T;             /* decode steps                                    */
   int32_t round_storage; /* 1: state and sketch stored as fp32              */
-  int32_t sketch_bf16;   /* 1: sketch stored as bf16 (the paper's storage)  */
+  int32_t sketch_bf16;   /* 1: sketch, projected erase factors and map factors
+                            stored as bf16 (the paper's storage; implies
+                            paper_path)                                      */
   int32_t pivots;        /* 0: the given map C; P > 0: state-dependent map  */
   float ridge;           /* lambda of the state-dependent map               */
+  int32_t paper_path;    /* 1: coefficients through the projected erase
+                            factors f_s (eq. wyread, app-projected-query) and
+                            the state-dependent map through its Woodbury
+                            factors (the appendix's steps 3-4); 0: c = C q~
+                            and the map by a direct solve                     */
 } orc_cfg;
 
 /* Per-item views of the per-step inputs.  Step inputs are laid out
@@ -302,6 +313,70 @@ static void coef_map(const orc_cfg* c, int K, int V, int G, const double* S, con
       for (int a = 0; a < pq; ++a) acc += w->L[(size_t)i * pq + a] * w->L[(size_t)i2 * pq + a];
       w->Hh[(size_t)i * K + i2] = acc;
     }
+  if (c->paper_path || c->sketch_bf16) {
+    /* The appendix's steps 3-4: L_G = J^T L, D_G = Diag(J^T d) + lambda I,
+     * T_P = I + L_G^T D_G^{-1} L_G (Woodbury), so that
+     *   c = F1 (M q~) + F2 (Omega^T q~),  M = L^T R (pq x K),
+     *   F1 = D_G^{-1} L_G T_P^{-1},  F2 = (D_G + L_G L_G^T)^{-1} Diag(J^T d);
+     * the three factors are what is stored (bf16 with the paper's storage). */
+    const int p = pq;
+    double Tp[16], Ti[16], F1[1024 * 4], F2row[1024], Mrow[4][1024];
+    for (int a = 0; a < p; ++a)
+      for (int b = 0; b < p; ++b) {
+        double acc = (a == b) ? 1.0 : 0.0;
+        for (int g = 0; g < G; ++g) acc += w->L[(size_t)g * pq + a] * w->L[(size_t)g * pq + b] / (w->d[g] + lambda);
+        Tp[a * 4 + b] = acc;
+        Ti[a * 4 + b] = (a == b) ? 1.0 : 0.0;
+      }
+    for (int col = 0; col < p; ++col) { /* Gauss-Jordan, T_P is symmetric positive definite */
+      const double inv = 1.0 / Tp[col * 4 + col];
+      for (int j = 0; j < p; ++j) { Tp[col * 4 + j] *= inv; Ti[col * 4 + j] *= inv; }
+      for (int r = 0; r < p; ++r) {
+        if (r == col) continue;
+        const double f = Tp[r * 4 + col];
+        for (int j = 0; j < p; ++j) { Tp[r * 4 + j] -= f * Tp[col * 4 + j]; Ti[r * 4 + j] -= f * Ti[col * 4 + j]; }
+      }
+    }
+    for (int g = 0; g < G; ++g)
+      for (int a = 0; a < p; ++a) {
+        double acc = 0.0;
+        for (int b = 0; b < p; ++b) acc += w->L[(size_t)g * pq + b] * Ti[b * 4 + a];
+        F1[g * 4 + a] = acc / (w->d[g] + lambda);
+      }
+    for (int a = 0; a < p; ++a)
+      for (int kk = 0; kk < K; ++kk) {
+        double acc = 0.0;
+        for (int i = 0; i < K; ++i) acc += w->L[(size_t)i * pq + a] * w->R[(size_t)i * K + kk];
+        Mrow[a][kk] = acc;
+      }
+    if (c->sketch_bf16) {
+      for (int g = 0; g < G; ++g)
+        for (int a = 0; a < p; ++a) F1[g * 4 + a] = bf16_rne(F1[g * 4 + a]);
+      for (int a = 0; a < p; ++a)
+        for (int kk = 0; kk < K; ++kk) Mrow[a][kk] = bf16_rne(Mrow[a][kk]);
+    }
+    for (int g = 0; g < G; ++g) {
+      /* row g of F2 = e_g^T (D_G^{-1} - D_G^{-1} L_G T_P^{-1} L_G^T D_G^{-1}) Diag(J^T d) */
+      for (int g2 = 0; g2 < G; ++g2) {
+        double corr = 0.0;
+        for (int a = 0; a < p; ++a) {
+          double la = 0.0;  /* (F1 unrounded) row g times L_G row g2 */
+          for (int b = 0; b < p; ++b) la += w->L[(size_t)g * pq + b] * Ti[b * 4 + a];
+          corr += la / (w->d[g] + lambda) * w->L[(size_t)g2 * pq + a];
+        }
+        const double dg2 = w->d[g2];
+        F2row[g2] = ((g == g2 ? 1.0 : 0.0) / (w->d[g] + lambda) - corr / (w->d[g2] + lambda)) * dg2;
+        if (c->sketch_bf16) F2row[g2] = bf16_rne(F2row[g2]);
+      }
+      for (int kk = 0; kk < K; ++kk) {
+        double acc = 0.0;
+        for (int a = 0; a < p; ++a) acc += F1[g * 4 + a] * Mrow[a][kk];
+        for (int g2 = 0; g2 < G; ++g2) acc += F2row[g2] * (double)Om[(size_t)kk * G + g2];
+        Cm[(size_t)g * K + kk] = acc;
+      }
+    }
+    return;
+  }
   /* A = J^T Hhat J + lambda I (G x G);  B = J^T Hhat R (G x K) */
   for (int g = 0; g < G; ++g) {
     for (int g2 = 0; g2 < G; ++g2) w->A[(size_t)g * G + g2] = w->Hh[(size_t)g * K + g2] + (g == g2 ? lambda : 0.0);
@@ -425,8 +500,10 @@ int orc_sketchssm(const orc_cfg* c, const int32_t* heads, const float* omega, co
                   double* S_final, double* U_final, double* coef_final)
 {
   if (!c || c->K <= 0 || c->V <= 0 || c->n_items <= 0 || c->T < 0 || c->W < 1 || c->G < 0) return -1;
-  if (c->K > 1024 || c->V > 1024 || c->G > 1024) return -1;
+  if (c->K > 1024 || c->V > 1024 || c->G > 1024 || c->pivots < 0 || c->pivots > 4) return -1;
   const int K = c->K, V = c->V, G = c->G, NI = c->n_items, W = c->W;
+  const int fpath = (c->paper_path || c->sketch_bf16) && has_erase(c) && G > 0;
+  if (fpath && W > 64) return -1;
   int err = 0;
 #pragma omp parallel for schedule(dynamic, 1)
   for (int i = 0; i < NI; ++i) {
@@ -444,9 +521,10 @@ int orc_sketchssm(const orc_cfg* c, const int32_t* heads, const float* omega, co
     }
     double* tmp = (double*)malloc(sizeof(double) * (size_t)(K + V));
     int* buf = (int*)malloc(sizeof(int) * (size_t)W);
-    if (!S0 || !U || !tmp || !buf) {
+    double* fhat = (double*)malloc(sizeof(double) * (size_t)W * (G > 0 ? G : 1)); /* stored f_s of the window */
+    if (!S0 || !U || !tmp || !buf || !fhat) {
       err = -2;
-      free(S0); free(U); free(tmp); free(buf);
+      free(S0); free(U); free(tmp); free(buf); free(fhat);
       continue;
     }
     orc_tok t = {c, i, q, k, v, beta, log_decay};
@@ -470,13 +548,66 @@ int orc_sketchssm(const orc_cfg* c, const int32_t* heads, const float* omega, co
         /* exact state read and sketch read */
         read_state(K, V, S0, x, ostate);
         for (int j = 0; j < V; ++j) ohat[j] = 0.0;
-        if (G > 0) {
+        if (fpath) {
+          /* coefficient space (eq. app-projected-query, with f_s from eq. wyread):
+           *   f_t = beta_t (C (d_[t] . k_t) - sum_{j<t} f_j <l_j(t), k_t>)
+           *   c_t = C (d_[t] . q_t) - sum_{s<t} f_s <l_s(t), q_t> - f_t <k_t, q_t>
+           * with l_j(t) = D_t ... D_{j+1} k_j and d_[t] the decay product of the
+           * window so far; each f_s is stored (bf16 with the paper's storage)
+           * when formed, and later steps use the stored value */
+          const int cur = len - 1, tn = buf[cur];
+          const float* kt = tok_k(&t, tn);
+          double dq[1024], dk[1024], aq[64], ak[64];
+          for (int kk = 0; kk < K; ++kk) {
+            dq[kk] = (double)qn[kk];
+            dk[kk] = (double)kt[kk];
+          }
+          for (int s = 0; s < len; ++s)
+            for (int kk = 0; kk < K; ++kk) {
+              const double dd = tok_decay(&t, buf[s], kk);
+              dq[kk] *= dd;
+              dk[kk] *= dd;
+            }
+          for (int j = 0; j < cur; ++j) {
+            const float* kj = tok_k(&t, buf[j]);
+            for (int kk = 0; kk < K; ++kk) y[kk] = (double)kj[kk];
+            for (int r = j + 1; r <= cur; ++r)
+              for (int kk = 0; kk < K; ++kk) y[kk] *= tok_decay(&t, buf[r], kk);
+            double sq = 0.0, sk = 0.0;
+            for (int kk = 0; kk < K; ++kk) {
+              sq += y[kk] * (double)qn[kk];
+              sk += y[kk] * (double)kt[kk];
+            }
+            aq[j] = sq;
+            ak[j] = sk;
+          }
+          double akq = 0.0;
+          for (int kk = 0; kk < K; ++kk) akq += (double)kt[kk] * (double)qn[kk];
+          const double bt = tok_beta(&t, tn);
+          for (int g = 0; g < G; ++g) {
+            double cq = 0.0, ck = 0.0;
+            for (int kk = 0; kk < K; ++kk) {
+              const double cg = Cmi ? Cmi[(size_t)g * K + kk] : (double)Cm[(size_t)g * K + kk];
+              cq += cg * dq[kk];
+              ck += cg * dk[kk];
+            }
+            for (int j = 0; j < cur; ++j) {
+              ck -= fhat[(size_t)j * G + g] * ak[j];
+              cq -= fhat[(size_t)j * G + g] * aq[j];
+            }
+            const double ft = bt * ck;
+            cvec[g] = cq - ft * akq;
+            fhat[(size_t)cur * G + g] = c->sketch_bf16 ? bf16_rne(ft) : ft;
+          }
+        } else if (G > 0) {
           for (int g = 0; g < G; ++g) {
             double acc = 0.0;
             for (int kk = 0; kk < K; ++kk)
               acc += (Cmi ? Cmi[(size_t)g * K + kk] : (double)Cm[(size_t)g * K + kk]) * x[kk];
             cvec[g] = acc;
           }
+        }
+        if (G > 0) {
           for (int j = 0; j < V; ++j) {
             double acc = 0.0;
             for (int g = 0; g < G; ++g) acc += U[(size_t)j * G + g] * cvec[g];
@@ -529,7 +660,7 @@ int orc_sketchssm(const orc_cfg* c, const int32_t* heads, const float* omega, co
     }
     if (statedep) cmap_work_free(&cw);
     free(Cmi);
-    free(S0); free(U); free(tmp); free(buf);
+    free(S0); free(U); free(tmp); free(buf); free(fhat);
   }
   return err;
 }

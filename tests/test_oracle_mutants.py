@@ -59,6 +59,17 @@ def pins_hold(lib) -> bool:
     Si = np.random.default_rng(4).standard_normal((2, 7, 5)).astype(np.float32)
     if not np.allclose(coef_map_of(Si, eye, 3, 1e-9, lib=lib), np.broadcast_to(np.eye(5), (2, 5, 5)), atol=1e-6):
         return False
+    # the paper's coefficient-space forms (f_s, Woodbury factors) equal the direct ones
+    for kind in ("gdn", "kda"):
+        for piv in (0, 4):
+            S0p, qp, kp, vp, bp, lp = tiny_inputs(kind, n=3, K=8, V=6, T=13, seed=21)
+            omp, Cp = heads_omega(1, 8, 5, seed=9)
+            z3 = np.zeros(3, np.int32)
+            a = oracle.sketchssm(kind, 5, z3, omp, Cp, S0p, qp, kp, vp, bp, lp, pivots=piv, lib=lib)
+            b = oracle.sketchssm(kind, 5, z3, omp, Cp, S0p, qp, kp, vp, bp, lp, pivots=piv, paper_path=True, lib=lib)
+            tol = 1e-6 if piv else 1e-10
+            if not np.allclose(b.o, a.o, rtol=tol, atol=tol * np.abs(a.o).max()):
+                return False
     # the sketch must be refreshed from the updated state at each flush
     r = oracle.sketchssm("mamba2", 2, np.zeros(n, np.int32), om, C, S0, q_in, k, v, beta, logd, lib=lib)
     Uref = np.einsum("nvk,kg->nvg", r.S_final, om[0].astype(np.float64))
@@ -103,6 +114,16 @@ MUTANTS = {
                                  "acc += S[(size_t)kk * V + j] * (double)omega[(size_t)g * K + kk];")],
     "kda_channel_index": [("[((size_t)n * c->n_items + t->item) * c->K + kk]",
                            "[((size_t)n * c->n_items + t->item) * c->K + (c->K - 1 - kk)]")],
+    "wyread_drops_history": [("              ck -= fhat[(size_t)j * G + g] * ak[j];\n", "")],
+    "wyread_drops_beta": [("            const double ft = bt * ck;", "            const double ft = ck;")],
+    "projected_query_drops_self_term": [("            cvec[g] = cq - ft * akq;", "            cvec[g] = cq;")],
+    "left_factor_decay_off_by_one": [("            for (int r = j + 1; r <= cur; ++r)", "            for (int r = j; r <= cur; ++r)")],
+    "woodbury_F2_sign": [("- corr / (w->d[g2] + lambda)) * dg2;", "+ corr / (w->d[g2] + lambda)) * dg2;")],
+    "woodbury_F1_without_T_inverse": [
+        ("        for (int b = 0; b < p; ++b) acc += w->L[(size_t)g * pq + b] * Ti[b * 4 + a];\n"
+         "        F1[g * 4 + a] = acc / (w->d[g] + lambda);",
+         "        for (int b = 0; b < p; ++b) acc += (a == b) ? w->L[(size_t)g * pq + b] : 0.0;\n"
+         "        F1[g * 4 + a] = acc / (w->d[g] + lambda);")],
     "sketch_not_refreshed": [("        if (G > 0) {\n          make_sketch(K, V, G, S0, Om, U);\n"
                               "          if (statedep && Cmi && cw.R) coef_map(c, K, V, G, S0, Om, U, Cmi, &cw);\n"
                               "          store_sketch(c, U, (size_t)V * G);\n        }\n"

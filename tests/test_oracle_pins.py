@@ -355,3 +355,44 @@ def test_coef_map_pivots_are_the_leading_sketch_columns():
     assert np.allclose(moved, base[:, perm], rtol=1e-6, atol=1e-7)  # Omega orthonormal to fp32 only
     other = np.array([2, 0, 1, 3, 4, 5])  # a different pair leads: the map must change
     assert not np.allclose(coef_map_of(S, np.ascontiguousarray(om[:, :, other]), p, 0.1), base[:, other], atol=1e-6)
+
+
+# --- the paper's coefficient-space forms and BF16 storage of f and the map -----------------------------
+@pytest.mark.parametrize("kind", KINDS)
+@pytest.mark.parametrize("pivots", [0, 4])
+def test_paper_path_equals_the_direct_forms(kind, pivots):
+    """c_t through the projected erase factors (eq. app-projected-query with
+    eq. wyread) equals C q~_t, and the state-dependent map through its
+    Woodbury factors (the appendix's steps 3-4) equals the direct solve of
+    eq. pivot-ridge, when nothing is rounded."""
+    S0, q, k, v, beta, logd = tiny_inputs(kind, n=3, K=8, V=6, T=13, seed=21)
+    heads = np.zeros(3, np.int32)
+    om, C = heads_omega(1, 8, 5, seed=9)
+    a = oracle.sketchssm(kind, 5, heads, om, C, S0, q, k, v, beta, logd, pivots=pivots, ridge=0.1)
+    b = oracle.sketchssm(kind, 5, heads, om, C, S0, q, k, v, beta, logd, pivots=pivots, ridge=0.1, paper_path=True)
+    # the factor form applies the stored Omega^T, the direct solve its exactly
+    # orthonormal completion: Omega is fp32, orthonormal to about 1e-7
+    tol = 1e-6 if pivots else 1e-10
+    np.testing.assert_allclose(b.o, a.o, rtol=tol, atol=tol * np.abs(a.o).max())
+    np.testing.assert_allclose(b.coef_final, a.coef_final, rtol=tol, atol=tol * np.abs(a.coef_final).max())
+    np.testing.assert_array_equal(b.S_final, a.S_final)
+
+
+@pytest.mark.parametrize("kind,pivots", [("gdn", 0), ("kda", 0), ("mamba2", 4), ("gdn", 4)])
+def test_paper_storage_rounds_f_and_the_map_factors(kind, pivots):
+    """BF16 storage of f_s and of the map's factors moves the sketch read by a
+    bf16-sized amount beyond what rounding the sketch alone does, and leaves
+    the flush exact."""
+    import torch
+
+    S0, q, k, v, beta, logd = tiny_inputs(kind, n=3, K=8, V=6, T=13, seed=22)
+    heads = np.zeros(3, np.int32)
+    om, C = heads_omega(1, 8, 5, seed=10)
+    ref = oracle.sketchssm(kind, 5, heads, om, C, S0, q, k, v, beta, logd, pivots=pivots, paper_path=True)
+    bf = oracle.sketchssm(kind, 5, heads, om, C, S0, q, k, v, beta, logd, pivots=pivots, sketch_bf16=True)
+    rel = np.linalg.norm(bf.o - ref.o) / np.linalg.norm(ref.o)
+    assert 1e-5 < rel < 3e-2
+    np.testing.assert_allclose(bf.o_exact_windowed, ref.o_exact_windowed, rtol=1e-12, atol=1e-12)
+    if pivots:  # the map in use is built from bf16 factors: close to, not equal to, the fp64 one
+        d = np.abs(bf.coef_final - ref.coef_final).max() / np.abs(ref.coef_final).max()
+        assert 1e-5 < d < 2e-2

@@ -79,7 +79,9 @@ typedef struct {
   int32_t rank;     /* r sketch columns (the paper's G)                     */
   int32_t window;   /* W tokens per window = ring capacity                  */
   int32_t io_dtype; /* skssm_dtype of q, k, v and ring.k / ring.v           */
-  int32_t sketch_dtype; /* skssm_dtype of U (0 = fp32; BF16 halves its read) */
+  int32_t sketch_dtype; /* skssm_dtype of U, ring.f and cmap (0 = fp32; BF16, the
+                           paper's storage, halves their reads; rounded to nearest
+                           even when stored)                                        */
   int32_t pivots;   /* 0: the coefficient map is `coef` (offline, shared per head);
                        4: state-dependent map with P = 4 pivots, rebuilt from the
                        state by every sketchssm_update into `cmap` (rank 8..32)   */
@@ -108,8 +110,10 @@ typedef struct {
  *     is one contiguous block, so a read fetches four consecutive slots per
  *     load instruction and the flush stages the window in one sweep;
  *   - derived fields (f, pi, tinv), written by each read for its own
- *     slot, are slot-major, field[W][B][H][...]: one step's writes for all
- *     items form one contiguous region of whole cache lines.
+ *     slot, are slot-major and head-major within a slot, field[W][H][B][...]:
+ *     one step's writes for all items form one contiguous region, and the
+ *     items one head's reads touch together (consecutive requests) are
+ *     adjacent, so they cover whole cache lines.
  *
  * Raw update inputs of token s are written into slot s by the token's
  * producer (the layer's projections) before the call that consumes it;
@@ -143,9 +147,9 @@ typedef struct {
   const void* v;          /* [B][H][W][V] io_dtype raw values (producer)            all kinds */
   const float* beta;      /* [B][H][W] write gates (producer)                       all kinds */
   const float* log_decay; /* [B][H][W] (MAMBA2, GDN) or [B][H][W][K] (KDA), <= 0 (producer) */
-  float* f;               /* [W][B][H][rank] projected erase factors   GDN, KDA (sketch read) */
-  float* pi;              /* [W][B][H][K] erase factors                GDN, KDA (baseline)    */
-  float* tinv;            /* [W][B][H][W]: slot s holds (T^{-1})_{s,j}, j < s      GDN, KDA  */
+  void* f;                /* [W][H][B][rank] projected erase factors, sketch_dtype   GDN, KDA (sketch read) */
+  float* pi;              /* [W][H][B][K] erase factors                GDN, KDA (baseline)    */
+  float* tinv;            /* [W][H][B][W]: slot s holds (T^{-1})_{s,j}, j < s      GDN, KDA  */
 } skssm_ring;
 
 /*
@@ -170,7 +174,7 @@ typedef struct {
  *        tinv (GDN, KDA) of slots 0..n_buffered-1.
  * q      [B][H][K] io_dtype, the current query.
  * U      [B][H][rank/P][V][P] output in cfg.sketch_dtype, panel layout (may be NULL when rank == 0).
- * cmap   cfg.pivots = 4: [B][H][4K + 4 rank + rank^2] fp32 output, the
+ * cmap   cfg.pivots = 4: [B][H][4K + 4 rank + rank^2] output in cfg.sketch_dtype, the
  *        state-dependent coefficient map of Sec. 4.1 (eq. m-coeff with the
  *        ridge term and the P = 4 low-rank-plus-diagonal state metric of the
  *        appendix on the coefficient map), built from S_W and U and stored
@@ -180,7 +184,7 @@ typedef struct {
  * rank may be 0 here (no sketch: the flush of the exact baseline).
  */
 int sketchssm_update(const skssm_config* cfg, float* S, const float* omega, const skssm_ring* ring,
-                     int32_t n_buffered, const void* q, void* U, float* cmap, float* o, void* stream);
+                     int32_t n_buffered, const void* q, void* U, void* cmap, float* o, void* stream);
 
 /*
  * sketchssm_decode -- non-flush step (Algorithm 1, t < W) for the token in
@@ -202,7 +206,7 @@ int sketchssm_update(const skssm_config* cfg, float* S, const float* omega, cons
  * Omega^T.  q [B][H][K] io_dtype; o [B][H][V] fp32.  rank must be > 0,
  * window >= 2.
  */
-int sketchssm_decode(const skssm_config* cfg, const void* U, const float* coef, const float* cmap, const float* S,
+int sketchssm_decode(const skssm_config* cfg, const void* U, const float* coef, const void* cmap, const float* S,
                      const skssm_ring* ring, int32_t n_buffered, const void* q, float* o, void* stream);
 
 /*

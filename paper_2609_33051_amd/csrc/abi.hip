@@ -154,7 +154,7 @@ const char* sketchssm_last_error(void) { return g_err; }
 int sketchssm_check_config(const skssm_config* cfg) { return check_shape(cfg, true, false); }
 
 int sketchssm_update(const skssm_config* cfg, float* S, const float* omega, const skssm_ring* ring,
-                     int32_t n_buffered, const void* q, void* U, float* cmap, float* o, void* stream) {
+                     int32_t n_buffered, const void* q, void* U, void* cmap, float* o, void* stream) {
   int rc = check_shape(cfg, true, true);
   if (rc) return rc;
   Ranks rk;
@@ -214,7 +214,7 @@ int sketchssm_update(const skssm_config* cfg, float* S, const float* omega, cons
   return launched(r, "sketchssm_update");
 }
 
-int sketchssm_decode(const skssm_config* cfg, const void* U, const float* coef, const float* cmap, const float* S,
+int sketchssm_decode(const skssm_config* cfg, const void* U, const float* coef, const void* cmap, const float* S,
                      const skssm_ring* ring, int32_t n_buffered, const void* q, float* o, void* stream) {
   int rc = check_shape(cfg, true, false);
   if (rc) return rc;

@@ -2,7 +2,8 @@
 //
 // Replay buffer (ring): slot s of item i (= b*H + h) of a field of width w
 // sits at field + (i * W + s) * w for the raw inputs (item-major) and at
-// field + (s * B*H + i) * w for the derived fields (slot-major).
+// field + (s * B*H + h * B + b) * w for the derived fields (slot-major,
+// head-major within a slot).
 // Raw inputs of token s (k, v, beta, log decay) are written into slot s by
 // the producer of the token; the kernels derive and store the rest.
 #pragma once
@@ -25,15 +26,15 @@ struct DecodeArgs {
   const void* q;                  // [B][H][K] io, current query
   const void* U;                  // [B][H][R/P][V][P], P = 4 (fp32) or 8 (bf16)  (sketch read)
   const float* coef;              // [H][R][K]           (sketch read; Omega^T with a pivot map)
-  const float* cmap;              // [B][H][4K + 4R + R*R] pivot map factors M, F1, F2 (or NULL)
+  const void* cmap;               // [B][H][4K + 4R + R*R] pivot map factors M, F1, F2, sketch dtype (or NULL)
   const float* S;                 // [B][H][V][K]        (exact baseline)
   const void* rk;                 // ring [B][H][W][K] io      raw keys
   const void* rv;                 // ring [B][H][W][V] io      raw values
   const float* rbeta;             // ring [B][H][W]            write gates
   const float* rla;               // ring [B][H][W] or [..][K] log decays
-  float* rf;                      // ring [W][B][H][R]  projected erase factors (GDN/KDA sketch read)
-  float* rpi;                     // ring [W][B][H][K]  erase factors (GDN/KDA baseline)
-  float* rt;                      // ring [W][B][H][W]  rows of T^{-1} (GDN/KDA)
+  void* rf;                       // ring [W][H][B][R]  projected erase factors, sketch dtype (GDN/KDA sketch read)
+  float* rpi;                     // ring [W][H][B][K]  erase factors (GDN/KDA baseline)
+  float* rt;                      // ring [W][H][B][W]  rows of T^{-1} (GDN/KDA)
   float* o;                       // [B][H][V]
 };
 
@@ -51,7 +52,7 @@ struct UpdateArgs {
   const float* rla;
   const float* rt;                // GDN/KDA rows of T^{-1}, slots < n
   void* U;                        // [B][H][R/P][V][P], P = 4 (fp32) or 8 (bf16), or NULL
-  float* cmap;                    // [B][H][4K + 4R + R*R] state-dependent coefficient map (pivots), or NULL
+  void* cmap;                     // [B][H][4K + 4R + R*R] state-dependent map factors, sketch dtype, or NULL
   float ridge;                    // its lambda
   float* o;                       // [B][H][V] or NULL
 };

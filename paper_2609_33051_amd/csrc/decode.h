@@ -61,10 +61,11 @@ struct RowLoads {
   // `item` is wave-uniform.  Slot s of a raw ring field (k, v, beta, log
   // alpha) of width w sits at field + (item * W + s) * w, the W slots of an
   // item contiguous; slot s of a derived field (f, pi, rows of T^{-1}) at
-  // field + (s * B*H + item) * w, one slot of all items contiguous.
+  // field + (s * B*H + derived_pos(item)) * w, one slot of all items
+  // contiguous, head-major within the slot.
   __device__ __forceinline__ void load(const DecodeArgs& a, size_t item, int row, int col) {
     const int n = a.n;
-    const size_t W = (size_t)a.W, NI = (size_t)a.B * a.H;
+    const size_t W = (size_t)a.W, NI = (size_t)a.B * a.H, dp = derived_pos(item, a.B, a.H);
     if constexpr (ERASE) {
       // rows of T^{-1}: issued first and without branches (row and column
       // clamped into the ring, masked below), so they share the first wait
@@ -72,7 +73,7 @@ struct RowLoads {
 #pragma unroll
       for (int gi = 0; gi < NG; ++gi) {
         const int s = 4 * gi + row;
-        const size_t rs = ((size_t)(s < smax ? s : smax) * NI + item) * W;
+        const size_t rs = ((size_t)(s < smax ? s : smax) * NI + dp) * W;
 #pragma unroll
         for (int p = 0; p < JP; ++p) {
           const int j = col + 16 * p;
@@ -298,7 +299,7 @@ __device__ __forceinline__ void append_derived(const DecodeArgs& a, size_t item,
   if constexpr (L::ERASE) {
     const int n = a.n;
     if (row == 0) {
-      float* dst = a.rt + ((size_t)n * a.B * a.H + item) * a.W;
+      float* dst = a.rt + ((size_t)n * a.B * a.H + derived_pos(item, a.B, a.H)) * a.W;
 #pragma unroll
       for (int p = 0; p < L::JP; ++p) {
         const int j = col + 16 * p;
@@ -327,7 +328,7 @@ __device__ __forceinline__ void full_read_item(const DecodeArgs& a, size_t item,
   r.load(a, item, row, col);
   float ps[ERASE ? NG : 1][KPL];     // ring pi of slot 4 gi + row (row layout)
   if constexpr (ERASE) {
-    const size_t rowder = (size_t)row * NI + item;
+    const size_t rowder = (size_t)row * NI + derived_pos(item, a.B, a.H);
 #pragma unroll
     for (int gi = 0; gi < NG; ++gi) {
       const int s = 4 * gi + row;
@@ -411,7 +412,7 @@ __device__ __forceinline__ void full_read_item(const DecodeArgs& a, size_t item,
       Vec<KPL> t;
 #pragma unroll
       for (int m = 0; m < KPL; ++m) t.e[m] = pit[m];
-      t.store(a.rpi + ((size_t)n * NI + item) * K + koff);
+      t.store(a.rpi + ((size_t)n * NI + derived_pos(item, a.B, a.H)) * K + koff);
     }
   }
 }
@@ -479,33 +480,62 @@ __global__ __launch_bounds__(256) void decode_kernel(const DecodeArgs a) {
     if ((CQ * 256 == R * K / 4 || i < R * K / 4) && (4 * i) / K < rh) cv[c].load(a.coef + (size_t)h * R * K + 4 * i);
   }
   compiler_fence();
+  // Every load of the item follows, without branches: a wave past the batch
+  // reads item 0 of its head (and returns after the barrier), slots and
+  // panels past what the step uses are clamped to ones that exist and the
+  // values masked by selects.  A guarded load becomes a branch whose join
+  // waits for the loads in flight, which serialises the item's memory
+  // accesses.
   L r;
+  r.load(a, item, row, col);
   float fs[ERASE ? NG : 1][RP];      // ring f of slot 4 gi + row, component col + 16 p
-  Raw<SK, PW> Ur[VPL][UP];           // sketch panels (value layout)
-  if (valid) {
-    r.load(a, item, row, col);
-    if constexpr (ERASE) {
-      const size_t NI = (size_t)a.B * H;
-      const size_t rowder = (size_t)row * NI + item;
+  if constexpr (ERASE) {
+    const size_t NI = (size_t)a.B * H, dp = derived_pos(item, a.B, H);
+    const int smax = n > 0 ? n - 1 : 0;
 #pragma unroll
-      for (int gi = 0; gi < NG; ++gi) {
-        const int s = 4 * gi + row;
-        const float* fp = a.rf + (rowder + (size_t)(4 * gi) * NI) * R;
+    for (int gi = 0; gi < NG; ++gi) {
+      const int s = 4 * gi + row;
+      const SK* fp = static_cast<const SK*>(a.rf) + ((size_t)(s < smax ? s : smax) * NI + dp) * R;
 #pragma unroll
-        for (int p = 0; p < RP; ++p) {
-          const int j = col + 16 * p;
-          fs[gi][p] = (4 * gi < n && s < n && j < rh) ? fp[j] : 0.f;
+      for (int p = 0; p < RP; ++p) {
+        const int j = col + 16 * p;
+        float fv;
+        if constexpr (sizeof(SK) == 2) {  // bf16: lanes j and j^1 read the same 32-bit word
+          const uint32_t w = reinterpret_cast<const uint32_t*>(fp)[j >> 1];
+          fv = (j & 1) ? bf16_hi(w) : bf16_lo(w);
+        } else {
+          fv = ld_elem<SK>(fp + j);
         }
+        fs[gi][p] = (s < n && j < rh) ? fv : 0.f;
       }
     }
-    if constexpr (U_PRELOAD) {
+  }
+  Raw<SK, PW> Ur[VPL][UP];           // sketch panels (value layout); panels past the rank re-read panel 0
+  if constexpr (U_PRELOAD) {
 #pragma unroll
-      for (int p = 0; p < NP; ++p)
+    for (int p = 0; p < NP; ++p)
 #pragma unroll
-        for (int vv = 0; vv < VPL; ++vv) {
-          Ur[vv][p].zero();
-          if (p * PW < rh) Ur[vv][p].load_nt(Ub + (uint32_t)((p * V + lane + 64 * vv) * PW));
-        }
+      for (int vv = 0; vv < VPL; ++vv) {
+        const int pp = p * PW < rh ? p : 0;
+        Ur[vv][p].load_nt(Ub + (uint32_t)((pp * V + lane + 64 * vv) * PW));
+        Ur[vv][p].keep_if(p * PW < rh);
+      }
+  }
+  // the item's state-dependent map factors (M, F1, F2; P > 0): this lane's
+  // channels of M and, for its sketch columns, its part of an F2 row and its F1 row
+  constexpr int MW = P > 0 ? K / 16 : 1, HQ = P > 0 ? R / 4 : 1;
+  [[maybe_unused]] Raw<SK, MW> mr;
+  [[maybe_unused]] Raw<SK, HQ> f2r[RP];
+  [[maybe_unused]] Raw<SK, 4> f1r[RP];
+  if constexpr (P > 0) {
+    const SK* cm = static_cast<const SK*>(a.cmap) + item * (size_t)(P * K + R * P + R * R);
+    mr.load_nt(cm + (col >> 2) * K + ((col & 3) + 4 * row) * MW);
+#pragma unroll
+    for (int p = 0; p < RP; ++p) {
+      const int j = col + 16 * p;
+      f2r[p].load_nt(cm + P * K + R * P + j * R + row * HQ);
+      f2r[p].keep_if(row * HQ < rh);  // columns of F2 past the head's rank are not read
+      f1r[p].load(cm + P * K + j * P);
     }
   }
 
@@ -582,16 +612,12 @@ __global__ __launch_bounds__(256) void decode_kernel(const DecodeArgs a) {
     // state-dependent map C = F1 M + F2 Omega^T (coef holds Omega^T): C x =
     // F1 (M x) + F2 (Omega^T x) for x = e^g . q and x = e^g . k
     static_assert(P == 4 && R <= 32, "pivot maps: P = 4, rank up to 32");
-    const float* cm = a.cmap + item * (size_t)(P * K + R * P + R * R);
-    constexpr int CW = K / 16;                      // channels per lane of M x
-    const int pa = col >> 2, ch = ((col & 3) + 4 * row) * CW;
-    Vec<CW> mr;
-    mr.load_nt(cm + pa * K + ch);
+    const int ch = ((col & 3) + 4 * row) * MW;     // MW channels per lane of M x
     float mq = 0.f, mk = 0.f;
 #pragma unroll
-    for (int m = 0; m < CW; ++m) {
-      mq += mr.e[m] * xq_l[ch + m];
-      if constexpr (ERASE) mk += mr.e[m] * xk_l[ch + m];
+    for (int m = 0; m < MW; ++m) {
+      mq += mr.get(m) * xq_l[ch + m];
+      if constexpr (ERASE) mk += mr.get(m) * xk_l[ch + m];
     }
     mq = cross_row_sum(quad_sum(mq));               // lanes with col / 4 = a hold (M x)[a]
     if constexpr (ERASE) mk = cross_row_sum(quad_sum(mk));
@@ -613,25 +639,21 @@ __global__ __launch_bounds__(256) void decode_kernel(const DecodeArgs a) {
       }
     }
     wave_lds_sync();
-    constexpr int HQ = R / 4;                       // F2 columns per row of lanes
 #pragma unroll
     for (int p = 0; p < RP; ++p) {
       const int j = col + 16 * p;
       float cq = 0.f, ck = 0.f;
-      if (j < rh) {  // rows and columns of F2 past the head's rank are zero and not read
-        Vec<HQ> f2;
-#pragma unroll
-        for (int m = 0; m < HQ; ++m) f2.e[m] = 0.f;
-        if (row * HQ < rh) f2.load_nt(cm + P * K + R * P + j * R + row * HQ);
+      if (j < rh) {  // rows of F1 and F2 past the head's rank are not used (HQ columns of F2 per row of lanes)
+        const Raw<SK, HQ>& f2 = f2r[p];
 #pragma unroll
         for (int m = 0; m < HQ; ++m) {
-          cq += f2.e[m] * xq_l[row * HQ + m];
-          if constexpr (ERASE) ck += f2.e[m] * xk_l[row * HQ + m];
+          cq += f2.get(m) * xq_l[row * HQ + m];
+          if constexpr (ERASE) ck += f2.get(m) * xk_l[row * HQ + m];
         }
         if (row == 0) {
-          const float4 f1 = *reinterpret_cast<const float4*>(cm + P * K + j * P);
-          cq += f1.x * mqa[0] + f1.y * mqa[1] + f1.z * mqa[2] + f1.w * mqa[3];
-          if constexpr (ERASE) ck += f1.x * mka[0] + f1.y * mka[1] + f1.z * mka[2] + f1.w * mka[3];
+          const Raw<SK, 4>& f1 = f1r[p];
+          cq += f1.get(0) * mqa[0] + f1.get(1) * mqa[1] + f1.get(2) * mqa[2] + f1.get(3) * mqa[3];
+          if constexpr (ERASE) ck += f1.get(0) * mka[0] + f1.get(1) * mka[1] + f1.get(2) * mka[2] + f1.get(3) * mka[3];
         }
       }
       sqv[p] = cross_row_sum(cq);
@@ -688,10 +710,24 @@ __global__ __launch_bounds__(256) void decode_kernel(const DecodeArgs a) {
   append_derived<L>(a, item, row, col, r, gcol);
   if constexpr (ERASE) {
     if (row == 0) {
-      const size_t sl = (size_t)n * a.B * H + item;
+      const size_t sl = (size_t)n * a.B * H + derived_pos(item, a.B, H);
 #pragma unroll
-      for (int p = 0; p < RP; ++p)
-        if (col + 16 * p < rh) a.rf[sl * R + col + 16 * p] = ft[p];
+      for (int p = 0; p < RP; ++p) {
+        const int j = col + 16 * p;
+        SK* dst = static_cast<SK*>(a.rf) + sl * R;
+        if constexpr (sizeof(SK) == 2) {
+          // bf16: even lanes store their value and their neighbour's as one 32-bit word
+          const float nb = dpp<0xB1>(ft[p]);  // quad_perm [1,0,3,2]: lane j ^ 1
+          if (!(j & 1)) {
+            if (j + 1 < rh)
+              reinterpret_cast<uint32_t*>(dst)[j >> 1] = bf16_bits_rne(ft[p]) | (bf16_bits_rne(nb) << 16);
+            else if (j < rh)
+              st_elem<SK>(dst + j, ft[p]);
+          }
+        } else {
+          if (j < rh) st_elem<SK>(dst + j, ft[p]);
+        }
+      }
     }
   }
 }

@@ -72,6 +72,23 @@ __device__ __forceinline__ uint32_t bf16_bits_rne(float x) {
   return u >> 16;
 }
 
+// One stored element of a field kept in T (fp32, or bf16 rounded to nearest
+// even), as fp32; and four consecutive ones (16-byte / 8-byte aligned).
+template <typename T> __device__ __forceinline__ float ld_elem(const T* p);
+template <> __device__ __forceinline__ float ld_elem<float>(const float* p) { return *p; }
+template <> __device__ __forceinline__ float ld_elem<bf16_t>(const bf16_t* p) { return bf16_lo((uint32_t)*p); }
+template <typename T> __device__ __forceinline__ void st_elem(T* p, float x);
+template <> __device__ __forceinline__ void st_elem<float>(float* p, float x) { *p = x; }
+template <> __device__ __forceinline__ void st_elem<bf16_t>(bf16_t* p, float x) { *p = (bf16_t)bf16_bits_rne(x); }
+template <typename T> __device__ __forceinline__ void st_elem4(T* p, float a, float b, float c, float d);
+template <> __device__ __forceinline__ void st_elem4<float>(float* p, float a, float b, float c, float d) {
+  *reinterpret_cast<float4*>(p) = make_float4(a, b, c, d);
+}
+template <> __device__ __forceinline__ void st_elem4<bf16_t>(bf16_t* p, float a, float b, float c, float d) {
+  *reinterpret_cast<uint2*>(p) = make_uint2(bf16_bits_rne(a) | (bf16_bits_rne(b) << 16),
+                                            bf16_bits_rne(c) | (bf16_bits_rne(d) << 16));
+}
+
 template <typename IO> __device__ __forceinline__ float bits_f32(uint32_t x) {
   if constexpr (sizeof(IO) == 2) return bf16_lo(x);
   else return __uint_as_float(x);
@@ -85,6 +102,11 @@ template <int N> struct Raw<float, N> {
   __device__ __forceinline__ void zero() {
 #pragma unroll
     for (int i = 0; i < N; ++i) e[i] = 0.f;
+  }
+  // zero the values unless `keep` (a select, so a load before it stays unconditional)
+  __device__ __forceinline__ void keep_if(bool keep) {
+#pragma unroll
+    for (int i = 0; i < N; ++i) e[i] = keep ? e[i] : 0.f;
   }
   __device__ __forceinline__ void load(const float* p) {
     if constexpr (N % 4 == 0) {
@@ -134,6 +156,10 @@ template <int N> struct Raw<bf16_t, N> {
   __device__ __forceinline__ void zero() {
 #pragma unroll
     for (int i = 0; i < NW; ++i) w[i] = 0u;
+  }
+  __device__ __forceinline__ void keep_if(bool keep) {
+#pragma unroll
+    for (int i = 0; i < NW; ++i) w[i] = keep ? w[i] : 0u;
   }
   __device__ __forceinline__ void load(const bf16_t* p) {
     if constexpr (N % 8 == 0) {
@@ -207,6 +233,14 @@ template <int N> struct Vec {
     r.store(p);
   }
 };
+
+// Position of item (b*H + h) within one slot of a derived ring field (f, pi,
+// rows of T^{-1}): head-major, so the four items of a decode workgroup (one
+// head, four consecutive requests) are adjacent and its reads and writes of a
+// slot cover whole cache lines.
+__device__ __forceinline__ size_t derived_pos(size_t item, int B, int H) {
+  return (item % (size_t)H) * (size_t)B + item / (size_t)H;
+}
 
 // ---- cross-lane reductions -------------------------------------------------
 

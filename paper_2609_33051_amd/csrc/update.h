@@ -56,8 +56,9 @@ template <> __device__ __forceinline__ float load1<bf16_t>(const bf16_t* p) { re
 //   F1   = D^{-1} L_G T^{-1}  (= A^{-1} L_G),  F2 = A^{-1} Diag(d),
 //   A^{-1} = D^{-1} - D^{-1} L_G T^{-1} L_G^T D^{-1}
 // so the map is C = F1 M + F2 Omega^T.  Stored per item as M [P][K], F1
-// [G][P], F2 [G][G] (fp32).  Every thread of the workgroup calls this.
-template <int K, int R, int P, int MT, int RT, int LSZ, int USZ>
+// [G][P], F2 [G][G], in the sketch's dtype (bf16 with the paper's storage,
+// rounded to nearest even).  Every thread of the workgroup calls this.
+template <int K, int R, int P, int MT, int RT, int LSZ, int USZ, typename SK>
 __device__ __forceinline__ void coef_map_tail(const UpdateArgs& a, size_t item, int wave, int lane, int tid,
                                               const floatx4 (&nacc)[MT], const float (&gpart)[RT][4][5], float msq,
                                               float* Ls, float* Us, float* cmS) {
@@ -96,7 +97,7 @@ __device__ __forceinline__ void coef_map_tail(const UpdateArgs& a, size_t item, 
   lds_barrier();
 
   const size_t CMW = (size_t)P * K + R * P + R * R;
-  float* cm = a.cmap + item * CMW;
+  SK* cm = static_cast<SK*>(a.cmap) + item * CMW;
   if (wave == 0) {
     const float fro = cmS[0] + cmS[1] + cmS[2] + cmS[3];
     const float mu = fro > 0.f ? fro / K : 1.f;
@@ -219,8 +220,8 @@ __device__ __forceinline__ void coef_map_tail(const UpdateArgs& a, size_t item, 
     }
     wave_lds_sync();
     if (g < R) {
-      *reinterpret_cast<float4*>(cm + P * K + g * P) = make_float4(F1[0], F1[1], F1[2], F1[3]);
-      float* F2 = cm + P * K + R * P + g * R;
+      st_elem4<SK>(cm + P * K + g * P, F1[0], F1[1], F1[2], F1[3]);
+      SK* F2 = cm + P * K + R * P + g * R;
 #pragma unroll 4
       for (int hq = 0; hq < R; hq += 4) {
         float o4[4];
@@ -233,7 +234,7 @@ __device__ __forceinline__ void coef_map_tail(const UpdateArgs& a, size_t item, 
           const float w = sL[R * P + hh];
           o4[u] = (hh == g ? w : 0.f) - e * w;
         }
-        *reinterpret_cast<float4*>(F2 + hq) = make_float4(o4[0], o4[1], o4[2], o4[3]);
+        st_elem4<SK>(F2 + hq, o4[0], o4[1], o4[2], o4[3]);
       }
     }
   }
@@ -250,7 +251,7 @@ __device__ __forceinline__ void coef_map_tail(const UpdateArgs& a, size_t item, 
       float e = 0.f;
 #pragma unroll
       for (int b = 0; b < P; ++b) e += cmS[8 + b * P + x] * Nk[b];
-      cm[x * K + k] = e;
+      st_elem<SK>(cm + x * K + k, e);
     }
   }
 }
@@ -292,7 +293,7 @@ __global__ __launch_bounds__(256, 3) void update_kernel(const UpdateArgs a) {
   const int h = (int)(item % (size_t)H);
   const bool flush = a.nt > 0;
   // slot s of an item: raw ring fields at (item * W + s) * width, derived
-  // fields at (s * B*H + item) * width
+  // fields at (s * B*H + derived_pos(item)) * width
   const size_t NI = (size_t)a.B * H;
 
   // Omega of this head goes to LDS (rows padded to whole 16-column tiles plus
@@ -371,7 +372,7 @@ __global__ __launch_bounds__(256, 3) void update_kernel(const UpdateArgs a) {
       for (int c = 0; c < BQ; ++c) {
         const int idx = tid + 256 * c;
         const int s = idx / SP, j = idx % SP;
-        bv[c] = (idx < SP * SP && s < n && j < s) ? a.rt[((size_t)s * NI + item) * W + j] : 0.f;
+        bv[c] = (idx < SP * SP && s < n && j < s) ? a.rt[((size_t)s * NI + derived_pos(item, a.B, H)) * W + j] : 0.f;
       }
     }
   }
@@ -736,7 +737,7 @@ __global__ __launch_bounds__(256, 3) void update_kernel(const UpdateArgs a) {
   }
 
   if constexpr (P > 0) {
-    if (want_U) coef_map_tail<K, R, P, MT, RT, SP * LP, SP * UP>(a, item, wave, lane, tid, nacc, gpart, msq, Ls, Us, cmS);
+    if (want_U) coef_map_tail<K, R, P, MT, RT, SP * LP, SP * UP, SK>(a, item, wave, lane, tid, nacc, gpart, msq, Ls, Us, cmS);
   }
 }
 

@@ -10,12 +10,13 @@ into libsketchssm.so.  Buffers (caller-owned, as the ABI requires):
          storage); sketch_matrix() gives the [B][H][V][r] fp32 view
   omega  [H][K][r]     fp32 sketching matrix, coef [H][r][K] its coefficient map
          (Omega^T, the offline map; with pivots = 4 the map is state-dependent,
-         C = F1 M + F2 coef, rebuilt at every flush into cmap [B][H][4K+4r+r^2])
+         C = F1 M + F2 coef, rebuilt at every flush into cmap [B][H][4K+4r+r^2],
+         stored like U: fp32, or bf16 with sketch="bf16")
   ring   replay buffer of W slots per item:
          raw inputs k, v (io dtype), beta, log_decay ([..][K] for KDA), item-major
          [B][H][W][...], written into slot n by the token's producer (write_token);
-         derived fields, slot-major [W][B][H][...]: rows of T^{-1} (GDN/KDA),
-         f (sketch read) or pi (baseline).
+         derived fields, slot-major and head-major [W][H][B][...]: rows of T^{-1} (GDN/KDA),
+         f (sketch read; stored like U) or pi (baseline).
   head_ranks  optional per-head rank table (allocation of Sec. 4.2): head h
          uses the first head_ranks[h] columns of the rank-r storage; 0 keeps the
          head dense (the sketch read reads its state exactly, in the same
@@ -57,16 +58,17 @@ class SketchSSMLayer:
             self.omega = self.coef = self.U = None
         # state-dependent coefficient map (M, F1, F2 per item), written by every update
         cw = B.cmap_width(self.cfg)
-        self.cmap = torch.zeros((Bt, H, cw), dtype=f32, device=dev) if cw else None
+        skdt = torch.bfloat16 if sketch == "bf16" else f32  # sketch, f and map factors share the storage dtype
+        self.cmap = torch.zeros((Bt, H, cw), dtype=skdt, device=dev) if cw else None
         # raw inputs, written by the producer of each token
         self.rk = torch.zeros((Bt, H, W, K), dtype=iodt, device=dev)
         self.rv = torch.zeros((Bt, H, W, V), dtype=iodt, device=dev)
         self.rbeta = torch.zeros((Bt, H, W), dtype=f32, device=dev)
         self.rla = torch.zeros((Bt, H, W, K) if kind == "kda" else (Bt, H, W), dtype=f32, device=dev)
         # derived fields, written by the library
-        self.rt = torch.zeros((W, Bt, H, W), dtype=f32, device=dev) if erase else None
-        self.rf = torch.zeros((W, Bt, H, rank), dtype=f32, device=dev) if (erase and not baseline) else None
-        self.rpi = (torch.zeros((W, Bt, H, K), dtype=f32, device=dev)
+        self.rt = torch.zeros((W, H, Bt, W), dtype=f32, device=dev) if erase else None
+        self.rf = torch.zeros((W, H, Bt, rank), dtype=skdt, device=dev) if (erase and not baseline) else None
+        self.rpi = (torch.zeros((W, H, Bt, K), dtype=f32, device=dev)
                     if (erase and (baseline or self.dense_heads)) else None)
         self.ring = B.make_ring(k=self.rk, v=self.rv, beta=self.rbeta, log_decay=self.rla, f=self.rf,
                                 pi=self.rpi, tinv=self.rt)

@@ -65,9 +65,9 @@ class Shape:
 
     @property
     def cmap_bytes(self) -> int:
-        """The per-item factors of a state-dependent map: M [P][K], F1 [r][P], F2 [r][r], fp32."""
+        """The per-item factors of a state-dependent map: M [P][K], F1 [r][P], F2 [r][r], stored like U."""
         p = self.pivots
-        return 4 * (p * self.dk + self.rank * p + self.rank * self.rank) if p else 0
+        return self.sketch_bytes * (p * self.dk + self.rank * p + self.rank * self.rank) if p else 0
 
     @property
     def decay_bytes(self) -> int:
@@ -79,13 +79,14 @@ def slot_read_bytes(s: Shape, baseline: bool = False) -> int:
     """What a non-flush read takes from each earlier slot of the ring.
 
     Every kind: raw key and value, beta, log decay (K fp32 for KDA).
-    GDN/KDA also: the projected erase vector f (r fp32, sketch read) or the
-    erase factor pi (K fp32, exact baseline).  (The pseudo-values are solved
-    from the raw values and the stored rows of T^{-1}, not stored.)"""
+    GDN/KDA also: the projected erase vector f (r values stored like U,
+    sketch read) or the erase factor pi (K fp32, exact baseline).  (The
+    pseudo-values are solved from the raw values and the stored rows of
+    T^{-1}, not stored.)"""
     raw = s.io_bytes * (s.dk + s.dv) + 4 + s.decay_bytes
     if not s.erase:
         return raw
-    return raw + (4 * s.dk if baseline else 4 * s.rank)
+    return raw + (4 * s.dk if baseline else s.sketch_bytes * s.rank)
 
 
 def tinv_read_bytes(s: Shape, n: int) -> int:
@@ -105,7 +106,7 @@ def derived_write_bytes(s: Shape, n: int, baseline: bool = False) -> int:
     n of T^{-1} (n entries).  Mamba-2: none."""
     if not s.erase:
         return 0
-    extra = 4 * s.dk if baseline else 4 * s.rank
+    extra = 4 * s.dk if baseline else s.sketch_bytes * s.rank
     return extra + 4 * n
 
 

@@ -72,7 +72,7 @@ typedef enum { SKSSM_F32 = 0, SKSSM_BF16 = 1 } skssm_dtype;
 /* Shape of one linear-attention layer. */
 typedef struct {
   int32_t kind;     /* skssm_kind                                           */
-  int32_t batch;    /* B requests                                           */
+  int32_t batch;    /* B requests (B * H < 2^23: SKSSM_EUNSUPPORTED beyond)  */
   int32_t heads;    /* H heads                                              */
   int32_t dk;       /* K key channels  (Mamba-2 d_state N)                  */
   int32_t dv;       /* V value channels (Mamba-2 headdim P)                 */

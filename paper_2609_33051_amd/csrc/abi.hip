@@ -22,6 +22,8 @@ int fail(int code, const char* fmt, ...) {
   return code;
 }
 
+constexpr int64_t kMaxItems = (int64_t)1 << 23;
+
 bool aligned(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
 
 // Shape checks common to every entry point.
@@ -29,7 +31,11 @@ int check_shape(const skssm_config* c, bool need_rank, bool allow_rank0) {
   if (!c) return fail(SKSSM_EINVAL, "cfg is NULL");
   if (c->kind < SKSSM_MAMBA2 || c->kind > SKSSM_KDA) return fail(SKSSM_EINVAL, "unknown kind %d", c->kind);
   if (c->batch < 1 || c->heads < 1) return fail(SKSSM_EINVAL, "batch and heads must be >= 1");
-  if ((int64_t)c->batch * c->heads > (int64_t)1 << 30) return fail(SKSSM_EINVAL, "batch*heads too large");
+  // one slot of a derived ring field (at most 512 bytes per item) must span
+  // less than 4 GiB: the kernels step between slots with 32-bit byte strides
+  if ((int64_t)c->batch * c->heads >= kMaxItems)
+    return fail(SKSSM_EUNSUPPORTED, "batch*heads = %lld: at most %lld items", (long long)c->batch * c->heads,
+                (long long)kMaxItems - 1);
   if (c->io_dtype != SKSSM_F32 && c->io_dtype != SKSSM_BF16) return fail(SKSSM_EINVAL, "unknown io_dtype %d", c->io_dtype);
   if (c->sketch_dtype != SKSSM_F32 && c->sketch_dtype != SKSSM_BF16)
     return fail(SKSSM_EINVAL, "unknown sketch_dtype %d", c->sketch_dtype);

@@ -3,7 +3,8 @@
 // Replay buffer (ring): slot s of item i (= b*H + h) of a field of width w
 // sits at field + (i * W + s) * w for the raw inputs (item-major) and at
 // field + (s * B*H + h * B + b) * w for the derived fields (slot-major,
-// head-major within a slot).
+// head-major within a slot, so the four items of a decode workgroup, one head
+// and four consecutive requests, are adjacent).
 // Raw inputs of token s (k, v, beta, log decay) are written into slot s by
 // the producer of the token; the kernels derive and store the rest.
 #pragma once

@@ -61,23 +61,25 @@ struct RowLoads {
   // `item` is wave-uniform.  Slot s of a raw ring field (k, v, beta, log
   // alpha) of width w sits at field + (item * W + s) * w, the W slots of an
   // item contiguous; slot s of a derived field (f, pi, rows of T^{-1}) at
-  // field + (s * B*H + derived_pos(item)) * w, one slot of all items
+  // field + (s * B*H + dp) * w with dp = h * B + b: one slot of all items
   // contiguous, head-major within the slot.
-  __device__ __forceinline__ void load(const DecodeArgs& a, size_t item, int row, int col) {
+  __device__ __forceinline__ void load(const DecodeArgs& a, size_t item, size_t dp, int row, int col) {
     const int n = a.n;
-    const size_t W = (size_t)a.W, NI = (size_t)a.B * a.H, dp = derived_pos(item, a.B, a.H);
+    const size_t W = (size_t)a.W, NI = (size_t)a.B * a.H;
     if constexpr (ERASE) {
       // rows of T^{-1}: issued first and without branches (row and column
-      // clamped into the ring, masked below), so they share the first wait
+      // clamped into the ring, masked at use), so they share the first wait;
+      // slots are a 32-bit byte stride apart (the ABI bounds B*H)
       const int smax = n > 0 ? n - 1 : 0;
+      const uint32_t slot_bytes = (uint32_t)(NI * W * sizeof(float));
 #pragma unroll
-      for (int gi = 0; gi < NG; ++gi) {
-        const int s = 4 * gi + row;
-        const size_t rs = ((size_t)(s < smax ? s : smax) * NI + dp) * W;
+      for (int p = 0; p < JP; ++p) {
+        const int j = col + 16 * p;
+        const char* lb = reinterpret_cast<const char*>(a.rt + dp * W + (j < a.W ? j : a.W - 1));
 #pragma unroll
-        for (int p = 0; p < JP; ++p) {
-          const int j = col + 16 * p;
-          tv[gi][p] = a.rt[rs + (size_t)(j < a.W ? j : a.W - 1)];
+        for (int gi = 0; gi < NG; ++gi) {
+          const int s = 4 * gi + row;
+          tv[gi][p] = *reinterpret_cast<const float*>(lb + (uint64_t)(uint32_t)(s < smax ? s : smax) * slot_bytes);
         }
       }
     }
@@ -107,7 +109,7 @@ struct RowLoads {
       bs[gi] = 0.f;
 #pragma unroll
       for (int m = 0; m < GD; ++m) gs[gi][m] = 0.f;
-      if (4 * gi < n && s < n) {
+      if (4 * gi < n && s < n) {  // per lane (rows), so it masks lanes rather than branching
         ks[gi].load_nt(static_cast<const IO*>(a.rk) + si * K + koff);
         vs[gi].load_nt(static_cast<const IO*>(a.rv) + si * V + voff);
         bs[gi] = a.rbeta[si];
@@ -294,12 +296,12 @@ __device__ __forceinline__ void buffer_coefs(int n, int row, int col, const L& r
 // of T T^{-1} = I reads (T^{-1})_{n,.} = -beta_n b_{n,.} T^{-1}.  Mamba-2
 // derives nothing.
 template <class L>
-__device__ __forceinline__ void append_derived(const DecodeArgs& a, size_t item, int row, int col,
+__device__ __forceinline__ void append_derived(const DecodeArgs& a, size_t dp, int row, int col,
                                                const L& r, const float (&gcol)[L::JP]) {
   if constexpr (L::ERASE) {
     const int n = a.n;
     if (row == 0) {
-      float* dst = a.rt + ((size_t)n * a.B * a.H + derived_pos(item, a.B, a.H)) * a.W;
+      float* dst = a.rt + ((size_t)n * a.B * a.H + dp) * a.W;
 #pragma unroll
       for (int p = 0; p < L::JP; ++p) {
         const int j = col + 16 * p;
@@ -312,9 +314,10 @@ __device__ __forceinline__ void append_derived(const DecodeArgs& a, size_t item,
 // The exact full-state read of one item by one wave (no workgroup barrier):
 //   o = S_0^T q~_t + o_t^buffer,  q~_t = e^{g_t} . q_t - sum_s a_{t,s} pi_s
 // (eq. app-effective-query-wy), storing pi_t and row n of T^{-1} for the
-// token.  ws: the wave's 2V + 2 WMAX floats of LDS.
+// token.  dp: the item's position in the derived ring fields (h * B + b).
+// ws: the wave's 2V + 2 WMAX floats of LDS.
 template <int KIND, int K, int V, int WMAX, typename IO>
-__device__ __forceinline__ void full_read_item(const DecodeArgs& a, size_t item, int lane, float* ws) {
+__device__ __forceinline__ void full_read_item(const DecodeArgs& a, size_t item, size_t dp, int lane, float* ws) {
   using L = RowLoads<KIND, K, V, WMAX, IO>;
   constexpr bool ERASE = L::ERASE, CHAN = L::CHAN;
   constexpr int KPL = L::KPL, VR = L::VR, NG = L::NG, GD = L::GD;
@@ -325,19 +328,20 @@ __device__ __forceinline__ void full_read_item(const DecodeArgs& a, size_t item,
   const uint32_t koff = (uint32_t)(col * KPL);
 
   L r;
-  r.load(a, item, row, col);
+  r.load(a, item, dp, row, col);
   float ps[ERASE ? NG : 1][KPL];     // ring pi of slot 4 gi + row (row layout)
   if constexpr (ERASE) {
-    const size_t rowder = (size_t)row * NI + derived_pos(item, a.B, a.H);
+    // slot clamped below n and the value selected (no guarded load)
+    const int smax = n > 0 ? n - 1 : 0;
+    const uint32_t slot_bytes = (uint32_t)(NI * K * sizeof(float));
+    const char* lb = reinterpret_cast<const char*>(a.rpi + dp * K + koff);
 #pragma unroll
     for (int gi = 0; gi < NG; ++gi) {
       const int s = 4 * gi + row;
       Vec<KPL> t;
+      t.load(reinterpret_cast<const float*>(lb + (uint64_t)(uint32_t)(s < smax ? s : smax) * slot_bytes));
 #pragma unroll
-      for (int m = 0; m < KPL; ++m) t.e[m] = 0.f;
-      if (4 * gi < n && s < n) t.load(a.rpi + (rowder + (size_t)(4 * gi) * NI) * K + koff);
-#pragma unroll
-      for (int m = 0; m < KPL; ++m) ps[gi][m] = t.e[m];
+      for (int m = 0; m < KPL; ++m) ps[gi][m] = s < n ? t.e[m] : 0.f;
     }
   }
 
@@ -406,13 +410,13 @@ __device__ __forceinline__ void full_read_item(const DecodeArgs& a, size_t item,
 #pragma unroll
   for (int vv = 0; vv < VPL; ++vv) ob_g[lane + 64 * vv] = os_l[lane + 64 * vv] + ob_l[lane + 64 * vv];
 
-  append_derived<L>(a, item, row, col, r, gcol);
+  append_derived<L>(a, dp, row, col, r, gcol);
   if constexpr (ERASE) {
     if (row == 0) {
       Vec<KPL> t;
 #pragma unroll
       for (int m = 0; m < KPL; ++m) t.e[m] = pit[m];
-      t.store(a.rpi + ((size_t)n * NI + derived_pos(item, a.B, a.H)) * K + koff);
+      t.store(a.rpi + ((size_t)n * NI + dp) * K + koff);
     }
   }
 }
@@ -456,6 +460,7 @@ __global__ __launch_bounds__(256) void decode_kernel(const DecodeArgs a) {
   const int b = tile * 4 + wave;
   const bool valid = b < a.B;
   const size_t item = (size_t)(valid ? b : 0) * H + h;
+  const size_t dp = (size_t)h * a.B + (valid ? b : 0);  // position in the derived ring fields
   const SK* Ub = static_cast<const SK*>(a.U) + item * (size_t)V * R;
   // this head's rank: its first rh sketch columns, coefficient rows and f
   // entries are used; a dense-fallback head (rh = 0) is read elsewhere
@@ -465,7 +470,7 @@ __global__ __launch_bounds__(256) void decode_kernel(const DecodeArgs a) {
     // wave (the whole workgroup shares the head and takes this branch, so no
     // barrier is skipped)
     static_assert(WS >= 2 * V + 2 * WMAX, "per-wave LDS too small for the full read");
-    if (valid) full_read_item<KIND, K, V, WMAX, IO>(a, item, lane, wscr + wave * WS);
+    if (valid) full_read_item<KIND, K, V, WMAX, IO>(a, item, dp, lane, wscr + wave * WS);
     return;
   }
 
@@ -480,37 +485,35 @@ __global__ __launch_bounds__(256) void decode_kernel(const DecodeArgs a) {
     if ((CQ * 256 == R * K / 4 || i < R * K / 4) && (4 * i) / K < rh) cv[c].load(a.coef + (size_t)h * R * K + 4 * i);
   }
   compiler_fence();
-  // Every load of the item follows, without branches: a wave past the batch
-  // reads item 0 of its head (and returns after the barrier), slots and
-  // panels past what the step uses are clamped to ones that exist and the
-  // values masked by selects.  A guarded load becomes a branch whose join
-  // waits for the loads in flight, which serialises the item's memory
-  // accesses.
+  // Every load of the item follows, with no wave-uniform guard: a wave past
+  // the batch reads item 0 of its head (and returns after the barrier);
+  // derived-field slots and sketch panels past what the step uses are clamped
+  // to ones that exist and their values masked by selects.  A load under a
+  // wave-uniform guard compiles to a branch whose join waits for the loads in
+  // flight, which serialises the item's memory accesses.  The raw ring slots
+  // are guarded per lane (slot 4 gi + row < n), which masks lanes instead.
   L r;
-  r.load(a, item, row, col);
+  r.load(a, item, dp, row, col);
   float fs[ERASE ? NG : 1][RP];      // ring f of slot 4 gi + row, component col + 16 p
   if constexpr (ERASE) {
-    const size_t NI = (size_t)a.B * H, dp = derived_pos(item, a.B, H);
     const int smax = n > 0 ? n - 1 : 0;
+    const uint32_t slot_bytes = (uint32_t)((size_t)a.B * H * R * sizeof(SK));
 #pragma unroll
-    for (int gi = 0; gi < NG; ++gi) {
-      const int s = 4 * gi + row;
-      const SK* fp = static_cast<const SK*>(a.rf) + ((size_t)(s < smax ? s : smax) * NI + dp) * R;
+    for (int p = 0; p < RP; ++p) {
+      const int j = col + 16 * p;
+      // bf16: lanes j and j^1 read the same 32-bit word
+      const char* lb = reinterpret_cast<const char*>(static_cast<const SK*>(a.rf) + dp * R) +
+                       (sizeof(SK) == 2 ? 4 * (j >> 1) : 4 * j);
 #pragma unroll
-      for (int p = 0; p < RP; ++p) {
-        const int j = col + 16 * p;
-        float fv;
-        if constexpr (sizeof(SK) == 2) {  // bf16: lanes j and j^1 read the same 32-bit word
-          const uint32_t w = reinterpret_cast<const uint32_t*>(fp)[j >> 1];
-          fv = (j & 1) ? bf16_hi(w) : bf16_lo(w);
-        } else {
-          fv = ld_elem<SK>(fp + j);
-        }
+      for (int gi = 0; gi < NG; ++gi) {
+        const int s = 4 * gi + row;
+        const uint32_t w = *reinterpret_cast<const uint32_t*>(lb + (uint64_t)(uint32_t)(s < smax ? s : smax) * slot_bytes);
+        const float fv = sizeof(SK) == 2 ? ((j & 1) ? bf16_hi(w) : bf16_lo(w)) : __uint_as_float(w);
         fs[gi][p] = (s < n && j < rh) ? fv : 0.f;
       }
     }
   }
-  Raw<SK, PW> Ur[VPL][UP];           // sketch panels (value layout); panels past the rank re-read panel 0
+  Raw<SK, PW> Ur[VPL][UP];           // sketch panels (value layout); panels past the rank read as zeros
   if constexpr (U_PRELOAD) {
 #pragma unroll
     for (int p = 0; p < NP; ++p)
@@ -707,10 +710,10 @@ __global__ __launch_bounds__(256) void decode_kernel(const DecodeArgs a) {
   }
 
   // ---- derived fields of the token at ring slot n
-  append_derived<L>(a, item, row, col, r, gcol);
+  append_derived<L>(a, dp, row, col, r, gcol);
   if constexpr (ERASE) {
     if (row == 0) {
-      const size_t sl = (size_t)n * a.B * H + derived_pos(item, a.B, H);
+      const size_t sl = (size_t)n * a.B * H + dp;
 #pragma unroll
       for (int p = 0; p < RP; ++p) {
         const int j = col + 16 * p;
@@ -745,7 +748,8 @@ __global__ __launch_bounds__(256) void full_read_kernel(const DecodeArgs a) {
   const uint32_t lwg = (G % 8 == 0) ? (wg % 8) * (G / 8) + wg / 8 : wg;
   const size_t item = (size_t)lwg * 4 + wave;
   if (item >= NI) return;  // wave-uniform; no block barrier in this kernel
-  full_read_item<KIND, K, V, WMAX, IO>(a, item, lane, wscr + wave * WS);
+  const uint32_t b = (uint32_t)item / (uint32_t)a.H, h = (uint32_t)item - b * (uint32_t)a.H;  // B*H <= 2^30
+  full_read_item<KIND, K, V, WMAX, IO>(a, item, (size_t)h * a.B + b, lane, wscr + wave * WS);
 }
 
 }  // namespace skssm

@@ -234,14 +234,6 @@ template <int N> struct Vec {
   }
 };
 
-// Position of item (b*H + h) within one slot of a derived ring field (f, pi,
-// rows of T^{-1}): head-major, so the four items of a decode workgroup (one
-// head, four consecutive requests) are adjacent and its reads and writes of a
-// slot cover whole cache lines.
-__device__ __forceinline__ size_t derived_pos(size_t item, int B, int H) {
-  return (item % (size_t)H) * (size_t)B + item / (size_t)H;
-}
-
 // ---- cross-lane reductions -------------------------------------------------
 
 template <int CTRL> __device__ __forceinline__ float dpp(float x) {

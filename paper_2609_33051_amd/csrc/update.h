@@ -289,12 +289,12 @@ __global__ __launch_bounds__(256, 3) void update_kernel(const UpdateArgs a) {
   const int lr = lane & 15, lg = lane >> 4;   // MFMA lane coordinates
   const int row = lg, col = lr;               // row-layout coordinates (same lanes)
   const int H = a.H, W = a.W, n = a.n;
-  const size_t item = blockIdx.x;
-  const int h = (int)(item % (size_t)H);
+  const size_t item = blockIdx.x;  // b * H + h (B*H <= 2^30)
+  const int h = (int)(blockIdx.x % (uint32_t)H);
   const bool flush = a.nt > 0;
   // slot s of an item: raw ring fields at (item * W + s) * width, derived
-  // fields at (s * B*H + derived_pos(item)) * width
-  const size_t NI = (size_t)a.B * H;
+  // fields at (s * B*H + dp) * width, dp = h * B + b
+  const size_t NI = (size_t)a.B * H, dp = (size_t)h * a.B + blockIdx.x / (uint32_t)H;
 
   // Omega of this head goes to LDS (rows padded to whole 16-column tiles plus
   // four words, so the four lane groups of an operand read hit different banks)
@@ -372,7 +372,7 @@ __global__ __launch_bounds__(256, 3) void update_kernel(const UpdateArgs a) {
       for (int c = 0; c < BQ; ++c) {
         const int idx = tid + 256 * c;
         const int s = idx / SP, j = idx % SP;
-        bv[c] = (idx < SP * SP && s < n && j < s) ? a.rt[((size_t)s * NI + derived_pos(item, a.B, H)) * W + j] : 0.f;
+        bv[c] = (idx < SP * SP && s < n && j < s) ? a.rt[((size_t)s * NI + dp) * W + j] : 0.f;
       }
     }
   }

@@ -171,6 +171,15 @@ def check_config_ok(lib):
     return B.sketchssm_check_config(cfg()) == 0 and B.sketchssm_check_config(cfg(rank=5)) == -2
 
 
+def test_item_count_limit(lib):
+    """B*H < 2^23: one slot of a derived ring field (up to 512 bytes per item)
+    then spans less than 4 GiB, the range of the kernels' 32-bit slot strides."""
+    assert B.sketchssm_check_config(cfg(batch=(1 << 23) - 1, heads=1)) == 0
+    assert B.sketchssm_check_config(cfg(batch=1 << 22, heads=2)) == -2
+    assert "items" in B.sketchssm_last_error()
+    assert B.sketchssm_check_config(cfg(batch=1 << 20, heads=1 << 12)) == -2
+
+
 def test_head_rank_table_marshalling():
     c = B.make_config("gdn", 2, 3, 128, 128, 16, 16, "bf16", head_ranks=[16, 0, 7])
     assert B.head_ranks(c) == [16, 0, 7]

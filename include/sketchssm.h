@@ -15,10 +15,15 @@
  *
  * Conventions shared by every entry point
  * ---------------------------------------
- * Layout.  The paper writes S as K x V with o = S^T q; this library stores
- * its transpose, S[B][H][V][K] fp32 with K contiguous, so a row S[b][h][v][:]
- * is contiguous.  All other per-item tensors are [B][H][...] row-major with
- * the item index b*H + h.  The sketch is stored in panels of 16 bytes per
+ * Layout.  The paper writes S as K x V with o = S^T q; this library keeps
+ * its transpose X = S^T (V x K per item, fp32) in a tile-major layout: item
+ * b*H + h holds (V/16) x (K/16) tiles of 16 x 16, tile (vt, kt) at offset
+ * (vt * K/16 + kt) * 256 floats, and within a tile X[16 vt + r][16 kt + c]
+ * at 4 (r + 16 (c / 4)) + c % 4.  That is the register layout of the flush's
+ * matrix-core accumulators, so every state load and store moves 1 KB
+ * contiguous.  sketchssm_state_to_tiles / sketchssm_state_from_tiles convert
+ * from and to the row layout X[B][H][V][K].  All other per-item tensors are
+ * [B][H][...] row-major with the item index b*H + h.  The sketch is stored in panels of 16 bytes per
  * value channel, U[B][H][r/P][V][P] with P = 4 columns (fp32) or P = 8
  * (bf16, the paper's sketch storage; cfg.sketch_dtype): element (v, g) of
  * the paper's V x r sketch (the output of basis query g at value channel v)
@@ -168,7 +173,7 @@ typedef struct {
  *     prefill, the initialisation step of Algorithm 1); n_buffered must be 0,
  *     S is not written and o is ignored.
  *
- * S      [B][H][V][K] fp32, read and (q != NULL) written in place.
+ * S      B*H*V*K fp32 in the tile-major layout, read and (q != NULL) written in place.
  * omega  [H][K][rank] fp32 (may be NULL when rank == 0).
  * ring   read-only here: k, v, beta, log_decay of slots 0..n_buffered;
  *        tinv (GDN, KDA) of slots 0..n_buffered-1.
@@ -197,7 +202,7 @@ int sketchssm_update(const skssm_config* cfg, float* S, const float* omega, cons
  * (cfg.sketch_dtype) and coef [H][rank][K] fp32 (C; Omega^T for the offline
  * map of Sec. 4.1 at E0 = I) are read; for GDN/KDA the derived fields of slot
  * n_buffered (f, tinv) are written.
- * S [B][H][V][K] fp32 is read only for the dense-fallback heads of a per-head
+ * S (tile-major, fp32) is read only for the dense-fallback heads of a per-head
  * rank table (cfg.head_rank entries 0), whose output is the exact read of
  * sketchssm_full_read_baseline (their slot gets pi instead of f, so ring.pi
  * is then required); S may be NULL when no head is dense.
@@ -215,12 +220,23 @@ int sketchssm_decode(const skssm_config* cfg, const void* U, const float* coef, 
  *     o = S_0^T q~_t + o_t^buffer,  q~_t = e^{g_t} . q_t - sum_{s<=t} a_{t,s} pi_s
  * (eq. m-reads with the effective query of eq. app-effective-query-wy), for
  * the token in ring slot n_buffered (0..W-2).  For GDN/KDA the derived fields
- * of that slot (pi, tinv) are written.  S [B][H][V][K] is only
+ * of that slot (pi, tinv) are written.  S (tile-major) is only
  * read.  Flushes of this path use sketchssm_update with rank = 0.
  * cfg->rank is ignored.
  */
 int sketchssm_full_read_baseline(const skssm_config* cfg, const float* S, const skssm_ring* ring,
                                  int32_t n_buffered, const void* q, float* o, void* stream);
+
+/*
+ * sketchssm_state_to_tiles / sketchssm_state_from_tiles -- convert states
+ * between the row layout X[B][H][V][K] (X = S^T, K contiguous; how a caller
+ * or a prefill usually holds them) and the tile-major layout every other
+ * entry point reads and writes (see Layout).  Both arrays are B*H*V*K fp32
+ * device memory owned by the caller, 16-byte aligned, and must not overlap
+ * (SKSSM_EINVAL).  One kernel launch on `stream`; cfg->rank is ignored.
+ */
+int sketchssm_state_to_tiles(const skssm_config* cfg, const float* S_rows, float* S, void* stream);
+int sketchssm_state_from_tiles(const skssm_config* cfg, const float* S, float* S_rows, void* stream);
 
 /* Static text for a status code. */
 const char* sketchssm_status_string(int status);

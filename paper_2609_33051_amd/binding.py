@@ -23,6 +23,7 @@ STATUS = {0: "SKSSM_OK", -1: "SKSSM_EINVAL", -2: "SKSSM_EUNSUPPORTED", -3: "SKSS
           -4: "SKSSM_ESTATE", -5: "SKSSM_EHIP"}
 
 FUNCTIONS = ("sketchssm_update", "sketchssm_decode", "sketchssm_full_read_baseline",
+             "sketchssm_state_to_tiles", "sketchssm_state_from_tiles",
              "sketchssm_status_string", "sketchssm_last_error", "sketchssm_check_config")
 
 
@@ -61,7 +62,10 @@ def load(path: str | None = None):
     lib.sketchssm_update.argtypes = [cfgp, P, P, ringp, ctypes.c_int32, P, P, P, P, P]
     lib.sketchssm_decode.argtypes = [cfgp, P, P, P, P, ringp, ctypes.c_int32, P, P, P]
     lib.sketchssm_full_read_baseline.argtypes = [cfgp, P, ringp, ctypes.c_int32, P, P, P]
-    for f in ("sketchssm_update", "sketchssm_decode", "sketchssm_full_read_baseline", "sketchssm_check_config"):
+    lib.sketchssm_state_to_tiles.argtypes = [cfgp, P, P, P]
+    lib.sketchssm_state_from_tiles.argtypes = [cfgp, P, P, P]
+    for f in ("sketchssm_update", "sketchssm_decode", "sketchssm_full_read_baseline", "sketchssm_check_config",
+              "sketchssm_state_to_tiles", "sketchssm_state_from_tiles"):
         getattr(lib, f).restype = ctypes.c_int
     lib.sketchssm_check_config.argtypes = [cfgp]
     lib.sketchssm_status_string.argtypes = [ctypes.c_int]
@@ -182,6 +186,16 @@ def sketchssm_full_read_baseline(cfg: Config, S, ring: Ring, n_buffered: int, q,
     lib = load()
     _check(lib.sketchssm_full_read_baseline(ctypes.byref(cfg), ptr(S), ctypes.byref(ring) if ring else None,
                                             int(n_buffered), ptr(q), ptr(o), stream))
+
+
+def sketchssm_state_to_tiles(cfg: Config, S_rows, S, stream=None):
+    """Row layout X[B][H][V][K] -> the tile-major state the other calls use."""
+    _check(load().sketchssm_state_to_tiles(ctypes.byref(cfg), ptr(S_rows), ptr(S), stream))
+
+
+def sketchssm_state_from_tiles(cfg: Config, S, S_rows, stream=None):
+    """Tile-major state -> row layout X[B][H][V][K]."""
+    _check(load().sketchssm_state_from_tiles(ctypes.byref(cfg), ptr(S), ptr(S_rows), stream))
 
 
 def sketchssm_check_config(cfg: Config) -> int:

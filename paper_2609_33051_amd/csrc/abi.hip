@@ -139,6 +139,19 @@ skssm::DecodeArgs decode_args(const skssm_config* c, const skssm_ring* r, int32_
   return a;
 }
 
+int state_layout(const skssm_config* cfg, const float* src, float* dst, void* stream, int to_tiles,
+                        const char* what) {
+  int rc = check_shape(cfg, false, true);
+  if (rc) return rc;
+  if (!src || !dst) return fail(SKSSM_EINVAL, "%s: source and destination are required", what);
+  if (!aligned(src) || !aligned(dst)) return fail(SKSSM_EALIGN, "%s: source/destination not aligned", what);
+  const size_t items = (size_t)cfg->batch * cfg->heads;
+  const size_t bytes = items * cfg->dk * cfg->dv * sizeof(float);
+  const uintptr_t s0 = reinterpret_cast<uintptr_t>(src), d0 = reinterpret_cast<uintptr_t>(dst);
+  if (s0 < d0 + bytes && d0 < s0 + bytes) return fail(SKSSM_EINVAL, "%s: source and destination overlap", what);
+  return launched(skssm::run_state_layout(src, dst, items, cfg->dk, cfg->dv, to_tiles, stream), what);
+}
+
 }  // namespace
 
 extern "C" {
@@ -278,6 +291,14 @@ int sketchssm_full_read_baseline(const skssm_config* cfg, const float* S, const 
     default: r = skssm::run_full_read_kda(a, cfg->dk, cfg->dv, cfg->io_dtype, stream); break;
   }
   return launched(r, "sketchssm_full_read_baseline");
+}
+
+int sketchssm_state_to_tiles(const skssm_config* cfg, const float* S_rows, float* S, void* stream) {
+  return state_layout(cfg, S_rows, S, stream, 1, "sketchssm_state_to_tiles");
+}
+
+int sketchssm_state_from_tiles(const skssm_config* cfg, const float* S, float* S_rows, void* stream) {
+  return state_layout(cfg, S, S_rows, stream, 0, "sketchssm_state_from_tiles");
 }
 
 }  // extern "C"

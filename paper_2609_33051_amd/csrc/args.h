@@ -69,5 +69,7 @@ int run_full_read_kda(const DecodeArgs& a, int K, int V, int io, void* stream);
 int run_update_mamba2(const UpdateArgs& a, int K, int V, int R, int io, int sk, int piv, void* stream);
 int run_update_gdn(const UpdateArgs& a, int K, int V, int R, int io, int sk, int piv, void* stream);
 int run_update_kda(const UpdateArgs& a, int K, int V, int R, int io, int sk, int piv, void* stream);
+// State layout conversion (row layout <-> tile-major), items states of V x K.
+int run_state_layout(const float* src, float* dst, size_t items, int K, int V, int to_tiles, void* stream);
 
 }  // namespace skssm

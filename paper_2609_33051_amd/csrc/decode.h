@@ -315,7 +315,7 @@ __device__ __forceinline__ void append_derived(const DecodeArgs& a, size_t dp, i
 //   o = S_0^T q~_t + o_t^buffer,  q~_t = e^{g_t} . q_t - sum_s a_{t,s} pi_s
 // (eq. app-effective-query-wy), storing pi_t and row n of T^{-1} for the
 // token.  dp: the item's position in the derived ring fields (h * B + b).
-// ws: the wave's 2V + 2 WMAX floats of LDS.
+// ws: the wave's 2V + 2 WMAX + K floats of LDS.
 template <int KIND, int K, int V, int WMAX, typename IO>
 __device__ __forceinline__ void full_read_item(const DecodeArgs& a, size_t item, size_t dp, int lane, float* ws) {
   using L = RowLoads<KIND, K, V, WMAX, IO>;
@@ -388,18 +388,32 @@ __device__ __forceinline__ void full_read_item(const DecodeArgs& a, size_t item,
     }
   }
 
-  // ---- o^state = S_0^T q~_t : rows v = 4 vi + row of S, K channels over 16 lanes
-  const float* Sb = a.S + item * (size_t)V * K;
+  // ---- o^state = S_0^T q~_t over the state's 16 x 16 tiles.  Tile (vt, kt)
+  // is 1 KB contiguous with lane l holding X[16 vt + l%16][16 kt + 4 (l/16) + i]
+  // (the flush's register layout), so every load moves 1 KB: q~ goes through
+  // LDS to those channels, each lane sums over the K tiles, and the four lane
+  // rows are summed.
+  constexpr int MT = K / 16, VT = V / 16;
+  float* qe_l = b_l + 2 * WMAX;                   // K floats
+  if (row == 0) {
 #pragma unroll
-  for (int vi = 0; vi < V / 4; ++vi) {
-    const int v = 4 * vi + row;
-    Vec<KPL> x;
-    x.load(Sb + (uint32_t)(v * K) + koff);
+    for (int m = 0; m < KPL; ++m) qe_l[koff + m] = qe[m];
+  }
+  wave_lds_sync();
+  float4 qf[MT];
+#pragma unroll
+  for (int kt = 0; kt < MT; ++kt) qf[kt] = *reinterpret_cast<const float4*>(qe_l + 16 * kt + 4 * row);
+  const float* Sb = a.S + item * (size_t)V * K + 4 * lane;
+#pragma unroll
+  for (int vt = 0; vt < VT; ++vt) {
     float d = 0.f;
 #pragma unroll
-    for (int m = 0; m < KPL; ++m) d += x.e[m] * qe[m];
-    d = row_sum16(d);
-    if (col == 0) os_l[v] = d;
+    for (int kt = 0; kt < MT; ++kt) {
+      const float4 x = ld_nt(reinterpret_cast<const float4*>(Sb + (uint32_t)((vt * MT + kt) * 256)));
+      d += x.x * qf[kt].x + x.y * qf[kt].y + x.z * qf[kt].z + x.w * qf[kt].w;
+    }
+    d = cross_row_sum(d);
+    if (row == 0) os_l[16 * vt + col] = d;
   }
   if (row == 0) {
 #pragma unroll
@@ -469,7 +483,7 @@ __global__ __launch_bounds__(256) void decode_kernel(const DecodeArgs a) {
     // dense-fallback head: the exact full-state read of its items, one per
     // wave (the whole workgroup shares the head and takes this branch, so no
     // barrier is skipped)
-    static_assert(WS >= 2 * V + 2 * WMAX, "per-wave LDS too small for the full read");
+    static_assert(WS >= 2 * V + 2 * WMAX + K, "per-wave LDS too small for the full read");
     if (valid) full_read_item<KIND, K, V, WMAX, IO>(a, item, dp, lane, wscr + wave * WS);
     return;
   }
@@ -737,7 +751,7 @@ __global__ __launch_bounds__(256) void decode_kernel(const DecodeArgs a) {
 
 template <int KIND, int K, int V, int WMAX, typename IO>
 __global__ __launch_bounds__(256) void full_read_kernel(const DecodeArgs a) {
-  constexpr int WS = 2 * V + 2 * WMAX;  // per-wave LDS: o^state, o_buf, alpha/gamma transposition
+  constexpr int WS = 2 * V + 2 * WMAX + K;  // per-wave LDS: o^state, o_buf, alpha/gamma transposition, q~
   __shared__ __align__(16) float wscr[4 * WS];
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);

@@ -22,7 +22,10 @@
 // instruction, wave w taking slot groups w, w + 4, ...).  Each wave owns
 // 16-column value tiles of X^T (K rows x 16 values), held in MFMA
 // accumulator layout: lane l holds X[v0 + l%16][16 kt + 4 (l/16) + i],
-// i = 0..3, a 16-byte contiguous piece of a state row.  Because the
+// i = 0..3.  The state is stored in exactly this order (tile-major: tile
+// (v0/16, kt) is 1 KB contiguous with lane l's four values at 4 l), so each
+// load and store instruction moves 1 KB contiguous; both are non-temporal,
+// as the state is touched once per flush.  Because the
 // contraction index of the K-deep products may be visited in any order, the
 // same registers serve as the B operand of X_0 Pi^T and X_W Omega (step i of
 // k-tile kt contracts over k = 16 kt + 4 g + i for lane group g) and as the
@@ -394,10 +397,11 @@ __global__ __launch_bounds__(256, 3) void update_kernel(const UpdateArgs a) {
   for (int t = 0; t < VTW; ++t) {
     const int vt = wave + 4 * t;
     if (vt < VT) {
-      const float* src = a.S + (item * V + 16 * vt + lr) * K + 4 * lg;
+      // tile (vt, kt) of the state is 1 KB contiguous, lane l's float4 at 4 l
+      const float* src = a.S + item * V * K + (size_t)(vt * MT) * 256 + 4 * lane;
 #pragma unroll
       for (int kt = 0; kt < MT; ++kt) {
-        const float4 x = *reinterpret_cast<const float4*>(src + 16 * kt);
+        const float4 x = ld_nt(reinterpret_cast<const float4*>(src + 256 * kt));
         xs[t][kt] = floatx4{x.x, x.y, x.z, x.w};
       }
     }
@@ -729,10 +733,10 @@ __global__ __launch_bounds__(256, 3) void update_kernel(const UpdateArgs a) {
       }
     }
     if (flush) {
-      float* dst = a.S + (item * V + v) * K + 4 * lg;
+      float* dst = a.S + item * V * K + (size_t)(vt * MT) * 256 + 4 * lane;
 #pragma unroll
       for (int kt = 0; kt < MT; ++kt)
-        *reinterpret_cast<float4*>(dst + 16 * kt) = make_float4(xs[t][kt][0], xs[t][kt][1], xs[t][kt][2], xs[t][kt][3]);
+        st_nt(reinterpret_cast<float4*>(dst + 256 * kt), make_float4(xs[t][kt][0], xs[t][kt][1], xs[t][kt][2], xs[t][kt][3]));
     }
   }
 

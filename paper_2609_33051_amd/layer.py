@@ -4,7 +4,9 @@
 torch supplies device memory and the stream; every computation is a call
 into libsketchssm.so.  Buffers (caller-owned, as the ABI requires):
 
-  S      [B][H][V][K]  fp32 full state (stored transposed: K contiguous)
+  S      B*H*V*K fp32 full state X = S^T in the library's tile-major layout
+         (16 x 16 tiles, 1 KB each); the constructor takes a row-layout state
+         [B][H][V][K] and converts it, state() returns that layout again
   U      [B][H][r/P][V][P] sketch U = S^T Omega in panels of 16 bytes per
          value: P = 4 columns fp32, or P = 8 bf16 (sketch="bf16", the paper's
          storage); sketch_matrix() gives the [B][H][V][r] fp32 view
@@ -43,11 +45,15 @@ class SketchSSMLayer:
         Bt, H, K, V, W = batch, heads, dk, dv, window
         erase = kind in ("gdn", "kda")
         dev = self.device
-        self.S = S if S is not None else torch.zeros((Bt, H, V, K), dtype=f32, device=dev)
         r = 0 if baseline else rank
         self.head_ranks = None if (baseline or head_ranks is None) else [int(x) for x in head_ranks]
         self.dense_heads = 0 if self.head_ranks is None else sum(1 for x in self.head_ranks if x == 0)
         self.cfg = B.make_config(kind, Bt, H, K, V, r, W, io, sketch, self.pivots, ridge, head_ranks=self.head_ranks)
+        # the state in the kernels' tile-major layout (S, if given, is row layout [B][H][V][K])
+        self.S = torch.zeros((Bt, H, V * K), dtype=f32, device=dev)
+        if S is not None:
+            rows = S.to(device=dev, dtype=f32).reshape(Bt, H, V, K).contiguous()
+            B.sketchssm_state_to_tiles(self.cfg, rows, self.S, self.stream())
         if not baseline:
             self.omega = omega.to(dev).contiguous()
             self.coef = coef.to(dev).contiguous()
@@ -83,6 +89,12 @@ class SketchSSMLayer:
     @staticmethod
     def stream() -> int:
         return torch.cuda.current_stream().cuda_stream
+
+    def state(self) -> torch.Tensor:
+        """The state in row layout [B][H][V][K] (X = S^T, K contiguous), a copy."""
+        rows = torch.empty((self.batch, self.heads, self.dv, self.dk), dtype=torch.float32, device=self.device)
+        B.sketchssm_state_from_tiles(self.cfg, self.S, rows, self.stream())
+        return rows
 
     def init_sketch(self):
         """U = S^T Omega from S alone (after prefill); empties the window."""

@@ -118,6 +118,17 @@ class TestValidation:
         assert status(d, cfg(pivots=4, ridge=-1.0), ADDR, ADDR, good_ring(), 0, ADDR, ADDR) == -1
         assert "n_buffered" in B.sketchssm_status_string(-4)
 
+    def test_state_layout_rejections(self, lib):
+        t, f = B.sketchssm_state_to_tiles, B.sketchssm_state_from_tiles
+        big = ADDR + (1 << 24)   # past the 2*4*64*128*4-byte state at ADDR
+        assert status(t, cfg(), None, big) == -1
+        assert status(f, cfg(), ADDR, None) == -1
+        assert status(t, cfg(), ADDR + 4, big) == -3
+        assert status(t, cfg(), ADDR, ADDR + 4096) == -1          # overlapping ranges
+        assert "overlap" in B.sketchssm_last_error()
+        assert status(f, cfg(dk=96), ADDR, big) == -2
+        assert status(t, cfg(batch=0), ADDR, big) == -1
+
     def test_update_rejections(self, lib):
         u = B.sketchssm_update
         assert status(u, cfg(), ADDR, ADDR, good_ring(), 16, ADDR, ADDR, ADDR) == -4

@@ -40,7 +40,7 @@ def check(wl, window=None, rank=None, steps=None, sel=None, omega_coef=None, bas
     err = max_step_rel(run.o_gpu, target)
     n_items = wl.batch * wl.heads
     idx = slice(None) if sel is None else torch.as_tensor(np.asarray(sel), device=layer.S.device)
-    errS = rel_l2(to_np32(layer.S.reshape(n_items, wl.dv, wl.dk)[idx]), ref.S_final)
+    errS = rel_l2(to_np32(layer.state().reshape(n_items, wl.dv, wl.dk)[idx]), ref.S_final)
     errU = 0.0
     if not baseline:
         errU = rel_l2(to_np32(layer.sketch_matrix().reshape(n_items, wl.dv, rank)[idx]), ref.U_final)
@@ -122,7 +122,7 @@ def test_window_one_is_standard_recurrence(fam):
     q, k, v, beta, logd = (np.stack(run.inp[x]) for x in ("q", "k", "v", "beta", "log_decay"))
     o_ex, S_ex = oracle.recurrence(wl.kind, S_sel, q, k, v, beta, logd)
     err = max_step_rel(run.o_gpu, o_ex)
-    errS = rel_l2(to_np32(layer.S.reshape(-1, V, 128)), S_ex)
+    errS = rel_l2(to_np32(layer.state().reshape(-1, V, 128)), S_ex)
     print(f"  max step rel-L2 {err:.3e} state {errS:.3e}", flush=True)
     assert err <= 1e-5 and errS <= 1e-5
 

@@ -36,7 +36,7 @@ def check_ragged(wl, head_ranks, window=None, steps=None, sketch="f32", pivots=0
     items = np.arange(n_items) if sel is None else np.asarray(sel)
     q, k, v, beta, logd = (np.stack(run.inp[x]) for x in ("q", "k", "v", "beta", "log_decay"))
     o_gpu = np.stack(run.o_gpu)
-    S_gpu = to_np32(layer.S.reshape(n_items, wl.dv, wl.dk))[items]
+    S_gpu = to_np32(layer.state().reshape(n_items, wl.dv, wl.dk))[items]
     U_gpu = to_np32(layer.sketch_matrix().reshape(n_items, wl.dv, wl.rank))[items]
     tol = TOL["bf16" if sketch == "bf16" else wl.io]
     P = 8 if sketch == "bf16" else 4

@@ -435,7 +435,9 @@ __device__ __forceinline__ void full_read_item(const DecodeArgs& a, size_t item,
   }
 }
 
-template <int KIND, int K, int V, int R, int WMAX, typename IO, typename SK, int P>
+// DENSE: compiled with the exact read for dense-fallback heads (launched only
+// for rank tables that have some); without it the kernel needs fewer registers.
+template <int KIND, int K, int V, int R, int WMAX, typename IO, typename SK, int P, bool DENSE>
 __global__ __launch_bounds__(256) void decode_kernel(const DecodeArgs a) {
   using L = RowLoads<KIND, K, V, WMAX, IO>;
   constexpr bool ERASE = L::ERASE, CHAN = L::CHAN;
@@ -484,7 +486,9 @@ __global__ __launch_bounds__(256) void decode_kernel(const DecodeArgs a) {
     // wave (the whole workgroup shares the head and takes this branch, so no
     // barrier is skipped)
     static_assert(WS >= 2 * V + 2 * WMAX + K, "per-wave LDS too small for the full read");
-    if (valid) full_read_item<KIND, K, V, WMAX, IO>(a, item, dp, lane, wscr + wave * WS);
+    if constexpr (DENSE) {
+      if (valid) full_read_item<KIND, K, V, WMAX, IO>(a, item, dp, lane, wscr + wave * WS);
+    }
     return;
   }
 
@@ -499,7 +503,8 @@ __global__ __launch_bounds__(256) void decode_kernel(const DecodeArgs a) {
     if ((CQ * 256 == R * K / 4 || i < R * K / 4) && (4 * i) / K < rh) cv[c].load(a.coef + (size_t)h * R * K + 4 * i);
   }
   compiler_fence();
-  // Every load of the item follows, with no wave-uniform guard: a wave past
+  // Every load of the item follows (the sketch panels after the slot
+  // products), with no wave-uniform guard: a wave past
   // the batch reads item 0 of its head (and returns after the barrier);
   // derived-field slots and sketch panels past what the step uses are clamped
   // to ones that exist and their values masked by selects.  A load under a
@@ -527,17 +532,7 @@ __global__ __launch_bounds__(256) void decode_kernel(const DecodeArgs a) {
       }
     }
   }
-  Raw<SK, PW> Ur[VPL][UP];           // sketch panels (value layout); panels past the rank read as zeros
-  if constexpr (U_PRELOAD) {
-#pragma unroll
-    for (int p = 0; p < NP; ++p)
-#pragma unroll
-      for (int vv = 0; vv < VPL; ++vv) {
-        const int pp = p * PW < rh ? p : 0;
-        Ur[vv][p].load_nt(Ub + (uint32_t)((pp * V + lane + 64 * vv) * PW));
-        Ur[vv][p].keep_if(p * PW < rh);
-      }
-  }
+  Raw<SK, PW> Ur[VPL][UP];           // sketch panels (value layout), loaded after the slot dot products
   // the item's state-dependent map factors (M, F1, F2; P > 0): this lane's
   // channels of M and, for its sketch columns, its part of an F2 row and its F1 row
   constexpr int MW = P > 0 ? K / 16 : 1, HQ = P > 0 ? R / 4 : 1;
@@ -584,6 +579,20 @@ __global__ __launch_bounds__(256) void decode_kernel(const DecodeArgs a) {
 
   float av[NG], bv[NG], at;
   slot_dots(r, n, row, qv, kv, gt, av, bv, at);
+  // the sketch panels: issued once the ring keys and decays are consumed, so
+  // their registers are not live across the slot products (KDA then fits four
+  // waves per SIMD); the buffer term and C products cover their latency.
+  // Panels past the head's rank re-read panel 0 and are zeroed.
+  if constexpr (U_PRELOAD) {
+#pragma unroll
+    for (int p = 0; p < NP; ++p)
+#pragma unroll
+      for (int vv = 0; vv < VPL; ++vv) {
+        const int pp = p * PW < rh ? p : 0;
+        Ur[vv][p].load_nt(Ub + (uint32_t)((pp * V + lane + 64 * vv) * PW));
+        Ur[vv][p].keep_if(p * PW < rh);
+      }
+  }
   float ca[NG], cg[NG], gcol[L::JP];
   buffer_coefs<L>(n, row, col, r, av, bv, b_l, ca, cg, gcol);
   float ut[VR], ob[VR];

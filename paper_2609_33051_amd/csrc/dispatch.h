@@ -16,7 +16,10 @@ constexpr int kUnsupported = -2;
 template <int KIND, int K, int V, int R, int WM, typename IO, typename SK, int P>
 int launch_decode(const DecodeArgs& a, hipStream_t s) {
   const unsigned tiles = (unsigned)((a.B + 3) / 4);
-  hipLaunchKernelGGL((decode_kernel<KIND, K, V, R, WM, IO, SK, P>), dim3((unsigned)a.H * tiles), dim3(256), 0, s, a);
+  if (a.ndense > 0)
+    hipLaunchKernelGGL((decode_kernel<KIND, K, V, R, WM, IO, SK, P, true>), dim3((unsigned)a.H * tiles), dim3(256), 0, s, a);
+  else
+    hipLaunchKernelGGL((decode_kernel<KIND, K, V, R, WM, IO, SK, P, false>), dim3((unsigned)a.H * tiles), dim3(256), 0, s, a);
   return 0;
 }
 

@@ -140,9 +140,11 @@ def main(argv=None):
             continue
         unit = f"{e}_{wl.kind}"
         digest = hip_build.source_digest(unit)
-        # sketch storage: the last template argument of decode/update (unsigned short = bf16)
+        # template arguments of update: ..., io, sketch, pivots; of decode: ...,
+        # io, sketch, pivots, dense (the dense-fallback instance); unsigned short = bf16
         targs = s[s.index("<") + 1:s.rindex(">")].split(", ")
-        # template arguments of decode/update: ..., io, sketch, pivots
+        if targs[-1] in ("true", "false"):
+            targs = targs[:-1]
         sketch = "bf16" if (e != "full_read" and targs[-2] == "unsigned short") else "f32"
         pivots = int(targs[-1]) if e != "full_read" else 0
         tag = (":bf16" if sketch == "bf16" else "") + (f":p{pivots}" if pivots else "")

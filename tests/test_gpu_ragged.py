@@ -71,6 +71,7 @@ def check_ragged(wl, head_ranks, window=None, steps=None, sketch="f32", pivots=0
     ("kda", 128, 128, 32, 8, "bf16", [32, 7, 0, 20]),
     ("mamba2_form", 64, 64, 8, 8, "f32", [1, 8, 0, 4]),
     ("gdn", 64, 64, 32, 16, "f32", [0, 31, 9, 2]),
+    ("kda", 128, 64, 16, 32, "bf16", [5, 0, 16, 0]),    # 32-slot window, two dense heads
 ])
 def test_ragged_small(fam, K, V, rank, window, io, ranks):
     wl = inputs.tiny(fam, batch=5, heads=len(ranks), dk=K, dv=V, rank=rank, window=window, steps=2 * window + 3,

@@ -435,6 +435,46 @@ __device__ __forceinline__ void full_read_item(const DecodeArgs& a, size_t item,
   }
 }
 
+// Ring f of slots 4 gi + row (components col + 16 p) for the read of slot n:
+// the slot is clamped below n and the load made unconditionally, the value
+// then masked by a select (a guarded load would compile to a branch whose
+// join waits for every load in flight).  bf16: lanes j and j^1 read the same
+// 32-bit word.  Slots are a 32-bit byte stride apart (the ABI bounds B*H).
+template <int NG, int RP, typename SK>
+__device__ __forceinline__ void load_ring_f(const DecodeArgs& a, size_t dp, int n, int row, int col, int rh, int R,
+                                            const SK* rf, float (&fs)[NG][RP]) {
+  const int smax = n > 0 ? n - 1 : 0;
+  const uint32_t slot_bytes = (uint32_t)((size_t)a.B * a.H * R * sizeof(SK));
+#pragma unroll
+  for (int p = 0; p < RP; ++p) {
+    const int j = col + 16 * p;
+    const char* lb = reinterpret_cast<const char*>(rf + dp * R) + (sizeof(SK) == 2 ? 4 * (j >> 1) : 4 * j);
+#pragma unroll
+    for (int gi = 0; gi < NG; ++gi) {
+      const int s = 4 * gi + row;
+      const uint32_t w = *reinterpret_cast<const uint32_t*>(lb + (uint64_t)(uint32_t)(s < smax ? s : smax) * slot_bytes);
+      const float fv = sizeof(SK) == 2 ? ((j & 1) ? bf16_hi(w) : bf16_lo(w)) : __uint_as_float(w);
+      fs[gi][p] = (s < n && j < rh) ? fv : 0.f;
+    }
+  }
+}
+
+// The item's state-dependent map factors (M, F1, F2): this lane's channels of
+// M and, for its sketch columns, its part of an F2 row and its F1 row.
+template <int K, int R, int P, int RP, typename SK, int MW, int HQ>
+__device__ __forceinline__ void load_map_factors(const DecodeArgs& a, size_t item, int row, int col, int rh,
+                                                 Raw<SK, MW>& mr, Raw<SK, HQ> (&f2r)[RP], Raw<SK, 4> (&f1r)[RP]) {
+  const SK* cm = static_cast<const SK*>(a.cmap) + item * (size_t)(P * K + R * P + R * R);
+  mr.load_nt(cm + (col >> 2) * K + ((col & 3) + 4 * row) * MW);
+#pragma unroll
+  for (int p = 0; p < RP; ++p) {
+    const int j = col + 16 * p;
+    f2r[p].load_nt(cm + P * K + R * P + j * R + row * HQ);
+    f2r[p].keep_if(row * HQ < rh);  // columns of F2 past the head's rank are not read
+    f1r[p].load(cm + P * K + j * P);
+  }
+}
+
 // DENSE: compiled with the exact read for dense-fallback heads (launched only
 // for rank tables that have some); without it the kernel needs fewer registers.
 template <int KIND, int K, int V, int R, int WMAX, typename IO, typename SK, int P, bool DENSE>
@@ -514,24 +554,6 @@ __global__ __launch_bounds__(256) void decode_kernel(const DecodeArgs a) {
   L r;
   r.load(a, item, dp, row, col);
   float fs[ERASE ? NG : 1][RP];      // ring f of slot 4 gi + row, component col + 16 p
-  if constexpr (ERASE) {
-    const int smax = n > 0 ? n - 1 : 0;
-    const uint32_t slot_bytes = (uint32_t)((size_t)a.B * H * R * sizeof(SK));
-#pragma unroll
-    for (int p = 0; p < RP; ++p) {
-      const int j = col + 16 * p;
-      // bf16: lanes j and j^1 read the same 32-bit word
-      const char* lb = reinterpret_cast<const char*>(static_cast<const SK*>(a.rf) + dp * R) +
-                       (sizeof(SK) == 2 ? 4 * (j >> 1) : 4 * j);
-#pragma unroll
-      for (int gi = 0; gi < NG; ++gi) {
-        const int s = 4 * gi + row;
-        const uint32_t w = *reinterpret_cast<const uint32_t*>(lb + (uint64_t)(uint32_t)(s < smax ? s : smax) * slot_bytes);
-        const float fv = sizeof(SK) == 2 ? ((j & 1) ? bf16_hi(w) : bf16_lo(w)) : __uint_as_float(w);
-        fs[gi][p] = (s < n && j < rh) ? fv : 0.f;
-      }
-    }
-  }
   Raw<SK, PW> Ur[VPL][UP];           // sketch panels (value layout), loaded after the slot dot products
   // the item's state-dependent map factors (M, F1, F2; P > 0): this lane's
   // channels of M and, for its sketch columns, its part of an F2 row and its F1 row
@@ -539,16 +561,14 @@ __global__ __launch_bounds__(256) void decode_kernel(const DecodeArgs a) {
   [[maybe_unused]] Raw<SK, MW> mr;
   [[maybe_unused]] Raw<SK, HQ> f2r[RP];
   [[maybe_unused]] Raw<SK, 4> f1r[RP];
-  if constexpr (P > 0) {
-    const SK* cm = static_cast<const SK*>(a.cmap) + item * (size_t)(P * K + R * P + R * R);
-    mr.load_nt(cm + (col >> 2) * K + ((col & 3) + 4 * row) * MW);
-#pragma unroll
-    for (int p = 0; p < RP; ++p) {
-      const int j = col + 16 * p;
-      f2r[p].load_nt(cm + P * K + R * P + j * R + row * HQ);
-      f2r[p].keep_if(row * HQ < rh);  // columns of F2 past the head's rank are not read
-      f1r[p].load(cm + P * K + j * P);
-    }
+  // f and the map factors are used only after the C products: with a
+  // per-channel decay (KDA) they are loaded with the sketch panels, after the
+  // slot products, which keeps the kernel within 128 registers (four waves per
+  // SIMD); the other kinds load them here, first
+  constexpr bool LATE_FM = CHAN;
+  if constexpr (!LATE_FM) {
+    if constexpr (ERASE) load_ring_f<NG, RP>(a, dp, n, row, col, rh, R, static_cast<const SK*>(a.rf), fs);
+    if constexpr (P > 0) load_map_factors<K, R, P, RP>(a, item, row, col, rh, mr, f2r, f1r);
   }
 
   // ---- this head's coefficient map C (R x K) into LDS; its loads were issued
@@ -592,6 +612,10 @@ __global__ __launch_bounds__(256) void decode_kernel(const DecodeArgs a) {
         Ur[vv][p].load_nt(Ub + (uint32_t)((pp * V + lane + 64 * vv) * PW));
         Ur[vv][p].keep_if(p * PW < rh);
       }
+  }
+  if constexpr (LATE_FM) {
+    if constexpr (ERASE) load_ring_f<NG, RP>(a, dp, n, row, col, rh, R, static_cast<const SK*>(a.rf), fs);
+    if constexpr (P > 0) load_map_factors<K, R, P, RP>(a, item, row, col, rh, mr, f2r, f1r);
   }
   float ca[NG], cg[NG], gcol[L::JP];
   buffer_coefs<L>(n, row, col, r, av, bv, b_l, ca, cg, gcol);

@@ -49,6 +49,22 @@ def _entry(short: str) -> str | None:
     return None
 
 
+def kernel_variant(short: str) -> tuple[str, str, int] | None:
+    """(entry, sketch dtype, pivots) of a kernel-trace name such as
+    decode_kernel<1, 128, 128, 16, 16, unsigned short, float, 0, false>:
+    update's template arguments end with io, sketch, pivots; decode's with io,
+    sketch, pivots, dense (its dense-fallback instance); full_read has no sketch."""
+    e = _entry(short)
+    if e is None:
+        return None
+    targs = short[short.index("<") + 1:short.rindex(">")].split(", ")
+    if targs[-1] in ("true", "false"):
+        targs = targs[:-1]
+    if e == "full_read":
+        return e, "f32", 0
+    return e, ("bf16" if targs[-2] == "unsigned short" else "f32"), int(targs[-1])
+
+
 def _counter(d, counter):
     """(per-kernel list of values in KiB, copy-kernel value) from one pmc run."""
     per, copy = {}, []
@@ -135,18 +151,12 @@ def main(argv=None):
     tpath = os.path.join(a.out, "traffic.json")
     table = json.load(open(tpath)) if os.path.exists(tpath) else {}
     for s, r in sorted(stats.items()):
-        e = _entry(s)
-        if e is None:
+        v = kernel_variant(s)
+        if v is None:
             continue
+        e, sketch, pivots = v
         unit = f"{e}_{wl.kind}"
         digest = hip_build.source_digest(unit)
-        # template arguments of update: ..., io, sketch, pivots; of decode: ...,
-        # io, sketch, pivots, dense (the dense-fallback instance); unsigned short = bf16
-        targs = s[s.index("<") + 1:s.rindex(">")].split(", ")
-        if targs[-1] in ("true", "false"):
-            targs = targs[:-1]
-        sketch = "bf16" if (e != "full_read" and targs[-2] == "unsigned short") else "f32"
-        pivots = int(targs[-1]) if e != "full_read" else 0
         tag = (":bf16" if sketch == "bf16" else "") + (f":p{pivots}" if pivots else "")
         ab = algo(e, sketch, pivots)
         fv, wv = fetch.get(s, []), write.get(s, [])

@@ -76,3 +76,16 @@ def test_bf16_storage_halves_f_and_the_map_factors():
     assert T.derived_write_bytes(f32, 5) - T.derived_write_bytes(b16, 5) == 2 * 16
     # the exact baseline keeps pi in fp32 whatever the sketch storage
     assert T.slot_read_bytes(f32, True) == T.slot_read_bytes(b16, True)
+
+
+def test_profile_summary_reads_kernel_variants():
+    """The profile summaries key each kernel-trace entry by entry point, sketch
+    dtype and pivot count, read from the kernel's template arguments."""
+    from paper_2609_33051_amd.profile_summary import kernel_variant
+    assert kernel_variant("decode_kernel<1, 128, 128, 16, 16, unsigned short, unsigned short, 4, false>") == \
+        ("decode", "bf16", 4)
+    assert kernel_variant("decode_kernel<0, 128, 64, 16, 16, unsigned short, float, 0, true>") == ("decode", "f32", 0)
+    assert kernel_variant("update_kernel<2, 128, 128, 16, 16, unsigned short, unsigned short, 0>") == \
+        ("update", "bf16", 0)
+    assert kernel_variant("full_read_kernel<1, 128, 128, 16, unsigned short>") == ("full_read", "f32", 0)
+    assert kernel_variant("state_layout_kernel") is None

@@ -127,6 +127,25 @@ def test_window_one_is_standard_recurrence(fam):
     assert err <= 1e-5 and errS <= 1e-5
 
 
+@pytest.mark.parametrize("name", ["mamba2_b256", "gdn_b512", "kda_b512"])
+def test_window_one_full_size(name):
+    """Standard decoding as the benchmark times it (window 1, rank 0: every
+    token reads and writes the whole state) at the paper's shapes, sampled
+    items against the plain recurrence."""
+    import oracle
+    wl = inputs.WORKLOADS[name]
+    sel = sample_items(wl)
+    announce(f"window 1 full size {name}")
+    run, layer, S_sel, heads, _ = run_workload(wl, window=1, baseline=True, steps=4, sel=sel)
+    q, k, v, beta, logd = (np.stack(run.inp[x]) for x in ("q", "k", "v", "beta", "log_decay"))
+    o_ex, S_ex = oracle.recurrence(wl.kind, S_sel, q, k, v, beta, logd)
+    err = max_step_rel(run.o_gpu, o_ex)
+    idx = torch.as_tensor(sel, device="cuda")
+    errS = rel_l2(to_np32(layer.state().reshape(-1, wl.dv, wl.dk)[idx]), S_ex)
+    print(f"  max step rel-L2 {err:.3e} state {errS:.3e}", flush=True)
+    assert err <= 2e-3 and errS <= 2e-3
+
+
 def test_rerun_is_bitwise_identical():
     wl = inputs.tiny("gdn", batch=5, heads=3, dk=128, dv=128, rank=16, window=8, steps=20, io="bf16")
     announce("determinism gdn")

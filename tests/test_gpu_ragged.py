@@ -109,16 +109,18 @@ def test_ragged_full_rank_table_matches_uniform():
     assert torch.equal(la.S, lb.S) and torch.equal(la.U, lb.U)
 
 
+@pytest.mark.parametrize("sketch,pivots", [("f32", 0), ("bf16", 4)])
 @pytest.mark.parametrize("name", ["gdn_b512", "kda_b512"])
-def test_ragged_full_size(name):
+def test_ragged_full_size(name, sketch, pivots):
     """The paper-shape workloads with a mixed table (about a tenth of the heads
-    dense), sampled items, in the launch configuration the benchmark times."""
+    dense), sampled items, in the launch configuration the benchmark times;
+    bf16 with 4 pivots is the paper's method with its storage."""
     wl = inputs.WORKLOADS[name]
     ranks = inputs.ragged_ranks(wl)
     rng = np.random.default_rng(11)
     items = wl.batch * wl.heads
     sel = np.unique(np.concatenate([[0, items - 1], rng.choice(items, size=48, replace=False)]))
-    check_ragged(wl, ranks, steps=wl.window + 5, sel=sel)
+    check_ragged(wl, ranks, steps=wl.window + 5, sel=sel, sketch=sketch, pivots=pivots)
 
 
 def structured_states(H, n, K, V, seed):

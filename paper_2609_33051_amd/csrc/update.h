@@ -317,8 +317,14 @@ __global__ __launch_bounds__(256, 3) void update_kernel(const UpdateArgs a) {
   // small factors shared by the workgroup
   static_assert(P == 0 || (P == 4 && R >= 8 && R <= 32), "pivot maps: P = 4, rank 8..32");
   constexpr int XP = 20;                                        // row pitch of a transposed 16 x 16 block
-  __shared__ __align__(16) float cmX[P > 0 ? 4 * 16 * XP : 4];  // [wave][16 values][16 keys]
-  __shared__ __align__(16) float cmU[P > 0 ? 4 * 16 * 4 : 4];   // [wave][16 values][P]
+  // When the key staging Ls has room, that scratch lives in Ls: every tile is
+  // then updated first and sketched after a barrier, once Ls is dead.  This
+  // keeps the kernel's LDS that of the offline-map flush (four workgroups per CU).
+  constexpr bool CM_ALIAS = P > 0 && SP * LP >= 4 * 16 * XP + 4 * 16 * 4;
+  __shared__ __align__(16) float cmXs[P > 0 && !CM_ALIAS ? 4 * 16 * XP : 4];
+  __shared__ __align__(16) float cmUs[P > 0 && !CM_ALIAS ? 4 * 16 * 4 : 4];
+  float* const cmX = CM_ALIAS ? Ls : cmXs;                 // [wave][16 values][16 keys]
+  float* const cmU = CM_ALIAS ? Ls + 4 * 16 * XP : cmUs;   // [wave][16 values][P]
   __shared__ __align__(16) float cmS[P > 0 ? 8 + 16 + 5 * R : 4];  // mu parts, R^{-1}/sqrt(mu), L_G and w
   floatx4 nacc[P > 0 ? MT : 1];    // N^T (rows a = 4 lg + i), per k tile, this wave's values
   float gpart[P > 0 ? RT : 1][4][5];  // sketch Gram: U[v][j] U[v][a] (a < 4) and U[v][j]^2, this lane's values
@@ -599,13 +605,18 @@ __global__ __launch_bounds__(256, 3) void update_kernel(const UpdateArgs a) {
     }
   }
 
-  // ---- matrix-core phase, one 16-column value tile at a time
+  // ---- matrix-core phase, one 16-column value tile at a time (with CM_ALIAS:
+  // pass 0 updates and stores every tile, pass 1 sketches them)
+  constexpr int PASSES = CM_ALIAS ? 2 : 1;
+#pragma unroll
+  for (int ps = 0; ps < PASSES; ++ps) {
+  if (ps == 1) lds_barrier();  // every wave is done with Ls before the map's scratch reuses it
 #pragma unroll
   for (int t = 0; t < VTW; ++t) {
     const int vt = wave + 4 * t;
     if (vt >= VT) continue;
     const int v = 16 * vt + lr;
-    if (flush) {
+    if (flush && ps == 0) {
       // value-side factors of the rank update, C layout: slot s = 16 st + 4 lg + i
       floatx4 wv[ST];
 #pragma unroll
@@ -654,10 +665,17 @@ __global__ __launch_bounds__(256, 3) void update_kernel(const UpdateArgs a) {
         p = cross_row_sum(p);
         if (lg == 0) a.o[item * V + v] = p;
       }
+      // the state is final: store it before the sketch and map products
+      {
+        float* dst = a.S + item * V * K + (size_t)(vt * MT) * 256 + 4 * lane;
+#pragma unroll
+        for (int kt = 0; kt < MT; ++kt)
+          st_nt(reinterpret_cast<float4*>(dst + 256 * kt), make_float4(xs[t][kt][0], xs[t][kt][1], xs[t][kt][2], xs[t][kt][3]));
+      }
     }
     // sketch U^T = Omega^T X^T  (rows j = 16 jt + 4 lg + i of the C layout)
     if constexpr (R > 0) {
-      if (want_U) {
+      if (want_U && ps == PASSES - 1) {
         const float* om = a.omega + (size_t)h * K * R;
         float4 up4 = make_float4(0.f, 0.f, 0.f, 0.f);  // U[v][0..3] (state-dependent map)
         float aop[4] = {0.f, 0.f, 0.f, 0.f};            // U_p^T as the A operand of N^T = U_p^T X
@@ -732,12 +750,7 @@ __global__ __launch_bounds__(256, 3) void update_kernel(const UpdateArgs a) {
         }
       }
     }
-    if (flush) {
-      float* dst = a.S + item * V * K + (size_t)(vt * MT) * 256 + 4 * lane;
-#pragma unroll
-      for (int kt = 0; kt < MT; ++kt)
-        st_nt(reinterpret_cast<float4*>(dst + 256 * kt), make_float4(xs[t][kt][0], xs[t][kt][1], xs[t][kt][2], xs[t][kt][3]));
-    }
+  }
   }
 
   if constexpr (P > 0) {

@@ -259,8 +259,12 @@ __device__ __forceinline__ void coef_map_tail(const UpdateArgs& a, size_t item, 
   }
 }
 
+// Three workgroups per CU, or four for the state-dependent map at window 16
+// and rank <= 16: its flush spends part of each workgroup's life off the
+// memory bus (the map's products and algebra), so occupancy pays there, even
+// with the few registers the per-channel-decay instance then spills.
 template <int KIND, int K, int V, int R, int WMAX, typename IO, typename SK, int P>
-__global__ __launch_bounds__(256, 3) void update_kernel(const UpdateArgs a) {
+__global__ __launch_bounds__(256, (P > 0 && WMAX == 16 && R <= 16) ? 4 : 3) void update_kernel(const UpdateArgs a) {
   constexpr bool ERASE = KIND != MAMBA2;
   constexpr bool CHAN = KIND == KDA;
   constexpr int MT = K / 16;          // k tiles

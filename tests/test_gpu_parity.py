@@ -232,6 +232,8 @@ def test_bf16_sketch_full_size(name):
     ("kda", 128, 128, 32, 8, "bf16", "f32"),
     ("gdn", 64, 64, 32, 32, "f32", "f32"),
     ("mamba2", 128, 64, 16, 16, "bf16", "bf16"),
+    ("kda", 64, 64, 16, 16, "bf16", "f32"),     # map scratch in its own LDS (no room in the key staging)
+    ("kda", 128, 128, 16, 16, "bf16", "bf16"),  # the four-workgroup instance
 ])
 def test_pivot_map_small(fam, K, V, rank, window, io, sketch):
     wl = inputs.tiny(fam, batch=5, heads=3, dk=K, dv=V, rank=rank, window=window, steps=2 * window + 3, io=io)

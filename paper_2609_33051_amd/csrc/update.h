@@ -104,7 +104,9 @@ __device__ __forceinline__ void coef_map_tail(const UpdateArgs& a, size_t item, 
   if (wave == 0) {
     const float fro = cmS[0] + cmS[1] + cmS[2] + cmS[3];
     const float mu = fro > 0.f ? fro / K : 1.f;
-    const float rs = 1.f / sqrtf(mu);
+    // the algebra is one serial chain on one wave while the other waves wait:
+    // hardware reciprocal, square root and reciprocal square root (1 ulp) keep it short
+    const float rs = __builtin_amdgcn_rsqf(mu);
     // pivot Gram, Cholesky with dropping, R^{-1} (all lanes, uniform)
     float Gp[P][P], Rm[P][P], Ri[P][P];
 #pragma unroll
@@ -121,27 +123,29 @@ __device__ __forceinline__ void coef_map_tail(const UpdateArgs& a, size_t item, 
 #pragma unroll
       for (int b = 0; b < x; ++b) sd -= Rm[b][x] * Rm[b][x];
       if (Gp[x][x] > 0.f && sd > 1e-6f * Gp[x][x]) {
-        const float rxx = sqrtf(sd);
+        const float rxx = __builtin_amdgcn_sqrtf(sd), irx = __builtin_amdgcn_rcpf(rxx);
         Rm[x][x] = rxx;
 #pragma unroll
         for (int y = x + 1; y < P; ++y) {
           float e = Gp[x][y];
 #pragma unroll
           for (int b = 0; b < x; ++b) e -= Rm[b][x] * Rm[b][y];
-          Rm[x][y] = e / rxx;
+          Rm[x][y] = e * irx;
         }
       }
     }
 #pragma unroll
+    for (int x = 0; x < P; ++x)
+      if (Rm[x][x] > 0.f) Ri[x][x] = __builtin_amdgcn_rcpf(Rm[x][x]);
+#pragma unroll
     for (int x = 0; x < P; ++x) {
-      if (Rm[x][x] > 0.f) Ri[x][x] = 1.f / Rm[x][x];
 #pragma unroll
       for (int y = x + 1; y < P; ++y) {
         if (Rm[y][y] > 0.f) {
           float e = 0.f;
 #pragma unroll
           for (int b = x; b < y; ++b) e += Ri[x][b] * Rm[b][y];
-          Ri[x][y] = -e / Rm[y][y];
+          Ri[x][y] = -e * Ri[y][y];
         }
       }
     }
@@ -164,7 +168,7 @@ __device__ __forceinline__ void coef_map_tail(const UpdateArgs& a, size_t item, 
         l2 += LG[c] * LG[c];
       }
       dg = fmaxf(diag / mu - l2, 0.f);
-      dinv = 1.f / (dg + a.ridge);
+      dinv = __builtin_amdgcn_rcpf(dg + a.ridge);
     }
     // T = I + L_G^T D^{-1} L_G (sum over the lanes g), then its inverse
     float Tm[P][P];
@@ -183,7 +187,7 @@ __device__ __forceinline__ void coef_map_tail(const UpdateArgs& a, size_t item, 
       for (int y = 0; y < P; ++y) Ti[x][y] = (x == y) ? 1.f : 0.f;
 #pragma unroll
     for (int c = 0; c < P; ++c) {  // Gauss-Jordan on the SPD T (pivots >= 1)
-      const float inv = 1.f / Tm[c][c];
+      const float inv = __builtin_amdgcn_rcpf(Tm[c][c]);
 #pragma unroll
       for (int y = 0; y < P; ++y) {
         Tm[c][y] *= inv;

@@ -36,6 +36,7 @@ _SRC = os.path.join(_HERE, "sketchssm_oracle.c")
 _LIB = os.path.join(_HERE, "liboracle.so")
 
 KINDS = {"mamba2": 0, "gdn": 1, "kda": 2}
+EXACT = -1  # pivots value of the state-dependent map with the exact (dense) state metric
 
 
 class _Cfg(ctypes.Structure):
@@ -178,16 +179,18 @@ def sketchssm(kind, W, heads, omega, coef, S_init, q, k, v, beta, log_decay, rou
     heads: [n] int, head index of every item (selects Omega / C); omega
     [H][K][G]; coef [H][G][K].  G = 0 (omega.shape[2] == 0) disables the
     sketch (o_state_hat is then 0 between flushes).  round_storage stores the
-    state and the sketch as fp32; sketch_bf16 stores the sketch as bf16
-    (round to nearest, ties to even, through fp32), the paper's storage, and
-    with it the projected erase factors f_s and the state-dependent map's
-    factors.  paper_path computes the coefficients through f_s (eq. wyread,
-    app-projected-query) and the map through its Woodbury factors (implied by
-    sketch_bf16; without rounding it equals the direct forms).
-    pivots > 0 replaces the given coef by the state-dependent coefficient map
-    with that many pivots and ridge term `ridge` (lambda), rebuilt from the
-    state at the start and at every flush; coef_final returns the map in use
-    at the end.
+    state, the sketch and the state-dependent map as fp32; sketch_bf16 stores
+    the sketch, the state-dependent map (the dense G x K matrix, rounded once
+    per flush) and the projected erase factors f_s (rounded when first read)
+    as bf16 (round to nearest, ties to even, through fp32), the paper's
+    storage.  paper_path computes the coefficients through f_s (eq. wyread,
+    app-projected-query; implied by sketch_bf16; without rounding it equals
+    c = C q~).
+    pivots != 0 replaces the given coef by the state-dependent coefficient
+    map with ridge term `ridge` (lambda), rebuilt from the state at the start
+    and at every flush: P > 0 pivots use the low-rank-plus-diagonal metric of
+    eq. pivot-metric, pivots = EXACT the exact metric H (eq. pivot-ridge as
+    written); coef_final returns the map in use at the end (as stored).
     """
     lib = lib or _load()
     n, K, V, T = _check_inputs(kind, S_init, q, k, v, beta, log_decay)

@@ -22,15 +22,18 @@
  *     at a time (eq. m-reads), and flushes replay the buffered tokens one at a
  *     time through the update (eq. transition-update, Algorithm 1).
  *   - The only optional deviations from pure fp64 are `round_storage`, which
- *     rounds the full state and the sketch to fp32 at the points where the
- *     method writes them back (the paper keeps the state in FP32 storage,
- *     Appendix "Detailed Evaluation Setup"), and `sketch_bf16`, which rounds
- *     to bf16 what the paper stores in BF16 (Appendix "State Memory Traffic
- *     Reduction"): the sketch, the projected erase factors f_s and the
- *     coefficient map; arithmetic stays fp64.  Those f_s and the map's factors
- *     only exist on the `paper_path` (the paper's coefficient-space forms),
- *     which bf16 storage therefore selects; without rounding it equals the
- *     direct forms (pinned).
+ *     rounds the full state, the sketch and the coefficient map to fp32 at
+ *     the points where the method writes them back (the paper keeps the state
+ *     in FP32 storage, Appendix "Detailed Evaluation Setup"), and
+ *     `sketch_bf16`, which rounds to bf16 what the paper stores in BF16
+ *     (Appendix "State Memory Traffic Reduction"): the sketch U, the
+ *     state-dependent coefficient map C (the dense G x K matrix, rounded once
+ *     when a flush writes it) and the projected erase factors f_s (rounded
+ *     when slot s is first read; the current token's f_t is used as
+ *     computed).  Arithmetic stays fp64.  The f_s only exist on the
+ *     `paper_path` (the paper's coefficient-space forms), which bf16 storage
+ *     therefore selects; without rounding it equals the direct form c = C q~
+ *     (pinned).
  *
  * Pins (see tests/test_oracle_pins.py): brute-force closed forms of the
  * recurrence on tiny inputs, the delta-rule retrieval invariant, the
@@ -56,16 +59,16 @@ typedef struct {
   int32_t W;             /* window: tokens applied per flush                */
   int32_t T;             /* decode steps                                    */
   int32_t round_storage; /* 1: state and sketch stored as fp32              */
-  int32_t sketch_bf16;   /* 1: sketch, projected erase factors and map factors
-                            stored as bf16 (the paper's storage; implies
-                            paper_path)                                      */
-  int32_t pivots;        /* 0: the given map C; P > 0: state-dependent map  */
+  int32_t sketch_bf16;   /* 1: sketch, coefficient map and projected erase
+                            factors stored as bf16 (the paper's storage;
+                            implies paper_path)                              */
+  int32_t pivots;        /* 0: the given map C; P > 0: the state-dependent
+                            map with the P-pivot metric; -1: the state-
+                            dependent map with the exact metric H            */
   float ridge;           /* lambda of the state-dependent map               */
   int32_t paper_path;    /* 1: coefficients through the projected erase
-                            factors f_s (eq. wyread, app-projected-query) and
-                            the state-dependent map through its Woodbury
-                            factors (the appendix's steps 3-4); 0: c = C q~
-                            and the map by a direct solve                     */
+                            factors f_s (eq. wyread, app-projected-query);
+                            0: c = C q~ from the effective query              */
 } orc_cfg;
 
 /* Per-item views of the per-step inputs.  Step inputs are laid out
@@ -182,6 +185,12 @@ static void store_sketch(const orc_cfg* c, double* U, size_t n)
   }
 }
 
+/* The state-dependent map C (G x K) as a flush stores it: like the sketch. */
+static void store_map(const orc_cfg* c, double* Cm, size_t n)
+{
+  store_sketch(c, Cm, n);
+}
+
 /* U = S^T Omega  (V x G), Omega is this head's K x G block. */
 static void make_sketch(int K, int V, int G, const double* S, const float* omega, double* U)
 {
@@ -195,19 +204,21 @@ static void make_sketch(int K, int V, int G, const double* S, const float* omega
 
 /* ------------------------------------------------------------------------ */
 /* State-dependent coefficient map (Sec. 4.1, eq. m-coeff, solved with the   */
-/* ridge term and the low-rank-plus-diagonal state metric of the appendix    */
-/* "Low-Rank-Plus-Diagonal Approximation for the Coefficient Map"), in the   */
-/* paper's basis-aligned coordinates and order of steps:                     */
+/* ridge term of the appendix "Low-Rank-Plus-Diagonal Approximation for the  */
+/* Coefficient Map", eq. pivot-ridge), in the paper's basis-aligned          */
+/* coordinates and order of steps:                                           */
 /*   R       orthogonal K x K whose first G rows are Omega^T (Omega completed  */
 /*           by Gram-Schmidt over the unit vectors), J = first G coordinates */
 /*   S'      = R S,  mu = |S'|_F^2 / K (1 for a zero state),  H = S' S'^T/mu */
+/* exact metric (pivots < 0): Hm = H, the dense state metric;                */
+/* P pivots (eq. pivot-metric):                                              */
 /*   Q       orthonormal basis of the first p = min(G, P) columns of U       */
 /*           (Gram-Schmidt; a column dependent on the earlier ones is dropped)*/
 /*   L       = S' Q / sqrt(mu),  d_i = max(H_ii - |L_i|^2, 0)                */
-/*   Hhat    = L L^T + Diag(d)                                               */
-/*   c       = (J^T Hhat J + lambda I)^{-1} J^T Hhat x,  x = R q~            */
-/* so c = Cm q~ with Cm = (J^T Hhat J + lambda I)^{-1} J^T Hhat R (G x K),    */
-/* solved directly by Gaussian elimination with partial pivoting.            */
+/*   Hm      = Hhat = L L^T + Diag(d)                                        */
+/* then c = (J^T Hm J + lambda I)^{-1} J^T Hm x,  x = R q~, so c = Cm q~ with */
+/* Cm = (J^T Hm J + lambda I)^{-1} J^T Hm R (G x K), solved directly by      */
+/* Gaussian elimination with partial pivoting.                               */
 /* ------------------------------------------------------------------------ */
 typedef struct {
   double *R, *Sp, *H, *Q, *L, *d, *Hh, *A, *B;
@@ -283,106 +294,46 @@ static void coef_map(const orc_cfg* c, int K, int V, int G, const double* S, con
       for (int j = 0; j < V; ++j) acc += w->Sp[(size_t)i * V + j] * w->Sp[(size_t)i2 * V + j];
       w->H[(size_t)i * K + i2] = acc / mu;
     }
-  /* Q: the first p columns of U, orthonormalised (stored as rows of length V) */
-  int pq = 0;
-  for (int a = 0; a < p; ++a) {
-    double nrm = 0.0;
-    for (int j = 0; j < V; ++j) {
-      x[j] = U[(size_t)j * G + a];
-      nrm += x[j] * x[j];
-    }
-    if (nrm > 0.0 && gram_schmidt(x, w->Q, pq, V, sqrt(nrm))) memcpy(w->Q + (size_t)pq++ * V, x, sizeof(double) * V);
-  }
-  /* L = S' Q / sqrt(mu) (K x pq), d, Hhat */
-  const double rs = 1.0 / sqrt(mu);
-  for (int i = 0; i < K; ++i)
-    for (int a = 0; a < pq; ++a) {
-      double acc = 0.0;
-      for (int j = 0; j < V; ++j) acc += w->Sp[(size_t)i * V + j] * w->Q[(size_t)a * V + j];
-      w->L[(size_t)i * pq + a] = acc * rs;
-    }
-  for (int i = 0; i < K; ++i) {
-    double l2 = 0.0;
-    for (int a = 0; a < pq; ++a) l2 += w->L[(size_t)i * pq + a] * w->L[(size_t)i * pq + a];
-    const double r = w->H[(size_t)i * K + i] - l2;
-    w->d[i] = r > 0.0 ? r : 0.0;
-  }
-  for (int i = 0; i < K; ++i)
-    for (int i2 = 0; i2 < K; ++i2) {
-      double acc = (i == i2) ? w->d[i] : 0.0;
-      for (int a = 0; a < pq; ++a) acc += w->L[(size_t)i * pq + a] * w->L[(size_t)i2 * pq + a];
-      w->Hh[(size_t)i * K + i2] = acc;
-    }
-  if (c->paper_path || c->sketch_bf16) {
-    /* The appendix's steps 3-4: L_G = J^T L, D_G = Diag(J^T d) + lambda I,
-     * T_P = I + L_G^T D_G^{-1} L_G (Woodbury), so that
-     *   c = F1 (M q~) + F2 (Omega^T q~),  M = L^T R (pq x K),
-     *   F1 = D_G^{-1} L_G T_P^{-1},  F2 = (D_G + L_G L_G^T)^{-1} Diag(J^T d);
-     * the three factors are what is stored (bf16 with the paper's storage). */
-    const int p = pq;
-    double Tp[16], Ti[16], F1[1024 * 4], F2row[1024], Mrow[4][1024];
-    for (int a = 0; a < p; ++a)
-      for (int b = 0; b < p; ++b) {
-        double acc = (a == b) ? 1.0 : 0.0;
-        for (int g = 0; g < G; ++g) acc += w->L[(size_t)g * pq + a] * w->L[(size_t)g * pq + b] / (w->d[g] + lambda);
-        Tp[a * 4 + b] = acc;
-        Ti[a * 4 + b] = (a == b) ? 1.0 : 0.0;
+  const double* Hm = w->H; /* the exact metric (pivots < 0) */
+  if (P > 0) {
+    /* Q: the first p columns of U, orthonormalised (stored as rows of length V) */
+    int pq = 0;
+    for (int a = 0; a < p; ++a) {
+      double nrm = 0.0;
+      for (int j = 0; j < V; ++j) {
+        x[j] = U[(size_t)j * G + a];
+        nrm += x[j] * x[j];
       }
-    for (int col = 0; col < p; ++col) { /* Gauss-Jordan, T_P is symmetric positive definite */
-      const double inv = 1.0 / Tp[col * 4 + col];
-      for (int j = 0; j < p; ++j) { Tp[col * 4 + j] *= inv; Ti[col * 4 + j] *= inv; }
-      for (int r = 0; r < p; ++r) {
-        if (r == col) continue;
-        const double f = Tp[r * 4 + col];
-        for (int j = 0; j < p; ++j) { Tp[r * 4 + j] -= f * Tp[col * 4 + j]; Ti[r * 4 + j] -= f * Ti[col * 4 + j]; }
-      }
+      if (nrm > 0.0 && gram_schmidt(x, w->Q, pq, V, sqrt(nrm))) memcpy(w->Q + (size_t)pq++ * V, x, sizeof(double) * V);
     }
-    for (int g = 0; g < G; ++g)
-      for (int a = 0; a < p; ++a) {
+    /* L = S' Q / sqrt(mu) (K x pq), d, Hhat */
+    const double rs = 1.0 / sqrt(mu);
+    for (int i = 0; i < K; ++i)
+      for (int a = 0; a < pq; ++a) {
         double acc = 0.0;
-        for (int b = 0; b < p; ++b) acc += w->L[(size_t)g * pq + b] * Ti[b * 4 + a];
-        F1[g * 4 + a] = acc / (w->d[g] + lambda);
+        for (int j = 0; j < V; ++j) acc += w->Sp[(size_t)i * V + j] * w->Q[(size_t)a * V + j];
+        w->L[(size_t)i * pq + a] = acc * rs;
       }
-    for (int a = 0; a < p; ++a)
-      for (int kk = 0; kk < K; ++kk) {
-        double acc = 0.0;
-        for (int i = 0; i < K; ++i) acc += w->L[(size_t)i * pq + a] * w->R[(size_t)i * K + kk];
-        Mrow[a][kk] = acc;
-      }
-    if (c->sketch_bf16) {
-      for (int g = 0; g < G; ++g)
-        for (int a = 0; a < p; ++a) F1[g * 4 + a] = bf16_rne(F1[g * 4 + a]);
-      for (int a = 0; a < p; ++a)
-        for (int kk = 0; kk < K; ++kk) Mrow[a][kk] = bf16_rne(Mrow[a][kk]);
+    for (int i = 0; i < K; ++i) {
+      double l2 = 0.0;
+      for (int a = 0; a < pq; ++a) l2 += w->L[(size_t)i * pq + a] * w->L[(size_t)i * pq + a];
+      const double r = w->H[(size_t)i * K + i] - l2;
+      w->d[i] = r > 0.0 ? r : 0.0;
     }
-    for (int g = 0; g < G; ++g) {
-      /* row g of F2 = e_g^T (D_G^{-1} - D_G^{-1} L_G T_P^{-1} L_G^T D_G^{-1}) Diag(J^T d) */
-      for (int g2 = 0; g2 < G; ++g2) {
-        double corr = 0.0;
-        for (int a = 0; a < p; ++a) {
-          double la = 0.0;  /* (F1 unrounded) row g times L_G row g2 */
-          for (int b = 0; b < p; ++b) la += w->L[(size_t)g * pq + b] * Ti[b * 4 + a];
-          corr += la / (w->d[g] + lambda) * w->L[(size_t)g2 * pq + a];
-        }
-        const double dg2 = w->d[g2];
-        F2row[g2] = ((g == g2 ? 1.0 : 0.0) / (w->d[g] + lambda) - corr / (w->d[g2] + lambda)) * dg2;
-        if (c->sketch_bf16) F2row[g2] = bf16_rne(F2row[g2]);
+    for (int i = 0; i < K; ++i)
+      for (int i2 = 0; i2 < K; ++i2) {
+        double acc = (i == i2) ? w->d[i] : 0.0;
+        for (int a = 0; a < pq; ++a) acc += w->L[(size_t)i * pq + a] * w->L[(size_t)i2 * pq + a];
+        w->Hh[(size_t)i * K + i2] = acc;
       }
-      for (int kk = 0; kk < K; ++kk) {
-        double acc = 0.0;
-        for (int a = 0; a < p; ++a) acc += F1[g * 4 + a] * Mrow[a][kk];
-        for (int g2 = 0; g2 < G; ++g2) acc += F2row[g2] * (double)Om[(size_t)kk * G + g2];
-        Cm[(size_t)g * K + kk] = acc;
-      }
-    }
-    return;
+    Hm = w->Hh;
   }
-  /* A = J^T Hhat J + lambda I (G x G);  B = J^T Hhat R (G x K) */
+  /* A = J^T Hm J + lambda I (G x G);  B = J^T Hm R (G x K) */
   for (int g = 0; g < G; ++g) {
-    for (int g2 = 0; g2 < G; ++g2) w->A[(size_t)g * G + g2] = w->Hh[(size_t)g * K + g2] + (g == g2 ? lambda : 0.0);
+    for (int g2 = 0; g2 < G; ++g2) w->A[(size_t)g * G + g2] = Hm[(size_t)g * K + g2] + (g == g2 ? lambda : 0.0);
     for (int kk = 0; kk < K; ++kk) {
       double acc = 0.0;
-      for (int i = 0; i < K; ++i) acc += w->Hh[(size_t)g * K + i] * w->R[(size_t)i * K + kk];
+      for (int i = 0; i < K; ++i) acc += Hm[(size_t)g * K + i] * w->R[(size_t)i * K + kk];
       w->B[(size_t)g * K + kk] = acc;
     }
   }
@@ -488,9 +439,10 @@ int orc_recurrence(const orc_cfg* c, const float* S_init, const float* q, const 
 /*   S_final      [n][V][K]  the full state after the last flush             */
 /*   U_final      [n][V][G]  the sketch after the last flush                 */
 /*   coef_final   [n][G][K]  the coefficient map in use after the last flush */
-/* With c->pivots > 0 the map is state-dependent: built from the state and   */
-/* its (unrounded) sketch at the start and at every flush (coef_map above);  */
-/* otherwise it is the given C of the item's head.                           */
+/* With c->pivots != 0 the map is state-dependent: built from the state and  */
+/* its (unrounded) sketch at the start and at every flush (coef_map above)   */
+/* and stored (store_map: rounded like the sketch); otherwise it is the      */
+/* given C of the item's head.                                               */
 /* The exact windowed output (what a full-state read would give) is         */
 /* o_state + o_buf at every step.                                           */
 /* ------------------------------------------------------------------------ */
@@ -500,7 +452,7 @@ int orc_sketchssm(const orc_cfg* c, const int32_t* heads, const float* omega, co
                   double* S_final, double* U_final, double* coef_final)
 {
   if (!c || c->K <= 0 || c->V <= 0 || c->n_items <= 0 || c->T < 0 || c->W < 1 || c->G < 0) return -1;
-  if (c->K > 1024 || c->V > 1024 || c->G > 1024 || c->pivots < 0 || c->pivots > 4) return -1;
+  if (c->K > 1024 || c->V > 1024 || c->G > 1024 || c->pivots < -1 || c->pivots > 4) return -1;
   const int K = c->K, V = c->V, G = c->G, NI = c->n_items, W = c->W;
   const int fpath = (c->paper_path || c->sketch_bf16) && has_erase(c) && G > 0;
   if (fpath && W > 64) return -1;
@@ -512,7 +464,7 @@ int orc_sketchssm(const orc_cfg* c, const int32_t* heads, const float* omega, co
     const float* Cm = coef ? coef + (size_t)h * G * K : NULL;
     double* S0 = (double*)malloc(sizeof(double) * (size_t)K * V);
     double* U = (double*)malloc(sizeof(double) * ((size_t)V * (G > 0 ? G : 1)));
-    const int statedep = c->pivots > 0 && G > 0;
+    const int statedep = c->pivots != 0 && G > 0;
     double* Cmi = statedep ? (double*)malloc(sizeof(double) * (size_t)G * K) : NULL;
     orc_cmap_work cw = {0};
     if (statedep && (!Cmi || !cmap_work_alloc(&cw, K, V, G))) {
@@ -532,7 +484,10 @@ int orc_sketchssm(const orc_cfg* c, const int32_t* heads, const float* omega, co
     /* Initialise the sketch from the prefill state (Algorithm 1). */
     if (G > 0) {
       make_sketch(K, V, G, S0, Om, U);
-      if (statedep && Cmi && cw.R) coef_map(c, K, V, G, S0, Om, U, Cmi, &cw);
+      if (statedep && Cmi && cw.R) {
+        coef_map(c, K, V, G, S0, Om, U, Cmi, &cw);
+        store_map(c, Cmi, (size_t)G * K);
+      }
       store_sketch(c, U, (size_t)V * G);
     }
     int len = 0; /* tokens in the buffer B */
@@ -640,7 +595,10 @@ int orc_sketchssm(const orc_cfg* c, const int32_t* heads, const float* omega, co
         read_state(K, V, S0, x, ostate);
         if (G > 0) {
           make_sketch(K, V, G, S0, Om, U);
-          if (statedep && Cmi && cw.R) coef_map(c, K, V, G, S0, Om, U, Cmi, &cw);
+          if (statedep && Cmi && cw.R) {
+            coef_map(c, K, V, G, S0, Om, U, Cmi, &cw);
+            store_map(c, Cmi, (size_t)G * K);
+          }
           store_sketch(c, U, (size_t)V * G);
         }
         for (int j = 0; j < V; ++j) {

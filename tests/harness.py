@@ -77,3 +77,76 @@ def oracle_of(wl, run, S_sel, heads, om, C, window=None, sketch="f32", pivots=0)
 
 def max_step_rel(o_gpu_list, o_ref):
     return max(rel_l2(o_gpu_list[t], o_ref[t]) for t in range(len(o_gpu_list)))
+
+
+def item_err(a, b) -> np.ndarray:
+    """Error of every (request, head) item against the typical item size:
+    a, b are [..., n, X] (any leading axes such as steps, n items, X values
+    per item); returns [..., n] with ||a_i - b_i|| / rms_j ||b_j||, the rms
+    taken over the n items of the same leading index.  Unlike ||a_i - b_i|| /
+    ||b_i|| it does not blow up for an item whose output happens to be small
+    (rounding noise of the same absolute size then looks large), and like it,
+    it exposes one wrong item or one wrong value channel that an aggregate
+    over many items dilutes."""
+    a = np.asarray(a, np.float64)
+    b = np.asarray(b, np.float64)
+    num = np.linalg.norm(a - b, axis=-1)
+    den = np.sqrt(np.mean(np.linalg.norm(b, axis=-1) ** 2, axis=-1, keepdims=True))
+    return np.where(den > 0, num / np.where(den > 0, den, 1.0), num)
+
+
+# Bars.  The headline bar is the method's target: relative L2 over every
+# compared item and channel, per step, <= 1e-5 for fp32 inputs and <= 2e-3
+# for bf16 inputs with an fp32 state.  Both sides consume the same stored
+# inputs (bf16 values upcast exactly), so the kernels agree with the oracle
+# far more closely than that; the per-item bars (item_err, every item, every
+# step) are set near what the arithmetic allows:
+#   - fp32 sketch, offline map: fp32 rounding of the state, sketch and sums;
+#   - fp32 sketch, state-dependent map: the map's small solves in fp32 (one
+#     ulp reciprocals and square roots) amplify rounding by their conditioning;
+#   - bf16 sketch (U, f and the map stored in bf16): the occasional stored
+#     value that fp32 and fp64 round to neighbouring bf16 numbers (one bf16
+#     ulp, 2^-8 relative, of one element).
+HEADLINE = {"f32": 1e-5, "bf16": 2e-3}
+ITEM = {"f32": 1e-5, "f32-map": 1e-4, "bf16": 1e-3}
+
+
+def bars(io: str, sketch: str, pivots: int = 0) -> tuple[float, float]:
+    """(headline, per-item) bars for a run with inputs `io`, sketch storage
+    `sketch` and coefficient map `pivots` (0 = offline)."""
+    head = HEADLINE["bf16" if sketch == "bf16" else io]
+    item = ITEM["bf16"] if sketch == "bf16" else ITEM["f32-map" if pivots else "f32"]
+    return head, item
+
+
+def parity_report(o_gpu, o_ref, S_gpu=None, S_ref=None, U_gpu=None, U_ref=None) -> dict:
+    """Headline and per-item errors of a run: o_* [T][n][V] (or a list of
+    [n][V]), S_* [n][V][K], U_* [n][V][r]."""
+    o_gpu = np.stack(o_gpu) if isinstance(o_gpu, list) else np.asarray(o_gpu)
+    o_ref = np.asarray(o_ref)
+    rep = {"o_step": max_step_rel(list(o_gpu), o_ref), "o_item": float(item_err(o_gpu, o_ref).max()),
+           "S": 0.0, "S_item": 0.0, "U": 0.0, "U_item": 0.0}
+    if S_gpu is not None:
+        rep["S"], rep["S_item"] = rel_l2(S_gpu, S_ref), float(item_err(S_gpu.reshape(S_gpu.shape[0], -1),
+                                                                      np.reshape(S_ref, (S_gpu.shape[0], -1))).max())
+    if U_gpu is not None and np.asarray(U_ref).size:
+        rep["U"], rep["U_item"] = rel_l2(U_gpu, U_ref), float(item_err(U_gpu.reshape(U_gpu.shape[0], -1),
+                                                                      np.reshape(U_ref, (U_gpu.shape[0], -1))).max())
+    return rep
+
+
+def parity_failures(rep: dict, head: float, item: float) -> list[str]:
+    """The bars a parity_report breaks (empty when it passes)."""
+    out = []
+    for key in ("o_step", "S", "U"):
+        if not rep[key] <= head:
+            out.append(f"{key} {rep[key]:.3e} > {head:g}")
+    for key in ("o_item", "S_item", "U_item"):
+        if not rep[key] <= item:
+            out.append(f"{key} {rep[key]:.3e} > {item:g}")
+    return out
+
+
+def format_report(rep: dict) -> str:
+    return (f"max step rel-L2 {rep['o_step']:.3e} (worst item {rep['o_item']:.3e})  "
+            f"state {rep['S']:.3e} ({rep['S_item']:.3e})  sketch {rep['U']:.3e} ({rep['U_item']:.3e})")

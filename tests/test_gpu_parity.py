@@ -7,6 +7,13 @@ the same bound on the final state and sketch.  Relative L2 at step t is
 ||o_gpu[t] - o_oracle[t]|| / ||o_oracle[t]|| over every compared (b, h, v);
 the test asserts the maximum over steps.
 
+Beside that headline bar, every (request, head) item is held, at every
+step, to a per-item bar near what the arithmetic allows (tests/harness.py:
+an item's error over the typical item size, 1e-5 with an fp32 sketch and
+the offline map, 1e-4 with the state-dependent map, 1e-3 with a bf16
+sketch), so that one wrong item or one wrong value channel cannot hide in
+the aggregate.
+
 Small cases compare every item; the full-size workloads compare a seeded
 sample of items (the oracle computes them one by one) while the GPU runs the
 whole batch in the launch configuration the benchmark times.
@@ -16,11 +23,10 @@ import pytest
 import torch
 
 from paper_2609_33051_amd import inputs
-from harness import max_step_rel, oracle_of, rel_l2, run_workload, to_np32
+from harness import (bars, format_report, max_step_rel, oracle_of, parity_failures, parity_report, rel_l2,
+                     run_workload, to_np32)
 
 pytestmark = pytest.mark.gpu
-
-TOL = {"f32": 1e-5, "bf16": 2e-3}
 
 
 def announce(msg):
@@ -37,16 +43,15 @@ def check(wl, window=None, rank=None, steps=None, sel=None, omega_coef=None, bas
                                                      pivots=pivots)
     ref = oracle_of(wl, run, S_sel, heads, om, C, window, sketch=sketch, pivots=pivots)
     target = ref.o_exact_windowed if baseline else ref.o
-    err = max_step_rel(run.o_gpu, target)
     n_items = wl.batch * wl.heads
     idx = slice(None) if sel is None else torch.as_tensor(np.asarray(sel), device=layer.S.device)
-    errS = rel_l2(to_np32(layer.state().reshape(n_items, wl.dv, wl.dk)[idx]), ref.S_final)
-    errU = 0.0
-    if not baseline:
-        errU = rel_l2(to_np32(layer.sketch_matrix().reshape(n_items, wl.dv, rank)[idx]), ref.U_final)
-    print(f"  max step rel-L2 {err:.3e}  state {errS:.3e}  sketch {errU:.3e}", flush=True)
-    tol = TOL["bf16" if sketch == "bf16" else wl.io]  # a bf16 sketch is bf16 data
-    assert err <= tol and errS <= tol and errU <= tol
+    S_gpu = to_np32(layer.state().reshape(n_items, wl.dv, wl.dk)[idx])
+    U_gpu = None if baseline else to_np32(layer.sketch_matrix().reshape(n_items, wl.dv, rank)[idx])
+    rep = parity_report(run.o_gpu, target, S_gpu, ref.S_final, U_gpu, None if baseline else ref.U_final)
+    print("  " + format_report(rep), flush=True)
+    head, item = bars(wl.io, sketch, pivots)
+    bad = parity_failures(rep, head, item)
+    assert not bad, "; ".join(bad)
     return run, ref, layer
 
 
@@ -121,10 +126,10 @@ def test_window_one_is_standard_recurrence(fam):
     run, layer, S_sel, heads, _ = run_workload(wl, window=1, baseline=True)
     q, k, v, beta, logd = (np.stack(run.inp[x]) for x in ("q", "k", "v", "beta", "log_decay"))
     o_ex, S_ex = oracle.recurrence(wl.kind, S_sel, q, k, v, beta, logd)
-    err = max_step_rel(run.o_gpu, o_ex)
-    errS = rel_l2(to_np32(layer.state().reshape(-1, V, 128)), S_ex)
-    print(f"  max step rel-L2 {err:.3e} state {errS:.3e}", flush=True)
-    assert err <= 1e-5 and errS <= 1e-5
+    rep = parity_report(run.o_gpu, o_ex, to_np32(layer.state().reshape(-1, V, 128)), S_ex)
+    print("  " + format_report(rep), flush=True)
+    bad = parity_failures(rep, *bars("f32", "f32"))
+    assert not bad, "; ".join(bad)
 
 
 @pytest.mark.parametrize("name", ["mamba2_b256", "gdn_b512", "kda_b512"])
@@ -139,11 +144,11 @@ def test_window_one_full_size(name):
     run, layer, S_sel, heads, _ = run_workload(wl, window=1, baseline=True, steps=4, sel=sel)
     q, k, v, beta, logd = (np.stack(run.inp[x]) for x in ("q", "k", "v", "beta", "log_decay"))
     o_ex, S_ex = oracle.recurrence(wl.kind, S_sel, q, k, v, beta, logd)
-    err = max_step_rel(run.o_gpu, o_ex)
     idx = torch.as_tensor(sel, device="cuda")
-    errS = rel_l2(to_np32(layer.state().reshape(-1, wl.dv, wl.dk)[idx]), S_ex)
-    print(f"  max step rel-L2 {err:.3e} state {errS:.3e}", flush=True)
-    assert err <= 2e-3 and errS <= 2e-3
+    rep = parity_report(run.o_gpu, o_ex, to_np32(layer.state().reshape(-1, wl.dv, wl.dk)[idx]), S_ex)
+    print("  " + format_report(rep), flush=True)
+    bad = parity_failures(rep, *bars(wl.io, "f32"))
+    assert not bad, "; ".join(bad)
 
 
 def test_rerun_is_bitwise_identical():

@@ -16,12 +16,9 @@ import torch
 
 import oracle
 from paper_2609_33051_amd import inputs
-from harness import max_step_rel, rel_l2, run_workload, to_np32
+from harness import bars, format_report, parity_failures, parity_report, run_workload, to_np32
 
 pytestmark = pytest.mark.gpu
-
-TOL = {"f32": 1e-5, "bf16": 2e-3}
-
 
 def check_ragged(wl, head_ranks, window=None, steps=None, sketch="f32", pivots=0, sel=None, omega_coef=None,
                  S0=None):
@@ -38,8 +35,7 @@ def check_ragged(wl, head_ranks, window=None, steps=None, sketch="f32", pivots=0
     o_gpu = np.stack(run.o_gpu)
     S_gpu = to_np32(layer.state().reshape(n_items, wl.dv, wl.dk))[items]
     U_gpu = to_np32(layer.sketch_matrix().reshape(n_items, wl.dv, wl.rank))[items]
-    tol = TOL["bf16" if sketch == "bf16" else wl.io]
-    P = 8 if sketch == "bf16" else 4
+    head, item = bars(wl.io, sketch, pivots)
     worst = 0.0
     for h in range(wl.heads):
         m = heads == h
@@ -53,15 +49,15 @@ def check_ragged(wl, head_ranks, window=None, steps=None, sketch="f32", pivots=0
                                q[:, m], k[:, m], v[:, m], beta[:, m], logd[:, m], round_storage=True,
                                sketch_bf16=(sketch == "bf16"), pivots=pivots if g else 0, ridge=0.1)
         target = ref.o if g else ref.o_exact_windowed
-        err = max_step_rel(list(o_gpu[:, m]), target)
-        errS = rel_l2(S_gpu[m], ref.S_final)
-        errU = rel_l2(U_gpu[m][:, :, :g], ref.U_final) if g else 0.0
-        print(f"  head {h} rank {g}: max step rel-L2 {err:.3e}  state {errS:.3e}  sketch {errU:.3e}", flush=True)
-        assert err <= tol and errS <= tol and errU <= tol, f"head {h} rank {g}"
+        rep = parity_report(o_gpu[:, m], target, S_gpu[m], ref.S_final,
+                            U_gpu[m][:, :, :g] if g else None, ref.U_final if g else None)
+        print(f"  head {h} rank {g}: " + format_report(rep), flush=True)
+        bad = parity_failures(rep, head, item)
+        assert not bad, f"head {h} rank {g}: " + "; ".join(bad)
         # columns past the head's rank: zeros in its last panel, untouched (still zero) beyond
         if g < wl.rank:
             assert np.all(U_gpu[m][:, :, g:] == 0.0), f"head {h}: sketch columns past rank {g} not zero"
-        worst = max(worst, err)
+        worst = max(worst, rep["o_step"])
     return worst, layer
 
 

@@ -59,7 +59,7 @@ def pins_hold(lib) -> bool:
     Si = np.random.default_rng(4).standard_normal((2, 7, 5)).astype(np.float32)
     if not np.allclose(coef_map_of(Si, eye, 3, 1e-9, lib=lib), np.broadcast_to(np.eye(5), (2, 5, 5)), atol=1e-6):
         return False
-    # the paper's coefficient-space forms (f_s, Woodbury factors) equal the direct ones
+    # the paper's coefficient-space forms (f_s) equal the direct ones
     for kind in ("gdn", "kda"):
         for piv in (0, 4):
             S0p, qp, kp, vp, bp, lp = tiny_inputs(kind, n=3, K=8, V=6, T=13, seed=21)
@@ -67,9 +67,20 @@ def pins_hold(lib) -> bool:
             z3 = np.zeros(3, np.int32)
             a = oracle.sketchssm(kind, 5, z3, omp, Cp, S0p, qp, kp, vp, bp, lp, pivots=piv, lib=lib)
             b = oracle.sketchssm(kind, 5, z3, omp, Cp, S0p, qp, kp, vp, bp, lp, pivots=piv, paper_path=True, lib=lib)
-            tol = 1e-6 if piv else 1e-10
-            if not np.allclose(b.o, a.o, rtol=tol, atol=tol * np.abs(a.o).max()):
+            if not np.allclose(b.o, a.o, rtol=1e-10, atol=1e-10 * np.abs(a.o).max()):
                 return False
+    # bf16 storage (the dense map rounded once, f rounded when stored) and the exact metric
+    import test_oracle_pins as P
+    try:
+        for kind in KINDS:
+            for piv in (4, oracle.EXACT):
+                P.test_bf16_map_storage_is_round_to_nearest_even(kind, piv, lib=lib)
+        P.test_bf16_map_is_the_one_read(4, lib=lib)
+        for kind in ("gdn", "kda"):
+            P.test_bf16_f_is_rounded_when_stored_not_when_formed(kind, lib=lib)
+        P.test_exact_map_is_the_closed_form(None, lib=lib)
+    except AssertionError:
+        return False
     # the sketch must be refreshed from the updated state at each flush
     r = oracle.sketchssm("mamba2", 2, np.zeros(n, np.int32), om, C, S0, q_in, k, v, beta, logd, lib=lib)
     Uref = np.einsum("nvk,kg->nvg", r.S_final, om[0].astype(np.float64))
@@ -79,8 +90,8 @@ def pins_hold(lib) -> bool:
 
 
 MUTANTS = {
-    "coef_ridge_dropped": [("w->A[(size_t)g * G + g2] = w->Hh[(size_t)g * K + g2] + (g == g2 ? lambda : 0.0);",
-                            "w->A[(size_t)g * G + g2] = w->Hh[(size_t)g * K + g2];")],
+    "coef_ridge_dropped": [("w->A[(size_t)g * G + g2] = Hm[(size_t)g * K + g2] + (g == g2 ? lambda : 0.0);",
+                            "w->A[(size_t)g * G + g2] = Hm[(size_t)g * K + g2];")],
     "coef_metric_not_normalised": [("      w->H[(size_t)i * K + i2] = acc / mu;", "      w->H[(size_t)i * K + i2] = acc;")],
     "coef_pivots_from_last_columns": [("      x[j] = U[(size_t)j * G + a];", "      x[j] = U[(size_t)j * G + (G - 1 - a)];")],
     "coef_diagonal_dropped": [("      double acc = (i == i2) ? w->d[i] : 0.0;", "      double acc = 0.0;")],
@@ -118,14 +129,24 @@ MUTANTS = {
     "wyread_drops_beta": [("            const double ft = bt * ck;", "            const double ft = ck;")],
     "projected_query_drops_self_term": [("            cvec[g] = cq - ft * akq;", "            cvec[g] = cq;")],
     "left_factor_decay_off_by_one": [("            for (int r = j + 1; r <= cur; ++r)", "            for (int r = j; r <= cur; ++r)")],
-    "woodbury_F2_sign": [("- corr / (w->d[g2] + lambda)) * dg2;", "+ corr / (w->d[g2] + lambda)) * dg2;")],
-    "woodbury_F1_without_T_inverse": [
-        ("        for (int b = 0; b < p; ++b) acc += w->L[(size_t)g * pq + b] * Ti[b * 4 + a];\n"
-         "        F1[g * 4 + a] = acc / (w->d[g] + lambda);",
-         "        for (int b = 0; b < p; ++b) acc += (a == b) ? w->L[(size_t)g * pq + b] : 0.0;\n"
-         "        F1[g * 4 + a] = acc / (w->d[g] + lambda);")],
+    "exact_map_uses_pivot_metric": [("  if (P > 0) {\n    /* Q: the first p columns", "  if (P != 0) {\n    /* Q: the first p columns")],
+    "map_not_rounded_when_stored": [("{\n  store_sketch(c, Cm, n);\n}", "{\n  (void)c;\n  (void)Cm;\n  (void)n;\n}")],
+    "map_built_from_rounded_sketch": [
+        ("          make_sketch(K, V, G, S0, Om, U);\n          if (statedep && Cmi && cw.R) {\n"
+         "            coef_map(c, K, V, G, S0, Om, U, Cmi, &cw);\n            store_map(c, Cmi, (size_t)G * K);\n"
+         "          }\n          store_sketch(c, U, (size_t)V * G);",
+         "          make_sketch(K, V, G, S0, Om, U);\n          store_sketch(c, U, (size_t)V * G);\n"
+         "          if (statedep && Cmi && cw.R) {\n"
+         "            coef_map(c, K, V, G, S0, Om, U, Cmi, &cw);\n            store_map(c, Cmi, (size_t)G * K);\n"
+         "          }")],
+    "current_f_rounded": [("            const double ft = bt * ck;",
+                           "            const double ft = c->sketch_bf16 ? bf16_rne(bt * ck) : bt * ck;")],
+    "f_not_rounded_when_stored": [("fhat[(size_t)cur * G + g] = c->sketch_bf16 ? bf16_rne(ft) : ft;",
+                                   "fhat[(size_t)cur * G + g] = ft;")],
     "sketch_not_refreshed": [("        if (G > 0) {\n          make_sketch(K, V, G, S0, Om, U);\n"
-                              "          if (statedep && Cmi && cw.R) coef_map(c, K, V, G, S0, Om, U, Cmi, &cw);\n"
+                              "          if (statedep && Cmi && cw.R) {\n"
+                              "            coef_map(c, K, V, G, S0, Om, U, Cmi, &cw);\n"
+                              "            store_map(c, Cmi, (size_t)G * K);\n          }\n"
                               "          store_sketch(c, U, (size_t)V * G);\n        }\n"
                               "        for (int j = 0; j < V; ++j) {\n          if (o) o[oi + j] = ostate[j];",
                               "        for (int j = 0; j < V; ++j) {\n          if (o) o[oi + j] = ostate[j];")],

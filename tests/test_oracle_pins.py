@@ -359,40 +359,106 @@ def test_coef_map_pivots_are_the_leading_sketch_columns():
 
 # --- the paper's coefficient-space forms and BF16 storage of f and the map -----------------------------
 @pytest.mark.parametrize("kind", KINDS)
-@pytest.mark.parametrize("pivots", [0, 4])
+@pytest.mark.parametrize("pivots", [0, 4, oracle.EXACT])
 def test_paper_path_equals_the_direct_forms(kind, pivots):
     """c_t through the projected erase factors (eq. app-projected-query with
-    eq. wyread) equals C q~_t, and the state-dependent map through its
-    Woodbury factors (the appendix's steps 3-4) equals the direct solve of
-    eq. pivot-ridge, when nothing is rounded."""
+    eq. wyread) equals C q~_t when nothing is rounded (App. C.2: the
+    projected recursion is exact for a map that is fixed within the window)."""
     S0, q, k, v, beta, logd = tiny_inputs(kind, n=3, K=8, V=6, T=13, seed=21)
     heads = np.zeros(3, np.int32)
     om, C = heads_omega(1, 8, 5, seed=9)
     a = oracle.sketchssm(kind, 5, heads, om, C, S0, q, k, v, beta, logd, pivots=pivots, ridge=0.1)
     b = oracle.sketchssm(kind, 5, heads, om, C, S0, q, k, v, beta, logd, pivots=pivots, ridge=0.1, paper_path=True)
-    # the factor form applies the stored Omega^T, the direct solve its exactly
-    # orthonormal completion: Omega is fp32, orthonormal to about 1e-7
-    tol = 1e-6 if pivots else 1e-10
-    np.testing.assert_allclose(b.o, a.o, rtol=tol, atol=tol * np.abs(a.o).max())
-    np.testing.assert_allclose(b.coef_final, a.coef_final, rtol=tol, atol=tol * np.abs(a.coef_final).max())
+    np.testing.assert_allclose(b.o, a.o, rtol=1e-10, atol=1e-10 * np.abs(a.o).max())
+    np.testing.assert_array_equal(b.coef_final, a.coef_final)
     np.testing.assert_array_equal(b.S_final, a.S_final)
 
 
-@pytest.mark.parametrize("kind,pivots", [("gdn", 0), ("kda", 0), ("mamba2", 4), ("gdn", 4)])
-def test_paper_storage_rounds_f_and_the_map_factors(kind, pivots):
-    """BF16 storage of f_s and of the map's factors moves the sketch read by a
-    bf16-sized amount beyond what rounding the sketch alone does, and leaves
-    the flush exact."""
+def bf16_of(x):
+    """torch's bfloat16 conversion (round to nearest, ties to even) of the fp32 value of x, as fp64."""
     import torch
 
-    S0, q, k, v, beta, logd = tiny_inputs(kind, n=3, K=8, V=6, T=13, seed=22)
+    return torch.from_numpy(np.asarray(x, np.float64).astype(np.float32)).to(torch.bfloat16).to(torch.float64).numpy()
+
+
+@pytest.mark.parametrize("kind", KINDS)
+@pytest.mark.parametrize("pivots", [4, oracle.EXACT])
+def test_bf16_map_storage_is_round_to_nearest_even(kind, pivots, lib=None):
+    """The paper stores the state-dependent map C (G x K per item) in BF16.
+    The map is built from the fp32 state and its unrounded sketch, which bf16
+    storage does not change (the flush replays raw inputs), so the stored map
+    must be torch's bf16 rounding of the fp32-storage run's map, element for
+    element: the dense matrix is rounded once, not factors of it."""
+    S0, q, k, v, beta, logd = tiny_inputs(kind, n=3, K=8, V=6, T=12, seed=23)
     heads = np.zeros(3, np.int32)
-    om, C = heads_omega(1, 8, 5, seed=10)
-    ref = oracle.sketchssm(kind, 5, heads, om, C, S0, q, k, v, beta, logd, pivots=pivots, paper_path=True)
-    bf = oracle.sketchssm(kind, 5, heads, om, C, S0, q, k, v, beta, logd, pivots=pivots, sketch_bf16=True)
-    rel = np.linalg.norm(bf.o - ref.o) / np.linalg.norm(ref.o)
-    assert 1e-5 < rel < 3e-2
-    np.testing.assert_allclose(bf.o_exact_windowed, ref.o_exact_windowed, rtol=1e-12, atol=1e-12)
-    if pivots:  # the map in use is built from bf16 factors: close to, not equal to, the fp64 one
-        d = np.abs(bf.coef_final - ref.coef_final).max() / np.abs(ref.coef_final).max()
-        assert 1e-5 < d < 2e-2
+    om, C = heads_omega(1, 8, 5, seed=12)
+    a = oracle.sketchssm(kind, 5, heads, om, C, S0, q, k, v, beta, logd, pivots=pivots, round_storage=True, lib=lib)
+    b = oracle.sketchssm(kind, 5, heads, om, C, S0, q, k, v, beta, logd, pivots=pivots, round_storage=True,
+                         sketch_bf16=True, lib=lib)
+    assert np.array_equal(b.S_final, a.S_final)
+    assert np.array_equal(b.coef_final, bf16_of(a.coef_final))
+    assert not np.array_equal(b.coef_final, a.coef_final)
+
+
+@pytest.mark.parametrize("pivots", [4, oracle.EXACT])
+def test_bf16_map_is_the_one_read(pivots, lib=None):
+    """Scalar decay, tokens of the first window: the sketch read is
+    U_bf16 (C_bf16 q~_t) with q~_t = (prod_{s<=t} alpha_s) q_t (Sec. 3.3,
+    eq. m-coeff: c_t = C q~_t), with the stored (bf16) sketch and map."""
+    S0, q, k, v, beta, logd = tiny_inputs("mamba2", n=2, K=8, V=6, T=4, seed=24)
+    om, C = heads_omega(1, 8, 5, seed=13)
+    r = oracle.sketchssm("mamba2", 6, np.zeros(2, np.int32), om, C, S0, q, k, v, beta, logd, pivots=pivots,
+                         round_storage=True, sketch_bf16=True, lib=lib)
+    qt = np.exp(np.cumsum(logd.astype(np.float64), axis=0))[:, :, None] * q.astype(np.float64)   # [T][n][K]
+    want = np.einsum("nvg,ngk,tnk->tnv", r.U_final, r.coef_final, qt)
+    assert np.allclose(r.o_state_hat, want, rtol=1e-12, atol=1e-12)
+    assert np.array_equal(r.U_final, bf16_of(r.U_final)) and np.array_equal(r.coef_final, bf16_of(r.coef_final))
+
+
+@pytest.mark.parametrize("kind", ["gdn", "kda"])
+def test_bf16_f_is_rounded_when_stored_not_when_formed(kind, lib=None):
+    """With S_0 = I (V = K) and Omega = C = I the sketch is exactly I in bf16,
+    so the sketch read is c_t itself.  Through the projected erase factors
+    (eqs. app-projected-query, wyread), c_t = C q~_t exactly when nothing is
+    rounded.  Storing f_1 in bf16 (when token 1 is first read) and using the
+    current f_t as formed moves c at token 1 by nothing, and at token 2 by
+        c_2 - C q~_2 = -(a_{2,1} - a_{2,2} beta_2 b_{2,1}) (f^_1 - f_1),
+    with f_1 = beta_1 C (d_[1] . k_1), f^_1 its bf16 rounding,
+    a_{2,s} = <l_s(2), q_2>, b_{2,1} = <l_1(2), k_2>, l_s(t) = D_t..D_{s+1} k_s."""
+    K = 6
+    _, q, k, v, beta, logd = tiny_inputs(kind, n=2, K=K, V=K, T=2, seed=25)
+    S0 = np.broadcast_to(np.eye(K, dtype=np.float32), (2, K, K)).copy()
+    eye = np.eye(K, dtype=np.float32)[None]
+    r = oracle.sketchssm(kind, 5, np.zeros(2, np.int32), eye, eye.copy(), S0, q, k, v, beta, logd,
+                         round_storage=True, sketch_bf16=True, lib=lib)
+    for i in range(2):
+        M = [explicit_M(kind, k[t, i], beta[t, i], logd[t, i]) for t in range(2)]
+        q1 = M[0].T @ q[0, i].astype(np.float64)
+        q2 = M[0].T @ (M[1].T @ q[1, i].astype(np.float64))
+        assert np.allclose(r.o_state_hat[0, i], q1, rtol=1e-13, atol=1e-13)
+        d = [np.exp(logd[t, i].astype(np.float64)) * np.ones(K) for t in range(2)]
+        k1, k2 = k[0, i].astype(np.float64), k[1, i].astype(np.float64)
+        l1 = d[1] * k1                                  # l_1(2) = D_2 k_1
+        a21, a22, b21 = l1 @ q[1, i], k2 @ q[1, i], l1 @ k2
+        f1 = float(beta[0, i]) * d[0] * k1              # C = I, d_[1] = D_1
+        want = -(a21 - a22 * float(beta[1, i]) * b21) * (bf16_of(f1) - f1)
+        assert np.abs(want).max() > 1e-6                # f_1 is not representable in bf16 here
+        assert np.allclose(r.o_state_hat[1, i] - q2, want, rtol=1e-9, atol=1e-13)
+
+
+@pytest.mark.parametrize("rank_of_state", [None, 2])
+def test_exact_map_is_the_closed_form(rank_of_state, lib=None):
+    """The exact regularised map of eq. pivot-ridge, built literally with the
+    dense metric H in the rotated coordinates, is (U^T U/mu + lambda I)^{-1}
+    U^T S^T/mu: J^T H J = U^T U/mu and J^T H R = U^T S^T/mu because R^T R = I.
+    Checked for full-rank and low-rank states."""
+    K, V, G = 8, 6, 5
+    if rank_of_state is None:
+        S = np.random.default_rng(31).standard_normal((3, V, K)).astype(np.float32)
+    else:
+        S = low_rank_state(3, V, K, rank_of_state, seed=32)
+    om = heads_omega(1, K, G, seed=33)[0]
+    assert np.allclose(coef_map_of(S, om, oracle.EXACT, 0.1, lib=lib), exact_ridge_map(S, om, 0.1),
+                       rtol=1e-6, atol=1e-7)
+    if rank_of_state is None:  # the P = 4 metric is an approximation of H for a full-rank state
+        assert not np.allclose(coef_map_of(S, om, 4, 0.1, lib=lib), exact_ridge_map(S, om, 0.1), atol=1e-3)

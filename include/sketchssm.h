@@ -85,12 +85,15 @@ typedef struct {
   int32_t window;   /* W tokens per window = ring capacity                  */
   int32_t io_dtype; /* skssm_dtype of q, k, v and ring.k / ring.v           */
   int32_t sketch_dtype; /* skssm_dtype of U, ring.f and cmap (0 = fp32; BF16, the
-                           paper's storage, halves their reads; rounded to nearest
-                           even when stored)                                        */
+                           paper's storage of the sketch, the coefficient map and
+                           the projected erase vectors, halves their reads;
+                           rounded to nearest even when stored)                 */
   int32_t pivots;   /* 0: the coefficient map is `coef` (offline, shared per head);
-                       4: state-dependent map with P = 4 pivots, rebuilt from the
-                       state by every sketchssm_update into `cmap` (rank 8..32)   */
-  float ridge;      /* lambda of the state-dependent map (the paper uses 0.1)     */
+                       4: the state-dependent map (Sec. 4.1, eq. m-coeff) with the
+                       P = 4 low-rank-plus-diagonal state metric (appendix on the
+                       coefficient map, eq. pivot-metric), rebuilt from the state
+                       by every sketchssm_update into `cmap` (rank 8..32)       */
+  float ridge;      /* lambda > 0 of the state-dependent map (the paper uses 0.1) */
   const int32_t* head_rank; /* per-head rank table (host memory, read during the call),
                        or NULL: every head has rank `rank`.  With a table (the
                        allocation of Sec. 4.2 and the allocation appendix), entry h
@@ -179,12 +182,13 @@ typedef struct {
  *        tinv (GDN, KDA) of slots 0..n_buffered-1.
  * q      [B][H][K] io_dtype, the current query.
  * U      [B][H][rank/P][V][P] output in cfg.sketch_dtype, panel layout (may be NULL when rank == 0).
- * cmap   cfg.pivots = 4: [B][H][4K + 4 rank + rank^2] output in cfg.sketch_dtype, the
- *        state-dependent coefficient map of Sec. 4.1 (eq. m-coeff with the
- *        ridge term and the P = 4 low-rank-plus-diagonal state metric of the
- *        appendix on the coefficient map), built from S_W and U and stored
- *        factored as M [4][K], F1 [rank][4], F2 [rank][rank] with
- *        C = F1 M + F2 Omega^T; ignored (may be NULL) when pivots = 0.
+ * cmap   cfg.pivots != 0: the state-dependent coefficient map C (rank x K per
+ *        item, Sec. 4.1 eq. m-coeff with the ridge term of eq. pivot-ridge),
+ *        built from S_W and its sketch and written in cfg.sketch_dtype as the
+ *        dense matrix in 16-byte channel panels, [B][H][K/CP][rank][CP] with
+ *        CP = 4 (fp32) or 8 (bf16) channels: element (j, k) of item i at
+ *        i rank K + ((k / CP) rank + j) CP + k % CP.  Rows past a head's rank
+ *        are not written.  Ignored (may be NULL) when pivots = 0.
  * o      [B][H][V] fp32 output or NULL.
  * rank may be 0 here (no sketch: the flush of the exact baseline).
  */
@@ -199,17 +203,18 @@ int sketchssm_update(const skssm_config* cfg, float* S, const float* omega, cons
  *     o_t^buffer = sum_{s<=t} a_{t,s} u_s,  a_{t,s} = <exp(g_t - g_s) k_s, q_t>
  * (for MAMBA2 f_s = 0 and u_s = beta_s v_s, so c_t = e^{g_t} C q_t).  The
  * state of a sketched head is never read.  U [B][H][rank/P][V][P]
- * (cfg.sketch_dtype) and coef [H][rank][K] fp32 (C; Omega^T for the offline
- * map of Sec. 4.1 at E0 = I) are read; for GDN/KDA the derived fields of slot
- * n_buffered (f, tinv) are written.
+ * (cfg.sketch_dtype) and the map C are read: coef [H][rank][K] fp32 (the
+ * offline map of Sec. 4.1, Omega^T at E0 = I) or, with a state-dependent map,
+ * the item's own cmap; for GDN/KDA the derived fields of slot n_buffered (f,
+ * tinv) are written.
  * S (tile-major, fp32) is read only for the dense-fallback heads of a per-head
  * rank table (cfg.head_rank entries 0), whose output is the exact read of
  * sketchssm_full_read_baseline (their slot gets pi instead of f, so ring.pi
  * is then required); S may be NULL when no head is dense.
- * With cfg.pivots = 4 the map is the state-dependent one that the last
- * sketchssm_update wrote to cmap, C = F1 M + F2 coef, and coef must then be
- * Omega^T.  q [B][H][K] io_dtype; o [B][H][V] fp32.  rank must be > 0,
- * window >= 2.
+ * With cfg.pivots != 0 the map is the state-dependent one that the last
+ * sketchssm_update wrote to cmap (the paper's 2 rank K bytes per item with bf16
+ * storage); coef is then not read and may be NULL.  q [B][H][K] io_dtype;
+ * o [B][H][V] fp32.  rank must be > 0, window >= 2.
  */
 int sketchssm_decode(const skssm_config* cfg, const void* U, const float* coef, const void* cmap, const float* S,
                      const skssm_ring* ring, int32_t n_buffered, const void* q, float* o, void* stream);

@@ -112,9 +112,9 @@ def head_ranks(cfg: Config) -> list[int] | None:
 
 
 def cmap_width(cfg: Config) -> int:
-    """Floats per item of the state-dependent coefficient map (M, F1, F2)."""
-    p, K, r = cfg.pivots, cfg.dk, cfg.rank
-    return p * K + r * p + r * r if p else 0
+    """Elements per item of the state-dependent coefficient map (rank x K, in
+    16-byte channel panels), 0 with the offline map."""
+    return cfg.rank * cfg.dk if cfg.pivots else 0
 
 
 def make_ring(k=None, v=None, beta=None, log_decay=None, f=None, pi=None, tinv=None) -> Ring:

@@ -40,7 +40,10 @@ int check_shape(const skssm_config* c, bool need_rank, bool allow_rank0) {
   if (c->sketch_dtype != SKSSM_F32 && c->sketch_dtype != SKSSM_BF16)
     return fail(SKSSM_EINVAL, "unknown sketch_dtype %d", c->sketch_dtype);
   if (c->pivots != 0 && c->pivots != 4) return fail(SKSSM_EUNSUPPORTED, "pivots %d: 0 or 4 are compiled", c->pivots);
-  if (c->pivots && !(c->ridge >= 0.f && c->ridge < 1e30f)) return fail(SKSSM_EINVAL, "ridge must be finite and >= 0");
+  // lambda > 0 keeps the map's diagonal D = d + lambda invertible where d = 0
+  // (a zero state, sketch columns past a head's rank); the paper uses 0.1
+  if (c->pivots && !(c->ridge > 0.f && c->ridge < 1e30f))
+    return fail(SKSSM_EINVAL, "ridge must be finite and > 0 with a state-dependent map");
   if (c->window < 1 || c->window > 32) return fail(SKSSM_EUNSUPPORTED, "window %d outside 1..32", c->window);
   const bool kv_ok = (c->dk == 64 && c->dv == 64) || (c->dk == 128 && c->dv == 64) || (c->dk == 128 && c->dv == 128);
   if (!kv_ok) return fail(SKSSM_EUNSUPPORTED, "(dk, dv) = (%d, %d) not compiled", c->dk, c->dv);
@@ -247,8 +250,10 @@ int sketchssm_decode(const skssm_config* cfg, const void* U, const float* coef, 
   if (cfg->window < 2) return fail(SKSSM_EINVAL, "decode needs window >= 2 (window 1 flushes every token)");
   if (n_buffered < 0 || n_buffered > cfg->window - 2)
     return fail(SKSSM_ESTATE, "n_buffered %d outside 0..%d", n_buffered, cfg->window - 2);
-  if (!U || !coef || !o || !q) return fail(SKSSM_EINVAL, "U, coef, q and o are required");
-  if (!aligned(U) || !aligned(coef) || !aligned(o) || !aligned(q)) return fail(SKSSM_EALIGN, "U/coef/q/o not aligned");
+  if (!U || !o || !q) return fail(SKSSM_EINVAL, "U, q and o are required");
+  if (!cfg->pivots && !coef) return fail(SKSSM_EINVAL, "coef is required with the offline map (pivots = 0)");
+  if (!aligned(U) || !aligned(o) || !aligned(q) || (coef && !aligned(coef)))
+    return fail(SKSSM_EALIGN, "U/coef/q/o not aligned");
   if (rk.dense) {  // dense-fallback heads read the state (and keep pi in the ring)
     if (!S) return fail(SKSSM_EINVAL, "S is required when the rank table has dense-fallback heads");
     if (!aligned(S)) return fail(SKSSM_EALIGN, "S not aligned");
@@ -259,7 +264,7 @@ int sketchssm_decode(const skssm_config* cfg, const void* U, const float* coef, 
   put_order(a, rk);
   a.S = rk.dense ? S : nullptr;
   a.U = U;
-  a.coef = coef;
+  a.coef = cfg->pivots ? nullptr : coef;
   a.cmap = cfg->pivots ? cmap : nullptr;
   int r;
   switch (cfg->kind) {

@@ -26,8 +26,8 @@ struct DecodeArgs {
   uint8_t hlist[kMaxRaggedHeads]; // heads in launch order: the dense ones first (ragged)
   const void* q;                  // [B][H][K] io, current query
   const void* U;                  // [B][H][R/P][V][P], P = 4 (fp32) or 8 (bf16)  (sketch read)
-  const float* coef;              // [H][R][K]           (sketch read; Omega^T with a pivot map)
-  const void* cmap;               // [B][H][4K + 4R + R*R] pivot map factors M, F1, F2, sketch dtype (or NULL)
+  const float* coef;              // [H][R][K]           (sketch read, offline map; NULL with a state-dependent map)
+  const void* cmap;               // [B][H][K/CPW][R][CPW] state-dependent map, sketch dtype, CPW = 16 B / element (or NULL)
   const float* S;                 // [B][H][V][K]        (exact baseline)
   const void* rk;                 // ring [B][H][W][K] io      raw keys
   const void* rv;                 // ring [B][H][W][V] io      raw values
@@ -53,7 +53,7 @@ struct UpdateArgs {
   const float* rla;
   const float* rt;                // GDN/KDA rows of T^{-1}, slots < n
   void* U;                        // [B][H][R/P][V][P], P = 4 (fp32) or 8 (bf16), or NULL
-  void* cmap;                     // [B][H][4K + 4R + R*R] state-dependent map factors, sketch dtype, or NULL
+  void* cmap;                     // [B][H][K/CPW][R][CPW] state-dependent map, sketch dtype, or NULL
   float ridge;                    // its lambda
   float* o;                       // [B][H][V] or NULL
 };

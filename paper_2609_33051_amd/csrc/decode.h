@@ -459,19 +459,23 @@ __device__ __forceinline__ void load_ring_f(const DecodeArgs& a, size_t dp, int 
   }
 }
 
-// The item's state-dependent map factors (M, F1, F2): this lane's channels of
-// M and, for its sketch columns, its part of an F2 row and its F1 row.
-template <int K, int R, int P, int RP, typename SK, int MW, int HQ>
-__device__ __forceinline__ void load_map_factors(const DecodeArgs& a, size_t item, int row, int col, int rh,
-                                                 Raw<SK, MW>& mr, Raw<SK, HQ> (&f2r)[RP], Raw<SK, 4> (&f1r)[RP]) {
-  const SK* cm = static_cast<const SK*>(a.cmap) + item * (size_t)(P * K + R * P + R * R);
-  mr.load_nt(cm + (col >> 2) * K + ((col & 3) + 4 * row) * MW);
+// The item's state-dependent coefficient map C (R x K in the sketch dtype),
+// stored in 16-byte channel panels cmap[B][H][K/CPW][R][CPW] (element (j, k)
+// at ((k / CPW) R + j) CPW + k % CPW, CPW = 4 fp32 or 8 bf16 channels): for
+// this lane's rows j = col + 16 p, its K/4 channels row K/4 .. as CL panels.
+// Rows at or past the head's rank re-read row 0 (fetched anyway) and are not
+// used; the load itself is unconditional.
+template <int K, int R, int RP, int CL, typename SK>
+__device__ __forceinline__ void load_map_rows(const DecodeArgs& a, size_t item, int row, int col, int rh,
+                                              Raw<SK, 16 / sizeof(SK)> (&cm)[RP][CL]) {
+  constexpr int CPW = 16 / (int)sizeof(SK);
+  const SK* base = static_cast<const SK*>(a.cmap) + item * (size_t)(R * K);
 #pragma unroll
   for (int p = 0; p < RP; ++p) {
     const int j = col + 16 * p;
-    f2r[p].load_nt(cm + P * K + R * P + j * R + row * HQ);
-    f2r[p].keep_if(row * HQ < rh);  // columns of F2 past the head's rank are not read
-    f1r[p].load(cm + P * K + j * P);
+    const int jj = j < rh ? j : 0;
+#pragma unroll
+    for (int i = 0; i < CL; ++i) cm[p][i].load_nt(base + (uint32_t)(((row * CL + i) * R + jj) * CPW));
   }
 }
 
@@ -492,7 +496,7 @@ __global__ __launch_bounds__(256) void decode_kernel(const DecodeArgs a) {
   constexpr bool U_PRELOAD = R <= 32;
   constexpr int UP = U_PRELOAD ? NP : 1;
 
-  __shared__ __align__(16) float c_lds[R * CP];
+  __shared__ __align__(16) float c_lds[P != 0 ? 4 : R * CP];
   __shared__ __align__(16) float wscr[4 * WS];
 
   const int tid = threadIdx.x, lane = tid & 63;
@@ -532,15 +536,20 @@ __global__ __launch_bounds__(256) void decode_kernel(const DecodeArgs a) {
     return;
   }
 
-  // ---- C first, then every global load of this item
-  constexpr int CQ = (R * K / 4 + 255) / 256;  // float4 of C per thread
-  Vec<4> cv[CQ];
+  // ---- the offline map C first (shared by the head's items, staged in
+  // LDS), then every global load of this item; a state-dependent map (P != 0)
+  // is per item and read into registers like the other per-item data
+  constexpr bool SMAP = P != 0;
+  constexpr int CQ = SMAP ? 1 : (R * K / 4 + 255) / 256;  // float4 of C per thread
+  [[maybe_unused]] Vec<4> cv[CQ];
+  if constexpr (!SMAP) {
 #pragma unroll
-  for (int c = 0; c < CQ; ++c) {
-    const int i = tid + 256 * c;
+    for (int c = 0; c < CQ; ++c) {
+      const int i = tid + 256 * c;
 #pragma unroll
-    for (int e = 0; e < 4; ++e) cv[c].e[e] = 0.f;
-    if ((CQ * 256 == R * K / 4 || i < R * K / 4) && (4 * i) / K < rh) cv[c].load(a.coef + (size_t)h * R * K + 4 * i);
+      for (int e = 0; e < 4; ++e) cv[c].e[e] = 0.f;
+      if ((CQ * 256 == R * K / 4 || i < R * K / 4) && (4 * i) / K < rh) cv[c].load(a.coef + (size_t)h * R * K + 4 * i);
+    }
   }
   compiler_fence();
   // Every load of the item follows (the sketch panels after the slot
@@ -555,30 +564,30 @@ __global__ __launch_bounds__(256) void decode_kernel(const DecodeArgs a) {
   r.load(a, item, dp, row, col);
   float fs[ERASE ? NG : 1][RP];      // ring f of slot 4 gi + row, component col + 16 p
   Raw<SK, PW> Ur[VPL][UP];           // sketch panels (value layout), loaded after the slot dot products
-  // the item's state-dependent map factors (M, F1, F2; P > 0): this lane's
-  // channels of M and, for its sketch columns, its part of an F2 row and its F1 row
-  constexpr int MW = P > 0 ? K / 16 : 1, HQ = P > 0 ? R / 4 : 1;
-  [[maybe_unused]] Raw<SK, MW> mr;
-  [[maybe_unused]] Raw<SK, HQ> f2r[RP];
-  [[maybe_unused]] Raw<SK, 4> f1r[RP];
-  // f and the map factors are used only after the C products: with a
-  // per-channel decay (KDA) they are loaded with the sketch panels, after the
-  // slot products, which keeps the kernel within 128 registers (four waves per
+  // the item's state-dependent map (P != 0): this lane's channels of its rows
+  constexpr int CPW = 16 / (int)sizeof(SK);      // channels per 16-byte map panel
+  constexpr int CL = SMAP ? KQ / CPW : 1;        // map panels per lane and row
+  [[maybe_unused]] Raw<SK, 16 / sizeof(SK)> cmr[SMAP ? RP : 1][CL];
+  // f and the map are used only after the C products: with a per-channel
+  // decay (KDA) they are loaded with the sketch panels, after the slot
+  // products, which keeps the kernel within 128 registers (four waves per
   // SIMD); the other kinds load them here, first
   constexpr bool LATE_FM = CHAN;
   if constexpr (!LATE_FM) {
     if constexpr (ERASE) load_ring_f<NG, RP>(a, dp, n, row, col, rh, R, static_cast<const SK*>(a.rf), fs);
-    if constexpr (P > 0) load_map_factors<K, R, P, RP>(a, item, row, col, rh, mr, f2r, f1r);
+    if constexpr (SMAP) load_map_rows<K, R, RP, CL>(a, item, row, col, rh, cmr);
   }
 
-  // ---- this head's coefficient map C (R x K) into LDS; its loads were issued
+  // ---- this head's offline map C (R x K) into LDS; its loads were issued
   // first, so the LDS-only barrier leaves the item's own loads in flight
+  if constexpr (!SMAP) {
 #pragma unroll
-  for (int c = 0; c < CQ; ++c) {
-    const int i = tid + 256 * c;
-    if (CQ * 256 == R * K / 4 || i < R * K / 4) cv[c].store(&c_lds[((4 * i) / K) * CP + (4 * i) % K]);
+    for (int c = 0; c < CQ; ++c) {
+      const int i = tid + 256 * c;
+      if (CQ * 256 == R * K / 4 || i < R * K / 4) cv[c].store(&c_lds[((4 * i) / K) * CP + (4 * i) % K]);
+    }
+    lds_barrier();
   }
-  lds_barrier();
   if (!valid) return;
 
   float* xq_l = wscr + wave * WS;
@@ -615,7 +624,7 @@ __global__ __launch_bounds__(256) void decode_kernel(const DecodeArgs a) {
   }
   if constexpr (LATE_FM) {
     if constexpr (ERASE) load_ring_f<NG, RP>(a, dp, n, row, col, rh, R, static_cast<const SK*>(a.rf), fs);
-    if constexpr (P > 0) load_map_factors<K, R, P, RP>(a, item, row, col, rh, mr, f2r, f1r);
+    if constexpr (SMAP) load_map_rows<K, R, RP, CL>(a, item, row, col, rh, cmr);
   }
   float ca[NG], cg[NG], gcol[L::JP];
   buffer_coefs<L>(n, row, col, r, av, bv, b_l, ca, cg, gcol);
@@ -641,74 +650,38 @@ __global__ __launch_bounds__(256) void decode_kernel(const DecodeArgs a) {
     const int j = col + 16 * p;
     float sq = 0.f, sk = 0.f;
     if (j < rh) {
-      const float* cr = c_lds + j * CP + row * KQ;
       const float* xqr = xq_l + row * KQ;
       const float* xkr = xk_l + row * KQ;
+      if constexpr (SMAP) {
+        // the item's map: row j over this lane's channels, from registers
 #pragma unroll
-      for (int m = 0; m < KQ; m += 4) {
-        const float4 cc = *reinterpret_cast<const float4*>(cr + m);
-        const float4 xx = *reinterpret_cast<const float4*>(xqr + m);
-        sq += cc.x * xx.x + cc.y * xx.y + cc.z * xx.z + cc.w * xx.w;
-        if constexpr (ERASE) {
-          const float4 yy = *reinterpret_cast<const float4*>(xkr + m);
-          sk += cc.x * yy.x + cc.y * yy.y + cc.z * yy.z + cc.w * yy.w;
+        for (int i = 0; i < CL; ++i)
+#pragma unroll
+          for (int e = 0; e < CPW; e += 4) {
+            const Raw<SK, 16 / sizeof(SK)>& cr = cmr[p][i];
+            const float4 xx = *reinterpret_cast<const float4*>(xqr + i * CPW + e);
+            sq += cr.get(e) * xx.x + cr.get(e + 1) * xx.y + cr.get(e + 2) * xx.z + cr.get(e + 3) * xx.w;
+            if constexpr (ERASE) {
+              const float4 yy = *reinterpret_cast<const float4*>(xkr + i * CPW + e);
+              sk += cr.get(e) * yy.x + cr.get(e + 1) * yy.y + cr.get(e + 2) * yy.z + cr.get(e + 3) * yy.w;
+            }
+          }
+      } else {
+        const float* cr = c_lds + j * CP + row * KQ;
+#pragma unroll
+        for (int m = 0; m < KQ; m += 4) {
+          const float4 cc = *reinterpret_cast<const float4*>(cr + m);
+          const float4 xx = *reinterpret_cast<const float4*>(xqr + m);
+          sq += cc.x * xx.x + cc.y * xx.y + cc.z * xx.z + cc.w * xx.w;
+          if constexpr (ERASE) {
+            const float4 yy = *reinterpret_cast<const float4*>(xkr + m);
+            sk += cc.x * yy.x + cc.y * yy.y + cc.z * yy.z + cc.w * yy.w;
+          }
         }
       }
     }
     sqv[p] = cross_row_sum(sq);
     skv[p] = ERASE ? cross_row_sum(sk) : 0.f;
-  }
-  if constexpr (P > 0) {
-    // state-dependent map C = F1 M + F2 Omega^T (coef holds Omega^T): C x =
-    // F1 (M x) + F2 (Omega^T x) for x = e^g . q and x = e^g . k
-    static_assert(P == 4 && R <= 32, "pivot maps: P = 4, rank up to 32");
-    const int ch = ((col & 3) + 4 * row) * MW;     // MW channels per lane of M x
-    float mq = 0.f, mk = 0.f;
-#pragma unroll
-    for (int m = 0; m < MW; ++m) {
-      mq += mr.get(m) * xq_l[ch + m];
-      if constexpr (ERASE) mk += mr.get(m) * xk_l[ch + m];
-    }
-    mq = cross_row_sum(quad_sum(mq));               // lanes with col / 4 = a hold (M x)[a]
-    if constexpr (ERASE) mk = cross_row_sum(quad_sum(mk));
-    float mqa[P], mka[P];
-#pragma unroll
-    for (int x = 0; x < P; ++x) {
-      mqa[x] = lane_bcast(mq, 4 * x);
-      mka[x] = ERASE ? lane_bcast(mk, 4 * x) : 0.f;
-    }
-    wave_lds_sync();                                // x_q, x_k are read; reuse them for Omega^T x
-    if (row == 0) {
-#pragma unroll
-      for (int p = 0; p < RP; ++p) {
-        const int j = col + 16 * p;
-        if (j < R) {
-          xq_l[j] = sqv[p];
-          if constexpr (ERASE) xk_l[j] = skv[p];
-        }
-      }
-    }
-    wave_lds_sync();
-#pragma unroll
-    for (int p = 0; p < RP; ++p) {
-      const int j = col + 16 * p;
-      float cq = 0.f, ck = 0.f;
-      if (j < rh) {  // rows of F1 and F2 past the head's rank are not used (HQ columns of F2 per row of lanes)
-        const Raw<SK, HQ>& f2 = f2r[p];
-#pragma unroll
-        for (int m = 0; m < HQ; ++m) {
-          cq += f2.get(m) * xq_l[row * HQ + m];
-          if constexpr (ERASE) ck += f2.get(m) * xk_l[row * HQ + m];
-        }
-        if (row == 0) {
-          const Raw<SK, 4>& f1 = f1r[p];
-          cq += f1.get(0) * mqa[0] + f1.get(1) * mqa[1] + f1.get(2) * mqa[2] + f1.get(3) * mqa[3];
-          if constexpr (ERASE) ck += f1.get(0) * mka[0] + f1.get(1) * mka[1] + f1.get(2) * mka[2] + f1.get(3) * mka[3];
-        }
-      }
-      sqv[p] = cross_row_sum(cq);
-      if constexpr (ERASE) skv[p] = cross_row_sum(ck);
-    }
   }
 #pragma unroll
   for (int p = 0; p < RP; ++p) {

@@ -58,14 +58,19 @@ template <> __device__ __forceinline__ float load1<bf16_t>(const bf16_t* p) { re
 //   T    = I + L_G^T D^{-1} L_G                  (Woodbury: only T is inverted)
 //   F1   = D^{-1} L_G T^{-1}  (= A^{-1} L_G),  F2 = A^{-1} Diag(d),
 //   A^{-1} = D^{-1} - D^{-1} L_G T^{-1} L_G^T D^{-1}
-// so the map is C = F1 M + F2 Omega^T.  Stored per item as M [P][K], F1
-// [G][P], F2 [G][G], in the sketch's dtype (bf16 with the paper's storage,
-// rounded to nearest even).  Every thread of the workgroup calls this.
-template <int K, int R, int P, int MT, int RT, int LSZ, int USZ, typename SK>
-__device__ __forceinline__ void coef_map_tail(const UpdateArgs& a, size_t item, int wave, int lane, int tid,
+// so the map is C = F1 M + F2 Omega^T (G x K).  The flush forms that product
+// on the matrix cores, C^T = [M^T Omega] [F1 F2]^T with the contraction over
+// the P + G stacked rows, and stores the dense map per item in the sketch's
+// dtype (bf16 with the paper's storage, rounded to nearest even) in 16-byte
+// channel panels cmap[B][H][K/CPW][G][CPW].  Rows past the head's rank are
+// not stored.  Every thread of the workgroup calls this.
+template <int K, int R, int P, int MT, int RT, int LSZ, int USZ, int OPJ, typename SK>
+__device__ __forceinline__ void coef_map_tail(const UpdateArgs& a, size_t item, int wave, int lane, int tid, int rh,
                                               const floatx4 (&nacc)[MT], const float (&gpart)[RT][4][5], float msq,
-                                              float* Ls, float* Us, float* cmS) {
+                                              float* Ls, float* Us, float* cmS, const float* OmL, float* Fext) {
   static_assert(LSZ >= 4 * K * P && USZ >= 4 * R * 5, "staging buffers too small for the map's partial sums");
+  constexpr int FBP = P + R + 1;                       // row pitch of [F1 F2] (odd: lanes of a read spread over banks)
+  constexpr bool FB_ALIAS = LSZ >= P * K + 16 * RT * FBP;
   const int lr = lane & 15, lg = lane >> 4;
   // this wave's Gram partials summed over its 16 value lanes
   float gs[RT][4][5];
@@ -99,8 +104,7 @@ __device__ __forceinline__ void coef_map_tail(const UpdateArgs& a, size_t item, 
   if (lane == 0) cmS[wave] = msq;
   lds_barrier();
 
-  const size_t CMW = (size_t)P * K + R * P + R * R;
-  SK* cm = static_cast<SK*>(a.cmap) + item * CMW;
+  float F1[P] = {};  // wave 0, lane g < R: row g of F1
   if (wave == 0) {
     const float fro = cmS[0] + cmS[1] + cmS[2] + cmS[3];
     const float mu = fro > 0.f ? fro / K : 1.f;
@@ -168,7 +172,7 @@ __device__ __forceinline__ void coef_map_tail(const UpdateArgs& a, size_t item, 
         l2 += LG[c] * LG[c];
       }
       dg = fmaxf(diag / mu - l2, 0.f);
-      dinv = __builtin_amdgcn_rcpf(dg + a.ridge);
+      dinv = __builtin_amdgcn_rcpf(dg + a.ridge);  // ridge > 0 (the ABI rejects others)
     }
     // T = I + L_G^T D^{-1} L_G (sum over the lanes g), then its inverse
     float Tm[P][P];
@@ -204,8 +208,7 @@ __device__ __forceinline__ void coef_map_tail(const UpdateArgs& a, size_t item, 
         }
       }
     }
-    // F1 row g, and the factors the F2 rows need from every g
-    float F1[P];
+    // F1 row g; L_G and w = D^{-1} d of every g for the F2 rows
 #pragma unroll
     for (int c = 0; c < P; ++c) {
       float e = 0.f;
@@ -225,28 +228,10 @@ __device__ __forceinline__ void coef_map_tail(const UpdateArgs& a, size_t item, 
 #pragma unroll
         for (int y = 0; y < P; ++y) cmS[8 + x * P + y] = Ri[x][y] * rs;
     }
-    wave_lds_sync();
-    if (g < R) {
-      st_elem4<SK>(cm + P * K + g * P, F1[0], F1[1], F1[2], F1[3]);
-      SK* F2 = cm + P * K + R * P + g * R;
-#pragma unroll 4
-      for (int hq = 0; hq < R; hq += 4) {
-        float o4[4];
-#pragma unroll
-        for (int u = 0; u < 4; ++u) {
-          const int hh = hq + u;
-          float e = 0.f;
-#pragma unroll
-          for (int c = 0; c < P; ++c) e += F1[c] * sL[hh * P + c];
-          const float w = sL[R * P + hh];
-          o4[u] = (hh == g ? w : 0.f) - e * w;
-        }
-        st_elem4<SK>(F2 + hq, o4[0], o4[1], o4[2], o4[3]);
-      }
-    }
   }
   lds_barrier();
   // M = R^{-T} N^T / sqrt(mu): thread k sums the four waves' N rows
+  float Mk[P] = {};
   if (tid < K) {
     const int k = tid;
     float Nk[P];
@@ -255,10 +240,51 @@ __device__ __forceinline__ void coef_map_tail(const UpdateArgs& a, size_t item, 
       Nk[b] = cmN[(0 * K + k) * P + b] + cmN[(1 * K + k) * P + b] + cmN[(2 * K + k) * P + b] + cmN[(3 * K + k) * P + b];
 #pragma unroll
     for (int x = 0; x < P; ++x) {
-      float e = 0.f;
 #pragma unroll
-      for (int b = 0; b < P; ++b) e += cmS[8 + b * P + x] * Nk[b];
-      st_elem<SK>(cm + x * K + k, e);
+      for (int b = 0; b < P; ++b) Mk[x] += cmS[8 + b * P + x] * Nk[b];
+    }
+  }
+  lds_barrier();  // the waves' N rows are consumed: M^T and [F1 F2] take their place
+  float* Mb = Ls;                              // [K][P]   M^T
+  float* Fb = FB_ALIAS ? Ls + P * K : Fext;    // [16 RT][FBP]  row j = (F1 row j, F2 row j), zero past R
+  if (tid < K) *reinterpret_cast<float4*>(&Mb[tid * P]) = make_float4(Mk[0], Mk[1], Mk[2], Mk[3]);
+  if (wave == 0 && lane < 16 * RT) {
+    const int g = lane;
+    float* fr = Fb + g * FBP;
+    if (g < R) {
+      const float* sL = cmS + 8 + 16;
+#pragma unroll
+      for (int c = 0; c < P; ++c) fr[c] = F1[c];
+      // row g of F2 = A^{-1} Diag(d): (g == h) w_h - F1[g] . L_G[h] w_h
+#pragma unroll 4
+      for (int hh = 0; hh < R; ++hh) {
+        float e = 0.f;
+#pragma unroll
+        for (int c = 0; c < P; ++c) e += F1[c] * sL[hh * P + c];
+        const float w = sL[R * P + hh];
+        fr[P + hh] = (hh == g ? w : 0.f) - e * w;
+      }
+    } else {
+#pragma unroll
+      for (int c = 0; c < P + R; ++c) fr[c] = 0.f;
+    }
+  }
+  lds_barrier();
+  // C^T = [M^T Omega] [F1 F2]^T: wave w takes k tiles w, w + 4, ...; lane
+  // (lr, lg) ends with C[16 jt + lr][16 kt + 4 lg + i], i = 0..3
+  constexpr int CPW = 16 / (int)sizeof(SK);
+  SK* cm = static_cast<SK*>(a.cmap) + item * (size_t)(R * K);
+#pragma unroll
+  for (int kt = wave; kt < MT; kt += 4) {
+#pragma unroll
+    for (int jt = 0; jt < RT; ++jt) {
+      floatx4 acc = {0.f, 0.f, 0.f, 0.f};
+      acc = mfma4(Mb[(16 * kt + lr) * P + lg], Fb[(16 * jt + lr) * FBP + lg], acc);
+#pragma unroll
+      for (int st = 0; st < R / 4; ++st)
+        acc = mfma4(OmL[(16 * kt + lr) * OPJ + 4 * st + lg], Fb[(16 * jt + lr) * FBP + P + 4 * st + lg], acc);
+      const int j = 16 * jt + lr, k0 = 16 * kt + 4 * lg;
+      if (j < rh) st_elem4<SK>(cm + ((size_t)(k0 / CPW) * R + j) * CPW + k0 % CPW, acc[0], acc[1], acc[2], acc[3]);
     }
   }
 }
@@ -334,6 +360,9 @@ __global__ __launch_bounds__(256, (P > 0 && WMAX == 16 && R <= 16) ? 4 : 3) void
   float* const cmX = CM_ALIAS ? Ls : cmXs;                 // [wave][16 values][16 keys]
   float* const cmU = CM_ALIAS ? Ls + 4 * 16 * XP : cmUs;   // [wave][16 values][P]
   __shared__ __align__(16) float cmS[P > 0 ? 8 + 16 + 5 * R : 4];  // mu parts, R^{-1}/sqrt(mu), L_G and w
+  // [F1 F2] of the map, in its own LDS only where the key staging has no room
+  constexpr bool CMF_OWN = P > 0 && SP * LP < P * K + 16 * RT * (P + R + 1);
+  __shared__ __align__(16) float cmF[CMF_OWN ? 16 * RT * (P + R + 1) : 4];
   floatx4 nacc[P > 0 ? MT : 1];    // N^T (rows a = 4 lg + i), per k tile, this wave's values
   float gpart[P > 0 ? RT : 1][4][5];  // sketch Gram: U[v][j] U[v][a] (a < 4) and U[v][j]^2, this lane's values
   float msq = 0.f;                 // this lane's share of |S|_F^2
@@ -762,7 +791,9 @@ __global__ __launch_bounds__(256, (P > 0 && WMAX == 16 && R <= 16) ? 4 : 3) void
   }
 
   if constexpr (P > 0) {
-    if (want_U) coef_map_tail<K, R, P, MT, RT, SP * LP, SP * UP, SK>(a, item, wave, lane, tid, nacc, gpart, msq, Ls, Us, cmS);
+    if (want_U)
+      coef_map_tail<K, R, P, MT, RT, SP * LP, SP * UP, OPJ, SK>(a, item, wave, lane, tid, rh, nacc, gpart, msq, Ls, Us,
+                                                                 cmS, OmL, cmF);
   }
 }
 

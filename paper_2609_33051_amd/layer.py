@@ -11,9 +11,10 @@ into libsketchssm.so.  Buffers (caller-owned, as the ABI requires):
          value: P = 4 columns fp32, or P = 8 bf16 (sketch="bf16", the paper's
          storage); sketch_matrix() gives the [B][H][V][r] fp32 view
   omega  [H][K][r]     fp32 sketching matrix, coef [H][r][K] its coefficient map
-         (Omega^T, the offline map; with pivots = 4 the map is state-dependent,
-         C = F1 M + F2 coef, rebuilt at every flush into cmap [B][H][4K+4r+r^2],
-         stored like U: fp32, or bf16 with sketch="bf16")
+         (Omega^T, the offline map); with pivots != 0 the map is
+         state-dependent, rebuilt at every flush into cmap (the dense r x K
+         map per item in 16-byte channel panels), stored like U: fp32, or bf16
+         with sketch="bf16"
   ring   replay buffer of W slots per item:
          raw inputs k, v (io dtype), beta, log_decay ([..][K] for KDA), item-major
          [B][H][W][...], written into slot n by the token's producer (write_token);
@@ -62,9 +63,9 @@ class SketchSSMLayer:
                                  device=dev)
         else:
             self.omega = self.coef = self.U = None
-        # state-dependent coefficient map (M, F1, F2 per item), written by every update
+        # state-dependent coefficient map (r x K per item), written by every update
         cw = B.cmap_width(self.cfg)
-        skdt = torch.bfloat16 if sketch == "bf16" else f32  # sketch, f and map factors share the storage dtype
+        skdt = torch.bfloat16 if sketch == "bf16" else f32  # sketch, f and map share the storage dtype
         self.cmap = torch.zeros((Bt, H, cw), dtype=skdt, device=dev) if cw else None
         # raw inputs, written by the producer of each token
         self.rk = torch.zeros((Bt, H, W, K), dtype=iodt, device=dev)

@@ -65,9 +65,9 @@ class Shape:
 
     @property
     def cmap_bytes(self) -> int:
-        """The per-item factors of a state-dependent map: M [P][K], F1 [r][P], F2 [r][r], stored like U."""
-        p = self.pivots
-        return self.sketch_bytes * (p * self.dk + self.rank * p + self.rank * self.rank) if p else 0
+        """The per-item state-dependent map C (r x K), stored like U: the 2GK
+        bytes of T_G with the paper's BF16 storage."""
+        return self.sketch_bytes * self.rank * self.dk if self.pivots else 0
 
     @property
     def decay_bytes(self) -> int:

@@ -100,15 +100,21 @@ def item_err(a, b) -> np.ndarray:
 # for bf16 inputs with an fp32 state.  Both sides consume the same stored
 # inputs (bf16 values upcast exactly), so the kernels agree with the oracle
 # far more closely than that; the per-item bars (item_err, every item, every
-# step) are set near what the arithmetic allows:
-#   - fp32 sketch, offline map: fp32 rounding of the state, sketch and sums;
+# step) are set near what the arithmetic allows, with a margin of about 5x
+# over the largest values measured on MI355X:
+#   - fp32 sketch, offline map: fp32 rounding of the state, sketch and sums,
+#     growing with the tokens applied (up to 1.1e-5 after 69 tokens at W = 32);
 #   - fp32 sketch, state-dependent map: the map's small solves in fp32 (one
-#     ulp reciprocals and square roots) amplify rounding by their conditioning;
-#   - bf16 sketch (U, f and the map stored in bf16): the occasional stored
-#     value that fp32 and fp64 round to neighbouring bf16 numbers (one bf16
-#     ulp, 2^-8 relative, of one element).
+#     ulp reciprocals and square roots) amplify rounding by their
+#     conditioning (up to 1.1e-4);
+#   - bf16 sketch (U, f and the map stored in bf16): a stored value that fp32
+#     and fp64 round to neighbouring bf16 numbers moves by one bf16 ulp (2^-8
+#     relative); the map, computed to about 1e-5 in fp32, has a few such
+#     elements per flush (up to 6.7e-4).
+# A 0.6 % error of one item or a 10 % error of one value channel of one item
+# is above every per-item bar (tests/test_parity_bars.py).
 HEADLINE = {"f32": 1e-5, "bf16": 2e-3}
-ITEM = {"f32": 1e-5, "f32-map": 1e-4, "bf16": 1e-3}
+ITEM = {"f32": 5e-5, "f32-map": 5e-4, "bf16": 2e-3}
 
 
 def bars(io: str, sketch: str, pivots: int = 0) -> tuple[float, float]:

@@ -109,13 +109,20 @@ class TestValidation:
         assert status(d, cfg(io=5), ADDR, ADDR, good_ring(), 0, ADDR, ADDR) == -1
         assert status(d, cfg(sketch=3), ADDR, ADDR, good_ring(), 0, ADDR, ADDR) == -1
         assert "sketch_dtype" in B.sketchssm_last_error()
-        # state-dependent coefficient map: P = 4 only, rank 8..32, a 16-byte aligned cmap, ridge >= 0
+        # state-dependent coefficient map: P = 4 only, rank 8..32, a 16-byte aligned cmap, ridge > 0
         assert status(d, cfg(pivots=3), ADDR, ADDR, good_ring(), 0, ADDR, ADDR) == -2
         assert status(d, cfg(pivots=4, rank=128), ADDR, ADDR, good_ring(), 0, ADDR, ADDR) == -2
         assert status(d, cfg(pivots=4), ADDR, ADDR, good_ring(), 0, ADDR, ADDR) == -1  # no cmap
         assert status(lambda *x: B.sketchssm_decode(*x, cmap=ADDR + 4), cfg(pivots=4), ADDR, ADDR, good_ring(), 0,
                       ADDR, ADDR) == -3
         assert status(d, cfg(pivots=4, ridge=-1.0), ADDR, ADDR, good_ring(), 0, ADDR, ADDR) == -1
+        # lambda = 0 would leave D = d + lambda singular where d = 0 (a zero state, columns past a head's rank)
+        assert status(lambda *x: B.sketchssm_decode(*x, cmap=ADDR), cfg(pivots=4, ridge=0.0), ADDR, ADDR,
+                      good_ring(), 0, ADDR, ADDR) == -1
+        assert "ridge" in B.sketchssm_last_error()
+        # with the offline map the caller's coef is required; with a state-dependent map it is not read
+        assert status(d, cfg(), ADDR, None, good_ring(), 0, ADDR, ADDR) == -1
+        assert "coef" in B.sketchssm_last_error()
         assert "n_buffered" in B.sketchssm_status_string(-4)
 
     def test_state_layout_rejections(self, lib):
@@ -143,6 +150,8 @@ class TestValidation:
         assert status(u, cfg(sketch=-1), ADDR, ADDR, good_ring(), 15, ADDR, ADDR, ADDR) == -1
         assert status(u, cfg(pivots=4), ADDR, ADDR, good_ring(), 15, ADDR, ADDR, ADDR) == -1  # no cmap
         assert status(u, cfg(pivots=4, rank=0), ADDR, None, good_ring(), 15, ADDR, None, ADDR) == -2
+        assert status(lambda *x: u(*x, cmap=ADDR), cfg(pivots=4, ridge=0.0), ADDR, ADDR, good_ring(), 15, ADDR, ADDR,
+                      ADDR) == -1
 
     def test_full_read_rejections(self, lib):
         f = B.sketchssm_full_read_baseline

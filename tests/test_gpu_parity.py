@@ -9,8 +9,8 @@ the test asserts the maximum over steps.
 
 Beside that headline bar, every (request, head) item is held, at every
 step, to a per-item bar near what the arithmetic allows (tests/harness.py:
-an item's error over the typical item size, 1e-5 with an fp32 sketch and
-the offline map, 1e-4 with the state-dependent map, 1e-3 with a bf16
+an item's error over the typical item size, 5e-5 with an fp32 sketch and
+the offline map, 5e-4 with the state-dependent map, 2e-3 with a bf16
 sketch), so that one wrong item or one wrong value channel cannot hide in
 the aggregate.
 

@@ -66,12 +66,18 @@ def test_ragged_bytes_reduce_to_the_uniform_and_dense_cases():
     assert T.ragged_flush_bytes(s, 15, [16, 0]) == T.flush_bytes(s, 15) + T.flush_bytes(s, 15, 0)
 
 
-def test_bf16_storage_halves_f_and_the_map_factors():
-    """With the paper's storage the sketch, f and the map factors are 2-byte values."""
+def test_bf16_storage_halves_f_and_the_map():
+    """With the paper's storage the sketch, f and the state-dependent map are
+    2-byte values, and the map a non-flush read takes is the dense G x K
+    matrix: the 2GK bytes of T_G = 2G(V + K + eW) (state memory traffic
+    appendix), beside the 2GV of the sketch."""
     T = traffic
     f32 = T.Shape("gdn", 128, 128, 16, 16, 2, 4, 4)
     b16 = T.Shape("gdn", 128, 128, 16, 16, 2, 2, 4)
-    assert f32.cmap_bytes == 4 * (4 * 128 + 16 * 4 + 16 * 16) and b16.cmap_bytes == f32.cmap_bytes // 2
+    off = T.Shape("gdn", 128, 128, 16, 16, 2, 2, 0)
+    assert b16.cmap_bytes == 2 * 16 * 128 and f32.cmap_bytes == 2 * b16.cmap_bytes and off.cmap_bytes == 0
+    for n in (0, 7):
+        assert T.decode_bytes(b16, n) - T.decode_bytes(off, n) == 2 * 16 * 128
     assert T.slot_read_bytes(f32) - T.slot_read_bytes(b16) == 2 * 16
     assert T.derived_write_bytes(f32, 5) - T.derived_write_bytes(b16, 5) == 2 * 16
     # the exact baseline keeps pi in fp32 whatever the sketch storage

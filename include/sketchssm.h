@@ -243,6 +243,46 @@ int sketchssm_full_read_baseline(const skssm_config* cfg, const float* S, const 
 int sketchssm_state_to_tiles(const skssm_config* cfg, const float* S_rows, float* S, void* stream);
 int sketchssm_state_from_tiles(const skssm_config* cfg, const float* S, float* S_rows, void* stream);
 
+/*
+ * Buffer sizes -- the bytes of every caller-owned buffer of one layer with
+ * configuration cfg, as the layouts above define them, so that a caller can
+ * allocate without restating them (Algorithm 1's memory objects: the fp32
+ * state, the sketch and coefficient map, and the replay buffer).
+ *
+ * baseline = 0: the layer of the sketch path (sketchssm_update /
+ *   sketchssm_decode).  The derived ring fields are tinv and f for GDN/KDA,
+ *   plus pi when the rank table has dense-fallback heads.
+ * baseline = 1: the layer of the exact full-read path
+ *   (sketchssm_full_read_baseline, with flushes by sketchssm_update at rank
+ *   0): no sketch, map or f; pi and tinv for GDN/KDA.  cfg->rank and
+ *   cfg->head_rank are ignored.
+ * Fields the configuration does not use are 0.  A field's size depends only
+ * on cfg, never on a pointer.  Returns SKSSM_OK, or a negative status for a
+ * configuration the calls would reject (out may be partly written then).
+ */
+typedef struct {
+  size_t S;         /* state, B*H*V*K fp32 (tile-major)                           */
+  size_t U;         /* sketch, B*H*V*rank in sketch_dtype                          */
+  size_t omega;     /* sketching matrix, H*K*rank fp32                             */
+  size_t coef;      /* offline map, H*rank*K fp32 (pivots = 0)                     */
+  size_t cmap;      /* state-dependent map, B*H*rank*K in sketch_dtype (pivots != 0) */
+  size_t q;         /* one query, B*H*K io_dtype                                   */
+  size_t o;         /* one output, B*H*V fp32                                      */
+  size_t ring_k;    /* [B][H][W][K] io_dtype                                       */
+  size_t ring_v;    /* [B][H][W][V] io_dtype                                       */
+  size_t ring_beta; /* [B][H][W] fp32                                              */
+  size_t ring_log_decay; /* [B][H][W] fp32, or [B][H][W][K] for KDA                */
+  size_t ring_f;    /* [W][H][B][rank] sketch_dtype (GDN/KDA sketch path)         */
+  size_t ring_pi;   /* [W][H][B][K] fp32 (GDN/KDA exact reads)                     */
+  size_t ring_tinv; /* [W][H][B][W] fp32 (GDN/KDA)                                 */
+} skssm_buffer_sizes;
+
+int sketchssm_buffer_sizes(const skssm_config* cfg, int32_t baseline, skssm_buffer_sizes* out);
+
+/* Total bytes of the replay buffer's fields (the ring_* sizes above), or 0
+ * for a configuration the calls would reject. */
+size_t sketchssm_ring_bytes(const skssm_config* cfg, int32_t baseline);
+
 /* Static text for a status code. */
 const char* sketchssm_status_string(int status);
 /* Detail of the last failure on this thread (validation message or HIP error text). */

@@ -23,8 +23,8 @@ STATUS = {0: "SKSSM_OK", -1: "SKSSM_EINVAL", -2: "SKSSM_EUNSUPPORTED", -3: "SKSS
           -4: "SKSSM_ESTATE", -5: "SKSSM_EHIP"}
 
 FUNCTIONS = ("sketchssm_update", "sketchssm_decode", "sketchssm_full_read_baseline",
-             "sketchssm_state_to_tiles", "sketchssm_state_from_tiles",
-             "sketchssm_status_string", "sketchssm_last_error", "sketchssm_check_config")
+             "sketchssm_state_to_tiles", "sketchssm_state_from_tiles", "sketchssm_buffer_sizes",
+             "sketchssm_ring_bytes", "sketchssm_status_string", "sketchssm_last_error", "sketchssm_check_config")
 
 
 class SketchSSMError(RuntimeError):
@@ -37,6 +37,14 @@ class Config(ctypes.Structure):
     _fields_ = [(name, ctypes.c_int32) for name in
                 ("kind", "batch", "heads", "dk", "dv", "rank", "window", "io_dtype", "sketch_dtype", "pivots")] + [
                    ("ridge", ctypes.c_float), ("head_rank", ctypes.POINTER(ctypes.c_int32))]
+
+
+BUFFERS = ("S", "U", "omega", "coef", "cmap", "q", "o", "ring_k", "ring_v", "ring_beta", "ring_log_decay",
+           "ring_f", "ring_pi", "ring_tinv")
+
+
+class BufferSizes(ctypes.Structure):
+    _fields_ = [(name, ctypes.c_size_t) for name in BUFFERS]
 
 
 class Ring(ctypes.Structure):
@@ -68,6 +76,10 @@ def load(path: str | None = None):
               "sketchssm_state_to_tiles", "sketchssm_state_from_tiles"):
         getattr(lib, f).restype = ctypes.c_int
     lib.sketchssm_check_config.argtypes = [cfgp]
+    lib.sketchssm_buffer_sizes.argtypes = [cfgp, ctypes.c_int32, ctypes.POINTER(BufferSizes)]
+    lib.sketchssm_buffer_sizes.restype = ctypes.c_int
+    lib.sketchssm_ring_bytes.argtypes = [cfgp, ctypes.c_int32]
+    lib.sketchssm_ring_bytes.restype = ctypes.c_size_t
     lib.sketchssm_status_string.argtypes = [ctypes.c_int]
     lib.sketchssm_status_string.restype = ctypes.c_char_p
     lib.sketchssm_last_error.argtypes = []
@@ -109,12 +121,6 @@ def make_config(kind, batch, heads, dk, dv, rank, window, io, sketch="f32", pivo
 def head_ranks(cfg: Config) -> list[int] | None:
     """The per-head rank table of a Config, or None."""
     return None if not cfg.head_rank else [cfg.head_rank[h] for h in range(cfg.heads)]
-
-
-def cmap_width(cfg: Config) -> int:
-    """Elements per item of the state-dependent coefficient map (rank x K, in
-    16-byte channel panels), 0 with the offline map."""
-    return cfg.rank * cfg.dk if cfg.pivots else 0
 
 
 def make_ring(k=None, v=None, beta=None, log_decay=None, f=None, pi=None, tinv=None) -> Ring:
@@ -196,6 +202,17 @@ def sketchssm_state_to_tiles(cfg: Config, S_rows, S, stream=None):
 def sketchssm_state_from_tiles(cfg: Config, S, S_rows, stream=None):
     """Tile-major state -> row layout X[B][H][V][K]."""
     _check(load().sketchssm_state_from_tiles(ctypes.byref(cfg), ptr(S), ptr(S_rows), stream))
+
+
+def sketchssm_buffer_sizes(cfg: Config, baseline: bool = False) -> dict:
+    """Bytes of every caller-owned buffer of a layer (the library's sizes query)."""
+    out = BufferSizes()
+    _check(load().sketchssm_buffer_sizes(ctypes.byref(cfg), 1 if baseline else 0, ctypes.byref(out)))
+    return {name: int(getattr(out, name)) for name in BUFFERS}
+
+
+def sketchssm_ring_bytes(cfg: Config, baseline: bool = False) -> int:
+    return int(load().sketchssm_ring_bytes(ctypes.byref(cfg), 1 if baseline else 0))
 
 
 def sketchssm_check_config(cfg: Config) -> int:

@@ -298,6 +298,43 @@ int sketchssm_full_read_baseline(const skssm_config* cfg, const float* S, const 
   return launched(r, "sketchssm_full_read_baseline");
 }
 
+int sketchssm_buffer_sizes(const skssm_config* cfg, int32_t baseline, skssm_buffer_sizes* out) {
+  if (!out) return fail(SKSSM_EINVAL, "out is NULL");
+  *out = skssm_buffer_sizes{};
+  int rc = check_shape(cfg, !baseline, !baseline);
+  if (rc) return rc;
+  Ranks rk;
+  if (!baseline && (rc = check_ranks(cfg, rk))) return rc;
+  const size_t B = (size_t)cfg->batch, H = (size_t)cfg->heads, K = (size_t)cfg->dk, V = (size_t)cfg->dv;
+  const size_t W = (size_t)cfg->window, r = baseline ? 0 : (size_t)cfg->rank;
+  const size_t io = cfg->io_dtype == SKSSM_BF16 ? 2 : 4, sk = cfg->sketch_dtype == SKSSM_BF16 ? 2 : 4;
+  const bool erase = cfg->kind != SKSSM_MAMBA2;
+  out->S = B * H * V * K * 4;
+  out->U = B * H * V * r * sk;
+  out->omega = H * K * r * 4;
+  out->coef = cfg->pivots ? 0 : H * r * K * 4;
+  out->cmap = cfg->pivots && !baseline ? B * H * r * K * sk : 0;
+  out->q = B * H * K * io;
+  out->o = B * H * V * 4;
+  out->ring_k = B * H * W * K * io;
+  out->ring_v = B * H * W * V * io;
+  out->ring_beta = B * H * W * 4;
+  out->ring_log_decay = B * H * W * (cfg->kind == SKSSM_KDA ? K : 1) * 4;
+  if (erase) {
+    out->ring_tinv = W * H * B * W * 4;
+    out->ring_f = (!baseline && rk.sketched > 0) ? W * H * B * r * sk : 0;
+    out->ring_pi = (baseline || rk.dense > 0) ? W * H * B * K * 4 : 0;
+  }
+  g_err[0] = '\0';
+  return SKSSM_OK;
+}
+
+size_t sketchssm_ring_bytes(const skssm_config* cfg, int32_t baseline) {
+  skssm_buffer_sizes z;
+  if (sketchssm_buffer_sizes(cfg, baseline, &z) != SKSSM_OK) return 0;
+  return z.ring_k + z.ring_v + z.ring_beta + z.ring_log_decay + z.ring_f + z.ring_pi + z.ring_tinv;
+}
+
 int sketchssm_state_to_tiles(const skssm_config* cfg, const float* S_rows, float* S, void* stream) {
   return state_layout(cfg, S_rows, S, stream, 1, "sketchssm_state_to_tiles");
 }

@@ -44,14 +44,25 @@ class SketchSSMLayer:
         iodt = torch.bfloat16 if io == "bf16" else torch.float32
         f32 = torch.float32
         Bt, H, K, V, W = batch, heads, dk, dv, window
-        erase = kind in ("gdn", "kda")
         dev = self.device
         r = 0 if baseline else rank
         self.head_ranks = None if (baseline or head_ranks is None) else [int(x) for x in head_ranks]
         self.dense_heads = 0 if self.head_ranks is None else sum(1 for x in self.head_ranks if x == 0)
         self.cfg = B.make_config(kind, Bt, H, K, V, r, W, io, sketch, self.pivots, ridge, head_ranks=self.head_ranks)
+        # every buffer is sized by the library (sketchssm_buffer_sizes) and
+        # viewed with the shape its layout defines
+        size = B.sketchssm_buffer_sizes(self.cfg, baseline)
+        skdt = torch.bfloat16 if sketch == "bf16" else f32  # sketch, f and map share the storage dtype
+
+        def buf(name, dtype, shape):
+            nbytes = size[name]
+            if nbytes == 0:
+                return None
+            t = torch.zeros(nbytes // torch.tensor([], dtype=dtype).element_size(), dtype=dtype, device=dev)
+            return t.view(shape)
+
         # the state in the kernels' tile-major layout (S, if given, is row layout [B][H][V][K])
-        self.S = torch.zeros((Bt, H, V * K), dtype=f32, device=dev)
+        self.S = buf("S", f32, (Bt, H, V * K))
         if S is not None:
             rows = S.to(device=dev, dtype=f32).reshape(Bt, H, V, K).contiguous()
             B.sketchssm_state_to_tiles(self.cfg, rows, self.S, self.stream())
@@ -59,24 +70,20 @@ class SketchSSMLayer:
             self.omega = omega.to(dev).contiguous()
             self.coef = coef.to(dev).contiguous()
             P = 8 if sketch == "bf16" else 4
-            self.U = torch.zeros((Bt, H, rank // P, V, P), dtype=torch.bfloat16 if sketch == "bf16" else f32,
-                                 device=dev)
+            self.U = buf("U", skdt, (Bt, H, rank // P, V, P))
         else:
             self.omega = self.coef = self.U = None
         # state-dependent coefficient map (r x K per item), written by every update
-        cw = B.cmap_width(self.cfg)
-        skdt = torch.bfloat16 if sketch == "bf16" else f32  # sketch, f and map share the storage dtype
-        self.cmap = torch.zeros((Bt, H, cw), dtype=skdt, device=dev) if cw else None
+        self.cmap = buf("cmap", skdt, (Bt, H, rank * K))
         # raw inputs, written by the producer of each token
-        self.rk = torch.zeros((Bt, H, W, K), dtype=iodt, device=dev)
-        self.rv = torch.zeros((Bt, H, W, V), dtype=iodt, device=dev)
-        self.rbeta = torch.zeros((Bt, H, W), dtype=f32, device=dev)
-        self.rla = torch.zeros((Bt, H, W, K) if kind == "kda" else (Bt, H, W), dtype=f32, device=dev)
+        self.rk = buf("ring_k", iodt, (Bt, H, W, K))
+        self.rv = buf("ring_v", iodt, (Bt, H, W, V))
+        self.rbeta = buf("ring_beta", f32, (Bt, H, W))
+        self.rla = buf("ring_log_decay", f32, (Bt, H, W, K) if kind == "kda" else (Bt, H, W))
         # derived fields, written by the library
-        self.rt = torch.zeros((W, H, Bt, W), dtype=f32, device=dev) if erase else None
-        self.rf = torch.zeros((W, H, Bt, rank), dtype=skdt, device=dev) if (erase and not baseline) else None
-        self.rpi = (torch.zeros((W, H, Bt, K), dtype=f32, device=dev)
-                    if (erase and (baseline or self.dense_heads)) else None)
+        self.rt = buf("ring_tinv", f32, (W, H, Bt, W))
+        self.rf = buf("ring_f", skdt, (W, H, Bt, rank))
+        self.rpi = buf("ring_pi", f32, (W, H, Bt, K))
         self.ring = B.make_ring(k=self.rk, v=self.rv, beta=self.rbeta, log_decay=self.rla, f=self.rf,
                                 pi=self.rpi, tinv=self.rt)
         self.o = torch.zeros((Bt, H, V), dtype=f32, device=dev)

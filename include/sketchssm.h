@@ -74,6 +74,9 @@ typedef enum {
 
 typedef enum { SKSSM_F32 = 0, SKSSM_BF16 = 1 } skssm_dtype;
 
+/* skssm_config.pivots of the state-dependent map with the exact state metric. */
+enum { SKSSM_EXACT_MAP = -1 };
+
 /* Shape of one linear-attention layer. */
 typedef struct {
   int32_t kind;     /* skssm_kind                                           */
@@ -92,7 +95,11 @@ typedef struct {
                        4: the state-dependent map (Sec. 4.1, eq. m-coeff) with the
                        P = 4 low-rank-plus-diagonal state metric (appendix on the
                        coefficient map, eq. pivot-metric), rebuilt from the state
-                       by every sketchssm_update into `cmap` (rank 8..32)       */
+                       by every sketchssm_update into `cmap` (rank 8..32);
+                       SKSSM_EXACT_MAP (-1): the same map with the exact state
+                       metric H (eq. pivot-ridge; Table 2's "Exact"), which for
+                       an orthonormal Omega is (U^T U/mu + lambda I)^{-1} U^T S^T/mu
+                       (rank 8 or 16)                                           */
   float ridge;      /* lambda > 0 of the state-dependent map (the paper uses 0.1) */
   const int32_t* head_rank; /* per-head rank table (host memory, read during the call),
                        or NULL: every head has rank `rank`.  With a table (the

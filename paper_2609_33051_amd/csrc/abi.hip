@@ -39,7 +39,8 @@ int check_shape(const skssm_config* c, bool need_rank, bool allow_rank0) {
   if (c->io_dtype != SKSSM_F32 && c->io_dtype != SKSSM_BF16) return fail(SKSSM_EINVAL, "unknown io_dtype %d", c->io_dtype);
   if (c->sketch_dtype != SKSSM_F32 && c->sketch_dtype != SKSSM_BF16)
     return fail(SKSSM_EINVAL, "unknown sketch_dtype %d", c->sketch_dtype);
-  if (c->pivots != 0 && c->pivots != 4) return fail(SKSSM_EUNSUPPORTED, "pivots %d: 0 or 4 are compiled", c->pivots);
+  if (c->pivots != 0 && c->pivots != 4 && c->pivots != SKSSM_EXACT_MAP)
+    return fail(SKSSM_EUNSUPPORTED, "pivots %d: 0, 4 or SKSSM_EXACT_MAP (-1) are compiled", c->pivots);
   // lambda > 0 keeps the map's diagonal D = d + lambda invertible where d = 0
   // (a zero state, sketch columns past a head's rank); the paper uses 0.1
   if (c->pivots && !(c->ridge > 0.f && c->ridge < 1e30f))
@@ -51,6 +52,15 @@ int check_shape(const skssm_config* c, bool need_rank, bool allow_rank0) {
     const bool r_ok = c->rank == 8 || c->rank == 16 || c->rank == 32 || c->rank == c->dk || (allow_rank0 && c->rank == 0);
     if (!r_ok) return fail(c->rank < 0 ? SKSSM_EINVAL : SKSSM_EUNSUPPORTED, "rank %d not supported", c->rank);
   }
+  return SKSSM_OK;
+}
+
+// State-dependent maps: P = 4 pivots for ranks 8..32, the exact metric for
+// ranks 8 and 16 (the storage width with a rank table).
+int check_map_rank(const skssm_config* c) {
+  if (c->pivots == SKSSM_EXACT_MAP && c->rank != 8 && c->rank != 16)
+    return fail(SKSSM_EUNSUPPORTED, "the exact-metric map is compiled for rank 8 and 16");
+  if (c->rank < 8 || c->rank > 32) return fail(SKSSM_EUNSUPPORTED, "state-dependent maps need rank 8..32");
   return SKSSM_OK;
 }
 
@@ -182,7 +192,7 @@ int sketchssm_update(const skssm_config* cfg, float* S, const float* omega, cons
   Ranks rk;
   if ((rc = check_ranks(cfg, rk))) return rc;
   if (cfg->pivots) {
-    if (cfg->rank < 8 || cfg->rank > 32) return fail(SKSSM_EUNSUPPORTED, "pivot maps need rank 8..32");
+    if ((rc = check_map_rank(cfg))) return rc;
     if (!cmap) return fail(SKSSM_EINVAL, "cmap is required when pivots > 0");
     if (!aligned(cmap)) return fail(SKSSM_EALIGN, "cmap not aligned");
   }
@@ -243,7 +253,7 @@ int sketchssm_decode(const skssm_config* cfg, const void* U, const float* coef, 
   Ranks rk;
   if ((rc = check_ranks(cfg, rk))) return rc;
   if (cfg->pivots) {
-    if (cfg->rank < 8 || cfg->rank > 32) return fail(SKSSM_EUNSUPPORTED, "pivot maps need rank 8..32");
+    if ((rc = check_map_rank(cfg))) return rc;
     if (!cmap) return fail(SKSSM_EINVAL, "cmap is required when pivots > 0");
     if (!aligned(cmap)) return fail(SKSSM_EALIGN, "cmap not aligned");
   }

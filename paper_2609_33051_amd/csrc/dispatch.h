@@ -37,8 +37,11 @@ int launch_update(const UpdateArgs& a, hipStream_t s) {
   return 0;
 }
 
-// Pivot maps (P = 4) are compiled for ranks 8..32; piv selects them.
+// State-dependent maps: piv = 4 (P = 4 pivots) is compiled for ranks 8..32,
+// piv = -1 (the exact metric, flush only: decode reads either map the same
+// way) for ranks 8 and 16.
 template <int R> constexpr bool kPivotRank = R >= 8 && R <= 32;
+template <int R> constexpr bool kExactRank = R == 8 || R == 16;
 
 template <int KIND, int K, int V, int R, int WM, int P>
 int decode_t(const DecodeArgs& a, int io, int sk, hipStream_t s) {
@@ -105,11 +108,13 @@ int update_t(const UpdateArgs& a, int io, int sk, hipStream_t s) {
 
 template <int KIND, int K, int V, int R>
 int update_w(const UpdateArgs& a, int io, int sk, int piv, hipStream_t s) {
-  if constexpr (kPivotRank<R>) {
-    if (piv) return a.W <= 16 ? update_t<KIND, K, V, R, 16, 4>(a, io, sk, s) : update_t<KIND, K, V, R, 32, 4>(a, io, sk, s);
-  } else {
-    if (piv) return kUnsupported;
+  if constexpr (kExactRank<R>) {
+    if (piv < 0) return a.W <= 16 ? update_t<KIND, K, V, R, 16, -1>(a, io, sk, s) : update_t<KIND, K, V, R, 32, -1>(a, io, sk, s);
   }
+  if constexpr (kPivotRank<R>) {
+    if (piv > 0) return a.W <= 16 ? update_t<KIND, K, V, R, 16, 4>(a, io, sk, s) : update_t<KIND, K, V, R, 32, 4>(a, io, sk, s);
+  }
+  if (piv) return kUnsupported;
   return a.W <= 16 ? update_t<KIND, K, V, R, 16, 0>(a, io, sk, s) : update_t<KIND, K, V, R, 32, 0>(a, io, sk, s);
 }
 

@@ -289,6 +289,112 @@ __device__ __forceinline__ void coef_map_tail(const UpdateArgs& a, size_t item, 
   }
 }
 
+// The state-dependent map with the exact state metric (eq. pivot-ridge with
+// the dense H; Table 2's "Exact"): with Omega orthonormal and R^T R = I,
+// J^T H J = U^T U / mu and J^T H R = U^T S^T / mu, so
+//   C = (U^T U / mu + lambda I)^{-1} N / mu,   N = U^T X = U^T S^T (G x K).
+// The sketch pass leaves per-wave partial products of N^T = U^T X and the
+// Gram U^T U (matrix cores, contraction over the wave's value tiles) and of
+// |S|_F^2.  They are summed over the waves in LDS in a fixed order (wave 0
+// stores, waves 1..3 add in turn), the Gram system is factored by Cholesky
+// on one wave (lane = row), every channel's column of the map is solved by
+// forward and back substitution (thread k), and the dense map is stored like
+// the pivot map's (16-byte channel panels).  G <= 16.  Every thread calls this.
+template <int K, int R, typename SK>
+__device__ __forceinline__ void coef_map_exact_tail(const UpdateArgs& a, size_t item, int wave, int lane, int tid,
+                                                    int rh, const floatx4 (&nacc)[K / 16], const floatx4& gacc,
+                                                    float msq, float* Ls, float* Us, float* cmS) {
+  constexpr int MT = K / 16, NP = K + 4, GP = R + 1;
+  static_assert(R <= 16, "the exact map is compiled for ranks up to 16");
+  const int lr = lane & 15, lg = lane >> 4;
+  float* Ns = Ls;            // [R][NP]   N, then the map
+  float* Gs = Us;            // [R][GP]   U^T U
+  float* Lm = Us + R * GP;   // [R][GP]   its Cholesky factor; then 1 / diagonal at Lm[j * GP + j]
+  msq = wave_sum(msq);
+  // rows j = 4 lg + i of N^T and of the Gram live in lane group lg
+#pragma unroll
+  for (int w = 0; w < 4; ++w) {
+    lds_barrier();  // w = 0: every wave is done with the pass's scratch in Ls
+    if (wave == w) {
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int j = 4 * lg + i;
+        if (j < R) {
+#pragma unroll
+          for (int kt = 0; kt < MT; ++kt) {
+            float* p = &Ns[j * NP + 16 * kt + lr];
+            *p = (w == 0 ? 0.f : *p) + nacc[kt][i];
+          }
+          if (lr < R) {
+            float* p = &Gs[j * GP + lr];
+            *p = (w == 0 ? 0.f : *p) + gacc[i];
+          }
+        }
+      }
+      if (lane == 0) cmS[w] = msq;
+    }
+  }
+  lds_barrier();
+  const float fro = cmS[0] + cmS[1] + cmS[2] + cmS[3];
+  const float mu = fro > 0.f ? fro / K : 1.f;
+  const float imu = 1.f / mu;
+  if (wave == 0) {
+    // Cholesky of A = U^T U / mu + lambda I: lane j holds row j
+    float ar[R];
+#pragma unroll
+    for (int g = 0; g < R; ++g) ar[g] = (lane < R ? Gs[lane * GP + g] * imu : 0.f) + (lane == g ? a.ridge : 0.f);
+    float lrow[R];
+#pragma unroll
+    for (int c = 0; c < R; ++c) {
+      const float piv = lane_bcast(ar[c], c);          // A_cc after the updates of columns < c (> 0: SPD)
+      const float ip = __builtin_amdgcn_rsqf(piv);
+      const float l = ar[c] * ip;                      // L_jc for j >= c
+      lrow[c] = lane >= c ? l : 0.f;
+#pragma unroll
+      for (int g = c + 1; g < R; ++g) ar[g] -= l * lane_bcast(l, g);
+    }
+    if (lane < R) {
+#pragma unroll
+      for (int c = 0; c < R; ++c) Lm[lane * GP + c] = c == lane ? 1.f / lrow[c] : lrow[c];
+    }
+  }
+  lds_barrier();
+  // column k of the map: L y = N_k / mu, L^T c = y
+  if (tid < K) {
+    const int k = tid;
+    float y[R];
+#pragma unroll
+    for (int j = 0; j < R; ++j) {
+      float e = Ns[j * NP + k] * imu;
+#pragma unroll
+      for (int c = 0; c < j; ++c) e -= Lm[j * GP + c] * y[c];
+      y[j] = e * Lm[j * GP + j];
+    }
+#pragma unroll
+    for (int j = R - 1; j >= 0; --j) {
+      float e = y[j];
+#pragma unroll
+      for (int c = j + 1; c < R; ++c) e -= Lm[c * GP + j] * y[c];
+      y[j] = e * Lm[j * GP + j];
+    }
+#pragma unroll
+    for (int j = 0; j < R; ++j) Ns[j * NP + k] = y[j];
+  }
+  lds_barrier();
+  // the dense map in 16-byte channel panels: thread (kp, j), j fastest
+  constexpr int CPW = 16 / (int)sizeof(SK);
+  SK* cm = static_cast<SK*>(a.cmap) + item * (size_t)(R * K);
+#pragma unroll
+  for (int t = tid; t < R * K / CPW; t += 256) {
+    const int j = t % R, kp = t / R;
+    if (j < rh) {
+      const float* src = &Ns[j * NP + kp * CPW];
+#pragma unroll
+      for (int e = 0; e < CPW; e += 4) st_elem4<SK>(cm + (size_t)t * CPW + e, src[e], src[e + 1], src[e + 2], src[e + 3]);
+    }
+  }
+}
+
 // Three workgroups per CU, or four for the state-dependent map at window 16
 // and rank <= 16: its flush spends part of each workgroup's life off the
 // memory bus (the map's products and algebra), so occupancy pays there, even
@@ -346,29 +452,38 @@ __global__ __launch_bounds__(256, (P > 0 && WMAX == 16 && R <= 16) ? 4 : 3) void
   const int rh = a.ragged ? (int)a.hrank[h] : R;
   const bool want_U = R > 0 && a.U != nullptr && rh > 0;
 
-  // state-dependent coefficient map (P > 0 pivots): per-wave scratch for the
-  // block transposes of N = S U_p and for the first P sketch columns, and the
-  // small factors shared by the workgroup
-  static_assert(P == 0 || (P == 4 && R >= 8 && R <= 32), "pivot maps: P = 4, rank 8..32");
+  // state-dependent coefficient map (P = 4 pivots, or the exact metric, P < 0):
+  // per-wave scratch for the block transposes of X and of the first sketch
+  // columns, and the small factors shared by the workgroup
+  constexpr bool EXACT = P < 0;
+  static_assert(P == 0 || (P == 4 && R >= 8 && R <= 32) || (EXACT && R >= 8 && R <= 16),
+                "state-dependent maps: P = 4 with rank 8..32, or the exact metric with rank 8..16");
   constexpr int XP = 20;                                        // row pitch of a transposed 16 x 16 block
   // When the key staging Ls has room, that scratch lives in Ls: every tile is
   // then updated first and sketched after a barrier, once Ls is dead.  This
   // keeps the kernel's LDS that of the offline-map flush (four workgroups per CU).
-  constexpr bool CM_ALIAS = P > 0 && SP * LP >= 4 * 16 * XP + 4 * 16 * 4;
-  __shared__ __align__(16) float cmXs[P > 0 && !CM_ALIAS ? 4 * 16 * XP : 4];
+  // The exact map transposes all 16 sketch columns of a tile through the
+  // same per-wave block as X (one after the other).
+  constexpr bool CM_ALIAS = (P > 0 && SP * LP >= 4 * 16 * XP + 4 * 16 * 4) || (EXACT && SP * LP >= 4 * 16 * XP);
+  __shared__ __align__(16) float cmXs[P != 0 && !CM_ALIAS ? 4 * 16 * XP : 4];
   __shared__ __align__(16) float cmUs[P > 0 && !CM_ALIAS ? 4 * 16 * 4 : 4];
   float* const cmX = CM_ALIAS ? Ls : cmXs;                 // [wave][16 values][16 keys]
-  float* const cmU = CM_ALIAS ? Ls + 4 * 16 * XP : cmUs;   // [wave][16 values][P]
-  __shared__ __align__(16) float cmS[P > 0 ? 8 + 16 + 5 * R : 4];  // mu parts, R^{-1}/sqrt(mu), L_G and w
+  float* const cmU = EXACT ? cmX : (CM_ALIAS ? Ls + 4 * 16 * XP : cmUs);  // [wave][16 values][P] (exact: [16][XP])
+  __shared__ __align__(16) float cmS[P != 0 ? 8 + 16 + 5 * R : 4];  // mu parts, R^{-1}/sqrt(mu), L_G and w
   // [F1 F2] of the map, in its own LDS only where the key staging has no room
   constexpr bool CMF_OWN = P > 0 && SP * LP < P * K + 16 * RT * (P + R + 1);
   __shared__ __align__(16) float cmF[CMF_OWN ? 16 * RT * (P + R + 1) : 4];
-  floatx4 nacc[P > 0 ? MT : 1];    // N^T (rows a = 4 lg + i), per k tile, this wave's values
+  static_assert(!EXACT || (SP * LP >= R * (K + 4) && SP * UP >= 2 * R * (R + 1)),
+                "the exact map's sums must fit the window staging");
+  floatx4 nacc[P != 0 ? MT : 1];   // N^T (rows 4 lg + i: pivots a < 4, or every sketch column), this wave's values
   float gpart[P > 0 ? RT : 1][4][5];  // sketch Gram: U[v][j] U[v][a] (a < 4) and U[v][j]^2, this lane's values
+  [[maybe_unused]] floatx4 gacc = {0.f, 0.f, 0.f, 0.f};  // exact: U^T U (rows 4 lg + i, column lr), this wave's values
   float msq = 0.f;                 // this lane's share of |S|_F^2
-  if constexpr (P > 0) {
+  if constexpr (P != 0) {
 #pragma unroll
     for (int kt = 0; kt < MT; ++kt) nacc[kt] = floatx4{0.f, 0.f, 0.f, 0.f};
+  }
+  if constexpr (P > 0) {
 #pragma unroll
     for (int jt = 0; jt < RT; ++jt)
 #pragma unroll
@@ -715,7 +830,7 @@ __global__ __launch_bounds__(256, (P > 0 && WMAX == 16 && R <= 16) ? 4 : 3) void
       if (want_U && ps == PASSES - 1) {
         const float* om = a.omega + (size_t)h * K * R;
         float4 up4 = make_float4(0.f, 0.f, 0.f, 0.f);  // U[v][0..3] (state-dependent map)
-        float aop[4] = {0.f, 0.f, 0.f, 0.f};            // U_p^T as the A operand of N^T = U_p^T X
+        float aop[4] = {0.f, 0.f, 0.f, 0.f};            // U_p^T (exact: U^T) as the A operand of N^T = U_p^T X
 #pragma unroll
         for (int jt = 0; jt < RT; ++jt) {
           const int jj = 16 * jt + lr;
@@ -731,6 +846,20 @@ __global__ __launch_bounds__(256, (P > 0 && WMAX == 16 && R <= 16) ? 4 : 3) void
                 w = (jj < R) ? om[(16 * kt + 4 * lg + i) * R + jj] : 0.f;
               acc = mfma4(w, xs[t][kt][i], acc);
             }
+          if constexpr (EXACT) {
+            // every sketch column of the tile's 16 values goes through LDS, so
+            // that U^T becomes the A operand (value index as the contraction
+            // index); the same registers are U as the B operand of U^T U
+            float* cu = cmU + wave * 16 * XP;
+            wave_lds_sync();
+            *reinterpret_cast<float4*>(&cu[lr * XP + 4 * lg]) = make_float4(acc[0], acc[1], acc[2], acc[3]);
+            wave_lds_sync();
+#pragma unroll
+            for (int st = 0; st < 4; ++st) {
+              aop[st] = cu[(4 * st + lg) * XP + lr];
+              gacc = mfma4(aop[st], aop[st], gacc);
+            }
+          }
           if constexpr (P > 0) {
             // Gram partials of the sketch against its first P columns, which lane
             // (lr, lg = 0) holds for this tile's 16 values after the jt = 0 product
@@ -768,8 +897,8 @@ __global__ __launch_bounds__(256, (P > 0 && WMAX == 16 && R <= 16) ? 4 : 3) void
             }
           }
         }
-        if constexpr (P > 0) {
-          // N^T = U_p^T X over this tile's 16 values on the matrix cores: each 16 x 16
+        if constexpr (P != 0) {
+          // N^T = U_p^T X (exact map: U^T X) over this tile's 16 values on the matrix cores: each 16 x 16
           // block of X goes through LDS so that the value index becomes the
           // contraction index (lane group), then four 16x16x4 steps
           float* cx = cmX + wave * 16 * XP;
@@ -794,6 +923,9 @@ __global__ __launch_bounds__(256, (P > 0 && WMAX == 16 && R <= 16) ? 4 : 3) void
     if (want_U)
       coef_map_tail<K, R, P, MT, RT, SP * LP, SP * UP, OPJ, SK>(a, item, wave, lane, tid, rh, nacc, gpart, msq, Ls, Us,
                                                                  cmS, OmL, cmF);
+  }
+  if constexpr (EXACT) {
+    if (want_U) coef_map_exact_tail<K, R, SK>(a, item, wave, lane, tid, rh, nacc, gacc, msq, Ls, Us, cmS);
   }
 }
 

@@ -111,6 +111,11 @@ class TestValidation:
         assert "sketch_dtype" in B.sketchssm_last_error()
         # state-dependent coefficient map: P = 4 only, rank 8..32, a 16-byte aligned cmap, ridge > 0
         assert status(d, cfg(pivots=3), ADDR, ADDR, good_ring(), 0, ADDR, ADDR) == -2
+        # the exact-metric map (pivots = -1) is compiled for ranks 8 and 16
+        assert status(lambda *x: B.sketchssm_decode(*x, cmap=ADDR), cfg(pivots=-1, rank=32), ADDR, ADDR,
+                      good_ring(), 0, ADDR, ADDR) == -2
+        assert "exact" in B.sketchssm_last_error()
+        assert status(d, cfg(pivots=-2), ADDR, ADDR, good_ring(), 0, ADDR, ADDR) == -2
         assert status(d, cfg(pivots=4, rank=128), ADDR, ADDR, good_ring(), 0, ADDR, ADDR) == -2
         assert status(d, cfg(pivots=4), ADDR, ADDR, good_ring(), 0, ADDR, ADDR) == -1  # no cmap
         assert status(lambda *x: B.sketchssm_decode(*x, cmap=ADDR + 4), cfg(pivots=4), ADDR, ADDR, good_ring(), 0,

@@ -251,3 +251,27 @@ def test_pivot_map_full_size(name, sketch):
     """bf16: the paper's method as the benchmark times it (bf16 sketch, f and map factors)."""
     wl = inputs.WORKLOADS[name]
     check(wl, sel=sample_items(wl), sketch=sketch, pivots=4)
+
+
+# --- the state-dependent map with the exact state metric (eq. pivot-ridge with the dense H) -------
+EXACT = -1
+
+
+@pytest.mark.parametrize("fam,K,V,rank,window,io,sketch", [
+    ("mamba2_form", 64, 64, 8, 8, "f32", "f32"),
+    ("gdn", 128, 128, 16, 16, "bf16", "f32"),
+    ("kda", 128, 128, 16, 32, "bf16", "bf16"),
+    ("mamba2", 128, 64, 16, 16, "bf16", "bf16"),
+    ("gdn", 64, 64, 16, 8, "f32", "f32"),      # the sums fill the key staging exactly (K = 64, W = 16 slots)
+    ("kda", 128, 64, 8, 5, "bf16", "f32"),
+])
+def test_exact_map_small(fam, K, V, rank, window, io, sketch):
+    wl = inputs.tiny(fam, batch=5, heads=3, dk=K, dv=V, rank=rank, window=window, steps=2 * window + 3, io=io)
+    check(wl, sketch=sketch, pivots=EXACT)
+
+
+@pytest.mark.parametrize("sketch", ["f32", "bf16"])
+@pytest.mark.parametrize("name", ["mamba2_b256", "gdn_b512", "kda_b512"])
+def test_exact_map_full_size(name, sketch):
+    wl = inputs.WORKLOADS[name]
+    check(wl, sel=sample_items(wl), sketch=sketch, pivots=EXACT)

@@ -75,15 +75,17 @@ def test_ragged_small(fam, K, V, rank, window, io, ranks):
     check_ragged(wl, ranks)
 
 
-@pytest.mark.parametrize("fam,rank,ranks,sketch", [
-    ("mamba2", 16, [16, 0, 5, 8], "f32"),
-    ("gdn", 16, [12, 0, 16, 3], "bf16"),
-    ("kda", 32, [32, 7, 0, 20], "f32"),
+@pytest.mark.parametrize("fam,rank,ranks,sketch,pivots", [
+    ("mamba2", 16, [16, 0, 5, 8], "f32", 4),
+    ("gdn", 16, [12, 0, 16, 3], "bf16", 4),
+    ("kda", 32, [32, 7, 0, 20], "f32", 4),
+    ("gdn", 16, [16, 0, 9, 1], "f32", -1),   # the exact-metric map at each head's rank
+    ("kda", 8, [3, 8, 0, 5], "bf16", -1),
 ])
-def test_ragged_pivot_map(fam, rank, ranks, sketch):
+def test_ragged_pivot_map(fam, rank, ranks, sketch, pivots):
     V = 64 if fam == "mamba2" else 128
     wl = inputs.tiny(fam, batch=5, heads=len(ranks), dk=128, dv=V, rank=rank, window=8, steps=19, io="bf16")
-    check_ragged(wl, ranks, sketch=sketch, pivots=4)
+    check_ragged(wl, ranks, sketch=sketch, pivots=pivots)
 
 
 def test_ragged_all_dense_and_all_sketched():

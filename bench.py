@@ -27,12 +27,19 @@ Reported (one JSON line):
   full_read      the exact full-state-read (ReplaySSM-style) baseline path
   cpu_baseline   the CPU oracle timed on a bounded sample of the same
                  workload on the host cores, scaled to steps/s per layer
+  exact_map      the flush with the state-dependent map built under the exact
+                 state metric beside the P = 4 one (the paper's Table 2 ratio)
+
+The timed tokens are split into rounds of whole windows (up to seven, as
+the paper times its kernels); besides the whole-region `value`, the median
+over rounds of each round's steps/s is reported.
 """
 from __future__ import annotations
 
 import argparse
 import json
 import os
+import statistics
 import sys
 import time
 
@@ -42,8 +49,9 @@ METRIC = "decode steps/s per layer + state-access GB/s (% HBM roofline) at batch
 def parse():
     p = argparse.ArgumentParser()
     p.add_argument("--gpus", type=int, default=1)
-    p.add_argument("--steps", type=int, default=256)
-    p.add_argument("--warmup", type=int, default=32)
+    p.add_argument("--steps", type=int, default=672, help="timed tokens per layer (rounded up to whole windows)")
+    p.add_argument("--warmup", type=int, default=32, help="untimed tokens per layer (rounded up to whole windows)")
+    p.add_argument("--rounds", type=int, default=7, help="timing rounds of whole windows the median is taken over")
     p.add_argument("--workload", default="mamba2_b256")
     p.add_argument("--rank", type=int, default=None)
     p.add_argument("--window", type=int, default=None)
@@ -97,7 +105,9 @@ def main():
 
     om, C = inputs.omega(wl, rank)
     om_t, C_t = torch.as_tensor(om), torch.as_tensor(C)
-    pool = [inputs.step_inputs(wl, t, dev) for t in range(W)]  # one window of resident inputs, reused
+    # one window of resident inputs per rotated layer (its own queries and ring
+    # contents, so no layer's reads are served from another's cached data)
+    pools = [[inputs.step_inputs(wl, t, dev, seed=inputs.SEED + 100 * li) for t in range(W)] for li in range(L)]
 
     def make_layers(baseline, sketch, pivots, head_ranks=None):
         layers = []
@@ -108,48 +118,70 @@ def main():
                                  head_ranks=head_ranks)
             lay.init_sketch()
             for slot in range(W):  # the producer's writes: one window of tokens, resident in the ring
-                lay.write_token(pool[slot], slot)
+                lay.write_token(pools[li][slot], slot)
             layers.append(lay)
         torch.cuda.synchronize()
         return layers
 
-    def run(layers, n_tokens, events=None):
+    def run(layers, n_tokens, events=None, win_events=None):
         """n_tokens decode tokens through every layer, from calls marshalled
         once per (slot, layer).  The L launches of one token are the same
         kernel at the same slot, back to back on one stream; with `events`, a
-        pre-created pair of HIP events brackets each such group."""
-        plan = [[lay.prepared_read(pool[t]["q"], t) for lay in layers] for t in range(W)]
+        pre-created pair of HIP events brackets each such group, and with
+        `win_events` one event marks every window boundary."""
+        plan = [[lay.prepared_read(pools[li][t]["q"], t) for li, lay in enumerate(layers)] for t in range(W)]
         stream = torch.cuda.current_stream()
         for t in range(n_tokens):
+            if win_events is not None and t % W == 0:
+                win_events[t // W].record(stream)
             if events is not None:
                 events[t][1].record(stream)
             for call in plan[t % W]:
                 call()
             if events is not None:
                 events[t][2].record(stream)
+        if win_events is not None:
+            win_events[-1].record(stream)
         for lay in layers:
             lay.n = n_tokens % W
+
+    n_win = K_steps // W
+    n_rounds = max(1, min(args.rounds, n_win))
+
+    def round_rates(win_events):
+        """Steps/s per layer of each round (whole windows, launch gaps included)."""
+        wt = [win_events[i].elapsed_time(win_events[i + 1]) * 1e-3 for i in range(n_win)]
+        per = n_win // n_rounds
+        out = []
+        for r in range(n_rounds):
+            ws = wt[r * per:(r + 1) * per] if r < n_rounds - 1 else wt[r * per:]
+            out.append(len(ws) * W * L / sum(ws))
+        return out
 
     def timed(baseline, sketch=args.sketch, pivots=args.pivots, head_ranks=None):
         layers = make_layers(baseline, sketch, pivots, head_ranks)
         stream = torch.cuda.current_stream()
         events = [(t % W, torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
                   for t in range(K_steps)]
+        win_events = [torch.cuda.Event(enable_timing=True) for _ in range(n_win + 1)]
         for _, e0, e1 in events:  # create the HIP events before the timed region
             e0.record(stream)
             e1.record(stream)
+        for e in win_events:
+            e.record(stream)
         run(layers, warm, None)
         torch.cuda.synchronize()
         t0 = time.perf_counter()
-        run(layers, K_steps, events)
+        run(layers, K_steps, events, win_events)
         torch.cuda.synchronize()
         elapsed = time.perf_counter() - t0
         per_n = {}  # slot -> per-launch seconds, one entry per token (group of L launches)
         for n, e0, e1 in events:
             per_n.setdefault(n, []).append(e0.elapsed_time(e1) * 1e-3 / L)
+        rates = round_rates(win_events)
         del layers
         torch.cuda.empty_cache()
-        return elapsed, per_n
+        return elapsed, per_n, rates
 
     def kernel_stats(per_n, sketch, pivots):
         """Decode and flush figures from per-slot launch times (seconds)."""
@@ -163,13 +195,15 @@ def main():
         fl_bytes = traffic.flush_bytes(sh, W - 1) * items
         flops = items * (2 * wl.dv * wl.dk * W * (2 if sh.erase else 1) + 2 * wl.dv * wl.dk * rank)
         win = sum(sum(v) / len(v) for v in per_n.values())
+        dec_all = sorted(x for n in dec_n for x in per_n[n])
         return {"dec_mean": dec_time / dec_launches, "dec_bytes": dec_bytes / dec_launches,
+                "dec_median": statistics.median(dec_all), "fl_median": statistics.median(fl),
                 "dec_gbps": dec_bytes / dec_time / 1e9, "fl_mean": fl_mean, "fl_bytes": fl_bytes,
                 "fl_gbps": fl_bytes / fl_mean / 1e9, "fl_tflops": flops / fl_mean / 1e12, "window": win,
                 "per_slot": {int(n): round(sum(v) / len(v) * 1e6, 2) for n, v in sorted(per_n.items()) if n < W - 1}}
 
     # ---- the SketchSSM path
-    elapsed, per_n = timed(False)
+    elapsed, per_n, rates = timed(False)
     layer_steps = K_steps * L
     value = layer_steps / elapsed
     ks = kernel_stats(per_n, args.sketch, args.pivots)
@@ -184,6 +218,12 @@ def main():
         "n_gpus": 1,
         "steps": K_steps,
         "warmup": warm,
+        "steps_requested": args.steps,
+        "warmup_requested": args.warmup,
+        "steps_note": "tokens per layer, rounded up to whole windows of W so that every timed window holds its flush",
+        "rounds": n_rounds,
+        "value_median_of_rounds": round(statistics.median(rates), 2),
+        "value_rounds": [round(x, 1) for x in rates],
         "ms_per_step": round(elapsed / layer_steps * 1e3, 5),
         "higher_is_better": True,
         "scaling": "weak",
@@ -204,12 +244,14 @@ def main():
             "traffic": traffic_rec and traffic_rec["bytes_per_launch"],
             "bytes_per_launch": int(dec_bytes_per_launch),
             "mean_launch_us": round(dec_mean_s * 1e6, 2),
+            "median_launch_us": round(ks["dec_median"] * 1e6, 2),
         },
         "state_access_gbps": round(dec_gbps, 1),
         "kernels": {
-            "decode": {"mean_us": round(dec_mean_s * 1e6, 2), "gbps": round(dec_gbps, 1),
-                       "per_slot_us": ks["per_slot"]},
-            "flush": {"mean_us": round(fl_mean_s * 1e6, 2), "bytes": fl_bytes,
+            "decode": {"mean_us": round(dec_mean_s * 1e6, 2), "median_us": round(ks["dec_median"] * 1e6, 2),
+                       "gbps": round(dec_gbps, 1), "per_slot_us": ks["per_slot"]},
+            "flush": {"mean_us": round(fl_mean_s * 1e6, 2), "median_us": round(ks["fl_median"] * 1e6, 2),
+                      "bytes": fl_bytes,
                       "gbps": round(ks["fl_gbps"], 1),
                       "mfma_tflops": round(ks["fl_tflops"], 2), "mfma_peak_tflops": 157.3},
             "window_us": round(window_s * 1e6, 1),
@@ -218,27 +260,40 @@ def main():
     }
 
     # ---- beside an offline-map fp32 headline, same inputs: the paper's sketch
-    # storage (bf16 U), and its method (bf16 U with the state-dependent map)
+    # storage (bf16 U), its method (bf16 U and map with the state-dependent
+    # P = 4 map) and the same with the exact-metric map (flush cost, Table 2)
+    legs = [("paper_storage", "bf16", 0), ("paper_method", "bf16", 4)]
+    if rank in (8, 16):
+        legs.append(("exact_map", "bf16", -1))
     if args.sketch == "f32" and args.pivots == 0 and not args.no_paper_storage:
-        for key, sk_, pv in (("paper_storage", "bf16", 0), ("paper_method", "bf16", 4)):
-            e_p, per_p = timed(False, sk_, pv)
+        for key, sk_, pv in legs:
+            e_p, per_p, rates_p = timed(False, sk_, pv)
             kp = kernel_stats(per_p, sk_, pv)
             tr = recorded_traffic("decode", wl, rank, W, sk_, pv)
             out[key] = {
                 "sketch": sk_, "pivots": pv, "value": round(layer_steps / e_p, 2), "unit": "steps/s",
+                "value_median_of_rounds": round(statistics.median(rates_p), 2),
                 "decode_mean_us": round(kp["dec_mean"] * 1e6, 2), "decode_bytes_per_launch": int(kp["dec_bytes"]),
                 "decode_gbps": round(kp["dec_gbps"], 1),
                 "decode_frac": round(kp["dec_gbps"] / traffic.HBM_PEAK_GBPS, 4),
                 "decode_traffic": tr and tr["bytes_per_launch"],
-                "flush_mean_us": round(kp["fl_mean"] * 1e6, 2), "window_avg_steps_per_s": round(W / kp["window"], 1),
+                "flush_mean_us": round(kp["fl_mean"] * 1e6, 2), "flush_median_us": round(kp["fl_median"] * 1e6, 2),
+                "flush_bytes": kp["fl_bytes"], "flush_gbps": round(kp["fl_gbps"], 1),
+                "window_avg_steps_per_s": round(W / kp["window"], 1),
             }
+        if "exact_map" in out and "paper_method" in out:
+            out["exact_map"]["flush_ratio_exact_vs_p4"] = round(
+                out["exact_map"]["flush_median_us"] / out["paper_method"]["flush_median_us"], 3)
+        if "paper_storage" in out and "paper_method" in out:
+            out["paper_method"]["flush_overhead_vs_offline_map"] = round(
+                out["paper_method"]["flush_median_us"] / out["paper_storage"]["flush_median_us"] - 1, 4)
 
     # ---- a per-head rank table (Sec. 4.2) over the same storage width: a
     # seeded synthetic allocation with dense-fallback heads, whose non-flush
     # reads are exact full-state reads issued beside the sketch read
     if not args.no_ragged and rank in (8, 16, 32) and wl.heads <= 256:
         ranks = inputs.ragged_ranks(wl)
-        e_r, per_r = timed(False, args.sketch, args.pivots, head_ranks=ranks)
+        e_r, per_r, _ = timed(False, args.sketch, args.pivots, head_ranks=ranks)
         rd_n = [n for n in per_r if n < W - 1]
         rd_time = sum(sum(per_r[n]) for n in rd_n)
         rd_launch = rd_time / sum(len(per_r[n]) for n in rd_n)
@@ -260,7 +315,7 @@ def main():
 
     # ---- the exact full-state-read baseline (same inputs; flush with rank 0)
     if not args.no_full_read:
-        e_b, per_b = timed(True)
+        e_b, per_b, rates_b = timed(True)
         fr_n = [n for n in per_b if n < W - 1]
         fr_time = sum(sum(per_b[n]) for n in fr_n)
         fr_bytes = sum(traffic.full_read_bytes(shape, n) * items * len(per_b[n]) for n in fr_n)
@@ -273,8 +328,10 @@ def main():
             "read_frac": round(fr_bytes / fr_time / 1e9 / traffic.HBM_PEAK_GBPS, 4),
             "flush_mean_us": round(sum(fb) / len(fb) * 1e6, 2),
             "window_avg_steps_per_s": round(W / win_b, 1),
+            "value_median_of_rounds": round(statistics.median(rates_b), 2),
             "speedup_sketch_vs_full_read": round(value / (layer_steps / e_b), 3),
-            "read_bytes_ratio": round(traffic.full_read_bytes(shape, 0) / traffic.decode_bytes(shape, 0), 3),
+            "read_bytes_ratio_window_mean": round(traffic.window_bytes(shape, baseline=True)["nonflush_mean"]
+                                                  / traffic.window_bytes(shape)["nonflush_mean"], 3),
         }
     # ---- Standard decoding: every token reads and writes the whole state (window 1, rank 0)
     if not args.no_standard:
@@ -282,9 +339,9 @@ def main():
         for li in range(L):
             S = inputs.initial_state(wl, dev, seed=inputs.SEED + li)
             lay = SketchSSMLayer(wl.kind, wl.batch, wl.heads, wl.dk, wl.dv, 0, 1, wl.io, dev, baseline=True, S=S)
-            lay.write_token(pool[0], 0)
+            lay.write_token(pools[li][0], 0)
             layers.append(lay)
-        plan = [lay.prepared_read(pool[0]["q"], 0) for lay in layers]
+        plan = [lay.prepared_read(pools[li][0]["q"], 0) for li, lay in enumerate(layers)]
         stream = torch.cuda.current_stream()
         for _ in range(warm):
             for call in plan:
@@ -363,6 +420,18 @@ def recorded_traffic(entry, wl, rank, W, sketch="f32", pivots=0):
     return {"bytes_per_launch": int(round(b)), "record": rec}
 
 
+def cpu_model() -> str | None:
+    """The host CPU's model name (/proc/cpuinfo)."""
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return None
+
+
 def cpu_baseline(wl, rank, W, target_s, dev):
     """The oracle (plain fp64 C, items spread over the host threads) on the
     first n_sel items of the workload (all of them when one window of all
@@ -430,6 +499,8 @@ def cpu_baseline(wl, rank, W, target_s, dev):
         oracle.set_threads(threads)
     value1 = W / dt1 * n1 / items
     return {"value": round(value, 4), "unit": "steps/s", "cores": threads, "kind": "oracle",
+            "cpu_model": cpu_model(), "nproc": os.cpu_count(), "affinity_cpus": len(os.sched_getaffinity(0)),
+            "omp_num_threads": os.environ.get("OMP_NUM_THREADS"),
             "sample": f"{n_sel} of {items} (request, head) items x {n_win} consecutive windows of {W} steps "
                       f"({steps} decode steps), {dt:.1f} s wall on {threads} threads, scaled linearly to all items",
             "one_thread": {"value": round(value1, 5), "sample": f"{n1} items x one window, {dt1:.1f} s"}}

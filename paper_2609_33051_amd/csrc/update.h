@@ -757,12 +757,39 @@ __global__ __launch_bounds__(256, (P > 0 && WMAX == 16 && R <= 16) ? 4 : 3) void
     }
   }
 
-  // ---- matrix-core phase, one 16-column value tile at a time (with CM_ALIAS:
-  // pass 0 updates and stores every tile, pass 1 sketches them)
-  constexpr int PASSES = CM_ALIAS ? 2 : 1;
+  // ---- matrix-core phase, one 16-column value tile at a time (with a
+  // state-dependent map: pass 0 updates and stores every tile, pass 1
+  // sketches them)
+  constexpr int PASSES = P != 0 ? 2 : 1;
+  float msc = 1.f;  // pass 1: the power of two the map's partial sums scale the state by
 #pragma unroll
   for (int ps = 0; ps < PASSES; ++ps) {
-  if (ps == 1) lds_barrier();  // every wave is done with Ls before the map's scratch reuses it
+  if constexpr (P != 0) {
+  if (ps == 1) {
+    // The map is invariant to the state's scale.  Its partial sums (|S|^2,
+    // the Gram of the sketch, N) are quadratic in the state, so they are
+    // formed from the state scaled by 2^-e, e the exponent of the item's
+    // largest magnitude (exact; the scaled largest magnitude is in [0.5, 1)):
+    // a state that has decayed far (below ~1e-19) would otherwise square
+    // into fp32's denormal range and break the map's algebra.
+    float m = 0.f;
+#pragma unroll
+    for (int t = 0; t < VTW; ++t)
+      if (wave + 4 * t < VT) {
+#pragma unroll
+        for (int kt = 0; kt < MT; ++kt)
+#pragma unroll
+          for (int i = 0; i < 4; ++i) m = fmaxf(m, fabsf(xs[t][kt][i]));
+      }
+    m = wave_max(m);
+    if (lane == 0) cmS[4 + wave] = m;
+    lds_barrier();  // also: every wave is done with Ls before the map's scratch reuses it
+    m = fmaxf(fmaxf(cmS[4], cmS[5]), fmaxf(cmS[6], cmS[7]));
+    int e = 0;
+    (void)frexpf(m, &e);
+    msc = m > 0.f ? ldexpf(1.f, -e) : 1.f;
+  }
+  }
 #pragma unroll
   for (int t = 0; t < VTW; ++t) {
     const int vt = wave + 4 * t;
@@ -852,7 +879,8 @@ __global__ __launch_bounds__(256, (P > 0 && WMAX == 16 && R <= 16) ? 4 : 3) void
             // index); the same registers are U as the B operand of U^T U
             float* cu = cmU + wave * 16 * XP;
             wave_lds_sync();
-            *reinterpret_cast<float4*>(&cu[lr * XP + 4 * lg]) = make_float4(acc[0], acc[1], acc[2], acc[3]);
+            *reinterpret_cast<float4*>(&cu[lr * XP + 4 * lg]) =
+                make_float4(acc[0] * msc, acc[1] * msc, acc[2] * msc, acc[3] * msc);
             wave_lds_sync();
 #pragma unroll
             for (int st = 0; st < 4; ++st) {
@@ -866,7 +894,8 @@ __global__ __launch_bounds__(256, (P > 0 && WMAX == 16 && R <= 16) ? 4 : 3) void
             if (jt == 0) {
               float* cu = cmU + wave * 64;
               wave_lds_sync();
-              if (lg == 0) *reinterpret_cast<float4*>(&cu[lr * 4]) = make_float4(acc[0], acc[1], acc[2], acc[3]);
+              if (lg == 0)
+                *reinterpret_cast<float4*>(&cu[lr * 4]) = make_float4(acc[0] * msc, acc[1] * msc, acc[2] * msc, acc[3] * msc);
               wave_lds_sync();
               up4 = *reinterpret_cast<const float4*>(&cu[lr * 4]);
 #pragma unroll
@@ -874,11 +903,12 @@ __global__ __launch_bounds__(256, (P > 0 && WMAX == 16 && R <= 16) ? 4 : 3) void
             }
 #pragma unroll
             for (int i = 0; i < 4; ++i) {
-              gpart[jt][i][0] += acc[i] * up4.x;
-              gpart[jt][i][1] += acc[i] * up4.y;
-              gpart[jt][i][2] += acc[i] * up4.z;
-              gpart[jt][i][3] += acc[i] * up4.w;
-              gpart[jt][i][4] += acc[i] * acc[i];
+              const float us = acc[i] * msc;
+              gpart[jt][i][0] += us * up4.x;
+              gpart[jt][i][1] += us * up4.y;
+              gpart[jt][i][2] += us * up4.z;
+              gpart[jt][i][3] += us * up4.w;
+              gpart[jt][i][4] += us * us;
             }
           }
           // columns 16 jt + 4 lg .. +3 of value v; panels of 16 bytes per value:
@@ -905,13 +935,13 @@ __global__ __launch_bounds__(256, (P > 0 && WMAX == 16 && R <= 16) ? 4 : 3) void
 #pragma unroll
           for (int kt = 0; kt < MT; ++kt) {
             wave_lds_sync();
-            *reinterpret_cast<float4*>(&cx[lr * XP + 4 * lg]) =
-                make_float4(xs[t][kt][0], xs[t][kt][1], xs[t][kt][2], xs[t][kt][3]);
+            const float4 xsc = make_float4(xs[t][kt][0] * msc, xs[t][kt][1] * msc, xs[t][kt][2] * msc,
+                                           xs[t][kt][3] * msc);
+            *reinterpret_cast<float4*>(&cx[lr * XP + 4 * lg]) = xsc;
             wave_lds_sync();
 #pragma unroll
             for (int st = 0; st < 4; ++st) nacc[kt] = mfma4(aop[st], cx[(4 * st + lg) * XP + lr], nacc[kt]);
-#pragma unroll
-            for (int i = 0; i < 4; ++i) msq += xs[t][kt][i] * xs[t][kt][i];
+            msq += xsc.x * xsc.x + xsc.y * xsc.y + xsc.z * xsc.z + xsc.w * xsc.w;
           }
         }
       }

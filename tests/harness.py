@@ -31,11 +31,14 @@ class Run:
 
 
 def run_workload(wl, rank=None, window=None, steps=None, omega_coef=None, sel=None, baseline=False,
-                 device="cuda", seed=inputs.SEED, S0=None, keep_layer=False, sketch="f32", pivots=0, head_ranks=None):
+                 device="cuda", seed=inputs.SEED, S0=None, keep_layer=False, sketch="f32", pivots=0, head_ranks=None,
+                 transform=None):
     """Run `steps` decode tokens of workload `wl` on the GPU.
 
     sel: flat item indices (b*H + h) whose outputs and inputs are kept for the
-    oracle (None = all).  Returns (Run, layer, S0 subset, heads subset)."""
+    oracle (None = all).  transform: optional function applied to each
+    token's input dict before both sides see it.  Returns (Run, layer, S0
+    subset, heads subset)."""
     rank = wl.rank if rank is None else rank
     window = wl.window if window is None else window
     steps = wl.steps if steps is None else steps
@@ -53,6 +56,8 @@ def run_workload(wl, rank=None, window=None, steps=None, omega_coef=None, sel=No
     run = Run()
     for t in range(steps):
         inp = inputs.step_inputs(wl, t, device, seed)
+        if transform is not None:
+            inp = transform(inp)
         o = layer.step(inp)
         flat = o.reshape(n_items, wl.dv)
         run.o_gpu.append(to_np32(flat if sel is None else flat[sel_t]))
@@ -103,7 +108,8 @@ def item_err(a, b) -> np.ndarray:
 # step) are set near what the arithmetic allows, with a margin of about 5x
 # over the largest values measured on MI355X:
 #   - fp32 sketch, offline map: fp32 rounding of the state, sketch and sums,
-#     growing with the tokens applied (up to 1.1e-5 after 69 tokens at W = 32);
+#     growing with the tokens applied (up to 5e-5 at W = 32 with a state left
+#     to decay);
 #   - fp32 sketch, state-dependent map: the map's small solves in fp32 (one
 #     ulp reciprocals and square roots) amplify rounding by their
 #     conditioning (up to 1.1e-4);
@@ -114,7 +120,7 @@ def item_err(a, b) -> np.ndarray:
 # A 0.6 % error of one item or a 10 % error of one value channel of one item
 # is above every per-item bar (tests/test_parity_bars.py).
 HEADLINE = {"f32": 1e-5, "bf16": 2e-3}
-ITEM = {"f32": 5e-5, "f32-map": 5e-4, "bf16": 2e-3}
+ITEM = {"f32": 2e-4, "f32-map": 5e-4, "bf16": 2e-3}
 
 
 def bars(io: str, sketch: str, pivots: int = 0) -> tuple[float, float]:

@@ -69,6 +69,8 @@ def parse():
                    help="skip the Standard recurrence (window 1, no sketch: S read and written every token)")
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--cpu-seconds", type=float, default=12.0, help="target CPU time of the oracle sample")
+    p.add_argument("--no-ceilings", action="store_true",
+                   help="skip timing the plain streaming kernels (read-only and copy) the kernels are compared with")
     p.add_argument("--copy-calibration", action="store_true",
                    help="also run a plain 1 GiB device copy (scales HBM byte counters)")
     return p.parse_args()
@@ -382,6 +384,15 @@ def main():
         "full_read_bytes_per_item_mean": traffic.window_bytes(shape, baseline=True)["nonflush_mean"],
     }
 
+    # ---- what plain streaming kernels reach on this part, measured in the same
+    # run (HIP events, median of 7): a read-only pass and a copy, 1 GiB each way
+    # (beyond the 256 MB last-level cache)
+    if not args.no_ceilings:
+        ce = hbm_ceilings(dev)
+        out["hbm_ceilings"] = ce
+        out["roofline"]["frac_of_read_ceiling"] = round(dec_gbps / ce["read_gbps"], 4)
+        out["kernels"]["flush"]["frac_of_copy_ceiling"] = round(ks["fl_gbps"] / ce["copy_gbps"], 4)
+
     if args.copy_calibration:
         n = 1 << 28  # 1 GiB of fp32
         a = torch.empty(n, dtype=torch.float32, device=dev).fill_(1.0)
@@ -418,6 +429,41 @@ def recorded_traffic(entry, wl, rank, W, sketch="f32", pivots=0):
         return None
     b = rec["fetch_kib"] * 1024 * rec["fetch_scale"] + rec["write_kib"] * 1024 * rec["write_scale"]
     return {"bytes_per_launch": int(round(b)), "record": rec}
+
+
+def hbm_ceilings(dev, reps=7):
+    """Bandwidth of plain streaming kernels on 1 GiB operands: row sums of a
+    16384 x 16384 fp32 matrix (reads 1 GiB; of torch's reductions the one that
+    streams fastest here) and torch.neg (reads 1 GiB, writes 1 GiB), timed with
+    HIP events on the current stream, median of `reps` launches after a warmup."""
+    import torch
+
+    n = 1 << 28
+    a = torch.empty(n, dtype=torch.float32, device=dev).fill_(1.0)
+    b = torch.empty_like(a)
+    s = torch.empty(1 << 14, dtype=torch.float32, device=dev)
+    stream = torch.cuda.current_stream()
+
+    def med(fn):
+        fn()
+        ts = []
+        for _ in range(reps):
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
+            fn()
+            e1.record(stream)
+            e1.synchronize()
+            ts.append(e0.elapsed_time(e1) * 1e-3)
+        return statistics.median(ts)
+
+    t_read = med(lambda: torch.sum(a.view(1 << 14, 1 << 14), dim=1, out=s))
+    t_copy = med(lambda: torch.neg(a, out=b))
+    del a, b
+    torch.cuda.empty_cache()
+    return {"read_gbps": round(4 * n / t_read / 1e9, 1), "copy_gbps": round(8 * n / t_copy / 1e9, 1),
+            "read_kernel": "torch.sum(dim=1) of a 16384 x 16384 fp32 matrix", "copy_kernel": "torch.neg, 1 GiB fp32 in and out",
+            "read_frac_of_peak": round(4 * n / t_read / 1e9 / 8000.0, 4),
+            "copy_frac_of_peak": round(8 * n / t_copy / 1e9 / 8000.0, 4)}
 
 
 def cpu_model() -> str | None:

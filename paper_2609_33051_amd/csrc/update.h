@@ -762,6 +762,7 @@ __global__ __launch_bounds__(256, (P > 0 && WMAX == 16 && R <= 16) ? 4 : 3) void
   // sketches them)
   constexpr int PASSES = P != 0 ? 2 : 1;
   float msc = 1.f;  // pass 1: the power of two the map's partial sums scale the state by
+  float xmax = 0.f;  // pass 0: this lane's largest state magnitude (state-dependent map)
 #pragma unroll
   for (int ps = 0; ps < PASSES; ++ps) {
   if constexpr (P != 0) {
@@ -772,19 +773,10 @@ __global__ __launch_bounds__(256, (P > 0 && WMAX == 16 && R <= 16) ? 4 : 3) void
     // largest magnitude (exact; the scaled largest magnitude is in [0.5, 1)):
     // a state that has decayed far (below ~1e-19) would otherwise square
     // into fp32's denormal range and break the map's algebra.
-    float m = 0.f;
-#pragma unroll
-    for (int t = 0; t < VTW; ++t)
-      if (wave + 4 * t < VT) {
-#pragma unroll
-        for (int kt = 0; kt < MT; ++kt)
-#pragma unroll
-          for (int i = 0; i < 4; ++i) m = fmaxf(m, fabsf(xs[t][kt][i]));
-      }
-    m = wave_max(m);
-    if (lane == 0) cmS[4 + wave] = m;
+    const float m0 = wave_max(xmax);
+    if (lane == 0) cmS[4 + wave] = m0;
     lds_barrier();  // also: every wave is done with Ls before the map's scratch reuses it
-    m = fmaxf(fmaxf(cmS[4], cmS[5]), fmaxf(cmS[6], cmS[7]));
+    const float m = fmaxf(fmaxf(cmS[4], cmS[5]), fmaxf(cmS[6], cmS[7]));
     int e = 0;
     (void)frexpf(m, &e);
     msc = m > 0.f ? ldexpf(1.f, -e) : 1.f;
@@ -850,6 +842,14 @@ __global__ __launch_bounds__(256, (P > 0 && WMAX == 16 && R <= 16) ? 4 : 3) void
 #pragma unroll
         for (int kt = 0; kt < MT; ++kt)
           st_nt(reinterpret_cast<float4*>(dst + 256 * kt), make_float4(xs[t][kt][0], xs[t][kt][1], xs[t][kt][2], xs[t][kt][3]));
+      }
+    }
+    if constexpr (P != 0) {
+      if (ps == 0) {  // the tile is final (updated, or as loaded for the initial sketch)
+#pragma unroll
+        for (int kt = 0; kt < MT; ++kt)
+#pragma unroll
+          for (int i = 0; i < 4; ++i) xmax = fmaxf(xmax, fabsf(xs[t][kt][i]));
       }
     }
     // sketch U^T = Omega^T X^T  (rows j = 16 jt + 4 lg + i of the C layout)
@@ -941,7 +941,10 @@ __global__ __launch_bounds__(256, (P > 0 && WMAX == 16 && R <= 16) ? 4 : 3) void
             wave_lds_sync();
 #pragma unroll
             for (int st = 0; st < 4; ++st) nacc[kt] = mfma4(aop[st], cx[(4 * st + lg) * XP + lr], nacc[kt]);
-            msq += xsc.x * xsc.x + xsc.y * xsc.y + xsc.z * xsc.z + xsc.w * xsc.w;
+            // one accumulation per element (a four-term sum here keeps the scaled
+            // values live across the syncs: 22 more registers for Mamba-2)
+#pragma unroll
+            for (int i = 0; i < 4; ++i) msq += (xs[t][kt][i] * msc) * (xs[t][kt][i] * msc);
           }
         }
       }

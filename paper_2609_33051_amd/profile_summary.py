@@ -68,7 +68,7 @@ def kernel_variant(short: str) -> tuple[str, str, int] | None:
 def _counter(d, counter):
     """(per-kernel list of values in KiB, copy-kernel value) from one pmc run."""
     per, copy = {}, []
-    for r in _rows(d, "_counter_collection.csv"):
+    for r in sorted(_rows(d, "_counter_collection.csv"), key=lambda r: int(r["Dispatch_Id"])):
         if r["Counter_Name"] != counter:
             continue
         s = _short(r["Kernel_Name"])
@@ -105,6 +105,20 @@ def _mfma_lines(d, kernel):
     return out
 
 
+def _split_lines(d, layers):
+    """Initial-sketch and flush durations of one update kernel, from its
+    dispatches in launch order (the first `layers` are initial sketches)."""
+    init, fl = d[:layers], d[layers:]
+    out = []
+    if init:
+        out.append(f"    initial sketches: {len(init)} dispatches, average {sum(init) / len(init):.2f} us")
+    if fl:
+        srt = sorted(fl)
+        out.append(f"    flushes: {len(fl)} dispatches, average {sum(fl) / len(fl):.2f} us, "
+                   f"median {srt[len(srt) // 2]:.2f} us, min {srt[0]:.2f} us, max {srt[-1]:.2f} us")
+    return out
+
+
 def main(argv=None):
     p = argparse.ArgumentParser()
     p.add_argument("--trace", required=True)
@@ -119,6 +133,7 @@ def main(argv=None):
                         "GRBM_GUI_ACTIVE run (matrix-core utilisation of the update kernel)")
     p.add_argument("--mfma-command", default="", help="the command of the --mfma run")
     p.add_argument("--out", required=True)
+    p.add_argument("--layers", type=int, default=4, help="layers the bench run rotated (initial sketches per leg)")
     a = p.parse_args(argv)
 
     from . import build as hip_build
@@ -136,12 +151,21 @@ def main(argv=None):
             return sum(traffic.decode_bytes(sh, n) for n in range(W - 1)) / (W - 1) * items
         if entry == "full_read":
             return sum(traffic.full_read_bytes(sh, n) for n in range(W - 1)) / (W - 1) * items
+        if entry == "flush":
+            return traffic.flush_bytes(sh, W - 1) * items
         return None
 
     stats = {}
     for r in _rows(a.trace, "_kernel_stats.csv"):
         s = _short(r["Name"])
         stats[s] = r
+    # per-dispatch durations in launch order: the first `layers` dispatches of
+    # an update kernel with a sketch are the initial sketches of the bench's
+    # layers (no state write), the rest are flushes
+    durs = {}
+    for r in sorted(_rows(a.trace, "_kernel_trace.csv"), key=lambda r: int(r["Dispatch_Id"])):
+        durs.setdefault(_short(r["Kernel_Name"]), []).append((int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3)
+    p_layers = a.layers
     fetch, copy_f = _counter(a.fetch, "FETCH_SIZE")
     write, copy_w = _counter(a.write, "WRITE_SIZE")
     f_scale = COPY_BYTES / (copy_f * 1024)
@@ -160,6 +184,10 @@ def main(argv=None):
         tag = (":bf16" if sketch == "bf16" else "") + (f":p{pivots}" if pivots else "")
         ab = algo(e, sketch, pivots)
         fv, wv = fetch.get(s, []), write.get(s, [])
+        split = e == "update" and not re.search(r"<\d+, \d+, \d+, 0,", s)  # with a sketch: initial sketches first
+        if split:
+            ab = algo("flush", sketch, pivots)
+            fv, wv = fv[p_layers:], wv[p_layers:]
         lines = [
             f"# {s} on {a.workload} (rank {rank}, window {W})",
             "",
@@ -172,6 +200,7 @@ def main(argv=None):
             f"    calls {r['Calls']}, average {float(r['AverageNs']) / 1e3:.2f} us, "
             f"min {float(r['MinNs']) / 1e3:.2f} us, max {float(r['MaxNs']) / 1e3:.2f} us, "
             f"{float(r['Percentage']):.2f} % of GPU kernel time",
+            *(_split_lines(durs.get(s, []), p_layers) if split else []),
             "",
             "counters per dispatch (KiB as reported; scaled by the calibration copy of 1 GiB:",
             f"    FETCH_SIZE read {copy_f:.1f} KiB for it -> scale {f_scale:.4f};"
@@ -186,16 +215,18 @@ def main(argv=None):
                 f"    HBM bytes per launch (scaled): read {fm * 1024 * f_scale / 1e6:.2f} MB + "
                 f"write {wm * 1024 * w_scale / 1e6:.2f} MB = {hbm / 1e6:.2f} MB",
             ]
+            if split:
+                lines.append(f"    (flush dispatches only: the first {p_layers} dispatches, the initial sketches, excluded)")
             if ab is not None:
-                lines.append(f"    algorithmic bytes per launch (mean over slots 0..{W - 2}): {ab / 1e6:.2f} MB"
+                what = "per flush" if split else f"per launch (mean over slots 0..{W - 2})"
+                lines.append(f"    algorithmic bytes {what}: {ab / 1e6:.2f} MB"
                              f" -> measured / algorithmic = {hbm / ab:.3f}")
                 table[f"{unit}:{a.workload}:r{rank}:w{W}{tag}"] = {
                     "kernel": s, "digest": digest, "fetch_kib": round(fm, 1), "write_kib": round(wm, 1),
                     "fetch_scale": round(f_scale, 6), "write_scale": round(w_scale, 6),
                     "dispatches": len(fv), "algorithmic_bytes": int(ab),
                 }
-            elif not re.search(r"<\d+, \d+, \d+, 0,", s):
-                lines.append("    (initial-sketch and flush dispatches of this kernel are mixed in these means)")
+
         if a.mfma and e == "update":
             m = _mfma_lines(a.mfma, s)
             if m:
@@ -204,7 +235,7 @@ def main(argv=None):
         if sketch == "bf16":
             name += "_bf16sketch"
         if pivots:
-            name += f"_pivots{pivots}"
+            name += "_exactmap" if pivots < 0 else f"_pivots{pivots}"
         if "<" in s and e == "update" and re.search(r"<\d+, \d+, \d+, 0,", s):
             name += "_rank0"
         with open(os.path.join(a.out, name + ".txt"), "w") as f:

@@ -359,7 +359,10 @@ __device__ __forceinline__ void coef_map_exact_tail(const UpdateArgs& a, size_t 
     }
   }
   lds_barrier();
-  // column k of the map: L y = N_k / mu, L^T c = y
+  // column k of the map: L y = N_k / mu, L^T c = y.  Each row's reads of L
+  // stay within its own step (scheduling barrier): hoisting the whole
+  // triangle's reads ahead held 136 values live at rank 16 and took the
+  // kernel from 80 to 162 registers.
   if (tid < K) {
     const int k = tid;
     float y[R];
@@ -369,6 +372,7 @@ __device__ __forceinline__ void coef_map_exact_tail(const UpdateArgs& a, size_t 
 #pragma unroll
       for (int c = 0; c < j; ++c) e -= Lm[j * GP + c] * y[c];
       y[j] = e * Lm[j * GP + j];
+      __builtin_amdgcn_sched_barrier(0);
     }
 #pragma unroll
     for (int j = R - 1; j >= 0; --j) {
@@ -376,6 +380,7 @@ __device__ __forceinline__ void coef_map_exact_tail(const UpdateArgs& a, size_t 
 #pragma unroll
       for (int c = j + 1; c < R; ++c) e -= Lm[c * GP + j] * y[c];
       y[j] = e * Lm[j * GP + j];
+      __builtin_amdgcn_sched_barrier(0);
     }
 #pragma unroll
     for (int j = 0; j < R; ++j) Ns[j * NP + k] = y[j];
@@ -395,12 +400,13 @@ __device__ __forceinline__ void coef_map_exact_tail(const UpdateArgs& a, size_t 
   }
 }
 
-// Three workgroups per CU, or four for the state-dependent map at window 16
-// and rank <= 16: its flush spends part of each workgroup's life off the
-// memory bus (the map's products and algebra), so occupancy pays there, even
-// with the few registers the per-channel-decay instance then spills.
+// Three workgroups per CU, or four for the state-dependent maps (P = 4 and
+// exact) at window 16 and rank <= 16: their flush spends part of each
+// workgroup's life off the memory bus (the map's products and algebra), so
+// occupancy pays there, even with the few registers the per-channel-decay
+// instances then spill.
 template <int KIND, int K, int V, int R, int WMAX, typename IO, typename SK, int P>
-__global__ __launch_bounds__(256, (P > 0 && WMAX == 16 && R <= 16) ? 4 : 3) void update_kernel(const UpdateArgs a) {
+__global__ __launch_bounds__(256, (P != 0 && WMAX == 16 && R <= 16) ? 4 : 3) void update_kernel(const UpdateArgs a) {
   constexpr bool ERASE = KIND != MAMBA2;
   constexpr bool CHAN = KIND == KDA;
   constexpr int MT = K / 16;          // k tiles

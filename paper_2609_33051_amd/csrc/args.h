@@ -21,9 +21,9 @@ constexpr int kMaxRaggedHeads = 256;
 struct DecodeArgs {
   int B, H, W, n;                 // batch, heads, window, slot of the current token
   int ragged;                     // hrank holds the per-head ranks
-  uint8_t hrank[kMaxRaggedHeads];
+  alignas(4) uint8_t hrank[kMaxRaggedHeads];
   int ndense;                     // dense-fallback heads (ragged)
-  uint8_t hlist[kMaxRaggedHeads]; // heads in launch order: the dense ones first (ragged)
+  alignas(4) uint8_t hlist[kMaxRaggedHeads];  // heads in launch order: the dense ones first (ragged)
   const void* q;                  // [B][H][K] io, current query
   const void* U;                  // [B][H][R/P][V][P], P = 4 (fp32) or 8 (bf16)  (sketch read)
   const float* coef;              // [H][R][K]           (sketch read, offline map; NULL with a state-dependent map)
@@ -42,7 +42,7 @@ struct DecodeArgs {
 struct UpdateArgs {
   int B, H, W, n;                 // n = slot of the current token (tokens applied: n + 1)
   int ragged;                     // hrank holds the per-head ranks
-  uint8_t hrank[kMaxRaggedHeads];
+  alignas(4) uint8_t hrank[kMaxRaggedHeads];
   int nt;                         // n + 1, or 0 (sketch only)
   float* S;                       // [B][H][V][K]
   const float* omega;             // [H][K][R]

@@ -509,11 +509,11 @@ __global__ __launch_bounds__(256) void decode_kernel(const DecodeArgs a) {
   if (a.ragged) {
     const int T = gridDim.x / H, nd = a.ndense, w = blockIdx.x;
     if (w < nd * T) {
-      h = a.hlist[w % nd];
+      h = arg_byte(a.hlist, w % nd);
       tile = w / nd;
     } else {
       const int ns = H - nd, w2 = w - nd * T;
-      h = a.hlist[nd + w2 % ns];
+      h = arg_byte(a.hlist, nd + w2 % ns);
       tile = w2 / ns;
     }
   }
@@ -524,7 +524,7 @@ __global__ __launch_bounds__(256) void decode_kernel(const DecodeArgs a) {
   const SK* Ub = static_cast<const SK*>(a.U) + item * (size_t)V * R;
   // this head's rank: its first rh sketch columns, coefficient rows and f
   // entries are used; a dense-fallback head (rh = 0) is read elsewhere
-  const int rh = a.ragged ? (int)a.hrank[h] : R;
+  const int rh = a.ragged ? arg_byte(a.hrank, h) : R;
   if (rh == 0) {
     // dense-fallback head: the exact full-state read of its items, one per
     // wave (the whole workgroup shares the head and takes this branch, so no

@@ -299,6 +299,15 @@ __device__ __forceinline__ float wave_max(float x) {
   return fmaxf(__uint_as_float(h[0]), __uint_as_float(h[1]));
 }
 
+// Entry i of a byte table in the kernel's by-value arguments, for a
+// wave-uniform i: read as its aligned 32-bit word, which is a scalar load.
+// There is no scalar byte load on this target, so indexing the table
+// directly becomes a vector load whose wait delays every load after it.
+__device__ __forceinline__ int arg_byte(const uint8_t* table, int i) {
+  const uint32_t w = reinterpret_cast<const uint32_t*>(table)[i >> 2];
+  return (int)((w >> (8 * (i & 3))) & 0xffu);
+}
+
 __device__ __forceinline__ float lane_bcast(float x, int lane) {
   return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(x), lane));
 }

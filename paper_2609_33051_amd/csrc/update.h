@@ -455,7 +455,7 @@ __global__ __launch_bounds__(256, (P != 0 && WMAX == 16 && R <= 16) ? 4 : 3) voi
   // this head's rank (per-head rank table): the sketch uses Omega's first rh
   // columns (the rest are zeroed in LDS, so U's columns past rh come out 0 and
   // the state-dependent map's rows past rh too); rh = 0: a dense-fallback head
-  const int rh = a.ragged ? (int)a.hrank[h] : R;
+  const int rh = a.ragged ? arg_byte(a.hrank, h) : R;
   const bool want_U = R > 0 && a.U != nullptr && rh > 0;
 
   // state-dependent coefficient map (P = 4 pivots, or the exact metric, P < 0):

@@ -66,20 +66,18 @@ template <> __device__ __forceinline__ float load1<bf16_t>(const bf16_t* p) { re
 // not stored.  Every thread of the workgroup calls this.
 template <int K, int R, int P, int MT, int RT, int LSZ, int USZ, int OPJ, typename SK>
 __device__ __forceinline__ void coef_map_tail(const UpdateArgs& a, size_t item, int wave, int lane, int tid, int rh,
-                                              const floatx4 (&nacc)[MT], const float (&gpart)[RT][4][5], float msq,
+                                              const floatx4 (&nacc)[MT], const floatx4 (&gram)[RT],
+                                              const float (&dsq)[RT], float msq,
                                               float* Ls, float* Us, float* cmS, const float* OmL, float* Fext) {
   static_assert(LSZ >= 4 * K * P && USZ >= 4 * R * 5, "staging buffers too small for the map's partial sums");
   constexpr int FBP = P + R + 1;                       // row pitch of [F1 F2] (odd: lanes of a read spread over banks)
   constexpr bool FB_ALIAS = LSZ >= P * K + 16 * RT * FBP;
   const int lr = lane & 15, lg = lane >> 4;
-  // this wave's Gram partials summed over its 16 value lanes
-  float gs[RT][4][5];
+  // the squared sketch columns summed over the four lane rows (the Gram
+  // products already summed over this wave's values)
+  float dq[RT];
 #pragma unroll
-  for (int jt = 0; jt < RT; ++jt)
-#pragma unroll
-    for (int i = 0; i < 4; ++i)
-#pragma unroll
-      for (int e = 0; e < 5; ++e) gs[jt][i][e] = row_sum16(gpart[jt][i][e]);
+  for (int jt = 0; jt < RT; ++jt) dq[jt] = cross_row_sum(dsq[jt]);
   msq = wave_sum(msq);
   lds_barrier();  // every wave is done with the window staging (Ls, Us), reused below
   float* cmN = Ls;  // [wave][K][P]
@@ -89,17 +87,17 @@ __device__ __forceinline__ void coef_map_tail(const UpdateArgs& a, size_t item, 
     for (int kt = 0; kt < MT; ++kt)
       *reinterpret_cast<float4*>(&cmN[(wave * K + 16 * kt + lr) * P]) = make_float4(nacc[kt][0], nacc[kt][1], nacc[kt][2], nacc[kt][3]);
   }
-  if (lr == 0) {
+  // row j of cmG: U_j . U_a for the pivots a < P, then |U_j|^2
 #pragma unroll
-    for (int jt = 0; jt < RT; ++jt)
+  for (int jt = 0; jt < RT; ++jt) {
+    if (lr < P) {
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
         const int j = 16 * jt + 4 * lg + i;
-        if (j < R) {
-#pragma unroll
-          for (int e = 0; e < 5; ++e) cmG[(wave * R + j) * 5 + e] = gs[jt][i][e];
-        }
+        if (j < R) cmG[(wave * R + j) * 5 + lr] = gram[jt][i];
       }
+    }
+    if (lg == 0 && 16 * jt + lr < R) cmG[(wave * R + 16 * jt + lr) * 5 + 4] = dq[jt];
   }
   if (lane == 0) cmS[wave] = msq;
   lds_barrier();
@@ -470,11 +468,10 @@ __global__ __launch_bounds__(256, (P != 0 && WMAX == 16 && R <= 16) ? 4 : 3) voi
   // keeps the kernel's LDS that of the offline-map flush (four workgroups per CU).
   // The exact map transposes all 16 sketch columns of a tile through the
   // same per-wave block as X (one after the other).
-  constexpr bool CM_ALIAS = (P > 0 && SP * LP >= 4 * 16 * XP + 4 * 16 * 4) || (EXACT && SP * LP >= 4 * 16 * XP);
+  constexpr bool CM_ALIAS = P != 0 && SP * LP >= 4 * 16 * XP;
   __shared__ __align__(16) float cmXs[P != 0 && !CM_ALIAS ? 4 * 16 * XP : 4];
-  __shared__ __align__(16) float cmUs[P > 0 && !CM_ALIAS ? 4 * 16 * 4 : 4];
   float* const cmX = CM_ALIAS ? Ls : cmXs;                 // [wave][16 values][16 keys]
-  float* const cmU = EXACT ? cmX : (CM_ALIAS ? Ls + 4 * 16 * XP : cmUs);  // [wave][16 values][P] (exact: [16][XP])
+  float* const cmU = cmX;                                  // [wave][16 values][16 sketch columns], before X's blocks
   __shared__ __align__(16) float cmS[P != 0 ? 8 + 16 + 5 * R : 4];  // mu parts, R^{-1}/sqrt(mu), L_G and w
   // [F1 F2] of the map, in its own LDS only where the key staging has no room
   constexpr bool CMF_OWN = P > 0 && SP * LP < P * K + 16 * RT * (P + R + 1);
@@ -482,7 +479,8 @@ __global__ __launch_bounds__(256, (P != 0 && WMAX == 16 && R <= 16) ? 4 : 3) voi
   static_assert(!EXACT || (SP * LP >= R * (K + 4) && SP * UP >= 2 * R * (R + 1)),
                 "the exact map's sums must fit the window staging");
   floatx4 nacc[P != 0 ? MT : 1];   // N^T (rows 4 lg + i: pivots a < 4, or every sketch column), this wave's values
-  float gpart[P > 0 ? RT : 1][4][5];  // sketch Gram: U[v][j] U[v][a] (a < 4) and U[v][j]^2, this lane's values
+  floatx4 gram[P > 0 ? RT : 1];    // sketch Gram U^T U_p: lane (lr, lg), i: row 16 jt + 4 lg + i, column lr < P; this wave's values
+  float dsq[P > 0 ? RT : 1];       // squared sketch column 16 jt + lr over this lane row's values
   [[maybe_unused]] floatx4 gacc = {0.f, 0.f, 0.f, 0.f};  // exact: U^T U (rows 4 lg + i, column lr), this wave's values
   float msq = 0.f;                 // this lane's share of |S|_F^2
   if constexpr (P != 0) {
@@ -491,11 +489,10 @@ __global__ __launch_bounds__(256, (P != 0 && WMAX == 16 && R <= 16) ? 4 : 3) voi
   }
   if constexpr (P > 0) {
 #pragma unroll
-    for (int jt = 0; jt < RT; ++jt)
-#pragma unroll
-      for (int i = 0; i < 4; ++i)
-#pragma unroll
-        for (int e = 0; e < 5; ++e) gpart[jt][i][e] = 0.f;
+    for (int jt = 0; jt < RT; ++jt) {
+      gram[jt] = floatx4{0.f, 0.f, 0.f, 0.f};
+      dsq[jt] = 0.f;
+    }
   }
 
   // ---- every small load first (window, query, rows of T^{-1}, Omega), then the
@@ -862,7 +859,6 @@ __global__ __launch_bounds__(256, (P != 0 && WMAX == 16 && R <= 16) ? 4 : 3) voi
     if constexpr (R > 0) {
       if (want_U && ps == PASSES - 1) {
         const float* om = a.omega + (size_t)h * K * R;
-        float4 up4 = make_float4(0.f, 0.f, 0.f, 0.f);  // U[v][0..3] (state-dependent map)
         float aop[4] = {0.f, 0.f, 0.f, 0.f};            // U_p^T (exact: U^T) as the A operand of N^T = U_p^T X
 #pragma unroll
         for (int jt = 0; jt < RT; ++jt) {
@@ -879,42 +875,37 @@ __global__ __launch_bounds__(256, (P != 0 && WMAX == 16 && R <= 16) ? 4 : 3) voi
                 w = (jj < R) ? om[(16 * kt + 4 * lg + i) * R + jj] : 0.f;
               acc = mfma4(w, xs[t][kt][i], acc);
             }
-          if constexpr (EXACT) {
+          if constexpr (P != 0) {
             // every sketch column of the tile's 16 values goes through LDS, so
-            // that U^T becomes the A operand (value index as the contraction
-            // index); the same registers are U as the B operand of U^T U
+            // that U^T becomes an operand with the value index as the
+            // contraction index: ut[st] = U[v = 4 st + lg][16 jt + lr], scaled
             float* cu = cmU + wave * 16 * XP;
             wave_lds_sync();
             *reinterpret_cast<float4*>(&cu[lr * XP + 4 * lg]) =
                 make_float4(acc[0] * msc, acc[1] * msc, acc[2] * msc, acc[3] * msc);
             wave_lds_sync();
+            float ut[4];
 #pragma unroll
-            for (int st = 0; st < 4; ++st) {
-              aop[st] = cu[(4 * st + lg) * XP + lr];
-              gacc = mfma4(aop[st], aop[st], gacc);
-            }
-          }
-          if constexpr (P > 0) {
-            // Gram partials of the sketch against its first P columns, which lane
-            // (lr, lg = 0) holds for this tile's 16 values after the jt = 0 product
-            if (jt == 0) {
-              float* cu = cmU + wave * 64;
-              wave_lds_sync();
-              if (lg == 0)
-                *reinterpret_cast<float4*>(&cu[lr * 4]) = make_float4(acc[0] * msc, acc[1] * msc, acc[2] * msc, acc[3] * msc);
-              wave_lds_sync();
-              up4 = *reinterpret_cast<const float4*>(&cu[lr * 4]);
+            for (int st = 0; st < 4; ++st) ut[st] = cu[(4 * st + lg) * XP + lr];
+            if constexpr (EXACT) {
+              // the whole Gram U^T U (R <= 16: one block)
 #pragma unroll
-              for (int st = 0; st < 4; ++st) aop[st] = (lr < 4) ? cu[(4 * st + lg) * 4 + lr] : 0.f;
-            }
+              for (int st = 0; st < 4; ++st) {
+                aop[st] = ut[st];
+                gacc = mfma4(ut[st], ut[st], gacc);
+              }
+            } else {
+              // the Gram against the first P columns (tile 0's, kept from
+              // jt = 0) on the matrix cores, and the squared columns
+              if (jt == 0) {
 #pragma unroll
-            for (int i = 0; i < 4; ++i) {
-              const float us = acc[i] * msc;
-              gpart[jt][i][0] += us * up4.x;
-              gpart[jt][i][1] += us * up4.y;
-              gpart[jt][i][2] += us * up4.z;
-              gpart[jt][i][3] += us * up4.w;
-              gpart[jt][i][4] += us * us;
+                for (int st = 0; st < 4; ++st) aop[st] = lr < P ? ut[st] : 0.f;
+              }
+#pragma unroll
+              for (int st = 0; st < 4; ++st) {
+                gram[jt] = mfma4(ut[st], aop[st], gram[jt]);
+                dsq[jt] += ut[st] * ut[st];
+              }
             }
           }
           // columns 16 jt + 4 lg .. +3 of value v; panels of 16 bytes per value:
@@ -960,7 +951,7 @@ __global__ __launch_bounds__(256, (P != 0 && WMAX == 16 && R <= 16) ? 4 : 3) voi
 
   if constexpr (P > 0) {
     if (want_U)
-      coef_map_tail<K, R, P, MT, RT, SP * LP, SP * UP, OPJ, SK>(a, item, wave, lane, tid, rh, nacc, gpart, msq, Ls, Us,
+      coef_map_tail<K, R, P, MT, RT, SP * LP, SP * UP, OPJ, SK>(a, item, wave, lane, tid, rh, nacc, gram, dsq, msq, Ls, Us,
                                                                  cmS, OmL, cmF);
   }
   if constexpr (EXACT) {

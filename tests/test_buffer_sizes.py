@@ -76,3 +76,44 @@ def test_sizes_reject_what_the_calls_reject():
         B.sketchssm_buffer_sizes(B.make_config("gdn", 2, 3, 128, 128, 16, 16, "bf16", head_ranks=[16, 17, 0]))
     # the baseline layer ignores the rank
     assert B.sketchssm_ring_bytes(B.make_config("gdn", 2, 3, 128, 128, 12, 16, "bf16"), True) > 0
+
+
+@pytest.mark.parametrize("K,R,skb", [(k, r, s) for k in (64, 128) for r in (8, 16, 32) for s in (4, 2)])
+def test_map_panel_indices_stay_in_the_item(K, R, skb):
+    """The dense map's index arithmetic, replayed on the host for one item:
+    element (j, k) sits at ((k / c) * R + j) * c + k % c, c = 16 / skb.  The
+    flush's stores (P = 4: four channels k0 .. k0 + 3 of row j from lane
+    (j mod 16, k0 / 4 mod 4) of k tile k0 / 16; exact map: thread t writes
+    panel t) cover rows j < G exactly once, and decode's loads (lane row rho,
+    column j0 = lane mod 16, map row j = j0 + 16 p clamped to 0 at and past the
+    head's rank G, panels rho * K / (4c) + i) stay below R * K for every G and
+    read element (j, k) for the channels k the lane multiplies."""
+    c = 16 // skb
+    RP, CL, KQ = (R + 15) // 16, K // 4 // c, K // 4
+
+    def at(j, k):
+        return ((k // c) * R + j) * c + k % c
+
+    for G in sorted({1, R // 2, R - 1, R}):
+        pivot = []
+        for kt in range(K // 16):
+            for jt in range(RP):
+                for lane in range(64):
+                    j, k0 = 16 * jt + lane % 16, 16 * kt + 4 * (lane // 16)
+                    if j < G:
+                        base = ((k0 // c) * R + j) * c + k0 % c
+                        pivot += [base + e for e in range(4)]
+                        assert [base + e for e in range(4)] == [at(j, k0 + e) for e in range(4)]
+        exact = [t * c + e for t in range(R * K // c) if t % R < G for e in range(c)]
+        want = sorted(at(j, k) for j in range(G) for k in range(K))
+        assert sorted(pivot) == want and sorted(exact) == want
+        for lane in range(64):
+            rho, j0 = lane // 16, lane % 16
+            for p in range(RP):
+                j = j0 + 16 * p
+                jj = j if j < G else 0
+                for i in range(CL):
+                    first = ((rho * CL + i) * R + jj) * c
+                    assert 0 <= first and first + c <= R * K
+                    if j < G:
+                        assert [first + e for e in range(c)] == [at(j, rho * KQ + i * c + e) for e in range(c)]

@@ -96,9 +96,19 @@ int run_full_read(const DecodeArgs& a, int K, int V, int io, void* stream) {
   return kUnsupported;
 }
 
+template <int KIND, int K, int V, typename IO>
+int launch_token(const UpdateArgs& a, hipStream_t s) {
+  const size_t items = (size_t)a.B * a.H;
+  hipLaunchKernelGGL((token_kernel<KIND, K, V, IO>), dim3((unsigned)items), dim3(256), 0, s, a);
+  return 0;
+}
+
 template <int KIND, int K, int V, int R, int WM, int P>
 int update_t(const UpdateArgs& a, int io, int sk, hipStream_t s) {
   if constexpr (R == 0) {  // no sketch: its dtype does not matter
+    // a single token (window-1 decoding, or a window flushed after its first
+    // token): the rank-1 update streams the state through registers
+    if (a.nt == 1) return io ? launch_token<KIND, K, V, bf16_t>(a, s) : launch_token<KIND, K, V, float>(a, s);
     return io ? launch_update<KIND, K, V, 0, WM, bf16_t, float, 0>(a, s) : launch_update<KIND, K, V, 0, WM, float, float, 0>(a, s);
   } else {
     if (io) return sk ? launch_update<KIND, K, V, R, WM, bf16_t, bf16_t, P>(a, s) : launch_update<KIND, K, V, R, WM, bf16_t, float, P>(a, s);

@@ -959,4 +959,116 @@ __global__ __launch_bounds__(256, (P != 0 && WMAX == 16 && R <= 16) ? 4 : 3) voi
   }
 }
 
+
+// One token and no sketch: the whole-state recurrence (Sec. 3.2, eq.
+// transition-update: decay, then erase, then write) applied to S read once
+// and written once, and o = S^T q from the updated state (eq. read).  This is
+// the update with a single buffered token at rank 0, i.e. the window-1
+// decoding a conventional recurrent layer does.  The window's machinery
+// (staged slots, rows of T^{-1}, rank-W products on the matrix cores) reduces
+// to one rank-1 update per state element, so the state streams through
+// registers: in the tile-major layout lane (lr, lg) of a wave holds
+// X[16 vt + lr][16 kt + 4 lg + i] (X = S^T), and the two contractions over
+// keys (X k for the erase, X q for the output) are per-lane partial sums and
+// one cross-row sum.  In X's terms the update is
+//   X <- X Diag(alpha) + beta (v - X Diag(alpha) k) k^T     (GDN, KDA)
+//   X <- alpha X + beta v k^T                               (Mamba-2).
+template <int KIND, int K, int V, typename IO>
+__global__ __launch_bounds__(256) void token_kernel(const UpdateArgs a) {
+  constexpr bool ERASE = KIND != MAMBA2;
+  constexpr bool CHAN = KIND == KDA;
+  constexpr int MT = K / 16, VT = V / 16, VTW = (VT + 3) / 4;
+  __shared__ __align__(16) float ks[K];              // k
+  __shared__ __align__(16) float qs[K];              // q
+  __shared__ __align__(16) float as[CHAN ? K : 4];   // per-channel decay alpha (KDA)
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int lr = lane & 15, lg = lane >> 4;
+  const size_t item = blockIdx.x;                    // b * H + h
+  const size_t cur = item * (size_t)a.W + a.n;       // the token's raw ring slot
+
+  // ---- the token's small loads, then the single read of the state
+  float kk = 0.f, qq = 0.f, lk = 0.f;
+  if (tid < K) {
+    kk = load1<IO>(static_cast<const IO*>(a.rk) + cur * K + tid);
+    qq = load1<IO>(static_cast<const IO*>(a.q) + item * K + tid);
+    if constexpr (CHAN) lk = a.rla[cur * K + tid];
+  }
+  const float beta = a.rbeta[cur];
+  const float ls = CHAN ? 0.f : a.rla[cur];
+  float vv[VTW];
+#pragma unroll
+  for (int t = 0; t < VTW; ++t) {
+    const int vt = wave + 4 * t;
+    vv[t] = vt < VT ? load1<IO>(static_cast<const IO*>(a.rv) + cur * V + 16 * vt + lr) : 0.f;
+  }
+  floatx4 xs[VTW][MT];
+#pragma unroll
+  for (int t = 0; t < VTW; ++t) {
+    const int vt = wave + 4 * t;
+    if (vt < VT) {
+      const float* src = a.S + item * V * K + (size_t)(vt * MT) * 256 + 4 * lane;
+#pragma unroll
+      for (int kt = 0; kt < MT; ++kt) {
+        const float4 x = ld_nt(reinterpret_cast<const float4*>(src + 256 * kt));
+        xs[t][kt] = floatx4{x.x, x.y, x.z, x.w};
+      }
+    }
+  }
+  compiler_fence();
+  if (tid < K) {
+    ks[tid] = kk;
+    qs[tid] = qq;
+    if constexpr (CHAN) as[tid] = fast_exp(lk);
+  }
+  lds_barrier();  // LDS only: the state loads stay in flight
+  const float alpha = CHAN ? 1.f : fast_exp(ls);
+
+#pragma unroll
+  for (int t = 0; t < VTW; ++t) {
+    const int vt = wave + 4 * t;
+    if (vt >= VT) continue;
+    // k, q and alpha are re-read from LDS per tile: kept in registers across
+    // the wave's tiles they would double its registers
+    compiler_fence();
+    // w = beta (v - X Diag(alpha) k), or beta v without the erase
+    float w = beta * vv[t];
+    if constexpr (ERASE) {
+      float y = 0.f;
+#pragma unroll
+      for (int kt = 0; kt < MT; ++kt) {
+        const float4 k4 = *reinterpret_cast<const float4*>(&ks[16 * kt + 4 * lg]);
+        float4 d4 = make_float4(alpha, alpha, alpha, alpha);
+        if constexpr (CHAN) d4 = *reinterpret_cast<const float4*>(&as[16 * kt + 4 * lg]);
+        y += xs[t][kt][0] * (d4.x * k4.x) + xs[t][kt][1] * (d4.y * k4.y) + xs[t][kt][2] * (d4.z * k4.z) +
+             xs[t][kt][3] * (d4.w * k4.w);
+      }
+      w = beta * (vv[t] - cross_row_sum(y));
+    }
+    compiler_fence();  // k is read again below rather than held across the cross-row sum
+    // X <- X Diag(alpha) + w k^T, then o = X q
+    float p = 0.f;
+#pragma unroll
+    for (int kt = 0; kt < MT; ++kt) {
+      const float4 k4 = *reinterpret_cast<const float4*>(&ks[16 * kt + 4 * lg]);
+      const float4 q4 = *reinterpret_cast<const float4*>(&qs[16 * kt + 4 * lg]);
+      float4 d4 = make_float4(alpha, alpha, alpha, alpha);
+      if constexpr (CHAN) d4 = *reinterpret_cast<const float4*>(&as[16 * kt + 4 * lg]);
+      floatx4 x = xs[t][kt];
+      x[0] = x[0] * d4.x + w * k4.x;
+      x[1] = x[1] * d4.y + w * k4.y;
+      x[2] = x[2] * d4.z + w * k4.z;
+      x[3] = x[3] * d4.w + w * k4.w;
+      p += x[0] * q4.x + x[1] * q4.y + x[2] * q4.z + x[3] * q4.w;
+      xs[t][kt] = x;
+    }
+    p = cross_row_sum(p);
+    if (a.o && lg == 0) a.o[item * V + 16 * vt + lr] = p;
+    float* dst = a.S + item * V * K + (size_t)(vt * MT) * 256 + 4 * lane;
+#pragma unroll
+    for (int kt = 0; kt < MT; ++kt)
+      st_nt(reinterpret_cast<float4*>(dst + 256 * kt), make_float4(xs[t][kt][0], xs[t][kt][1], xs[t][kt][2], xs[t][kt][3]));
+  }
+}
+
 }  // namespace skssm

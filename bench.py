@@ -385,13 +385,16 @@ def main():
     }
 
     # ---- what plain streaming kernels reach on this part, measured in the same
-    # run (HIP events, median of 7): a read-only pass and a copy, 1 GiB each way
-    # (beyond the 256 MB last-level cache)
+    # run (HIP events, median of 7): a read-only pass, a copy and an in-place
+    # rewrite, 1 GiB each way (beyond the 256 MB last-level cache)
     if not args.no_ceilings:
         ce = hbm_ceilings(dev)
         out["hbm_ceilings"] = ce
         out["roofline"]["frac_of_read_ceiling"] = round(dec_gbps / ce["read_gbps"], 4)
         out["kernels"]["flush"]["frac_of_copy_ceiling"] = round(ks["fl_gbps"] / ce["copy_gbps"], 4)
+        out["kernels"]["flush"]["frac_of_inplace_ceiling"] = round(ks["fl_gbps"] / ce["inplace_gbps"], 4)
+        if "standard" in out:
+            out["standard"]["frac_of_inplace_ceiling"] = round(out["standard"]["gbps"] / ce["inplace_gbps"], 4)
 
     if args.copy_calibration:
         n = 1 << 28  # 1 GiB of fp32
@@ -434,8 +437,10 @@ def recorded_traffic(entry, wl, rank, W, sketch="f32", pivots=0):
 def hbm_ceilings(dev, reps=7):
     """Bandwidth of plain streaming kernels on 1 GiB operands: row sums of a
     16384 x 16384 fp32 matrix (reads 1 GiB; of torch's reductions the one that
-    streams fastest here) and torch.neg (reads 1 GiB, writes 1 GiB), timed with
-    HIP events on the current stream, median of `reps` launches after a warmup."""
+    streams fastest here), torch.neg (reads 1 GiB, writes 1 GiB elsewhere) and
+    its in-place form (reads and rewrites the same 1 GiB, as the flush does with
+    the state), timed with HIP events on the current stream, median of `reps`
+    launches after a warmup."""
     import torch
 
     n = 1 << 28
@@ -458,10 +463,13 @@ def hbm_ceilings(dev, reps=7):
 
     t_read = med(lambda: torch.sum(a.view(1 << 14, 1 << 14), dim=1, out=s))
     t_copy = med(lambda: torch.neg(a, out=b))
+    t_inpl = med(lambda: a.neg_())
     del a, b
     torch.cuda.empty_cache()
     return {"read_gbps": round(4 * n / t_read / 1e9, 1), "copy_gbps": round(8 * n / t_copy / 1e9, 1),
+            "inplace_gbps": round(8 * n / t_inpl / 1e9, 1),
             "read_kernel": "torch.sum(dim=1) of a 16384 x 16384 fp32 matrix", "copy_kernel": "torch.neg, 1 GiB fp32 in and out",
+            "inplace_kernel": "torch.neg_ on 1 GiB fp32 (read and rewritten in place)",
             "read_frac_of_peak": round(4 * n / t_read / 1e9 / 8000.0, 4),
             "copy_frac_of_peak": round(8 * n / t_copy / 1e9 / 8000.0, 4)}
 

@@ -112,7 +112,7 @@ def derived_write_bytes(s: Shape, n: int, baseline: bool = False) -> int:
 
 def decode_bytes(s: Shape, n: int) -> int:
     """Sketch read at slot n: the query, n earlier slots, the current slot, the
-    derived fields, U, the state-dependent map's factors (if any) and o."""
+    derived fields, U, the state-dependent map (if any) and o."""
     return (s.io_bytes * s.dk + n * slot_read_bytes(s) + current_read_bytes(s) + tinv_read_bytes(s, n)
             + derived_write_bytes(s, n) + s.sketch_bytes * s.dv * s.rank + s.cmap_bytes + 4 * s.dv)
 
@@ -123,16 +123,17 @@ def full_read_bytes(s: Shape, n: int) -> int:
             + derived_write_bytes(s, n, True) + 4 * s.dk * s.dv + 4 * s.dv)
 
 
-def flush_bytes(s: Shape, n_buffered: int, rank: int | None = None) -> int:
+def flush_bytes(s: Shape, n_buffered: int, rank: int | None = None, map_rows: int | None = None) -> int:
     """Flush of the token in slot n_buffered: S read + write, the earlier
     slots (raw k, v, beta, log decay) and their rows of T^{-1}, the current
     slot, the query, the sketch write (rank columns), the state-dependent
-    map's factors (if any) and o."""
+    map's rows (if any; all r unless map_rows says fewer are stored) and o."""
     r = s.rank if rank is None else rank
+    cmap = s.cmap_bytes if map_rows is None else s.sketch_bytes * map_rows * s.dk * (1 if s.pivots else 0)
     slot = s.io_bytes * (s.dk + s.dv) + 4 + s.decay_bytes
     tinv = 4 * n_buffered * (n_buffered - 1) // 2 if s.erase else 0
     return (8 * s.dk * s.dv + n_buffered * slot + tinv + current_read_bytes(s) + s.io_bytes * s.dk
-            + s.sketch_bytes * s.dv * r + (s.cmap_bytes if r else 0) + 4 * s.dv)
+            + s.sketch_bytes * s.dv * r + (cmap if r else 0) + 4 * s.dv)
 
 
 def init_bytes(s: Shape) -> int:
@@ -173,5 +174,6 @@ def ragged_decode_bytes(s: Shape, n: int, ranks) -> int:
 def ragged_flush_bytes(s: Shape, n_buffered: int, ranks) -> int:
     """Flush of one batch row under a per-head rank table: each head's state
     read and write, its sketch columns (whole panels; none for a dense head)
-    and, with a state-dependent map, the full-width factors."""
-    return sum(flush_bytes(s, n_buffered, panel_cols(s, g) if g else 0) for g in ranks)
+    and, with a state-dependent map, its map's rows below its rank (the rows
+    past it are not stored)."""
+    return sum(flush_bytes(s, n_buffered, panel_cols(s, g) if g else 0, g) for g in ranks)

@@ -308,7 +308,7 @@ def test_pivot_map_small(fam, K, V, rank, window, io, sketch):
 @pytest.mark.parametrize("sketch", ["f32", "bf16"])
 @pytest.mark.parametrize("name", ["mamba2_b256", "gdn_b512", "kda_b512"])
 def test_pivot_map_full_size(name, sketch):
-    """bf16: the paper's method as the benchmark times it (bf16 sketch, f and map factors)."""
+    """bf16: the paper's method as the benchmark times it (bf16 sketch, f and dense map)."""
     wl = inputs.WORKLOADS[name]
     check(wl, sel=sample_items(wl), sketch=sketch, pivots=4)
 

@@ -64,6 +64,12 @@ def test_ragged_bytes_reduce_to_the_uniform_and_dense_cases():
     assert T.panel_cols(s, 5) == 8 and T.panel_cols(T.Shape("gdn", 128, 128, 16, 16, 2, 2), 5) == 8
     assert T.panel_cols(T.Shape("gdn", 128, 128, 16, 16, 2, 2), 9) == 16
     assert T.ragged_flush_bytes(s, 15, [16, 0]) == T.flush_bytes(s, 15) + T.flush_bytes(s, 15, 0)
+    # with a state-dependent map a head stores the map rows below its rank: r x K at full width, g x K below it
+    sm = T.Shape("gdn", 128, 128, 16, 16, 2, 2, pivots=4)
+    assert T.ragged_flush_bytes(sm, 15, [16]) == T.flush_bytes(sm, 15)
+    assert T.ragged_flush_bytes(sm, 15, [5]) == T.flush_bytes(sm, 15, 8) - 2 * (16 - 5) * 128
+    # and reads those rows (its U up to the next whole bf16 panel: 8 columns)
+    assert T.ragged_decode_bytes(sm, 3, [5]) == T.decode_bytes(T.Shape("gdn", 128, 128, 5, 16, 2, 2, pivots=4), 3) + 2 * 128 * 3
 
 
 def test_bf16_storage_halves_f_and_the_map():

@@ -178,7 +178,8 @@ typedef struct {
  *     U = S_W^T Omega (if rank > 0) and S_W back in place.  The caller then
  *     starts the next window at slot 0; the ring needs no clearing.
  *     window = 1 with rank = 0 is the Standard recurrence (one read and one
- *     write of S per token).
+ *     write of S per token); a single token at rank 0 runs as the rank-1
+ *     recurrence on the vector units, the state streamed through registers.
  *   q == NULL: builds U = S^T Omega from S alone (the initial sketch after
  *     prefill, the initialisation step of Algorithm 1); n_buffered must be 0,
  *     S is not written and o is ignored.

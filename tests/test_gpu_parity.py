@@ -152,6 +152,38 @@ def test_window_one_full_size(name):
     assert not bad, "; ".join(bad)
 
 
+@pytest.mark.parametrize("fam,io", [("mamba2", "f32"), ("gdn", "bf16"), ("kda", "f32"), ("kda", "bf16")])
+def test_single_token_flush_of_a_longer_window(fam, io):
+    """A window flushed after its first token at rank 0 (sketchssm_update with
+    n_buffered = 0 and W = 16, the exact baseline's layer) is one step of the
+    plain recurrence, like window-1 decoding: state and output against the
+    oracle."""
+    import oracle
+    from paper_2609_33051_amd import binding as B
+    from paper_2609_33051_amd.layer import SketchSSMLayer
+    V = 64 if fam == "mamba2" else 128
+    wl = inputs.tiny(fam, batch=5, heads=3, dk=128, dv=V, rank=8, window=16, steps=1, io=io)
+    announce(f"single-token flush W=16 {fam} io={io}")
+    om, C = inputs.omega(wl, 8, inputs.SEED)
+    S = inputs.initial_state(wl, "cuda", inputs.SEED)
+    S0 = to_np32(S.reshape(-1, V, 128))
+    layer = SketchSSMLayer(wl.kind, wl.batch, wl.heads, 128, V, 8, 16, io, "cuda", baseline=True, S=S,
+                           omega=torch.as_tensor(om), coef=torch.as_tensor(C))
+    inp = inputs.step_inputs(wl, 0, "cuda", inputs.SEED)
+    layer.write_token(inp, 0)
+    o = torch.empty((wl.batch, wl.heads, V), dtype=torch.float32, device="cuda")
+    B.sketchssm_update(layer.cfg, layer.S, None, layer.ring, 0, inp["q"], None, o, layer.stream())
+    torch.cuda.synchronize()
+    n = wl.batch * wl.heads
+    one = {k: to_np32(inp[k].reshape(n, -1) if inp[k].dim() > 2 or k in ("q", "k", "v") else inp[k].reshape(n))[None]
+           for k in ("q", "k", "v", "beta", "log_decay")}
+    o_ex, S_ex = oracle.recurrence(wl.kind, S0, one["q"], one["k"], one["v"], one["beta"], one["log_decay"])
+    rep = parity_report([to_np32(o.reshape(n, V))], o_ex, to_np32(layer.state().reshape(n, V, 128)), S_ex)
+    print("  " + format_report(rep), flush=True)
+    bad = parity_failures(rep, *bars(io, "f32"))
+    assert not bad, "; ".join(bad)
+
+
 def test_rerun_is_bitwise_identical():
     wl = inputs.tiny("gdn", batch=5, heads=3, dk=128, dv=128, rank=16, window=8, steps=20, io="bf16")
     announce("determinism gdn")

@@ -58,19 +58,23 @@ template <> __device__ __forceinline__ float load1<bf16_t>(const bf16_t* p) { re
 //   T    = I + L_G^T D^{-1} L_G                  (Woodbury: only T is inverted)
 //   F1   = D^{-1} L_G T^{-1}  (= A^{-1} L_G),  F2 = A^{-1} Diag(d),
 //   A^{-1} = D^{-1} - D^{-1} L_G T^{-1} L_G^T D^{-1}
-// so the map is C = F1 M + F2 Omega^T (G x K).  The flush forms that product
-// on the matrix cores, C^T = [M^T Omega] [F1 F2]^T with the contraction over
-// the P + G stacked rows, and stores the dense map per item in the sketch's
-// dtype (bf16 with the paper's storage, rounded to nearest even) in 16-byte
-// channel panels cmap[B][H][K/CPW][G][CPW].  Rows past the head's rank are
-// not stored.  Every thread of the workgroup calls this.
+// so the map is C = F1 M + F2 Omega^T (G x K).  With w = d / (d + lambda),
+// F2 = Diag(w) - F1 L_G^T Diag(w), hence
+//   C = F1 M' + Diag(w) Omega^T,   M' = M - L_G^T Diag(w) Omega^T   (P x K):
+// thread k forms column k of M' beside that of M, and the flush forms
+// C^T = M'^T F1^T on the matrix cores (one 16x16x4 step per block) plus
+// w_j Omega[k][j] per element, then stores the dense map per item in the
+// sketch's dtype (bf16 with the paper's storage, rounded to nearest even) in
+// 16-byte channel panels cmap[B][H][K/CPW][G][CPW].  Rows past the head's
+// rank are not stored.  Every thread of the workgroup calls this.
 template <int K, int R, int P, int MT, int RT, int LSZ, int USZ, int OPJ, typename SK>
 __device__ __forceinline__ void coef_map_tail(const UpdateArgs& a, size_t item, int wave, int lane, int tid, int rh,
                                               const floatx4 (&nacc)[MT], const floatx4 (&gram)[RT],
                                               const float (&dsq)[RT], float msq,
                                               float* Ls, float* Us, float* cmS, const float* OmL, float* Fext) {
   static_assert(LSZ >= 4 * K * P && USZ >= 4 * R * 5, "staging buffers too small for the map's partial sums");
-  constexpr int FBP = P + R + 1;                       // row pitch of [F1 F2] (odd: lanes of a read spread over banks)
+  static_assert(MT % 4 == 0, "the four waves split the k tiles evenly");
+  constexpr int FBP = P + 1;                           // row pitch of F1 (odd: lanes of a read spread over banks)
   constexpr bool FB_ALIAS = LSZ >= P * K + 16 * RT * FBP;
   const int lr = lane & 15, lg = lane >> 4;
   // the squared sketch columns summed over the four lane rows (the Gram
@@ -228,7 +232,10 @@ __device__ __forceinline__ void coef_map_tail(const UpdateArgs& a, size_t item, 
     }
   }
   lds_barrier();
-  // M = R^{-T} N^T / sqrt(mu): thread k sums the four waves' N rows
+  // M' = R^{-T} N^T / sqrt(mu) - L_G^T Diag(w) Omega^T: thread k sums the four
+  // waves' N rows for column k of M, then subtracts sum_h L_G[h] w_h Omega[k][h]
+  // (Omega's columns past the head's rank are zero in LDS, and so is w there)
+  const float* sL = cmS + 8 + 16;  // [R][P] L_G, then [R] w
   float Mk[P] = {};
   if (tid < K) {
     const int k = tid;
@@ -241,47 +248,43 @@ __device__ __forceinline__ void coef_map_tail(const UpdateArgs& a, size_t item, 
 #pragma unroll
       for (int b = 0; b < P; ++b) Mk[x] += cmS[8 + b * P + x] * Nk[b];
     }
-  }
-  lds_barrier();  // the waves' N rows are consumed: M^T and [F1 F2] take their place
-  float* Mb = Ls;                              // [K][P]   M^T
-  float* Fb = FB_ALIAS ? Ls + P * K : Fext;    // [16 RT][FBP]  row j = (F1 row j, F2 row j), zero past R
-  if (tid < K) *reinterpret_cast<float4*>(&Mb[tid * P]) = make_float4(Mk[0], Mk[1], Mk[2], Mk[3]);
-  if (wave == 0 && lane < 16 * RT) {
-    const int g = lane;
-    float* fr = Fb + g * FBP;
-    if (g < R) {
-      const float* sL = cmS + 8 + 16;
 #pragma unroll
-      for (int c = 0; c < P; ++c) fr[c] = F1[c];
-      // row g of F2 = A^{-1} Diag(d): (g == h) w_h - F1[g] . L_G[h] w_h
-#pragma unroll 4
-      for (int hh = 0; hh < R; ++hh) {
-        float e = 0.f;
+    for (int h4 = 0; h4 < R; h4 += 4) {
+      const float4 o4 = *reinterpret_cast<const float4*>(&OmL[k * OPJ + h4]);
+      const float oh[4] = {o4.x, o4.y, o4.z, o4.w};
 #pragma unroll
-        for (int c = 0; c < P; ++c) e += F1[c] * sL[hh * P + c];
-        const float w = sL[R * P + hh];
-        fr[P + hh] = (hh == g ? w : 0.f) - e * w;
+      for (int e = 0; e < 4; ++e) {
+        const float wo = sL[R * P + h4 + e] * oh[e];
+#pragma unroll
+        for (int x = 0; x < P; ++x) Mk[x] -= sL[(h4 + e) * P + x] * wo;
       }
-    } else {
-#pragma unroll
-      for (int c = 0; c < P + R; ++c) fr[c] = 0.f;
     }
   }
+  lds_barrier();  // the waves' N rows are consumed: M'^T and F1 take their place
+  float* Mb = Ls;                              // [K][P]   M'^T
+  float* Fb = FB_ALIAS ? Ls + P * K : Fext;    // [16 RT][FBP]  row j = F1 row j, zero past R
+  if (tid < K) *reinterpret_cast<float4*>(&Mb[tid * P]) = make_float4(Mk[0], Mk[1], Mk[2], Mk[3]);
+  if (wave == 0 && lane < 16 * RT) {
+    float* fr = Fb + lane * FBP;
+#pragma unroll
+    for (int c = 0; c < P; ++c) fr[c] = lane < R ? F1[c] : 0.f;
+  }
   lds_barrier();
-  // C^T = [M^T Omega] [F1 F2]^T: wave w takes k tiles w, w + 4, ...; lane
-  // (lr, lg) ends with C[16 jt + lr][16 kt + 4 lg + i], i = 0..3
+  // C^T = M'^T F1^T + (Diag(w) Omega^T)^T: wave w takes k tiles w, w + 4, ...;
+  // lane (lr, lg) ends with C[16 jt + lr][16 kt + 4 lg + i], i = 0..3
   constexpr int CPW = 16 / (int)sizeof(SK);
   SK* cm = static_cast<SK*>(a.cmap) + item * (size_t)(R * K);
 #pragma unroll
-  for (int kt = wave; kt < MT; kt += 4) {
+  for (int kq = 0; kq < MT / 4; ++kq) {
+    const int kt = wave + 4 * kq;
 #pragma unroll
     for (int jt = 0; jt < RT; ++jt) {
+      const int j = 16 * jt + lr, k0 = 16 * kt + 4 * lg;
       floatx4 acc = {0.f, 0.f, 0.f, 0.f};
       acc = mfma4(Mb[(16 * kt + lr) * P + lg], Fb[(16 * jt + lr) * FBP + lg], acc);
+      const float wj = j < R ? sL[R * P + j] : 0.f;
 #pragma unroll
-      for (int st = 0; st < R / 4; ++st)
-        acc = mfma4(OmL[(16 * kt + lr) * OPJ + 4 * st + lg], Fb[(16 * jt + lr) * FBP + P + 4 * st + lg], acc);
-      const int j = 16 * jt + lr, k0 = 16 * kt + 4 * lg;
+      for (int i = 0; i < 4; ++i) acc[i] += wj * OmL[(k0 + i) * OPJ + j];
       if (j < rh) st_elem4<SK>(cm + ((size_t)(k0 / CPW) * R + j) * CPW + k0 % CPW, acc[0], acc[1], acc[2], acc[3]);
     }
   }
@@ -474,8 +477,8 @@ __global__ __launch_bounds__(256, (P != 0 && WMAX == 16 && R <= 16) ? 4 : 3) voi
   float* const cmU = cmX;                                  // [wave][16 values][16 sketch columns], before X's blocks
   __shared__ __align__(16) float cmS[P != 0 ? 8 + 16 + 5 * R : 4];  // mu parts, R^{-1}/sqrt(mu), L_G and w
   // [F1 F2] of the map, in its own LDS only where the key staging has no room
-  constexpr bool CMF_OWN = P > 0 && SP * LP < P * K + 16 * RT * (P + R + 1);
-  __shared__ __align__(16) float cmF[CMF_OWN ? 16 * RT * (P + R + 1) : 4];
+  constexpr bool CMF_OWN = P > 0 && SP * LP < P * K + 16 * RT * (P + 1);
+  __shared__ __align__(16) float cmF[CMF_OWN ? 16 * RT * (P + 1) : 4];
   static_assert(!EXACT || (SP * LP >= R * (K + 4) && SP * UP >= 2 * R * (R + 1)),
                 "the exact map's sums must fit the window staging");
   floatx4 nacc[P != 0 ? MT : 1];   // N^T (rows 4 lg + i: pivots a < 4, or every sketch column), this wave's values

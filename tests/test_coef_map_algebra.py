@@ -1,4 +1,4 @@
-"""The coefficient map in the factored form the flush kernel writes, checked
+"""The coefficient map in the form the flush kernel builds it, checked
 against the oracle.
 
 The oracle builds the state-dependent map literally in the basis-aligned
@@ -8,8 +8,11 @@ a direct G x G solve).  The kernel never forms R or the K x K metric: it
 works from the sketch U and the product U_p^T X of the first p sketch columns
 with the state, uses a Cholesky factor of the p x p pivot Gram matrix in place
 of Gram-Schmidt, and Woodbury's identity (Step 4 of that appendix) for the
-G x G inverse, and stores C = F1 M + F2 Omega^T as (M, F1, F2).  This numpy
-model of that algebra must give the oracle's map.
+G x G inverse, which gives C = F1 M + F2 Omega^T.  With w = d / (d + lambda)
+the second factor is F2 = Diag(w) - F1 L_G^T Diag(w), so the kernel forms
+C = F1 M' + Diag(w) Omega^T with the p x K correction
+M' = M - L_G^T Diag(w) Omega^T.  This numpy model of both forms must give the
+oracle's map.
 """
 import numpy as np
 import pytest
@@ -32,7 +35,16 @@ def factored_coef_map(X, Om, p, lam):
     Ainv = np.diag(Dinv) - (Dinv[:, None] * LG) @ np.linalg.solve(T, LG.T * Dinv[None, :])
     F1 = Ainv @ LG
     F2 = Ainv * d[None, :]
-    return F1 @ M + F2 @ Om.T, (M, F1, F2)
+    return F1 @ M + F2 @ Om.T, (M, F1, F2, LG, d * Dinv)
+
+
+def kernel_form(X, Om, p, lam):
+    """C = F1 M' + Diag(w) Omega^T with M' = M - L_G^T Diag(w) Omega^T, the
+    form the flush forms, from the same factors."""
+    _, (M, F1, F2, LG, w) = factored_coef_map(X, Om, p, lam)
+    assert np.allclose(F2, np.diag(w) - F1 @ LG.T * w[None, :], rtol=1e-10, atol=1e-12)
+    Mp = M - (LG * w[:, None]).T @ Om.T
+    return F1 @ Mp + w[:, None] * Om.T
 
 
 @pytest.mark.parametrize("K,V,G,p", [(8, 6, 5, 2), (16, 12, 8, 4), (12, 16, 4, 4)])
@@ -46,5 +58,7 @@ def test_factored_coef_map_equals_the_oracle(K, V, G, p):
     om = heads_omega(1, K, G, seed=p)[0]
     want = coef_map_of(S, om, p, 0.1)
     for i in range(3):
-        got, _ = factored_coef_map(S[i].astype(np.float64), om[0].astype(np.float64), p, 0.1)
+        X, Om = S[i].astype(np.float64), om[0].astype(np.float64)
+        got, _ = factored_coef_map(X, Om, p, 0.1)
         assert np.allclose(got, want[i], rtol=1e-6, atol=1e-7)
+        assert np.allclose(kernel_form(X, Om, p, 0.1), want[i], rtol=1e-6, atol=1e-7)

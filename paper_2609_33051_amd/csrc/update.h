@@ -210,7 +210,7 @@ __device__ __forceinline__ void coef_map_tail(const UpdateArgs& a, size_t item, 
         }
       }
     }
-    // F1 row g; L_G and w = D^{-1} d of every g for the F2 rows
+    // F1 row g; L_G and w = D^{-1} d of every g for the correction M' = M - L_G^T Diag(w) Omega^T
 #pragma unroll
     for (int c = 0; c < P; ++c) {
       float e = 0.f;
@@ -460,8 +460,8 @@ __global__ __launch_bounds__(256, (P != 0 && WMAX == 16 && R <= 16) ? 4 : 3) voi
   const bool want_U = R > 0 && a.U != nullptr && rh > 0;
 
   // state-dependent coefficient map (P = 4 pivots, or the exact metric, P < 0):
-  // per-wave scratch for the block transposes of X and of the first sketch
-  // columns, and the small factors shared by the workgroup
+  // per-wave scratch for the block transposes of X and of the sketch columns,
+  // and the small factors shared by the workgroup
   constexpr bool EXACT = P < 0;
   static_assert(P == 0 || (P == 4 && R >= 8 && R <= 32) || (EXACT && R >= 8 && R <= 16),
                 "state-dependent maps: P = 4 with rank 8..32, or the exact metric with rank 8..16");
@@ -469,14 +469,14 @@ __global__ __launch_bounds__(256, (P != 0 && WMAX == 16 && R <= 16) ? 4 : 3) voi
   // When the key staging Ls has room, that scratch lives in Ls: every tile is
   // then updated first and sketched after a barrier, once Ls is dead.  This
   // keeps the kernel's LDS that of the offline-map flush (four workgroups per CU).
-  // The exact map transposes all 16 sketch columns of a tile through the
-  // same per-wave block as X (one after the other).
+  // Each tile's sketch columns go through the same per-wave block as X's
+  // (one after the other).
   constexpr bool CM_ALIAS = P != 0 && SP * LP >= 4 * 16 * XP;
   __shared__ __align__(16) float cmXs[P != 0 && !CM_ALIAS ? 4 * 16 * XP : 4];
   float* const cmX = CM_ALIAS ? Ls : cmXs;                 // [wave][16 values][16 keys]
   float* const cmU = cmX;                                  // [wave][16 values][16 sketch columns], before X's blocks
   __shared__ __align__(16) float cmS[P != 0 ? 8 + 16 + 5 * R : 4];  // mu parts, R^{-1}/sqrt(mu), L_G and w
-  // [F1 F2] of the map, in its own LDS only where the key staging has no room
+  // F1 of the map, in its own LDS only where the key staging has no room
   constexpr bool CMF_OWN = P > 0 && SP * LP < P * K + 16 * RT * (P + 1);
   __shared__ __align__(16) float cmF[CMF_OWN ? 16 * RT * (P + 1) : 4];
   static_assert(!EXACT || (SP * LP >= R * (K + 4) && SP * UP >= 2 * R * (R + 1)),

@@ -7,7 +7,8 @@ fp32-level noise), and mistakes are planted in that copy: one value channel
 of one item at one step off by 10 %, one item's whole output off by 0.6 %, one
 item's state or sketch off by 1 %.  Over a sampled batch the aggregate
 (headline) relative L2 can stay under the bf16 bar for these, so each must
-be caught by the per-item bars, whatever the storage dtype.  No GPU is used.
+be caught by the per-item bars, whatever the storage dtype (with fp32
+storage the tighter aggregate bar sees them as well).  No GPU is used.
 """
 import numpy as np
 import pytest
@@ -58,9 +59,10 @@ def test_one_channel_of_one_item_off_by_ten_percent(run, io, sketch):
     bad[t, i, c] = ref.o[t, i, c] * 1.1
     rep = parity_report(bad, ref.o, S, ref.S_final, U, ref.U_final)
     head, item = bars(io, sketch)
-    assert rep["o_step"] <= head, "the aggregate alone does not see it (the point of the per-item bar)"
-    fails = parity_failures(rep, head, item)
-    assert fails and fails[0].startswith("o_item")
+    if sketch == "bf16":  # under the bf16 bar the aggregate alone does not see it: the point of the per-item bar
+        assert rep["o_step"] <= head
+    assert rep["o_item"] > item, "the per-item bar catches it whatever the storage"
+    assert any(f.startswith("o_item") for f in parity_failures(rep, head, item))
 
 
 @pytest.mark.parametrize("io,sketch", [("bf16", "f32"), ("bf16", "bf16")])
@@ -72,7 +74,8 @@ def test_one_item_off_by_a_little_over_half_a_percent(run, io, sketch):
     bad[:, i] = ref.o[:, i] * 1.006
     rep = parity_report(bad, ref.o, S, ref.S_final, U, ref.U_final)
     head, item = bars(io, sketch)
-    assert rep["o_step"] <= head
+    if sketch == "bf16":
+        assert rep["o_step"] <= head
     assert any(f.startswith("o_item") for f in parity_failures(rep, head, item))
 
 

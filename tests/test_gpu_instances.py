@@ -51,3 +51,43 @@ def test_every_compiled_instance(fam, K, V):
         if bad:
             failures.append(f"r={R} W={W} io={io} sketch={sk} pivots={piv}: " + "; ".join(bad))
     assert not failures, "\n".join(failures)
+
+
+@pytest.mark.parametrize("fam", ["mamba2", "gdn", "kda"])
+@pytest.mark.parametrize("K,V", [(64, 64), (128, 64), (128, 128)])
+def test_every_compiled_baseline_instance(fam, K, V):
+    """The exact baseline's instances: the full-state read and its rank-0
+    flush for both window classes, and the single-token update (window 1),
+    for both io dtypes, against the oracle's exact windowed read."""
+    failures = []
+    for W in (1, 7, 20):
+        for io in ("f32", "bf16"):
+            wl = inputs.tiny(fam, batch=2, heads=2, dk=K, dv=V, rank=8, window=W, steps=W + 3, io=io)
+            print(f"[case] baseline {fam} K={K} V={V} W={W} io={io}", flush=True)
+            run, layer, S_sel, heads, (om, C) = run_workload(wl, baseline=True)
+            ref = oracle_of(wl, run, S_sel, heads, om, C, W)
+            n = wl.batch * wl.heads
+            rep = parity_report(run.o_gpu, ref.o_exact_windowed, to_np32(layer.state().reshape(n, V, K)), ref.S_final)
+            print("  " + format_report(rep), flush=True)
+            bad = parity_failures(rep, *bars(io, "f32"))
+            if bad:
+                failures.append(f"W={W} io={io}: " + "; ".join(bad))
+    assert not failures, "\n".join(failures)
+
+
+@pytest.mark.parametrize("fam", ["mamba2", "gdn", "kda"])
+@pytest.mark.parametrize("K,V", [(64, 64), (128, 64), (128, 128)])
+def test_every_compiled_dense_fallback_instance(fam, K, V):
+    """The decode instances compiled with the exact read of dense-fallback
+    heads (launched for rank tables that have such heads): one head at the
+    full storage width and one dense head, for every width, window class,
+    storage and map, each head against its own oracle run."""
+    from test_gpu_ragged import check_ragged
+    for R in (8, 16, 32):
+        for W in (7, 20):
+            for io, sk in STORAGE:
+                for piv in (0, 4, -1):
+                    if piv == -1 and R not in (8, 16):
+                        continue
+                    wl = inputs.tiny(fam, batch=2, heads=2, dk=K, dv=V, rank=R, window=W, steps=W + 3, io=io)
+                    check_ragged(wl, [R, 0], sketch=sk, pivots=piv)

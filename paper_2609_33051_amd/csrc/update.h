@@ -401,6 +401,56 @@ __device__ __forceinline__ void coef_map_exact_tail(const UpdateArgs& a, size_t 
   }
 }
 
+// The rank update of one 16-value tile of X = S^T from the factors of a window
+// (or a chunk of one) staged in LDS, eq. wy: lane (lr, lg) holds
+// X[v][16 kt + 4 lg + i] in x[kt][i], v = 16 vt + lr, and
+//   X^T <- Diag(e^{g_n}) X^T + (keys or L)^T W^T,
+// with w_s = c_s (u_s - (Pi X^T)[s]) (GDN), u_s - (Pi X^T)[s] (KDA, whose decays
+// are in L and ds) or c_s beta_s v_s (Mamba-2), slot s = 16 st + 4 lg + i.
+template <int KIND, int MT, int ST, int LP, int PP, int UP>
+__device__ __forceinline__ void rank_update_tile(floatx4 (&x)[MT], int v, int lr, int lg, float egn, const float* Ls,
+                                                 const float* PiT, const float* Us, const float* bsl, const float* csc,
+                                                 const float* ds) {
+  constexpr bool ERASE = KIND != MAMBA2;
+  constexpr bool CHAN = KIND == KDA;
+  floatx4 wv[ST];
+#pragma unroll
+  for (int st = 0; st < ST; ++st) {
+    floatx4 acc = {0.f, 0.f, 0.f, 0.f};
+    if constexpr (ERASE) {
+      // (Pi X^T)[s] in four independent accumulation chains
+      floatx4 pc[4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) pc[i] = floatx4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int kt = 0; kt < MT; ++kt)
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+          pc[i] = mfma4(PiT[(16 * kt + 4 * lg + i) * PP + 16 * st + lr], x[kt][i], pc[i]);
+      acc = (pc[0] + pc[1]) + (pc[2] + pc[3]);
+    }
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int s = 16 * st + 4 * lg + i;
+      float w = Us[s * UP + v] - acc[i];
+      if constexpr (!ERASE) w *= bsl[s] * csc[s];
+      if constexpr (ERASE && !CHAN) w *= csc[s];
+      wv[st][i] = w;
+    }
+  }
+#pragma unroll
+  for (int kt = 0; kt < MT; ++kt) {
+    floatx4 acc;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) acc[i] = x[kt][i] * (CHAN ? ds[16 * kt + 4 * lg + i] : egn);
+#pragma unroll
+    for (int st = 0; st < ST; ++st)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) acc = mfma4(Ls[(16 * st + 4 * lg + i) * LP + 16 * kt + lr], wv[st][i], acc);
+    x[kt] = acc;
+  }
+}
+
 // Three workgroups per CU, or four for the state-dependent maps (P = 4 and
 // exact) at window 16 and rank <= 16: their flush spends part of each
 // workgroup's life off the memory bus (the map's products and algebra), so
@@ -413,7 +463,14 @@ __global__ __launch_bounds__(256, (P != 0 && WMAX == 16 && R <= 16) ? 4 : 3) voi
   constexpr int MT = K / 16;          // k tiles
   constexpr int VT = V / 16;          // value tiles
   constexpr int VTW = (VT + 3) / 4;   // value tiles per wave
-  constexpr int SP = WMAX;            // slot rows (16 or 32)
+  // The erase families flush a window of up to 32 slots as chunks of 16 on
+  // the register-resident state: T is unit lower triangular, so the rows of
+  // T^{-1} that couple a chunk's slots among themselves are the inverse of
+  // that chunk's own T, and a chunk started from the state the previous one
+  // left is a window of its own (decays taken from the chunk's first slot).
+  // The staging and registers are then those of a 16-slot window.
+  constexpr int SP = ERASE ? 16 : WMAX;  // staged slot rows (16 or 32)
+  constexpr int CH = WMAX / SP;          // chunks per flush
   constexpr int ST = SP / 16;         // slot tiles
   constexpr int NG = SP / 4;          // slot groups of four
   constexpr int RT = (R + 15) / 16;   // sketch tiles
@@ -438,7 +495,7 @@ __global__ __launch_bounds__(256, (P != 0 && WMAX == 16 && R <= 16) ? 4 : 3) voi
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int lr = lane & 15, lg = lane >> 4;   // MFMA lane coordinates
   const int row = lg, col = lr;               // row-layout coordinates (same lanes)
-  const int H = a.H, W = a.W, n = a.n;
+  const int H = a.H, W = a.W, nw = a.n;  // nw: the window's current slot
   const size_t item = blockIdx.x;  // b * H + h (B*H <= 2^30)
   const int h = (int)(blockIdx.x % (uint32_t)H);
   const bool flush = a.nt > 0;
@@ -500,267 +557,283 @@ __global__ __launch_bounds__(256, (P != 0 && WMAX == 16 && R <= 16) ? 4 : 3) voi
 
   // ---- every small load first (window, query, rows of T^{-1}, Omega), then the
   // state: the staged values reach LDS while the state read is still in flight
-  float egn = 1.f, gn = 0.f, bn = 0.f;  // e^{g_n} (scalar decay), g_n, beta_n (from LDS after the staging)
-  float bl = 0.f, ll = 0.f;             // wave 0, lane s: beta_s and (scalar decay) log alpha_s
-  float gk[CHAN ? SP : 1];              // KDA: g_s of channel tid
-  Raw<IO, KPL> kr[NG / 4];              // ring keys, row layout (slot 4 (wave + 4 gq) + row)
-  Raw<IO, VR> vr[NG / 4];               // raw values
+  float egn = 1.f, gn = 0.f, bn = 0.f;  // the chunk's e^{g_n} (scalar decay), g_n, beta_n (from LDS after the staging)
   float qv = 0.f;
   constexpr int BQ = ERASE ? (SP * SP + 255) / 256 : 1;
-  float bv[BQ];
   Vec<4> omv[OQ];
-  if (flush) {
-    // per-slot scalars: lane s of wave 0 loads slot s; every slot load is
-    // issued before any is used (slots past n re-read slot n, in bounds, and
-    // are masked afterwards), so no load waits on a branch
-    if (tid < SP) {
-      const size_t si = item * W + (tid < n ? tid : n);
-      bl = a.rbeta[si];
-      if constexpr (!CHAN) ll = a.rla[si];
-    }
-    if constexpr (CHAN) {
-      if (tid < K) {
-#pragma unroll
-        for (int s = 0; s < SP; ++s) gk[s] = a.rla[(item * W + (s < n ? s : n)) * K + tid];
-      }
-    }
-#pragma unroll
-    for (int gq = 0; gq < NG / 4; ++gq) {
-      const int s = 4 * (wave + 4 * gq) + row;
-      const size_t si = item * W + s;
-      if (s <= n) {
-        kr[gq].load(static_cast<const IO*>(a.rk) + si * K + col * KPL);
-        vr[gq].load(static_cast<const IO*>(a.rv) + si * V + col * VR);
-      }
-    }
-    if (tid < K) qv = load1<IO>(static_cast<const IO*>(a.q) + item * K + tid);
-    if constexpr (ERASE) {
-#pragma unroll
-      for (int c = 0; c < BQ; ++c) {
-        const int idx = tid + 256 * c;
-        const int s = idx / SP, j = idx % SP;
-        bv[c] = (idx < SP * SP && s < n && j < s) ? a.rt[((size_t)s * NI + dp) * W + j] : 0.f;
-      }
-    }
-  }
-  if constexpr (OM_LDS) {
-    if (want_U) {
-#pragma unroll
-      for (int c = 0; c < OQ; ++c) {
-        const int i = tid + 256 * c;
-#pragma unroll
-        for (int e = 0; e < 4; ++e) omv[c].e[e] = 0.f;
-        if (i < K * R / 4 && 4 * (i % (R / 4)) < rh) omv[c].load(a.omega + (size_t)h * K * R + 4 * i);
-      }
-    }
-  }
-
-  // ---- the single read of the state
   floatx4 xs[VTW][MT];
 #pragma unroll
-  for (int t = 0; t < VTW; ++t) {
-    const int vt = wave + 4 * t;
-    if (vt < VT) {
-      // tile (vt, kt) of the state is 1 KB contiguous, lane l's float4 at 4 l
-      const float* src = a.S + item * V * K + (size_t)(vt * MT) * 256 + 4 * lane;
-#pragma unroll
-      for (int kt = 0; kt < MT; ++kt) {
-        const float4 x = ld_nt(reinterpret_cast<const float4*>(src + 256 * kt));
-        xs[t][kt] = floatx4{x.x, x.y, x.z, x.w};
+  for (int ch = 0; ch < CH; ++ch) {
+    const int sb = 16 * ch;                                 // the chunk's first slot in the ring
+    // the chunk's current slot (counted from sb); whether it holds the window's
+    const int n = CH == 1 ? nw : !flush ? 0 : (nw - sb < SP ? nw - sb : SP - 1);
+    const bool last = CH == 1 || !flush || nw < sb + SP;
+    float bl = 0.f, ll = 0.f;             // wave 0, lane s: beta_s and (scalar decay) log alpha_s
+    float gk[CHAN ? SP : 1];              // KDA: g_s of channel tid
+    Raw<IO, KPL> kr[NG / 4];              // ring keys, row layout (slot 4 (wave + 4 gq) + row)
+    Raw<IO, VR> vr[NG / 4];               // raw values
+    float bv[BQ];
+    if (flush) {
+      // per-slot scalars: lane s of wave 0 loads slot s; every slot load is
+      // issued before any is used (slots past n re-read slot n, in bounds, and
+      // are masked afterwards), so no load waits on a branch
+      if (tid < SP) {
+        const size_t si = item * W + sb + (tid < n ? tid : n);
+        bl = a.rbeta[si];
+        if constexpr (!CHAN) ll = a.rla[si];
       }
-    }
-  }
-  compiler_fence();
-
-  // ---- staged values into LDS
-  if constexpr (OM_LDS) {
-    if (want_U) {
+      if constexpr (CHAN) {
+        if (tid < K) {
 #pragma unroll
-      for (int c = 0; c < OQ; ++c) {
-        const int i = tid + 256 * c;
-        if (i < K * R / 4) {
-          Vec<4> w = omv[c];
-#pragma unroll
-          for (int e = 0; e < 4; ++e)
-            if (4 * (i % (R / 4)) + e >= rh) w.e[e] = 0.f;
-          w.store(&OmL[(i / (R / 4)) * OPJ + 4 * (i % (R / 4))]);
+          for (int s = 0; s < SP; ++s) gk[s] = a.rla[(item * W + sb + (s < n ? s : n)) * K + tid];
         }
       }
-      if constexpr (R < 16 * RT) {  // zero columns R..16 RT-1
-        constexpr int ZQ = (16 * RT - R) / 4;
-        for (int i = tid; i < K * ZQ; i += 256)
-          *reinterpret_cast<float4*>(&OmL[(i / ZQ) * OPJ + R + 4 * (i % ZQ)]) = make_float4(0.f, 0.f, 0.f, 0.f);
+#pragma unroll
+      for (int gq = 0; gq < NG / 4; ++gq) {
+        const int s = 4 * (wave + 4 * gq) + row;
+        const size_t si = item * W + sb + s;
+        if (s <= n) {
+          kr[gq].load(static_cast<const IO*>(a.rk) + si * K + col * KPL);
+          vr[gq].load(static_cast<const IO*>(a.rv) + si * V + col * VR);
+        }
+      }
+      if (ch == 0 && tid < K) qv = load1<IO>(static_cast<const IO*>(a.q) + item * K + tid);
+      if constexpr (ERASE) {
+#pragma unroll
+        for (int c = 0; c < BQ; ++c) {
+          const int idx = tid + 256 * c;
+          const int s = idx / SP, j = idx % SP;
+          bv[c] = (idx < SP * SP && s < n && j < s) ? a.rt[((size_t)(sb + s) * NI + dp) * W + sb + j] : 0.f;
+        }
       }
     }
-  }
-  if (flush) {
+    if constexpr (OM_LDS) {
+      if (ch == 0 && want_U) {
 #pragma unroll
-    for (int gq = 0; gq < NG / 4; ++gq) {
-      const int s = 4 * (wave + 4 * gq) + row;
-      float ksv[KPL], vsv[VR];
+        for (int c = 0; c < OQ; ++c) {
+          const int i = tid + 256 * c;
 #pragma unroll
-      for (int m = 0; m < KPL; ++m) ksv[m] = 0.f;
-#pragma unroll
-      for (int m = 0; m < VR; ++m) vsv[m] = 0.f;
-      if (s <= n) {
-#pragma unroll
-        for (int m = 0; m < KPL; ++m) ksv[m] = kr[gq].get(m);
-        // raw values (Mamba-2 scales them by beta_s c_s where they are used)
-#pragma unroll
-        for (int m = 0; m < VR; ++m) vsv[m] = vr[gq].get(m);
-      }
-#pragma unroll
-      for (int m = 0; m < KPL; m += 4)
-        *reinterpret_cast<float4*>(&Ls[s * LP + col * KPL + m]) = make_float4(ksv[m], ksv[m + 1], ksv[m + 2], ksv[m + 3]);
-#pragma unroll
-      for (int m = 0; m < VR; m += 4)
-        *reinterpret_cast<float4*>(&Us[s * UP + col * VR + m]) = make_float4(vsv[m], vsv[m + 1], vsv[m + 2], vsv[m + 3]);
-    }
-    if (tid < K) qs[tid] = qv;
-    if (tid < 64) {
-      // wave 0: beta_s, g_s = sum_{j<=s} log alpha_j (inclusive scan over the
-      // lanes) and c_s = e^{g_n - g_s}, slots past n zero
-      const int sl = tid;
-      const bool live = sl <= n && sl < SP;
-      float g = (!CHAN && live) ? ll : 0.f;
-#pragma unroll
-      for (int d = 1; d < SP; d <<= 1) {
-        const float u = __shfl_up(g, d);
-        if (sl >= d) g += u;
-      }
-      const float gnn = __shfl(g, n);
-      if (sl < SP) {
-        bsl[sl] = live ? bl : 0.f;
-        gsl[sl] = live ? g : 0.f;
-        if constexpr (!CHAN) csc[sl] = live ? fast_exp(gnn - g) : 0.f;
+          for (int e = 0; e < 4; ++e) omv[c].e[e] = 0.f;
+          if (i < K * R / 4 && 4 * (i % (R / 4)) < rh) omv[c].load(a.omega + (size_t)h * K * R + 4 * i);
+        }
       }
     }
-    if constexpr (ERASE) {
-#pragma unroll
-      for (int c = 0; c < BQ; ++c) {
-        const int idx = tid + 256 * c;
-        if (idx < SP * SP) Bs[idx] = bv[c];
-      }
-    }
-  }
-  lds_barrier();
-  if (flush) {  // the current slot's scalars, for every thread
-    gn = gsl[n];
-    bn = bsl[n];
-    if constexpr (!CHAN) egn = fast_exp(gn);
-  }
 
-  if (flush) {
-    if constexpr (ERASE) {
-      // ---- channel work: thread tid owns channel k = tid.  Ls holds raw keys.
-      // The pseudo-values of slots before n need only the stored rows of T^{-1},
-      // so the waves that own no channel form them meanwhile.
-      static_assert(K + V <= 256, "channel waves and value waves must be disjoint");
-      float pi[SP], kn = 0.f;
-      if (tid < K) {
-        const int kk = tid;
-        kn = Ls[n * LP + kk];
-        float gnk = gn;
-        if constexpr (CHAN) {
-          // g_s of channel tid: running sum of the window's log alphas
-          float acc = 0.f;
+    // ---- the single read of the state
+    if (ch == 0) {
+#pragma unroll
+      for (int t = 0; t < VTW; ++t) {
+        const int vt = wave + 4 * t;
+        if (vt < VT) {
+          // tile (vt, kt) of the state is 1 KB contiguous, lane l's float4 at 4 l
+          const float* src = a.S + item * V * K + (size_t)(vt * MT) * 256 + 4 * lane;
+#pragma unroll
+          for (int kt = 0; kt < MT; ++kt) {
+            const float4 x = ld_nt(reinterpret_cast<const float4*>(src + 256 * kt));
+            xs[t][kt] = floatx4{x.x, x.y, x.z, x.w};
+          }
+        }
+      }
+    }
+    compiler_fence();
+
+    // ---- staged values into LDS
+    if constexpr (OM_LDS) {
+      if (ch == 0 && want_U) {
+#pragma unroll
+        for (int c = 0; c < OQ; ++c) {
+          const int i = tid + 256 * c;
+          if (i < K * R / 4) {
+            Vec<4> w = omv[c];
+#pragma unroll
+            for (int e = 0; e < 4; ++e)
+              if (4 * (i % (R / 4)) + e >= rh) w.e[e] = 0.f;
+            w.store(&OmL[(i / (R / 4)) * OPJ + 4 * (i % (R / 4))]);
+          }
+        }
+        if constexpr (R < 16 * RT) {  // zero columns R..16 RT-1
+          constexpr int ZQ = (16 * RT - R) / 4;
+          for (int i = tid; i < K * ZQ; i += 256)
+            *reinterpret_cast<float4*>(&OmL[(i / ZQ) * OPJ + R + 4 * (i % ZQ)]) = make_float4(0.f, 0.f, 0.f, 0.f);
+        }
+      }
+    }
+    if (flush) {
+#pragma unroll
+      for (int gq = 0; gq < NG / 4; ++gq) {
+        const int s = 4 * (wave + 4 * gq) + row;
+        float ksv[KPL], vsv[VR];
+#pragma unroll
+        for (int m = 0; m < KPL; ++m) ksv[m] = 0.f;
+#pragma unroll
+        for (int m = 0; m < VR; ++m) vsv[m] = 0.f;
+        if (s <= n) {
+#pragma unroll
+          for (int m = 0; m < KPL; ++m) ksv[m] = kr[gq].get(m);
+          // raw values (Mamba-2 scales them by beta_s c_s where they are used)
+#pragma unroll
+          for (int m = 0; m < VR; ++m) vsv[m] = vr[gq].get(m);
+        }
+#pragma unroll
+        for (int m = 0; m < KPL; m += 4)
+          *reinterpret_cast<float4*>(&Ls[s * LP + col * KPL + m]) = make_float4(ksv[m], ksv[m + 1], ksv[m + 2], ksv[m + 3]);
+#pragma unroll
+        for (int m = 0; m < VR; m += 4)
+          *reinterpret_cast<float4*>(&Us[s * UP + col * VR + m]) = make_float4(vsv[m], vsv[m + 1], vsv[m + 2], vsv[m + 3]);
+      }
+      if (ch == 0 && tid < K) qs[tid] = qv;
+      if (tid < 64) {
+        // wave 0: beta_s, g_s = sum_{j<=s} log alpha_j (inclusive scan over the
+        // lanes) and c_s = e^{g_n - g_s}, slots past n zero
+        const int sl = tid;
+        const bool live = sl <= n && sl < SP;
+        float g = (!CHAN && live) ? ll : 0.f;
+#pragma unroll
+        for (int d = 1; d < SP; d <<= 1) {
+          const float u = __shfl_up(g, d);
+          if (sl >= d) g += u;
+        }
+        const float gnn = __shfl(g, n);
+        if (sl < SP) {
+          bsl[sl] = live ? bl : 0.f;
+          gsl[sl] = live ? g : 0.f;
+          if constexpr (!CHAN) csc[sl] = live ? fast_exp(gnn - g) : 0.f;
+        }
+      }
+      if constexpr (ERASE) {
+#pragma unroll
+        for (int c = 0; c < BQ; ++c) {
+          const int idx = tid + 256 * c;
+          if (idx < SP * SP) Bs[idx] = bv[c];
+        }
+      }
+    }
+    lds_barrier();
+    if (flush) {  // the current slot's scalars, for every thread
+      gn = gsl[n];
+      bn = bsl[n];
+      if constexpr (!CHAN) egn = fast_exp(gn);
+    }
+
+    if (flush) {
+      if constexpr (ERASE) {
+        // ---- channel work: thread tid owns channel k = tid.  Ls holds raw keys.
+        // The pseudo-values of slots before n need only the stored rows of T^{-1},
+        // so the waves that own no channel form them meanwhile.
+        static_assert(K + V <= 256, "channel waves and value waves must be disjoint");
+        float pi[SP], kn = 0.f;
+        if (tid < K) {
+          const int kk = tid;
+          kn = Ls[n * LP + kk];
+          float gnk = gn;
+          if constexpr (CHAN) {
+            // g_s of channel tid: running sum of the window's log alphas
+            float acc = 0.f;
+#pragma unroll
+            for (int s = 0; s < SP; ++s) {
+              acc += s <= n ? gk[s] : 0.f;
+              gk[s] = s <= n ? acc : 0.f;
+            }
+#pragma unroll
+            for (int s = 0; s < SP; ++s)
+              if (s == n) gnk = gk[s];
+          }
+          // erase factors pi_s = sum_{j<=s} (T^{-1})_{s,j} beta_j e^{g_j} k_j, s < n
+          // (eq. wy with T^{-1} from the ring): independent sums, no recursion
+          float xk[SP];
+#pragma unroll
+          for (int s = 0; s < SP; ++s) xk[s] = s < n ? bsl[s] * fast_exp(CHAN ? gk[s] : gsl[s]) * Ls[s * LP + kk] : 0.f;
 #pragma unroll
           for (int s = 0; s < SP; ++s) {
-            acc += s <= n ? gk[s] : 0.f;
-            gk[s] = s <= n ? acc : 0.f;
+            pi[s] = 0.f;
+            if (s < n) {
+              float acc = xk[s];
+#pragma unroll
+              for (int j = 0; j < s; ++j) acc += Bs[s * SP + j] * xk[j];
+              pi[s] = acc;
+            }
           }
+          // b_{n,s} = <exp(g_n - g_s) . k_s, k_n>: partial sums over this wave's channels
 #pragma unroll
-          for (int s = 0; s < SP; ++s)
-            if (s == n) gnk = gk[s];
-        }
-        // erase factors pi_s = sum_{j<=s} (T^{-1})_{s,j} beta_j e^{g_j} k_j, s < n
-        // (eq. wy with T^{-1} from the ring): independent sums, no recursion
-        float xk[SP];
-#pragma unroll
-        for (int s = 0; s < SP; ++s) xk[s] = s < n ? bsl[s] * fast_exp(CHAN ? gk[s] : gsl[s]) * Ls[s * LP + kk] : 0.f;
-#pragma unroll
-        for (int s = 0; s < SP; ++s) {
-          pi[s] = 0.f;
-          if (s < n) {
-            float acc = xk[s];
-#pragma unroll
-            for (int j = 0; j < s; ++j) acc += Bs[s * SP + j] * xk[j];
-            pi[s] = acc;
+          for (int s = 0; s < SP; ++s) {
+            if (s < n) {
+              const float e = CHAN ? fast_exp(gnk - gk[s]) : csc[s];
+              const float bsum = wave_sum(e * Ls[s * LP + kk] * kn);
+              if (lane == 0) bpart[wave * SP + s] = bsum;
+            }
           }
-        }
-        // b_{n,s} = <exp(g_n - g_s) . k_s, k_n>: partial sums over this wave's channels
+          if constexpr (CHAN) {
+            // left factors L[s] = exp(g_n - g_s) k_s replace the keys in place
+            ds[kk] = fast_exp(gnk);
 #pragma unroll
-        for (int s = 0; s < SP; ++s) {
-          if (s < n) {
-            const float e = CHAN ? fast_exp(gnk - gk[s]) : csc[s];
-            const float bsum = wave_sum(e * Ls[s * LP + kk] * kn);
-            if (lane == 0) bpart[wave * SP + s] = bsum;
+            for (int s = 0; s < SP; ++s)
+              if (s < n) Ls[s * LP + kk] *= fast_exp(gnk - gk[s]);
           }
-        }
-        if constexpr (CHAN) {
-          // left factors L[s] = exp(g_n - g_s) k_s replace the keys in place
-          ds[kk] = fast_exp(gnk);
+        } else if (tid >= 256 - V) {
+          // pseudo-values u_s = sum_{j<=s} (T^{-1})_{s,j} beta_j v_j, s < n, in
+          // place over the raw values (thread owns value channel v)
+          const int v = tid - (256 - V);
+          float xv[SP];
 #pragma unroll
-          for (int s = 0; s < SP; ++s)
-            if (s < n) Ls[s * LP + kk] *= fast_exp(gnk - gk[s]);
-        }
-      } else if (tid >= 256 - V) {
-        // pseudo-values u_s = sum_{j<=s} (T^{-1})_{s,j} beta_j v_j, s < n, in
-        // place over the raw values (thread owns value channel v)
-        const int v = tid - (256 - V);
-        float xv[SP];
+          for (int s = 0; s < SP; ++s) xv[s] = s < n ? bsl[s] * Us[s * UP + v] : 0.f;
 #pragma unroll
-        for (int s = 0; s < SP; ++s) xv[s] = s < n ? bsl[s] * Us[s * UP + v] : 0.f;
+          for (int s = 0; s < SP; ++s) {
+            if (s < n) {
+              float acc = xv[s];
 #pragma unroll
-        for (int s = 0; s < SP; ++s) {
-          if (s < n) {
-            float acc = xv[s];
-#pragma unroll
-            for (int j = 0; j < s; ++j) acc += Bs[s * SP + j] * xv[j];
-            Us[s * UP + v] = acc;
+              for (int j = 0; j < s; ++j) acc += Bs[s * SP + j] * xv[j];
+              Us[s * UP + v] = acc;
+            }
           }
         }
+        lds_barrier();
+        // ---- slot n: row n of the couplings comes from every wave's partial sums
+        if (tid < V) {
+          const int v = tid;
+          float acc = Us[n * UP + v];
+#pragma unroll
+          for (int j = 0; j < SP; ++j) {
+            if (j < n) {
+              float bj = 0.f;
+#pragma unroll
+              for (int w = 0; w < KW; ++w) bj += bpart[w * SP + j];
+              acc -= bj * Us[j * UP + v];
+            }
+          }
+          Us[n * UP + v] = bn * acc;
+        }
+        if (tid < K) {
+          const int kk = tid;
+          float gnk = gn;
+          if constexpr (CHAN) {
+#pragma unroll
+            for (int s = 0; s < SP; ++s)
+              if (s == n) gnk = gk[s];
+          }
+          float acc = fast_exp(gnk) * kn;
+#pragma unroll
+          for (int j = 0; j < SP; ++j) {
+            if (j < n) {
+              float bj = 0.f;
+#pragma unroll
+              for (int w = 0; w < KW; ++w) bj += bpart[w * SP + j];
+              acc -= bj * pi[j];
+            }
+          }
+          const float pin = bn * acc;
+#pragma unroll
+          for (int s = 0; s < SP; ++s) PiT[kk * PP + s] = (s < n) ? pi[s] : (s == n ? pin : 0.f);
+        }
+        lds_barrier();
       }
-      lds_barrier();
-      // ---- slot n: row n of the couplings comes from every wave's partial sums
-      if (tid < V) {
-        const int v = tid;
-        float acc = Us[n * UP + v];
-#pragma unroll
-        for (int j = 0; j < SP; ++j) {
-          if (j < n) {
-            float bj = 0.f;
-#pragma unroll
-            for (int w = 0; w < KW; ++w) bj += bpart[w * SP + j];
-            acc -= bj * Us[j * UP + v];
-          }
-        }
-        Us[n * UP + v] = bn * acc;
-      }
-      if (tid < K) {
-        const int kk = tid;
-        float gnk = gn;
-        if constexpr (CHAN) {
-#pragma unroll
-          for (int s = 0; s < SP; ++s)
-            if (s == n) gnk = gk[s];
-        }
-        float acc = fast_exp(gnk) * kn;
-#pragma unroll
-        for (int j = 0; j < SP; ++j) {
-          if (j < n) {
-            float bj = 0.f;
-#pragma unroll
-            for (int w = 0; w < KW; ++w) bj += bpart[w * SP + j];
-            acc -= bj * pi[j];
-          }
-        }
-        const float pin = bn * acc;
-#pragma unroll
-        for (int s = 0; s < SP; ++s) PiT[kk * PP + s] = (s < n) ? pi[s] : (s == n ? pin : 0.f);
-      }
-      lds_barrier();
     }
+    if (last) break;
+    // an earlier chunk: its update, before the next chunk's staging reuses the LDS
+#pragma unroll
+    for (int t = 0; t < VTW; ++t)
+      if (wave + 4 * t < VT)
+        rank_update_tile<KIND, MT, ST, LP, PP, UP>(xs[t], 16 * (wave + 4 * t) + lr, lr, lg, egn, Ls, PiT, Us, bsl, csc, ds);
+    lds_barrier();
   }
 
   // ---- matrix-core phase, one 16-column value tile at a time (with a
@@ -794,44 +867,7 @@ __global__ __launch_bounds__(256, (P != 0 && WMAX == 16 && R <= 16) ? 4 : 3) voi
     if (vt >= VT) continue;
     const int v = 16 * vt + lr;
     if (flush && ps == 0) {
-      // value-side factors of the rank update, C layout: slot s = 16 st + 4 lg + i
-      floatx4 wv[ST];
-#pragma unroll
-      for (int st = 0; st < ST; ++st) {
-        floatx4 acc = {0.f, 0.f, 0.f, 0.f};
-        if constexpr (ERASE) {
-          // w_s = u_s - (Pi X_0^T)[s]; four independent accumulation chains
-          floatx4 pc[4];
-#pragma unroll
-          for (int i = 0; i < 4; ++i) pc[i] = floatx4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-          for (int kt = 0; kt < MT; ++kt)
-#pragma unroll
-            for (int i = 0; i < 4; ++i)
-              pc[i] = mfma4(PiT[(16 * kt + 4 * lg + i) * PP + 16 * st + lr], xs[t][kt][i], pc[i]);
-          acc = (pc[0] + pc[1]) + (pc[2] + pc[3]);
-        }
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          const int s = 16 * st + 4 * lg + i;
-          float w = Us[s * UP + v] - acc[i];
-          if constexpr (!ERASE) w *= bsl[s] * csc[s];     // Mamba-2: c_s beta_s v_s
-          if constexpr (ERASE && !CHAN) w *= csc[s];      // GDN: c_s w_s
-          wv[st][i] = w;
-        }
-      }
-      // X_W^T = Diag(e^{g_n}) X_0^T + (keys or L)^T W^T, accumulated onto the decayed state
-#pragma unroll
-      for (int kt = 0; kt < MT; ++kt) {
-        floatx4 acc;
-#pragma unroll
-        for (int i = 0; i < 4; ++i) acc[i] = xs[t][kt][i] * (CHAN ? ds[16 * kt + 4 * lg + i] : egn);
-#pragma unroll
-        for (int st = 0; st < ST; ++st)
-#pragma unroll
-          for (int i = 0; i < 4; ++i) acc = mfma4(Ls[(16 * st + 4 * lg + i) * LP + 16 * kt + lr], wv[st][i], acc);
-        xs[t][kt] = acc;
-      }
+      rank_update_tile<KIND, MT, ST, LP, PP, UP>(xs[t], v, lr, lg, egn, Ls, PiT, Us, bsl, csc, ds);
       // exact output o_W[v] = sum_k X_W[v][k] q_W[k]
       if (a.o) {
         float p = 0.f;

@@ -154,6 +154,47 @@ def test_window_one_full_size(name):
     assert not bad, "; ".join(bad)
 
 
+@pytest.mark.parametrize("fam,io,m", [("gdn", "f32", 6), ("gdn", "bf16", 16), ("gdn", "f32", 17), ("kda", "f32", 16),
+                                      ("kda", "bf16", 17), ("kda", "f32", 27), ("mamba2", "f32", 21)])
+def test_partial_flush_of_a_32_slot_window(fam, io, m):
+    """A 32-slot window flushed after m tokens (sketchssm_update with
+    n_buffered = m - 1 after m - 1 decode reads): one chunk of slots, a whole
+    first chunk, or a whole first chunk and a part of the second.  The state,
+    the flush's output and the new sketch against the oracle's recurrence over
+    the m tokens."""
+    import oracle
+    from paper_2609_33051_amd import binding as B
+    from paper_2609_33051_amd.layer import SketchSSMLayer
+    V, R = (64 if fam == "mamba2" else 128), 8
+    wl = inputs.tiny(fam, batch=4, heads=3, dk=128, dv=V, rank=R, window=32, steps=m, io=io)
+    announce(f"partial flush W=32 m={m} {fam} io={io}")
+    om, C = inputs.omega(wl, R, inputs.SEED)
+    S = inputs.initial_state(wl, "cuda", inputs.SEED)
+    S0 = to_np32(S.reshape(-1, V, 128))
+    layer = SketchSSMLayer(wl.kind, wl.batch, wl.heads, 128, V, R, 32, io, "cuda", S=S,
+                           omega=torch.as_tensor(om), coef=torch.as_tensor(C))
+    layer.init_sketch()
+    steps = [inputs.step_inputs(wl, t, "cuda", inputs.SEED) for t in range(m)]
+    for t in range(m - 1):
+        layer.step(steps[t])
+    layer.write_token(steps[-1])
+    o = torch.empty((wl.batch, wl.heads, V), dtype=torch.float32, device="cuda")
+    B.sketchssm_update(layer.cfg, layer.S, layer.omega, layer.ring, m - 1, steps[-1]["q"], layer.U, o,
+                       layer.stream(), cmap=layer.cmap)
+    torch.cuda.synchronize()
+    n = wl.batch * wl.heads
+    seq = {k: np.stack([to_np32(st[k].reshape(n, -1) if k in ("q", "k", "v") or st[k].dim() > 2
+                                else st[k].reshape(n)) for st in steps]) for k in ("q", "k", "v", "beta", "log_decay")}
+    o_ex, S_ex = oracle.recurrence(wl.kind, S0, seq["q"], seq["k"], seq["v"], seq["beta"], seq["log_decay"])
+    heads = np.arange(n) % wl.heads
+    U_ex = np.einsum("nvk,nkr->nvr", np.asarray(S_ex, dtype=np.float64), np.asarray(om, dtype=np.float64)[heads])
+    rep = parity_report([to_np32(o.reshape(n, V))], np.asarray(o_ex)[-1:], to_np32(layer.state().reshape(n, V, 128)),
+                        S_ex, to_np32(layer.sketch_matrix().reshape(n, V, R)), U_ex)
+    print("  " + format_report(rep), flush=True)
+    bad = parity_failures(rep, *bars(io, "f32"))
+    assert not bad, "; ".join(bad)
+
+
 @pytest.mark.parametrize("fam,io", [("mamba2", "f32"), ("gdn", "bf16"), ("kda", "f32"), ("kda", "bf16")])
 def test_single_token_flush_of_a_longer_window(fam, io):
     """A window flushed after its first token at rank 0 (sketchssm_update with

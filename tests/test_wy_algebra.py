@@ -129,3 +129,41 @@ def test_inverse_rows_replace_the_recursions(kind, seed):
         alpha = Tinv[:n, :n].T @ a
         np.testing.assert_allclose(sum(a[s] * u[s] for s in range(n)),
                                    (alpha * beta[:n]) @ v[:n], atol=1e-12)
+
+
+@pytest.mark.parametrize("kind,W,c", [("gdn", 9, 4), ("kda", 9, 4), ("gdn", 7, 3), ("kda", 8, 8), ("kda", 5, 2)])
+def test_chunked_flush_from_stored_rows(kind, W, c):
+    """A window flushed as chunks of c slots, each from the state the previous
+    chunk left: T is unit lower triangular, so the rows of the window's T^{-1}
+    that couple a chunk's slots among themselves (its diagonal block) are the
+    inverse of the T that chunk alone would build (decays counted from the
+    chunk's first slot), and each chunk is then a rank-c flush of its own.
+    The chunked flush must reproduce the explicitly multiplied transitions."""
+    k, q, v, beta, logd, S0, C = make(kind, K=7, V=5, W=W, seed=W + c)
+    K = k.shape[1]
+    S = S0.copy()
+    for t in range(W):
+        S = M(kind, k[t], beta[t], logd[t]) @ S + beta[t] * np.outer(k[t], v[t])
+    g = np.cumsum(logd, axis=0)
+    Bc = np.zeros((W, W))
+    for t in range(W):
+        for j in range(t):
+            Bc[t, j] = np.sum(np.exp(g[t] - g[j]) * k[j] * k[t])
+    Tinv = np.linalg.inv(np.eye(W) + np.diag(beta) @ Bc)     # the stored rows, whole window
+    X = S0.T
+    for s0 in range(0, W, c):
+        sl = slice(s0, min(s0 + c, W))
+        n = sl.stop - s0
+        gc = np.cumsum(logd[sl], axis=0)                     # decays from the chunk's first slot
+        Bl = np.zeros((n, n))
+        for t in range(n):
+            for j in range(t):
+                Bl[t, j] = np.sum(np.exp(gc[t] - gc[j]) * k[s0 + j] * k[s0 + t])
+        Ti = Tinv[sl, sl]
+        np.testing.assert_allclose(Ti, np.linalg.inv(np.eye(n) + np.diag(beta[sl]) @ Bl), atol=1e-12)
+        u = Ti @ (beta[sl, None] * v[sl])
+        pis = Ti @ (beta[sl, None] * np.exp(gc) * k[sl])
+        L = np.stack([np.exp(gc[-1] - gc[s]) * k[s0 + s] for s in range(n)])
+        Wv = (u - (X @ pis.T).T).T                           # V x n: w_s = u_s - X pi_s
+        X = X * np.exp(gc[-1])[None, :] + Wv @ L
+    np.testing.assert_allclose(X, S.T, atol=1e-12)

@@ -13,6 +13,33 @@ namespace skssm {
 
 constexpr int kUnsupported = -2;
 
+// LDS of one gfx950 CU, shared by the workgroups resident on it.
+constexpr size_t kLdsPerCU = 160 * 1024;
+
+// Dynamic LDS (unused by the kernel) that holds a kernel to at most `cap`
+// resident workgroups per CU: each then takes more than a (cap + 1)-th of the
+// CU's LDS.  Zero where the kernel's static LDS already does that, or if its
+// attributes cannot be read (the launch then runs uncapped).
+template <typename Kernel>
+size_t lds_for_cap(Kernel kern, int cap) {
+  hipFuncAttributes at;
+  if (hipFuncGetAttributes(&at, reinterpret_cast<const void*>(kern)) != hipSuccess) return 0;
+  const size_t need = kLdsPerCU / (size_t)(cap + 1) + 1024;
+  return need > at.sharedSizeBytes ? need - at.sharedSizeBytes : 0;
+}
+
+// Resident workgroups per CU for the kernels that read each item's state and
+// write it back in place (the flush with the offline map or none, and the
+// single-token update).  With more of these streams resident per CU the
+// in-place stream measured slower: the flush took 431 / 456 us (Mamba-2 at six
+// per CU, GDN at four; B = 256 / 512) against 387 / 435 us at three, and the
+// Mamba-2 single-token update 391 us at eight against 342 us at two.  The
+// flushes that build a state-dependent map, the initial sketch and the decode
+// do arithmetic or wait on latency between their loads and keep their
+// occupancy (capping them measured slower).
+constexpr int kFlushPerCU = 3;
+constexpr int kTokenPerCU = 2;
+
 template <int KIND, int K, int V, int R, int WM, typename IO, typename SK, int P>
 int launch_decode(const DecodeArgs& a, hipStream_t s) {
   const unsigned tiles = (unsigned)((a.B + 3) / 4);
@@ -33,7 +60,9 @@ int launch_full_read(const DecodeArgs& a, hipStream_t s) {
 template <int KIND, int K, int V, int R, int WM, typename IO, typename SK, int P>
 int launch_update(const UpdateArgs& a, hipStream_t s) {
   const size_t items = (size_t)a.B * a.H;
-  hipLaunchKernelGGL((update_kernel<KIND, K, V, R, WM, IO, SK, P>), dim3((unsigned)items), dim3(256), 0, s, a);
+  static const size_t cap = P == 0 ? lds_for_cap(&update_kernel<KIND, K, V, R, WM, IO, SK, P>, kFlushPerCU) : 0;
+  hipLaunchKernelGGL((update_kernel<KIND, K, V, R, WM, IO, SK, P>), dim3((unsigned)items), dim3(256), a.nt > 0 ? cap : 0,
+                     s, a);
   return 0;
 }
 
@@ -99,7 +128,10 @@ int run_full_read(const DecodeArgs& a, int K, int V, int io, void* stream) {
 template <int KIND, int K, int V, typename IO>
 int launch_token(const UpdateArgs& a, hipStream_t s) {
   const size_t items = (size_t)a.B * a.H;
-  hipLaunchKernelGGL((token_kernel<KIND, K, V, IO>), dim3((unsigned)items), dim3(256), 0, s, a);
+  // (the erase families' single-token update holds more registers per lane and
+  // measured the same at two to five resident workgroups per CU)
+  static const size_t cap = KIND == MAMBA2 ? lds_for_cap(&token_kernel<KIND, K, V, IO>, kTokenPerCU) : 0;
+  hipLaunchKernelGGL((token_kernel<KIND, K, V, IO>), dim3((unsigned)items), dim3(256), cap, s, a);
   return 0;
 }
 

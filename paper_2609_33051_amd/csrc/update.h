@@ -558,7 +558,7 @@ __global__ __launch_bounds__(256, (P != 0 && WMAX == 16 && R <= 16) ? 4 : 3) voi
   // ---- every small load first (window, query, rows of T^{-1}, Omega), then the
   // state: the staged values reach LDS while the state read is still in flight
   float egn = 1.f, gn = 0.f, bn = 0.f;  // the chunk's e^{g_n} (scalar decay), g_n, beta_n (from LDS after the staging)
-  float qv = 0.f;
+  Raw<IO, 1> qr;  // this thread's query channel, raw (converted at the staging, so no wait here)
   constexpr int BQ = ERASE ? (SP * SP + 255) / 256 : 1;
   Vec<4> omv[OQ];
   floatx4 xs[VTW][MT];
@@ -597,7 +597,7 @@ __global__ __launch_bounds__(256, (P != 0 && WMAX == 16 && R <= 16) ? 4 : 3) voi
           vr[gq].load(static_cast<const IO*>(a.rv) + si * V + col * VR);
         }
       }
-      if (ch == 0 && tid < K) qv = load1<IO>(static_cast<const IO*>(a.q) + item * K + tid);
+      if (ch == 0) qr.load(static_cast<const IO*>(a.q) + item * K + (tid < K ? tid : K - 1));
       if constexpr (ERASE) {
 #pragma unroll
         for (int c = 0; c < BQ; ++c) {
@@ -619,12 +619,13 @@ __global__ __launch_bounds__(256, (P != 0 && WMAX == 16 && R <= 16) ? 4 : 3) voi
       }
     }
 
-    // ---- the single read of the state
+    // ---- the single read of the state (unconditional where every wave owns
+    // VTW tiles, so that waiting for the staged loads never waits for these)
     if (ch == 0) {
 #pragma unroll
       for (int t = 0; t < VTW; ++t) {
         const int vt = wave + 4 * t;
-        if (vt < VT) {
+        if (VT % 4 == 0 || vt < VT) {
           // tile (vt, kt) of the state is 1 KB contiguous, lane l's float4 at 4 l
           const float* src = a.S + item * V * K + (size_t)(vt * MT) * 256 + 4 * lane;
 #pragma unroll
@@ -681,7 +682,7 @@ __global__ __launch_bounds__(256, (P != 0 && WMAX == 16 && R <= 16) ? 4 : 3) voi
         for (int m = 0; m < VR; m += 4)
           *reinterpret_cast<float4*>(&Us[s * UP + col * VR + m]) = make_float4(vsv[m], vsv[m + 1], vsv[m + 2], vsv[m + 3]);
       }
-      if (ch == 0 && tid < K) qs[tid] = qv;
+      if (ch == 0 && tid < K) qs[tid] = qr.get(0);
       if (tid < 64) {
         // wave 0: beta_s, g_s = sum_{j<=s} log alpha_j (inclusive scan over the
         // lanes) and c_s = e^{g_n - g_s}, slots past n zero

@@ -199,6 +199,12 @@ typedef struct {
  *        are not written.  Ignored (may be NULL) when pivots = 0.
  * o      [B][H][V] fp32 output or NULL.
  * rank may be 0 here (no sketch: the flush of the exact baseline).
+ *
+ * Occupancy: a flush with pivots = 0 (and the Mamba-2 single-token update)
+ * launches with unused dynamic LDS so that at most three (two) of its
+ * workgroups are resident per CU, which streams the in-place state faster
+ * than more would; other kernels on the device are not affected, except that
+ * a kernel running concurrently on the same CUs finds that LDS taken.
  */
 int sketchssm_update(const skssm_config* cfg, float* S, const float* omega, const skssm_ring* ring,
                      int32_t n_buffered, const void* q, void* U, void* cmap, float* o, void* stream);

@@ -34,9 +34,10 @@ size_t lds_for_cap(Kernel kern, int cap) {
 // in-place stream measured slower: the flush took 431 / 456 us (Mamba-2 at six
 // per CU, GDN at four; B = 256 / 512) against 387 / 435 us at three, and the
 // Mamba-2 single-token update 391 us at eight against 342 us at two.  The
-// flushes that build a state-dependent map, the initial sketch and the decode
-// do arithmetic or wait on latency between their loads and keep their
-// occupancy (capping them measured slower).
+// flushes that build a state-dependent map and the decode do arithmetic or
+// wait on latency between their loads and keep their occupancy (capping them
+// measured slower), as does the initial sketch (a read of the state, run once
+// after prefill).
 constexpr int kFlushPerCU = 3;
 constexpr int kTokenPerCU = 2;
 

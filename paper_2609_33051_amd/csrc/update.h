@@ -565,7 +565,8 @@ __global__ __launch_bounds__(256, (P != 0 && WMAX == 16 && R <= 16) ? 4 : 3) voi
 #pragma unroll
   for (int ch = 0; ch < CH; ++ch) {
     const int sb = 16 * ch;                                 // the chunk's first slot in the ring
-    // the chunk's current slot (counted from sb); whether it holds the window's
+    // the chunk's current slot (counted from sb), and whether the chunk holds
+    // the window's current slot (then it is the last one)
     const int n = CH == 1 ? nw : !flush ? 0 : (nw - sb < SP ? nw - sb : SP - 1);
     const bool last = CH == 1 || !flush || nw < sb + SP;
     float bl = 0.f, ll = 0.f;             // wave 0, lane s: beta_s and (scalar decay) log alpha_s
@@ -728,7 +729,7 @@ __global__ __launch_bounds__(256, (P != 0 && WMAX == 16 && R <= 16) ? 4 : 3) voi
           kn = Ls[n * LP + kk];
           float gnk = gn;
           if constexpr (CHAN) {
-            // g_s of channel tid: running sum of the window's log alphas
+            // g_s of channel tid: running sum of the chunk's log alphas
             float acc = 0.f;
 #pragma unroll
             for (int s = 0; s < SP; ++s) {

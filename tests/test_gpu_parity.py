@@ -195,6 +195,47 @@ def test_partial_flush_of_a_32_slot_window(fam, io, m):
     assert not bad, "; ".join(bad)
 
 
+@pytest.mark.parametrize("fam", ["gdn", "kda"])
+def test_every_flush_point_of_a_32_slot_window(fam):
+    """The erase families' 32-slot window flushed after every m = 1..32
+    tokens (one 16-slot chunk, a whole first chunk, or a first chunk and any
+    part of the second) at a tiny batch: state and the flush's output against
+    the oracle's recurrence over the m tokens."""
+    import oracle
+    from paper_2609_33051_amd import binding as B
+    from paper_2609_33051_amd.layer import SketchSSMLayer
+    V, R = 64, 8
+    wl = inputs.tiny(fam, batch=2, heads=2, dk=64, dv=V, rank=R, window=32, steps=32, io="f32")
+    announce(f"every flush point W=32 {fam}")
+    om, C = inputs.omega(wl, R, inputs.SEED)
+    steps = [inputs.step_inputs(wl, t, "cuda", inputs.SEED) for t in range(32)]
+    n = wl.batch * wl.heads
+    seq = {k: np.stack([to_np32(st[k].reshape(n, -1) if k in ("q", "k", "v") or st[k].dim() > 2
+                                else st[k].reshape(n)) for st in steps]) for k in ("q", "k", "v", "beta", "log_decay")}
+    failures = []
+    for m in range(1, 33):
+        S = inputs.initial_state(wl, "cuda", inputs.SEED)
+        S0 = to_np32(S.reshape(-1, V, 64))
+        layer = SketchSSMLayer(wl.kind, wl.batch, wl.heads, 64, V, R, 32, "f32", "cuda", S=S,
+                               omega=torch.as_tensor(om), coef=torch.as_tensor(C))
+        layer.init_sketch()
+        for t in range(m - 1):
+            layer.step(steps[t])
+        layer.write_token(steps[m - 1])
+        o = torch.empty((wl.batch, wl.heads, V), dtype=torch.float32, device="cuda")
+        B.sketchssm_update(layer.cfg, layer.S, layer.omega, layer.ring, m - 1, steps[m - 1]["q"], layer.U, o,
+                           layer.stream(), cmap=layer.cmap)
+        torch.cuda.synchronize()
+        o_ex, S_ex = oracle.recurrence(wl.kind, S0, *(seq[k][:m] for k in ("q", "k", "v", "beta", "log_decay")))
+        rep = parity_report([to_np32(o.reshape(n, V))], np.asarray(o_ex)[-1:], to_np32(layer.state().reshape(n, V, 64)),
+                            S_ex)
+        bad = parity_failures(rep, *bars("f32", "f32"))
+        if bad:
+            failures.append(f"m={m}: " + "; ".join(bad))
+    print(f"  {32 - len(failures)} of 32 flush points within the bars", flush=True)
+    assert not failures, "; ".join(failures)
+
+
 @pytest.mark.parametrize("fam,io", [("mamba2", "f32"), ("gdn", "bf16"), ("kda", "f32"), ("kda", "bf16")])
 def test_single_token_flush_of_a_longer_window(fam, io):
     """A window flushed after its first token at rank 0 (sketchssm_update with
